@@ -1,0 +1,472 @@
+#!/usr/bin/env python3
+"""Benchmark of the collective copy/reduce path on one MI355X.
+
+Default workload (one JSON line on stdout): one-shot all-reduce, bf16 data
+with fp32 accumulation, P=8 simulated ranks, decode-shaped messages [T, 8192]
+for T in {1, 4, 16, 64} (16 KiB - 1 MiB per rank).  One step = one
+all-reduce at each of the four sizes.  Calls are captured in a HIP graph and
+replayed; each call works on buffers carved from a rotating 1.5 GiB pool, so
+its inputs are not resident in L2 or the 256 MB Infinity Cache when it runs
+(cold).  NUNA-aware (XCD) and locality-unaware (LINEAR) placement are timed
+interleaved A/B; ``value`` is the XCD-placement throughput.
+
+Throughput = algorithmic bytes / time.  Algorithmic bytes of an all-reduce
+call are (P reads + P writes) * n * element size.
+
+``--full`` instead sweeps every workload (fp32 integer all-reduce, decode and
+prefill all-reduce, MoE all-to-all dispatch, P=64 all-reduce) in both modes,
+cold and warm, and writes JSONL to ``--out``.
+"""
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+METRIC = ("collective latency (µs) + effective HBM GB/s vs msg size, NUNA-aware vs unaware, 1 GPU")
+HBM_PEAK_GBPS = 8000.0
+POOL_BYTES_MAIN = 3 << 29  # 1.5 GiB
+ALIGN = 4096
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1280, help="timed steps per placement mode")
+    ap.add_argument("--warmup", type=int, default=3, help="untimed graph replays before timing")
+    ap.add_argument("--reps", type=int, default=15, help="timed replays per size in the sweeps")
+    ap.add_argument("--full", action="store_true", help="sweep every workload and write JSONL")
+    ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"))
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle timing budget (cpu_baseline)")
+    ap.add_argument("--no-cpu", action="store_true")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------------------------- buffers
+
+class Pool:
+    """One big device allocation carved into 4 KiB-aligned buffer sets at rotating offsets."""
+
+    def __init__(self, torch, nbytes):
+        self.torch = torch
+        self.buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        self.nbytes = nbytes
+        self.off = 0
+
+    def take(self, nbytes):
+        nbytes = (nbytes + ALIGN - 1) // ALIGN * ALIGN
+        if self.off + nbytes > self.nbytes:
+            self.off = 0
+        v = self.buf[self.off:self.off + nbytes]
+        self.off += nbytes
+        return v
+
+    def rank_views(self, P, nelem, dtype, region):
+        es = 2 if dtype == self.torch.bfloat16 else 4
+        per = (nelem * es + ALIGN - 1) // ALIGN * ALIGN
+        return [region[r * per:r * per + nelem * es].view(dtype) for r in range(P)]
+
+
+def ar_footprint(P, n, es):
+    per = (n * es + ALIGN - 1) // ALIGN * ALIGN
+    return 2 * P * per
+
+
+# ---------------------------------------------------------------------------------------------- timing
+
+def time_graphs(torch, graphs, calls_per_graph, reps, warmup):
+    """Replay each graph `warmup` times, then `reps` rounds interleaving all graphs (A/B/A/B).
+    Returns {name: [us per call, ...]} from HIP events on the current stream."""
+    for _ in range(warmup):
+        for g in graphs.values():
+            g.replay()
+    torch.cuda.synchronize()
+    res = {k: [] for k in graphs}
+    for _ in range(reps):
+        for k, g in graphs.items():
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            g.replay()
+            b.record()
+            b.synchronize()
+            res[k].append(a.elapsed_time(b) * 1e3 / calls_per_graph)
+    return res
+
+
+def capture(torch, fn, ncalls):
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn(0)  # warm-up launch outside capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(ncalls):
+            fn(i)
+    torch.cuda.synchronize()
+    return g
+
+
+def stats(v):
+    v = sorted(v)
+    q = lambda p: v[min(len(v) - 1, max(0, int(round(p * (len(v) - 1)))))]  # noqa: E731
+    return {"median": statistics.median(v), "p10": q(0.1), "p90": q(0.9)}
+
+
+# ---------------------------------------------------------------------------------------------- workloads
+
+COLD_SPAN = 512 << 20  # bytes a graph replay must sweep to leave L2 and the Infinity Cache cold
+
+
+def dev_copy_of(torch, a):
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16).copy()).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def ar_sets(torch, pool, x_np, nsets, src=None):
+    """`nsets` (ins, outs) buffer sets at rotating pool offsets, inputs filled with x."""
+    P, n = len(x_np), x_np[0].size
+    dt = torch.bfloat16 if x_np[0].dtype == np.uint16 else torch.float32
+    es = 2 if dt == torch.bfloat16 else 4
+    if src is None:
+        src = [dev_copy_of(torch, a) for a in x_np]
+    sets = []
+    for _ in range(nsets):
+        region = pool.take(ar_footprint(P, n, es))
+        half = region.numel() // 2
+        ins = pool.rank_views(P, n, dt, region[:half])
+        outs = pool.rank_views(P, n, dt, region[half:])
+        for a, b in zip(ins, src):
+            a.copy_(b)
+        sets.append((ins, outs))
+    return sets
+
+
+def oracle_check_ar(nuna, torch, x_np, algo, place):
+    """One call on fresh buffers compared bit for bit with the oracle."""
+    import oracle
+    ref = oracle.allreduce(x_np)
+    dt = torch.bfloat16 if x_np[0].dtype == np.uint16 else torch.float32
+    ins = [dev_copy_of(torch, a) for a in x_np]
+    outs = nuna.allreduce(ins, algo=algo, placement=place)
+    torch.cuda.synchronize()
+    for d, o in enumerate(outs):
+        g = o.cpu()
+        g = g.view(torch.int16).numpy().view(np.uint16) if dt == torch.bfloat16 else g.numpy()
+        if not np.array_equal(g.view(ref[d].dtype), ref[d]):
+            return False
+    return True
+
+
+def calls_for(fp, cold, max_calls=4096):
+    return int(min(max_calls, max(4, math.ceil(COLD_SPAN / fp)))) if cold else int(min(max_calls, max(
+        4, math.ceil((64 << 20) / fp))))
+
+
+def bench_allreduce(nuna, torch, pool, x_np, algo, reps, warmup, cold=True, places=("linear", "xcd")):
+    P, n = len(x_np), x_np[0].size
+    es = 2 if x_np[0].dtype == np.uint16 else 4
+    fp = ar_footprint(P, n, es)
+    calls = calls_for(fp, cold)
+    nsets = max(1, min(calls, pool.nbytes // fp)) if cold else 1
+    pool.off = 0
+    sets = ar_sets(torch, pool, x_np, nsets)
+    graphs = {}
+    for place in places:
+        graphs[place] = capture(torch, lambda i, place=place: nuna.allreduce(
+            sets[i % nsets][0], sets[i % nsets][1], algo=algo, placement=place), calls)
+    t = time_graphs(torch, graphs, calls, reps, warmup)
+    alg_bytes = 2 * P * n * es
+    out = {}
+    for place in places:
+        st = stats(t[place])
+        out[place] = {"us": st, "gbps": alg_bytes / (st["median"] * 1e-6) / 1e9}
+    del graphs, sets
+    return alg_bytes, out, calls
+
+
+# ---------------------------------------------------------------------------------------------- main line
+
+DECODE_STEPS_PER_GRAPH = 64
+
+
+def decode_steps_timed(nuna, torch, pool, args):
+    """The timed region: K steps per placement mode, a step being one all-reduce at each decode size.
+    Steps are replayed from a graph holding 64 steps, each on its own pool region (cold)."""
+    from paper_2608_00867_amd import workloads as wl
+    xs = [wl.ar_bf16_decode(T) for T in wl.DECODE_TOKENS]
+    step_fp = sum(ar_footprint(8, x[0].size, 2) for x in xs)
+    nsteps = DECODE_STEPS_PER_GRAPH
+    assert step_fp * nsteps <= pool.nbytes
+    pool.off = 0
+    srcs = [[dev_copy_of(torch, a) for a in x] for x in xs]
+    sets = [[ar_sets(torch, pool, x, 1, src)[0] for x, src in zip(xs, srcs)] for _ in range(nsteps)]
+
+    def step(i, place):
+        for ins, outs in sets[i]:
+            nuna.allreduce(ins, outs, algo="auto", placement=place)
+
+    graphs = {p: capture(torch, lambda i, p=p: step(i, p), nsteps) for p in ("linear", "xcd")}
+    reps = max(1, math.ceil(args.steps / nsteps))
+    for _ in range(args.warmup):
+        for g in graphs.values():
+            g.replay()
+    torch.cuda.synchronize()
+    ev = {p: [] for p in graphs}
+    for _ in range(reps):
+        for p, g in graphs.items():
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            g.replay()
+            b.record()
+            b.synchronize()
+            ev[p].append(a.elapsed_time(b))
+    torch.cuda.synchronize()
+    step_bytes = sum(2 * 8 * x[0].size * 2 for x in xs)
+    out = {}
+    for p in graphs:
+        ms = sum(ev[p]) / (reps * nsteps)
+        out[p] = {"ms_per_step": ms, "gbps": step_bytes / (ms * 1e-3) / 1e9,
+                  "replay_ms": stats(ev[p])}
+    del graphs, sets
+    return step_bytes, reps * nsteps, out
+
+
+def decode_sweep(nuna, torch, pool, args):
+    from paper_2608_00867_amd import workloads as wl
+    sweep = []
+    for T in wl.DECODE_TOKENS:
+        x = wl.ar_bf16_decode(T)
+        ok = oracle_check_ar(nuna, torch, x, "auto", "xcd") and oracle_check_ar(nuna, torch, x, "auto", "linear")
+        nbytes, res, calls = bench_allreduce(nuna, torch, pool, x, "auto", args.reps, args.warmup)
+        sweep.append({"tokens": T, "bytes_per_rank": T * 8192 * 2, "alg_bytes": nbytes, "parity": ok,
+                      "calls_per_graph": calls,
+                      "xcd_us": {k: round(v, 3) for k, v in res["xcd"]["us"].items()},
+                      "linear_us": {k: round(v, 3) for k, v in res["linear"]["us"].items()},
+                      "xcd_gbps": round(res["xcd"]["gbps"], 1), "linear_gbps": round(res["linear"]["gbps"], 1),
+                      "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
+    return sweep
+
+
+def roofline_dominant(sweep):
+    """Dominant kernel of the step: the all-reduce at T=64 (1 MiB per rank), XCD placement.  Its
+    average launch duration comes from HIP events around back-to-back cold launches replayed from a
+    graph on the launching stream."""
+    row = sweep[-1]
+    us = row["xcd_us"]["median"]
+    achieved = row["alg_bytes"] / (us * 1e-6) / 1e9
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+            "kernel": "k_allreduce<P=8,bf16,VPT=1> one-shot, [64,8192] bf16 per rank, XCD placement",
+            "alg_bytes_per_launch": row["alg_bytes"], "avg_launch_us": us}
+
+
+def cpu_baseline(seconds):
+    """The oracle (single-threaded C) on the same decode step, repeated for about `seconds`."""
+    import oracle
+    from paper_2608_00867_amd import workloads as wl
+    xs = [wl.ar_bf16_decode(T) for T in wl.DECODE_TOKENS]
+    step_bytes = sum(2 * len(x) * x[0].size * 2 for x in xs)
+    outs = [[np.empty_like(a) for a in x] for x in xs]
+    oracle.get()
+    steps = 0
+    t0 = time.perf_counter()
+    while True:
+        for x, o in zip(xs, outs):
+            oracle.allreduce(x, o)
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return {"value": round(step_bytes * steps / el / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{steps} decode steps (all-reduce bf16 P=8 at T=1,4,16,64) in {el:.1f} s, "
+                      f"single thread, inputs resident in host memory; host reports {os.cpu_count()} CPUs",
+            "ms_per_step": round(el / steps * 1e3, 3)}
+
+
+# ---------------------------------------------------------------------------------------------- --full sweep
+
+def full_sweep(nuna, torch, pool, args):
+    from paper_2608_00867_amd import workloads as wl
+    os.makedirs(os.path.dirname(args.out), exist_ok=True)
+    f = open(args.out, "w")
+
+    def emit(rec):
+        f.write(json.dumps(rec) + "\n")
+        f.flush()
+        print(json.dumps(rec), flush=True)
+
+    def ar_case(name, x, algos):
+        P, n = len(x), x[0].size
+        es = 2 if x[0].dtype == np.uint16 else 4
+        for algo in algos:
+            ok = all(oracle_check_ar(nuna, torch, x, algo, p) for p in ("linear", "xcd"))
+            for cold in (True, False):
+                nb, res, calls = bench_allreduce(nuna, torch, pool, x, algo, args.reps, args.warmup, cold=cold)
+                emit({"workload": name, "P": P, "bytes_per_rank": n * es, "algo": algo,
+                      "cache": "cold" if cold else "warm", "alg_bytes": nb, "calls_per_graph": calls,
+                      "parity": ok,
+                      **{f"{p}_us": {k: round(v, 3) for k, v in res[p]["us"].items()} for p in res},
+                      **{f"{p}_gbps": round(res[p]["gbps"], 1) for p in res},
+                      **{f"{p}_frac_hbm": round(res[p]["gbps"] / HBM_PEAK_GBPS, 4) for p in res},
+                      "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
+
+    ar_case("ar_f32_int_p8", wl.ar_f32_int(), ["one_shot", "one_shot_split", "two_shot"])
+    for T in wl.DECODE_TOKENS:
+        ar_case(f"ar_bf16_decode_T{T}", wl.ar_bf16_decode(T), ["one_shot", "one_shot_split", "two_shot"])
+    for T in wl.PREFILL_TOKENS:
+        ar_case(f"ar_bf16_prefill_T{T}", wl.ar_bf16_prefill(T), ["two_shot", "one_shot"])
+    for kib in wl.P64_KIB:
+        ar_case(f"ar_bf16_p64_{kib}KiB", wl.ar_bf16_p64(kib), ["one_shot", "one_shot_split", "two_shot"])
+    a2a_case(nuna, torch, pool, args, emit)
+    copy_case(nuna, torch, pool, args, emit)
+    f.close()
+
+
+def a2a_case(nuna, torch, pool, args, emit):
+    import oracle
+    from paper_2608_00867_amd import workloads as wl
+    send_np, topk = wl.a2a_moe()
+    E = wl.MOE_EXPERTS
+    lay = nuna.A2ALayout(topk, E).upload()
+    rows = lay.recv_rows()
+    P, T, H = len(send_np), send_np[0].shape[0], send_np[0].shape[1]
+    cap = int(rows.max())
+    rb = H * 2
+    alg_bytes = int(P * T * rb + rows.sum() * rb)
+    set_bytes = P * T * rb + P * cap * rb
+    src = [dev_copy_of(torch, a.reshape(-1)) for a in send_np]
+    for cold in (True, False):
+        nsets = max(1, min(pool.nbytes // (set_bytes + 16 * ALIGN), math.ceil(COLD_SPAN / set_bytes) + 1)) \
+            if cold else 1
+        pool.off = 0
+        sets = []
+        for _ in range(nsets):
+            send = [pool.take(T * rb).view(torch.bfloat16).view(T, H) for _ in range(P)]
+            recv = [pool.take(cap * rb).view(torch.bfloat16).view(cap, H) for _ in range(P)]
+            for a, b in zip(send, src):
+                a.view(-1).copy_(b)
+            sets.append((send, recv))
+        calls = max(4, nsets)
+        ref = oracle.all_to_all(send_np, topk, E)
+        ok = True
+        for p in ("linear", "xcd"):
+            nuna.all_to_all(sets[0][0], sets[0][1], lay, placement=p)
+            torch.cuda.synchronize()
+            for d in range(P):
+                g = sets[0][1][d][:int(rows[d])].cpu().view(torch.int16).numpy().view(np.uint16)
+                ok = ok and np.array_equal(g, ref[d])
+        graphs = {p: capture(torch, lambda i, p=p: nuna.all_to_all(sets[i % nsets][0], sets[i % nsets][1], lay,
+                                                                    placement=p), calls)
+                  for p in ("linear", "xcd")}
+        t = time_graphs(torch, graphs, calls, args.reps, args.warmup)
+        res = {p: stats(t[p]) for p in t}
+        emit({"workload": "a2a_moe_dispatch_bf16_p8", "P": P, "tokens_per_rank": T, "hidden": H,
+              "rows_received": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
+              "calls_per_graph": calls, "parity": bool(ok),
+              **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
+              **{f"{p}_gbps": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9, 1) for p in res},
+              **{f"{p}_frac_hbm": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+                 for p in res},
+              "linear_over_xcd_time": round(res["linear"]["median"] / res["xcd"]["median"], 4)})
+        del graphs, sets
+    lay.close()
+
+
+def copy_case(nuna, torch, pool, args, emit):
+    """Plain streaming copy: the bandwidth ceiling a read+write kernel reaches on this GPU."""
+    for mib in (16, 64, 256):
+        nb = mib << 20
+        nsets = max(1, min(pool.nbytes // (2 * nb), math.ceil(COLD_SPAN / (2 * nb))))
+        pool.off = 0
+        pairs = [(pool.take(nb), pool.take(nb)) for _ in range(nsets)]
+        calls = max(4, nsets)
+        s = torch.cuda.current_stream()
+
+        def fn(i):
+            a, b = pairs[i % nsets]
+            nuna.lib().nuna_copy(b.data_ptr(), a.data_ptr(), nb, torch.cuda.current_stream().cuda_stream)
+
+        g = {"copy": capture(torch, fn, calls)}
+        t = stats(time_graphs(torch, g, calls, args.reps, args.warmup)["copy"])
+        emit({"workload": "copy_reference", "bytes": nb, "cache": "cold", "us": {k: round(v, 3) for k, v in t.items()},
+              "gbps_read_plus_write": round(2 * nb / (t["median"] * 1e-6) / 1e9, 1)})
+        del g, pairs
+        del s
+
+
+# ---------------------------------------------------------------------------------------------- main
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path runs all P "
+              f"simulated ranks on one GPU, and no figure across GPUs is produced).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2608_00867_amd import nuna
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    nuna.init()
+    pool = Pool(torch, POOL_BYTES_MAIN)
+
+    if args.full:
+        full_sweep(nuna, torch, pool, args)
+        return
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    step_bytes, ksteps, main_res = decode_steps_timed(nuna, torch, pool, args)
+    t_timed = time.perf_counter() - t0
+    sweep = decode_sweep(nuna, torch, pool, args)
+    roof = roofline_dominant(sweep)
+    x = main_res["xcd"]
+    line = {
+        "metric": METRIC,
+        "value": round(x["gbps"], 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": ksteps,
+        "warmup": args.warmup,
+        "ms_per_step": round(x["ms_per_step"], 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "allreduce_bf16_p8_decode", "ranks": 8, "tokens": list(wl_tokens()),
+                   "hidden": 8192, "data_dtype": "bf16", "accumulate": "fp32", "placement": "xcd",
+                   "algo": "auto", "cache": "cold (each call on fresh memory of a 1.5 GiB pool)",
+                   "timing": f"HIP graph of {DECODE_STEPS_PER_GRAPH} steps replayed; HIP events"},
+        "step_alg_bytes": step_bytes,
+        "linear": {"value": round(main_res["linear"]["gbps"], 2),
+                   "ms_per_step": round(main_res["linear"]["ms_per_step"], 6)},
+        "linear_over_xcd_time": round(main_res["linear"]["ms_per_step"] / x["ms_per_step"], 4),
+        "sweep": sweep,
+        "roofline": roof,
+        "parity": all(s["parity"] for s in sweep),
+        "timed_region_s": round(t_timed, 3),
+    }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+def wl_tokens():
+    from paper_2608_00867_amd import workloads as wl
+    return wl.DECODE_TOKENS
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,228 @@
+/*
+ * nuna.h -- C ABI of libnuna: single-GPU collective copy/reduce kernels for
+ * MI355X (gfx950) with NUNA-aware (XCD) or locality-unaware (linear)
+ * placement of workgroups and the data chunks they touch.
+ *
+ * What is computed.  The collectives are the ones the paper names as the
+ * common AI patterns (Sec. 2.1 "Collective Communications": all-reduce for
+ * gradients and partial activations, all-gather for split weights,
+ * all-to-all for MoE token routing; reduce-scatter with all-gather in the
+ * tensor-parallel traces of the same section).  P "ranks" are P buffers in
+ * this GPU's own HBM: one call runs the copy/reduce work of all P ranks of a
+ * direct (all-pairs) collective (Sec. 5.1 evaluates that algorithm).
+ *
+ * Numerics.  Reductions are sums.  Each output element is
+ *     acc = in[0][i]; acc = acc + in[1][i]; ... ; acc = acc + in[P-1][i]
+ * in fp32 (bf16 inputs are widened exactly), then rounded once to the buffer
+ * dtype with round-to-nearest-even.  The order is fixed (ascending rank), so
+ * results are bitwise reproducible and independent of placement mode,
+ * algorithm and launch shape.  Copies (all-gather, all-to-all) move bytes.
+ *
+ * Placement (Sec. 4.2, Algorithm 1; configurations UA and NAP* of Sec. 5.3).
+ * Workgroup b of a launch runs on XCD (b mod 8) on MI355X.
+ *   NUNA_PLACE_LINEAR  work item w runs on workgroup w (grid-stride): the
+ *                      round-robin, locality-unaware baseline (UA).
+ *   NUNA_PLACE_XCD     work items that touch the same data chunk form one
+ *                      logical group; groups are spread over the 8 XCDs and
+ *                      each XCD owns a contiguous, group-aligned range of work
+ *                      items (NAP* -- aware workgroup placement, default page
+ *                      placement).  Chunks are multiples of 4 KiB so no page is
+ *                      shared by two XCDs' work items (Sec. 4.2, 4 kB pages).
+ * The mode changes which workgroup computes what, never the result.
+ *
+ * Buffers and ownership.  All data buffers are device memory owned by the
+ * caller.  `in`/`out`/`send`/`recv` are HOST arrays of P device pointers; they
+ * are read during the call only (their values are copied into kernel
+ * arguments, so a captured HIP graph keeps them).  The library allocates no
+ * device memory inside the collective calls; only nuna_a2a_layout_upload
+ * does, and the layout owns it until nuna_a2a_layout_destroy.
+ *
+ * Streams.  Collective calls enqueue on `stream` (NULL = the null stream),
+ * return without synchronising, and make no allocation, blocking copy or
+ * synchronisation, so they can be captured into a HIP graph.
+ *
+ * Errors.  Every call returns a status and never aborts.  All argument checks
+ * run on the host before any HIP call.  On failure,
+ * nuna_last_error_string() describes the problem (per thread).  A launch
+ * failure is NUNA_ERR_HIP.
+ */
+#ifndef NUNA_H
+#define NUNA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    NUNA_OK = 0,
+    NUNA_ERR_INVALID_ARG = 1, /* null pointer, P out of [1,64], bad enum, size overflow, bad layout */
+    NUNA_ERR_UNSUPPORTED = 2, /* dtype / combination not provided */
+    NUNA_ERR_MISALIGNED = 3,  /* a data pointer is not 16-byte aligned */
+    NUNA_ERR_OVERLAP = 4,     /* buffers overlap other than in the documented in-place forms */
+    NUNA_ERR_HIP = 5          /* the HIP runtime reported an error (no device, launch failure, ...) */
+} nuna_status_t;
+
+typedef enum { NUNA_F32 = 0, NUNA_BF16 = 1 } nuna_dtype_t;
+
+typedef enum { NUNA_PLACE_LINEAR = 0, NUNA_PLACE_XCD = 1 } nuna_placement_t;
+
+typedef enum {
+    NUNA_ALGO_AUTO = 0,           /* library picks by size (one-shot family on one GPU) */
+    NUNA_ALGO_ONE_SHOT = 1,       /* one kernel: read P inputs, write P outputs per element */
+    NUNA_ALGO_TWO_SHOT = 2,       /* reduce-scatter kernel, then all-gather kernel (stream ordered) */
+    NUNA_ALGO_ONE_SHOT_SPLIT = 3  /* one kernel, work item = (chunk, destination group): more
+                                     workgroups for small messages; inputs re-read per group */
+} nuna_algo_t;
+
+#define NUNA_MAX_RANKS 64
+#define NUNA_NUM_XCD 8
+
+/* Probe the current device once (architecture and compute-unit count) and
+ * cache the result.  Optional: collective calls work without it.  Returns
+ * NUNA_ERR_UNSUPPORTED if the device is not gfx950, NUNA_ERR_HIP if there is
+ * no device.  Idempotent and thread-safe. */
+nuna_status_t nuna_init(void);
+
+/* Text of the last error raised on the calling thread ("" if none).  The
+ * string is owned by the library and valid until the thread's next call. */
+const char* nuna_last_error_string(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int nuna_version(void);
+
+/* Cap on workgroups per kernel launch for all later calls of the process
+ * (0 restores the default, 16384).  Work beyond the cap is looped over by
+ * each workgroup (persistent loop), in the same placement.  Changes the
+ * launch shape only, never results; lets a caller leave compute units free
+ * for concurrent kernels.  Returns NUNA_ERR_INVALID_ARG for values < 0. */
+nuna_status_t nuna_set_max_workgroups(int max_workgroups);
+
+/*
+ * All-reduce (sum).  Sec. 2.1 (all-reduce of gradients / partial
+ * activations); direct algorithm as in Sec. 5.1.
+ *   in[r]   P device pointers, each `count` elements of `dtype`, rank order
+ *           r = 0..P-1 is the summation order.
+ *   out[d]  P device pointers, each `count` elements; every out[d] receives
+ *           the same result.
+ *   algo    ONE_SHOT, ONE_SHOT_SPLIT, TWO_SHOT or AUTO.  TWO_SHOT needs
+ *           count % P == 0; otherwise it runs one-shot (same bits).
+ *           ONE_SHOT_SPLIT with in-place buffers runs ONE_SHOT (a split
+ *           work item would overwrite an input another group still reads).
+ * In-place: out[r] == in[r] is allowed.  Any other overlap between an input
+ * and an output, or between two outputs, is NUNA_ERR_OVERLAP.  Inputs may
+ * alias each other.  count == 0 returns NUNA_OK with no launch.
+ * Alignment: every pointer 16-byte aligned (NUNA_ERR_MISALIGNED).
+ */
+nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, size_t count,
+                             nuna_dtype_t dtype, nuna_algo_t algo, nuna_placement_t place,
+                             hipStream_t stream);
+
+/*
+ * Reduce-scatter (sum).  Sec. 2.1 (tensor-parallel traces).
+ *   in[q]   P device pointers, each P*recvcount elements.  Rank r owns the
+ *           contiguous shard [r*recvcount, (r+1)*recvcount).
+ *   out[r]  P device pointers, each recvcount elements:
+ *           out[r][j] = sum over q ascending of in[q][r*recvcount + j].
+ * In-place: out[r] == in[r] + r*recvcount (elements) is allowed.  Other
+ * overlaps are NUNA_ERR_OVERLAP.  recvcount == 0 is a no-op.
+ */
+nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P, size_t recvcount,
+                                  nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream);
+
+/*
+ * All-gather (byte copy).  Sec. 2.1; the paper's worked placement example
+ * (Sec. 4.2, the two-GPU all-gather figure) is an all-gather done as local
+ * load, remote store.
+ *   in[r]   P device pointers, each sendcount elements.
+ *   out[d]  P device pointers, each P*sendcount elements:
+ *           out[d][r*sendcount + j] = in[r][j] for every d.
+ * In-place: in[r] == out[r] + r*sendcount (elements) is allowed.  Other
+ * overlaps are NUNA_ERR_OVERLAP.  sendcount == 0 is a no-op.
+ */
+nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, size_t sendcount,
+                              nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream);
+
+/*
+ * All-to-all dispatch of MoE token rows (Sec. 2.1: all-to-all routes tokens
+ * to experts; Sec. 6.7: expert token routing).
+ *
+ * A layout is the routing plan of one dispatch.  Expert e lives on rank
+ * e / (num_experts / P).  Token t of rank s is sent once to every distinct
+ * rank that owns one of its top-k experts; rank d receives its rows ordered
+ * by source rank, then token (both ascending).
+ *
+ * nuna_a2a_layout_create: host-only planning, no HIP call.
+ *   topk_idx  HOST int32 array [P][tokens_per_rank][topk], read during the
+ *             call; every entry in [0, num_experts).
+ *   Requires 1 <= P <= 64, tokens_per_rank >= 0, 1 <= topk <= num_experts,
+ *   num_experts % P == 0.  *out receives a layout owned by the caller.
+ * nuna_a2a_layout_upload: copies the layout's descriptor tables to the
+ *   current device (allocates device memory; synchronous; not capturable).
+ *   A layout must be uploaded before nuna_all_to_all uses it.
+ * nuna_a2a_layout_recv_rows: rows_per_rank[d] = rows rank d receives (HOST
+ *   int64 array of P).
+ * nuna_a2a_layout_recv_map: for destination d, the source rank and token of
+ *   each received row in receive order (HOST int32 arrays of
+ *   rows_per_rank[d] entries each).
+ * nuna_a2a_layout_destroy: frees host and device parts; NULL is a no-op.
+ *   The caller must ensure no enqueued all-to-all still uses the layout.
+ */
+typedef struct nuna_a2a_layout nuna_a2a_layout_t;
+
+nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int num_experts,
+                                     const int32_t* topk_idx, nuna_a2a_layout_t** out);
+nuna_status_t nuna_a2a_layout_upload(nuna_a2a_layout_t* layout);
+nuna_status_t nuna_a2a_layout_recv_rows(const nuna_a2a_layout_t* layout, int64_t* rows_per_rank);
+nuna_status_t nuna_a2a_layout_recv_map(const nuna_a2a_layout_t* layout, int d, int32_t* src_rank,
+                                       int32_t* src_token);
+void nuna_a2a_layout_destroy(nuna_a2a_layout_t* layout);
+
+/*
+ * All-to-all dispatch: recv[d][j, :] = send[s][t, :] for the j-th row (s, t)
+ * of destination d in the layout.
+ *   send[s]  P device pointers, each [tokens_per_rank][row_elems] of dtype.
+ *   recv[d]  P device pointers, each with room for recv_capacity_rows rows of
+ *            row_elems; rows beyond rows_per_rank[d] are left untouched.
+ *   Returns NUNA_ERR_INVALID_ARG if the layout is not uploaded or any
+ *   rows_per_rank[d] exceeds recv_capacity_rows.  Send and receive buffers
+ *   must not overlap (NUNA_ERR_OVERLAP).
+ */
+nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const nuna_a2a_layout_t* layout,
+                              size_t row_elems, size_t recv_capacity_rows, nuna_dtype_t dtype,
+                              nuna_placement_t place, hipStream_t stream);
+
+/*
+ * Placement map, host mirror of what the kernels compute (for inspection and
+ * tests; no HIP call).  For workgroup b of a G-workgroup launch over
+ * `groups` logical groups of `group_size` work items each, returns the first
+ * work item, the end (exclusive) and the stride of the items workgroup b runs.
+ * Items are numbered group-major: item = group * group_size + member.
+ */
+nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G, int64_t groups,
+                                   int64_t group_size, int64_t* first, int64_t* end, int64_t* stride);
+
+/*
+ * Dispatch probe (verifies the workgroup -> XCD assumption behind
+ * NUNA_PLACE_XCD).  Launches G workgroups; workgroup b writes the hardware
+ * XCC id it ran on to xcc[b] and its raw HW_ID register to hw_id[b]
+ * (hw_id may be NULL).  xcc/hw_id: device int32 arrays of G entries.
+ */
+nuna_status_t nuna_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
+
+/*
+ * Plain device copy of `bytes` bytes (16-byte aligned pointers, no overlap):
+ * the reference streaming kernel used to calibrate memory-traffic counters
+ * and the copy-bandwidth ceiling.
+ */
+nuna_status_t nuna_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NUNA_H */

@@ -1,0 +1,53 @@
+// kernels.h -- launchers of the gfx950 kernels (internal to libnuna).
+//
+// Every launcher assumes the host API has validated its arguments: pointers
+// non-null and 16-byte aligned, 1 <= P <= 64, sizes within range.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace nuna {
+
+constexpr int kDtF32 = 0;
+constexpr int kDtBf16 = 1;
+
+inline size_t dtype_size(int dt) { return dt == kDtF32 ? 4u : 2u; }
+
+// Tunables (read once from the environment by the host API; they change the
+// launch shape only, never the arithmetic).
+struct Tuning {
+    int max_grid = 16384;  // cap on workgroups per launch (persistent loop beyond)
+    int ar_vpt = 0;        // all-reduce vectors per thread per item (0 = by size)
+};
+const Tuning& tuning();
+// Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
+int max_workgroups();
+
+// One-shot all-reduce.  `dest_groups` > 1 selects the split variant: a work
+// item is (chunk, destination group) and writes P/dest_groups outputs.
+hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size_t count, int dtype,
+                            int dest_groups, int mode, hipStream_t stream);
+
+// Reduce-scatter: in[q] holds P*m elements; out[r][j] = sum_q in[q][r*m+j].
+hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P, size_t m, int dtype,
+                                 int mode, hipStream_t stream);
+
+// All-gather: out[d][r*m + j] = in[r][j]; a destination whose shard region
+// is the source itself (in-place form) is skipped.
+hipError_t launch_all_gather(const void* const* in, void* const* out, int P, size_t m, int dtype,
+                             int mode, hipStream_t stream);
+
+// All-to-all row copy driven by a descriptor table (device int4 per item:
+// src rank, src token, dst rank, dst row).  xcd_start: 9 item offsets
+// (group-aligned) used by the XCD mode; ignored by LINEAR.
+hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, const void* desc,
+                             int64_t nitems, const int64_t* group_start, int64_t ngroups,
+                             size_t row_bytes, int esize, int mode, hipStream_t stream);
+
+hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
+
+hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
+
+}  // namespace nuna

@@ -1,0 +1,477 @@
+// nuna_api.cpp -- host side of libnuna: argument validation, algorithm and
+// launch-shape choice, the all-to-all routing planner, and the C ABI.
+//
+// Every argument check runs before the first HIP call, so invalid calls are
+// rejected identically on machines without a GPU.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "nuna.h"
+#include "placement.h"
+
+namespace {
+
+thread_local std::string t_err;
+
+nuna_status_t fail(nuna_status_t st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    std::vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_err = buf;
+    return st;
+}
+
+nuna_status_t ok() {
+    t_err.clear();
+    return NUNA_OK;
+}
+
+nuna_status_t hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return ok();
+    return fail(NUNA_ERR_HIP, "%s: HIP error %d (%s)", what, static_cast<int>(e), hipGetErrorString(e));
+}
+
+// Largest byte count a single rank buffer may have (2^48 B keeps every
+// index computation far from int64 overflow).
+constexpr size_t kMaxBytes = size_t(1) << 48;
+
+bool valid_dtype(int dt) { return dt == NUNA_F32 || dt == NUNA_BF16; }
+bool valid_place(int p) { return p == NUNA_PLACE_LINEAR || p == NUNA_PLACE_XCD; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Span {
+    uintptr_t lo, hi;  // [lo, hi)
+    int rank;
+};
+
+bool spans_overlap(const Span& a, const Span& b) { return a.lo < b.hi && b.lo < a.hi; }
+
+// Outputs must be pairwise disjoint.  An input may overlap an output only
+// when it is the documented in-place alias of that rank: input span equal to
+// `alias(rank)` exactly.  Sorting keeps the check O(P log P).
+template <class AllowFn>
+nuna_status_t check_overlaps(std::vector<Span> ins, std::vector<Span> outs, AllowFn allowed) {
+    std::sort(outs.begin(), outs.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
+    for (size_t i = 1; i < outs.size(); ++i)
+        if (outs[i].lo < outs[i - 1].hi)
+            return fail(NUNA_ERR_OVERLAP, "output buffers of ranks %d and %d overlap", outs[i - 1].rank, outs[i].rank);
+    for (const Span& s : ins) {
+        // first output whose end is above s.lo
+        auto it = std::lower_bound(outs.begin(), outs.end(), s.lo,
+                                   [](const Span& o, uintptr_t lo) { return o.hi <= lo; });
+        for (; it != outs.end() && it->lo < s.hi; ++it) {
+            if (!spans_overlap(s, *it)) continue;
+            if (!allowed(s, *it))
+                return fail(NUNA_ERR_OVERLAP, "input of rank %d overlaps output of rank %d outside the in-place form",
+                            s.rank, it->rank);
+        }
+    }
+    return NUNA_OK;
+}
+
+nuna_status_t check_ptr_array(const void* const* a, int P, const char* name) {
+    if (!a) return fail(NUNA_ERR_INVALID_ARG, "%s is NULL", name);
+    for (int r = 0; r < P; ++r) {
+        if (!a[r]) return fail(NUNA_ERR_INVALID_ARG, "%s[%d] is NULL", name, r);
+        if (!aligned16(a[r])) return fail(NUNA_ERR_MISALIGNED, "%s[%d] is not 16-byte aligned", name, r);
+    }
+    return NUNA_OK;
+}
+
+nuna_status_t check_common(int P, int dtype, int place) {
+    if (P < 1 || P > NUNA_MAX_RANKS) return fail(NUNA_ERR_INVALID_ARG, "P=%d outside [1, %d]", P, NUNA_MAX_RANKS);
+    if (!valid_dtype(dtype)) return fail(NUNA_ERR_UNSUPPORTED, "unsupported dtype %d", dtype);
+    if (!valid_place(place)) return fail(NUNA_ERR_INVALID_ARG, "invalid placement mode %d", place);
+    return NUNA_OK;
+}
+
+nuna::Tuning g_tuning;
+std::once_flag g_tuning_once;
+
+int env_int(const char* name, int dflt) {
+    const char* v = std::getenv(name);
+    if (!v || !*v) return dflt;
+    return std::atoi(v);
+}
+
+}  // namespace
+
+namespace nuna {
+const Tuning& tuning() {
+    std::call_once(g_tuning_once, [] {
+        g_tuning.max_grid = env_int("NUNA_MAX_GRID", g_tuning.max_grid);
+        g_tuning.ar_vpt = env_int("NUNA_AR_VPT", g_tuning.ar_vpt);
+    });
+    return g_tuning;
+}
+
+std::atomic<int> g_max_workgroups{0};
+
+int max_workgroups() {
+    const int v = g_max_workgroups.load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    return tuning().max_grid > 0 ? tuning().max_grid : 16384;
+}
+}  // namespace nuna
+
+// ============================================================== C ABI
+
+extern "C" {
+
+const char* nuna_last_error_string(void) { return t_err.c_str(); }
+
+int nuna_version(void) { return 100; }
+
+nuna_status_t nuna_set_max_workgroups(int max_workgroups) {
+    if (max_workgroups < 0) return fail(NUNA_ERR_INVALID_ARG, "max_workgroups=%d < 0", max_workgroups);
+    nuna::g_max_workgroups.store(max_workgroups, std::memory_order_relaxed);
+    return ok();
+}
+
+nuna_status_t nuna_init(void) {
+    static std::mutex mu;
+    static int state = 0;  // 0 unknown, 1 ok
+    std::lock_guard<std::mutex> lock(mu);
+    if (state == 1) return ok();
+    int n = 0;
+    hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess || n < 1) return fail(NUNA_ERR_HIP, "no HIP device (%s)", hipGetErrorString(e));
+    int dev = 0;
+    e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) return hip_status(e, "hipGetDeviceProperties");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(NUNA_ERR_UNSUPPORTED, "device %d is %s, libnuna is built for gfx950", dev, prop.gcnArchName);
+    (void)nuna::tuning();
+    state = 1;
+    return ok();
+}
+
+nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, size_t count, nuna_dtype_t dtype,
+                             nuna_algo_t algo, nuna_placement_t place, hipStream_t stream) {
+    nuna_status_t st = check_common(P, dtype, place);
+    if (st) return st;
+    if (algo < NUNA_ALGO_AUTO || algo > NUNA_ALGO_ONE_SHOT_SPLIT)
+        return fail(NUNA_ERR_INVALID_ARG, "invalid algorithm %d", static_cast<int>(algo));
+    if ((st = check_ptr_array(in, P, "in"))) return st;
+    if ((st = check_ptr_array(const_cast<const void* const*>(out), P, "out"))) return st;
+    const size_t es = nuna::dtype_size(dtype);
+    if (count > kMaxBytes / es) return fail(NUNA_ERR_INVALID_ARG, "count %zu too large", count);
+    const size_t bytes = count * es;
+    if (count == 0) return ok();
+    std::vector<Span> is(P), os(P);
+    bool in_place = false;
+    for (int r = 0; r < P; ++r) {
+        is[r] = {reinterpret_cast<uintptr_t>(in[r]), reinterpret_cast<uintptr_t>(in[r]) + bytes, r};
+        os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + bytes, r};
+        in_place = in_place || in[r] == out[r];
+    }
+    st = check_overlaps(is, os, [](const Span& i, const Span& o) { return i.rank == o.rank && i.lo == o.lo; });
+    if (st) return st;
+
+    int a = algo;
+    if (a == NUNA_ALGO_AUTO) a = NUNA_ALGO_ONE_SHOT;
+    if (a == NUNA_ALGO_TWO_SHOT && count % static_cast<size_t>(P) != 0) a = NUNA_ALGO_ONE_SHOT;
+    if (a == NUNA_ALGO_ONE_SHOT_SPLIT && in_place) a = NUNA_ALGO_ONE_SHOT;
+
+    hipError_t e;
+    if (a == NUNA_ALGO_TWO_SHOT) {
+        const size_t m = count / P;
+        const void* shard_in[NUNA_MAX_RANKS];
+        void* shard_out[NUNA_MAX_RANKS];
+        for (int r = 0; r < P; ++r) {
+            shard_out[r] = static_cast<char*>(out[r]) + static_cast<size_t>(r) * m * es;
+            shard_in[r] = shard_out[r];
+        }
+        e = nuna::launch_reduce_scatter(in, shard_out, P, m, dtype, place, stream);
+        if (e != hipSuccess) return hip_status(e, "reduce-scatter phase launch");
+        e = nuna::launch_all_gather(shard_in, out, P, m, dtype, place, stream);
+        return hip_status(e, "all-gather phase launch");
+    }
+    int groups = 1;
+    if (a == NUNA_ALGO_ONE_SHOT_SPLIT) {
+        for (int d = P < 8 ? P : 8; d > 1; --d)
+            if (P % d == 0) {
+                groups = d;
+                break;
+            }
+    }
+    e = nuna::launch_allreduce(in, out, P, count, dtype, groups, place, stream);
+    return hip_status(e, "all-reduce launch");
+}
+
+nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P, size_t recvcount,
+                                  nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream) {
+    nuna_status_t st = check_common(P, dtype, place);
+    if (st) return st;
+    if ((st = check_ptr_array(in, P, "in"))) return st;
+    if ((st = check_ptr_array(const_cast<const void* const*>(out), P, "out"))) return st;
+    const size_t es = nuna::dtype_size(dtype);
+    if (recvcount > kMaxBytes / es / static_cast<size_t>(P))
+        return fail(NUNA_ERR_INVALID_ARG, "recvcount %zu too large", recvcount);
+    if (recvcount == 0) return ok();
+    const size_t mb = recvcount * es;
+    std::vector<Span> is(P), os(P);
+    for (int r = 0; r < P; ++r) {
+        is[r] = {reinterpret_cast<uintptr_t>(in[r]), reinterpret_cast<uintptr_t>(in[r]) + mb * P, r};
+        os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + mb, r};
+    }
+    st = check_overlaps(is, os, [mb](const Span& i, const Span& o) {
+        return i.rank == o.rank && o.lo == i.lo + static_cast<uintptr_t>(o.rank) * mb;
+    });
+    if (st) return st;
+    return hip_status(nuna::launch_reduce_scatter(in, out, P, recvcount, dtype, place, stream),
+                      "reduce-scatter launch");
+}
+
+nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, size_t sendcount, nuna_dtype_t dtype,
+                              nuna_placement_t place, hipStream_t stream) {
+    nuna_status_t st = check_common(P, dtype, place);
+    if (st) return st;
+    if ((st = check_ptr_array(in, P, "in"))) return st;
+    if ((st = check_ptr_array(const_cast<const void* const*>(out), P, "out"))) return st;
+    const size_t es = nuna::dtype_size(dtype);
+    if (sendcount > kMaxBytes / es / static_cast<size_t>(P))
+        return fail(NUNA_ERR_INVALID_ARG, "sendcount %zu too large", sendcount);
+    if (sendcount == 0) return ok();
+    const size_t mb = sendcount * es;
+    std::vector<Span> is(P), os(P);
+    for (int r = 0; r < P; ++r) {
+        is[r] = {reinterpret_cast<uintptr_t>(in[r]), reinterpret_cast<uintptr_t>(in[r]) + mb, r};
+        os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + mb * P, r};
+    }
+    st = check_overlaps(is, os, [mb](const Span& i, const Span& o) {
+        return i.rank == o.rank && i.lo == o.lo + static_cast<uintptr_t>(i.rank) * mb;
+    });
+    if (st) return st;
+    return hip_status(nuna::launch_all_gather(in, out, P, sendcount, dtype, place, stream), "all-gather launch");
+}
+
+// ------------------------------------------------------------ all-to-all layout
+
+struct nuna_a2a_layout {
+    int P = 0, T = 0, k = 0, E = 0;
+    std::vector<int64_t> rows;        // rows received per destination
+    std::vector<int64_t> dst_off;     // P+1 offsets into the per-destination maps
+    std::vector<int32_t> map_src;     // source rank of each received row, destination-major
+    std::vector<int32_t> map_tok;     // source token of each received row
+    std::vector<int32_t> desc_linear; // 4 ints per item, ordered by (dst, row)
+    std::vector<int32_t> desc_group;  // 4 ints per item, ordered by (src, token, dst)
+    std::vector<int64_t> group_start; // item offset of each source-row group in desc_group, + total
+    int64_t nitems = 0;
+    void* dev_linear = nullptr;
+    void* dev_group = nullptr;
+    int device = -1;
+};
+
+nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int num_experts, const int32_t* topk_idx,
+                                     nuna_a2a_layout_t** out) {
+    if (!out) return fail(NUNA_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (P < 1 || P > NUNA_MAX_RANKS) return fail(NUNA_ERR_INVALID_ARG, "P=%d outside [1, %d]", P, NUNA_MAX_RANKS);
+    if (tokens_per_rank < 0) return fail(NUNA_ERR_INVALID_ARG, "tokens_per_rank=%d < 0", tokens_per_rank);
+    if (num_experts < P || num_experts % P != 0)
+        return fail(NUNA_ERR_INVALID_ARG, "num_experts=%d is not a positive multiple of P=%d", num_experts, P);
+    if (topk < 1 || topk > num_experts)
+        return fail(NUNA_ERR_INVALID_ARG, "topk=%d outside [1, num_experts=%d]", topk, num_experts);
+    if (tokens_per_rank > 0 && !topk_idx) return fail(NUNA_ERR_INVALID_ARG, "topk_idx is NULL");
+    const int per = num_experts / P;
+    const int64_t ntok = static_cast<int64_t>(P) * tokens_per_rank;
+    for (int64_t i = 0; i < ntok * topk; ++i)
+        if (topk_idx[i] < 0 || topk_idx[i] >= num_experts)
+            return fail(NUNA_ERR_INVALID_ARG, "topk_idx[%lld]=%d outside [0, %d)", static_cast<long long>(i),
+                        topk_idx[i], num_experts);
+
+    auto* L = new nuna_a2a_layout();
+    L->P = P;
+    L->T = tokens_per_rank;
+    L->k = topk;
+    L->E = num_experts;
+    L->rows.assign(P, 0);
+    // Pass 1: destination mask per token, rows per destination.
+    std::vector<uint64_t> mask(static_cast<size_t>(ntok));
+    for (int64_t i = 0; i < ntok; ++i) {
+        uint64_t m = 0;
+        for (int j = 0; j < topk; ++j) m |= uint64_t(1) << (topk_idx[i * topk + j] / per);
+        mask[i] = m;
+        for (int d = 0; d < P; ++d)
+            if (m >> d & 1u) ++L->rows[d];
+    }
+    L->dst_off.assign(P + 1, 0);
+    for (int d = 0; d < P; ++d) L->dst_off[d + 1] = L->dst_off[d] + L->rows[d];
+    L->nitems = L->dst_off[P];
+    L->map_src.resize(L->nitems);
+    L->map_tok.resize(L->nitems);
+    L->desc_linear.resize(4 * L->nitems);
+    L->desc_group.reserve(4 * L->nitems);
+    L->group_start.reserve(static_cast<size_t>(ntok) + 1);
+    // Pass 2: walk tokens in (source, token) order; each destination's row
+    // counter therefore advances in receive order.
+    std::vector<int64_t> next(P, 0);
+    for (int s = 0; s < P; ++s) {
+        for (int t = 0; t < tokens_per_rank; ++t) {
+            const uint64_t m = mask[static_cast<size_t>(s) * tokens_per_rank + t];
+            if (!m) continue;
+            L->group_start.push_back(static_cast<int64_t>(L->desc_group.size() / 4));
+            for (int d = 0; d < P; ++d) {
+                if (!(m >> d & 1u)) continue;
+                const int64_t j = next[d]++;
+                const int64_t pos = L->dst_off[d] + j;
+                L->map_src[pos] = s;
+                L->map_tok[pos] = t;
+                const int32_t q[4] = {s, t, d, static_cast<int32_t>(j)};
+                std::memcpy(&L->desc_linear[4 * pos], q, sizeof q);
+                L->desc_group.insert(L->desc_group.end(), q, q + 4);
+            }
+        }
+    }
+    L->group_start.push_back(L->nitems);
+    *out = L;
+    return ok();
+}
+
+nuna_status_t nuna_a2a_layout_upload(nuna_a2a_layout_t* L) {
+    if (!L) return fail(NUNA_ERR_INVALID_ARG, "layout is NULL");
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+    if (L->dev_linear) {
+        if (L->device == dev) return ok();
+        return fail(NUNA_ERR_INVALID_ARG, "layout already uploaded to device %d (current %d)", L->device, dev);
+    }
+    const size_t bytes = static_cast<size_t>(L->nitems) * 16;
+    if (bytes == 0) {
+        L->device = dev;
+        L->dev_linear = L->dev_group = nullptr;
+        L->device = dev;
+        return ok();
+    }
+    void* a = nullptr;
+    void* b = nullptr;
+    if ((e = hipMalloc(&a, bytes)) != hipSuccess) return hip_status(e, "hipMalloc (a2a descriptors)");
+    if ((e = hipMalloc(&b, bytes)) != hipSuccess) {
+        (void)hipFree(a);
+        return hip_status(e, "hipMalloc (a2a descriptors)");
+    }
+    if ((e = hipMemcpy(a, L->desc_linear.data(), bytes, hipMemcpyHostToDevice)) != hipSuccess ||
+        (e = hipMemcpy(b, L->desc_group.data(), bytes, hipMemcpyHostToDevice)) != hipSuccess) {
+        (void)hipFree(a);
+        (void)hipFree(b);
+        return hip_status(e, "hipMemcpy (a2a descriptors)");
+    }
+    L->dev_linear = a;
+    L->dev_group = b;
+    L->device = dev;
+    return ok();
+}
+
+nuna_status_t nuna_a2a_layout_recv_rows(const nuna_a2a_layout_t* L, int64_t* rows_per_rank) {
+    if (!L || !rows_per_rank) return fail(NUNA_ERR_INVALID_ARG, "NULL argument");
+    for (int d = 0; d < L->P; ++d) rows_per_rank[d] = L->rows[d];
+    return ok();
+}
+
+nuna_status_t nuna_a2a_layout_recv_map(const nuna_a2a_layout_t* L, int d, int32_t* src_rank, int32_t* src_token) {
+    if (!L || !src_rank || !src_token) return fail(NUNA_ERR_INVALID_ARG, "NULL argument");
+    if (d < 0 || d >= L->P) return fail(NUNA_ERR_INVALID_ARG, "destination %d outside [0, %d)", d, L->P);
+    for (int64_t j = 0; j < L->rows[d]; ++j) {
+        src_rank[j] = L->map_src[L->dst_off[d] + j];
+        src_token[j] = L->map_tok[L->dst_off[d] + j];
+    }
+    return ok();
+}
+
+void nuna_a2a_layout_destroy(nuna_a2a_layout_t* L) {
+    if (!L) return;
+    if (L->dev_linear) (void)hipFree(L->dev_linear);
+    if (L->dev_group) (void)hipFree(L->dev_group);
+    delete L;
+}
+
+nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const nuna_a2a_layout_t* L,
+                              size_t row_elems, size_t recv_capacity_rows, nuna_dtype_t dtype,
+                              nuna_placement_t place, hipStream_t stream) {
+    if (!L) return fail(NUNA_ERR_INVALID_ARG, "layout is NULL");
+    const int P = L->P;
+    nuna_status_t st = check_common(P, dtype, place);
+    if (st) return st;
+    if ((st = check_ptr_array(send, P, "send"))) return st;
+    if ((st = check_ptr_array(const_cast<const void* const*>(recv), P, "recv"))) return st;
+    const size_t es = nuna::dtype_size(dtype);
+    if (row_elems == 0) return fail(NUNA_ERR_INVALID_ARG, "row_elems is 0");
+    if (row_elems > kMaxBytes / es) return fail(NUNA_ERR_INVALID_ARG, "row_elems %zu too large", row_elems);
+    const size_t row_bytes = row_elems * es;
+    for (int d = 0; d < P; ++d)
+        if (static_cast<size_t>(L->rows[d]) > recv_capacity_rows)
+            return fail(NUNA_ERR_INVALID_ARG, "rank %d receives %lld rows, capacity is %zu", d,
+                        static_cast<long long>(L->rows[d]), recv_capacity_rows);
+    if (static_cast<size_t>(L->T) > kMaxBytes / row_bytes || recv_capacity_rows > kMaxBytes / row_bytes)
+        return fail(NUNA_ERR_INVALID_ARG, "buffer sizes too large");
+    std::vector<Span> ss(P), rs(P);
+    for (int r = 0; r < P; ++r) {
+        ss[r] = {reinterpret_cast<uintptr_t>(send[r]), reinterpret_cast<uintptr_t>(send[r]) + row_bytes * L->T, r};
+        rs[r] = {reinterpret_cast<uintptr_t>(recv[r]),
+                 reinterpret_cast<uintptr_t>(recv[r]) + row_bytes * recv_capacity_rows, r};
+    }
+    st = check_overlaps(ss, rs, [](const Span&, const Span&) { return false; });
+    if (st) return st;
+    if (L->nitems == 0) return ok();
+    if (!L->dev_linear) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
+    const void* desc = place == NUNA_PLACE_XCD ? L->dev_group : L->dev_linear;
+    hipError_t e = nuna::launch_all_to_all(send, recv, P, desc, L->nitems, L->group_start.data(),
+                                           static_cast<int64_t>(L->group_start.size()) - 1, row_bytes,
+                                           static_cast<int>(es), place, stream);
+    return hip_status(e, "all-to-all launch");
+}
+
+nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G, int64_t groups, int64_t group_size,
+                                   int64_t* first, int64_t* end, int64_t* stride) {
+    if (!valid_place(place)) return fail(NUNA_ERR_INVALID_ARG, "invalid placement mode %d", static_cast<int>(place));
+    if (!first || !end || !stride) return fail(NUNA_ERR_INVALID_ARG, "NULL output");
+    if (G < 1 || b < 0 || b >= G || groups < 0 || group_size < 1 || groups > (int64_t(1) << 40) ||
+        G > (int64_t(1) << 31))
+        return fail(NUNA_ERR_INVALID_ARG, "invalid geometry b=%lld G=%lld groups=%lld group_size=%lld",
+                    static_cast<long long>(b), static_cast<long long>(G), static_cast<long long>(groups),
+                    static_cast<long long>(group_size));
+    const nuna::Place pl = nuna::make_place_uniform(place, G, groups, group_size);
+    const nuna::ItemRange r = nuna::items_of(pl, b, G);
+    *first = r.first;
+    *end = r.end;
+    *stride = r.stride;
+    return ok();
+}
+
+nuna_status_t nuna_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream) {
+    if (G < 1 || G > (1 << 24)) return fail(NUNA_ERR_INVALID_ARG, "G=%d outside [1, 2^24]", G);
+    if (!xcc) return fail(NUNA_ERR_INVALID_ARG, "xcc is NULL");
+    if ((reinterpret_cast<uintptr_t>(xcc) & 3u) || (reinterpret_cast<uintptr_t>(hw_id) & 3u))
+        return fail(NUNA_ERR_MISALIGNED, "probe outputs must be 4-byte aligned");
+    return hip_status(nuna::launch_probe_xcc(G, xcc, hw_id, stream), "probe launch");
+}
+
+nuna_status_t nuna_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+    if (!dst || !src) return fail(NUNA_ERR_INVALID_ARG, "NULL pointer");
+    if (!aligned16(dst) || !aligned16(src)) return fail(NUNA_ERR_MISALIGNED, "copy pointers must be 16-byte aligned");
+    if (bytes > kMaxBytes) return fail(NUNA_ERR_INVALID_ARG, "bytes %zu too large", bytes);
+    if (bytes == 0) return ok();
+    const uintptr_t d = reinterpret_cast<uintptr_t>(dst), s = reinterpret_cast<uintptr_t>(src);
+    if (d < s + bytes && s < d + bytes) return fail(NUNA_ERR_OVERLAP, "copy source and destination overlap");
+    return hip_status(nuna::launch_copy(dst, src, bytes, stream), "copy launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,648 @@
+// nuna_kernels.hip -- gfx950 kernels of the collective copy/reduce path.
+//
+// Memory-bound streaming kernels: every lane moves 16-byte vectors
+// (global_load/store_dwordx4), so one wavefront instruction touches 1 KiB of
+// contiguous memory.  Reductions widen bf16 to fp32 (exact), add ranks in
+// ascending order with one fp32 rounding per add, and round once to the
+// buffer dtype with round-to-nearest-even.  No MFMA: there is no contraction,
+// and the arithmetic intensity (P-1 adds per 2P element transfers) is far
+// below any compute roof.
+//
+// Workgroup -> work item mapping comes from placement.h (LINEAR / XCD modes).
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "kernels.h"
+#include "placement.h"
+
+namespace nuna {
+namespace {
+
+constexpr int kWG = 256;  // 4 wavefronts of 64 lanes
+
+// ---------------------------------------------------------------- numerics
+
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+
+// fp32 -> bf16 round-to-nearest-even.  NaN keeps its sign and upper payload
+// and is made quiet; overflow rounds to infinity.
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <int DT>
+struct Arith;
+
+template <>
+struct Arith<kDtF32> {
+    static constexpr int kLanes = 4;
+    static constexpr int kEsize = 4;
+    __device__ static __forceinline__ void init(float (&a)[4], const uint4& v) {
+        a[0] = __uint_as_float(v.x);
+        a[1] = __uint_as_float(v.y);
+        a[2] = __uint_as_float(v.z);
+        a[3] = __uint_as_float(v.w);
+    }
+    __device__ static __forceinline__ void add(float (&a)[4], const uint4& v) {
+        a[0] = a[0] + __uint_as_float(v.x);
+        a[1] = a[1] + __uint_as_float(v.y);
+        a[2] = a[2] + __uint_as_float(v.z);
+        a[3] = a[3] + __uint_as_float(v.w);
+    }
+    __device__ static __forceinline__ uint4 narrow(const float (&a)[4]) {
+        return make_uint4(__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
+                          __float_as_uint(a[3]));
+    }
+    __device__ static __forceinline__ float load1(const void* p, int64_t i) {
+        return static_cast<const float*>(p)[i];
+    }
+    __device__ static __forceinline__ void store1(void* p, int64_t i, float v) { static_cast<float*>(p)[i] = v; }
+};
+
+template <>
+struct Arith<kDtBf16> {
+    static constexpr int kLanes = 8;
+    static constexpr int kEsize = 2;
+    __device__ static __forceinline__ void init(float (&a)[8], const uint4& v) {
+        a[0] = bf16_lo(v.x);
+        a[1] = bf16_hi(v.x);
+        a[2] = bf16_lo(v.y);
+        a[3] = bf16_hi(v.y);
+        a[4] = bf16_lo(v.z);
+        a[5] = bf16_hi(v.z);
+        a[6] = bf16_lo(v.w);
+        a[7] = bf16_hi(v.w);
+    }
+    __device__ static __forceinline__ void add(float (&a)[8], const uint4& v) {
+        a[0] = a[0] + bf16_lo(v.x);
+        a[1] = a[1] + bf16_hi(v.x);
+        a[2] = a[2] + bf16_lo(v.y);
+        a[3] = a[3] + bf16_hi(v.y);
+        a[4] = a[4] + bf16_lo(v.z);
+        a[5] = a[5] + bf16_hi(v.z);
+        a[6] = a[6] + bf16_lo(v.w);
+        a[7] = a[7] + bf16_hi(v.w);
+    }
+    __device__ static __forceinline__ uint4 narrow(const float (&a)[8]) {
+        return make_uint4(f32_to_bf16(a[0]) | (f32_to_bf16(a[1]) << 16), f32_to_bf16(a[2]) | (f32_to_bf16(a[3]) << 16),
+                          f32_to_bf16(a[4]) | (f32_to_bf16(a[5]) << 16), f32_to_bf16(a[6]) | (f32_to_bf16(a[7]) << 16));
+    }
+    __device__ static __forceinline__ float load1(const void* p, int64_t i) {
+        return bf16_lo(static_cast<const uint16_t*>(p)[i]);
+    }
+    __device__ static __forceinline__ void store1(void* p, int64_t i, float v) {
+        static_cast<uint16_t*>(p)[i] = static_cast<uint16_t>(f32_to_bf16(v));
+    }
+};
+
+// ---------------------------------------------------------------- kernel arguments
+
+template <int MAXP>
+struct Ptrs {
+    const uint4* in[MAXP];
+    uint4* out[MAXP];
+};
+
+template <int MAXP>
+Ptrs<MAXP> make_ptrs(const void* const* in, void* const* out, int nin, int nout) {
+    Ptrs<MAXP> p{};
+    for (int r = 0; r < nin; ++r) p.in[r] = static_cast<const uint4*>(in[r]);
+    for (int r = 0; r < nout; ++r) p.out[r] = static_cast<uint4*>(out[r]);
+    return p;
+}
+
+// Ranks loaded per batch: all loads of a batch are issued before its adds.
+template <int PT>
+constexpr int rank_batch() {
+    return PT == 0 ? 16 : (PT < 16 ? PT : 16);
+}
+
+// dst[j] = src[v0 + j*kWG] for j < VPT.  FULL: every index is in range (a
+// uniform property of the chunk), so no per-lane guard is emitted.
+template <bool FULL, int VPT>
+__device__ __forceinline__ void load_vecs(uint4 (&dst)[VPT], const uint4* src, int64_t v0, int64_t limit) {
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+        if (FULL || v0 + j * kWG < limit)
+            dst[j] = src[v0 + j * kWG];
+        else
+            dst[j] = make_uint4(0u, 0u, 0u, 0u);
+    }
+}
+
+template <bool FULL, int VPT>
+__device__ __forceinline__ void store_vecs(uint4* dst, const uint4 (&y)[VPT], int64_t v0, int64_t limit) {
+#pragma unroll
+    for (int j = 0; j < VPT; ++j)
+        if (FULL || v0 + j * kWG < limit) dst[v0 + j * kWG] = y[j];
+}
+
+// acc[j] = sum over ranks r = 0, 1, ..., P-1 (in that order) of
+// in[r][base + v0 + j*kWG], for vectors below `limit` (relative to base).
+// Lanes past the limit add zeros and are never stored.
+template <int PT, int DT, int VPT, bool FULL, int MAXP>
+__device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, int P, int64_t base, int64_t v0, int64_t limit,
+                                             float (&acc)[VPT][Arith<DT>::kLanes]) {
+    using A = Arith<DT>;
+    constexpr int B = rank_batch<PT>();
+    if constexpr (PT > 0) {
+#pragma unroll
+        for (int r0 = 0; r0 < PT; r0 += B) {
+            uint4 buf[B][VPT];
+#pragma unroll
+            for (int q = 0; q < B; ++q) load_vecs<FULL, VPT>(buf[q], p.in[r0 + q] + base, v0, limit);
+#pragma unroll
+            for (int q = 0; q < B; ++q)
+#pragma unroll
+                for (int j = 0; j < VPT; ++j) {
+                    if (r0 + q == 0)
+                        A::init(acc[j], buf[q][j]);
+                    else
+                        A::add(acc[j], buf[q][j]);
+                }
+        }
+    } else {
+        // Runtime P: batches of B ranks; the last batch may be partial.
+        for (int r0 = 0; r0 < P; r0 += B) {
+            uint4 buf[B][VPT];
+#pragma unroll
+            for (int q = 0; q < B; ++q)
+                if (r0 + q < P) load_vecs<FULL, VPT>(buf[q], p.in[r0 + q] + base, v0, limit);
+#pragma unroll
+            for (int q = 0; q < B; ++q)
+                if (r0 + q < P) {
+#pragma unroll
+                    for (int j = 0; j < VPT; ++j) {
+                        if (r0 + q == 0)
+                            A::init(acc[j], buf[q][j]);
+                        else
+                            A::add(acc[j], buf[q][j]);
+                    }
+                }
+        }
+    }
+}
+
+// Split a work item into (group, member): shift when the group size is a
+// power of two, divide otherwise.
+__device__ __forceinline__ void split_item(int64_t w, int32_t gsize, int32_t gshift, int64_t& grp, int& member) {
+    if (gshift >= 0) {
+        grp = w >> gshift;
+        member = static_cast<int>(w & ((int64_t(1) << gshift) - 1));
+    } else {
+        grp = w / gsize;
+        member = static_cast<int>(w - grp * gsize);
+    }
+}
+
+// ---------------------------------------------------------------- all-reduce (one-shot, optional split)
+
+struct ArShape {
+    int64_t nvec;    // full 16-byte vectors per rank buffer
+    int32_t gsize;   // work items per chunk (destination groups)
+    int32_t gshift;  // log2(gsize) if a power of two, else -1
+    int32_t dpi;     // destinations per work item (P / gsize)
+    int32_t P;
+    int32_t tail;    // elements after the last full vector
+    int32_t pad;
+};
+
+template <int PT, int DT, int VPT, bool FULL, int MAXP>
+__device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const ArShape& s, int P, int64_t v0, int g) {
+    using A = Arith<DT>;
+    float acc[VPT][A::kLanes];
+    reduce_ranks<PT, DT, VPT, FULL>(p, P, 0, v0, s.nvec, acc);
+    uint4 y[VPT];
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
+    if (PT > 0 && s.gsize == 1) {
+#pragma unroll
+        for (int d = 0; d < (PT > 0 ? PT : 1); ++d) store_vecs<FULL, VPT>(p.out[d], y, v0, s.nvec);
+    } else {
+        const int d0 = g * s.dpi;
+        for (int d = d0; d < d0 + s.dpi; ++d) store_vecs<FULL, VPT>(p.out[d], y, v0, s.nvec);
+    }
+}
+
+template <int PT, int MAXP, int DT, int VPT>
+__global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Place pl) {
+    using A = Arith<DT>;
+    constexpr int CV = kWG * VPT;
+    const int P = PT > 0 ? PT : s.P;
+    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
+    for (int64_t w = it.first; w < it.end; w += it.stride) {
+        int64_t c;
+        int g;
+        split_item(w, s.gsize, s.gshift, c, g);
+        const int64_t v0 = c * CV + threadIdx.x;
+        if ((c + 1) * CV <= s.nvec)
+            allreduce_chunk<PT, DT, VPT, true>(p, s, P, v0, g);
+        else
+            allreduce_chunk<PT, DT, VPT, false>(p, s, P, v0, g);
+    }
+    if (s.tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < s.tail) {
+        const int64_t i = s.nvec * (16 / A::kEsize) + threadIdx.x;
+        float a = A::load1(p.in[0], i);
+        for (int r = 1; r < P; ++r) a = a + A::load1(p.in[r], i);
+        for (int d = 0; d < P; ++d) A::store1(p.out[d], i, a);
+    }
+}
+
+// ---------------------------------------------------------------- reduce-scatter
+
+struct RsShape {
+    int64_t mv;   // vectors per shard
+    int64_t wcs;  // chunks per shard
+    int32_t P;
+    int32_t pad;
+};
+
+template <int PT, int DT, int VPT, bool FULL, int MAXP>
+__device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const RsShape& s, int P, int64_t r,
+                                                     int64_t v0) {
+    using A = Arith<DT>;
+    float acc[VPT][A::kLanes];
+    reduce_ranks<PT, DT, VPT, FULL>(p, P, r * s.mv, v0, s.mv, acc);
+    uint4 y[VPT];
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
+    store_vecs<FULL, VPT>(p.out[r], y, v0, s.mv);
+}
+
+template <int PT, int MAXP, int DT, int VPT>
+__global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s, Place pl) {
+    constexpr int CV = kWG * VPT;
+    const int P = PT > 0 ? PT : s.P;
+    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
+    for (int64_t w = it.first; w < it.end; w += it.stride) {
+        const int64_t r = w / s.wcs;
+        const int64_t c = w - r * s.wcs;
+        const int64_t v0 = c * CV + threadIdx.x;
+        if ((c + 1) * CV <= s.mv)
+            reduce_scatter_chunk<PT, DT, VPT, true>(p, s, P, r, v0);
+        else
+            reduce_scatter_chunk<PT, DT, VPT, false>(p, s, P, r, v0);
+    }
+}
+
+// Element-wise fallback when a shard is not a whole number of 16-byte vectors.
+template <int DT>
+__global__ __launch_bounds__(kWG) void k_reduce_scatter_elem(Ptrs<64> p, int P, int64_t m) {
+    using A = Arith<DT>;
+    const int64_t total = m * P;
+    for (int64_t i = blockIdx.x * static_cast<int64_t>(kWG) + threadIdx.x; i < total;
+         i += static_cast<int64_t>(gridDim.x) * kWG) {
+        const int64_t r = i / m;
+        float a = A::load1(p.in[0], i);
+        for (int q = 1; q < P; ++q) a = a + A::load1(p.in[q], i);
+        A::store1(p.out[r], i - r * m, a);
+    }
+}
+
+// ---------------------------------------------------------------- all-gather
+
+struct AgShape {
+    int64_t mv;     // vectors per shard
+    int64_t wcs;    // chunks per shard
+    int32_t P;
+    int32_t gsize;  // destination groups per chunk
+    int32_t gshift;
+    int32_t dpi;    // destinations per item
+};
+
+template <int VPT, bool FULL, int MAXP>
+__device__ __forceinline__ void all_gather_chunk(const Ptrs<MAXP>& p, const AgShape& s, int64_t r, int64_t v0,
+                                                 int g) {
+    const uint4* src = p.in[r];
+    uint4 y[VPT];
+    load_vecs<FULL, VPT>(y, src, v0, s.mv);
+    const int d0 = g * s.dpi;
+    for (int d = d0; d < d0 + s.dpi; ++d) {
+        uint4* dst = p.out[d] + r * s.mv;
+        if (dst == src) continue;  // in-place shard
+        store_vecs<FULL, VPT>(dst, y, v0, s.mv);
+    }
+}
+
+template <int MAXP, int VPT>
+__global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Place pl) {
+    constexpr int CV = kWG * VPT;
+    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
+    for (int64_t w = it.first; w < it.end; w += it.stride) {
+        int64_t grp;
+        int g;
+        split_item(w, s.gsize, s.gshift, grp, g);
+        const int64_t r = grp / s.wcs;
+        const int64_t c = grp - r * s.wcs;
+        const int64_t v0 = c * CV + threadIdx.x;
+        if ((c + 1) * CV <= s.mv)
+            all_gather_chunk<VPT, true>(p, s, r, v0, g);
+        else
+            all_gather_chunk<VPT, false>(p, s, r, v0, g);
+    }
+}
+
+template <int ES>
+__global__ __launch_bounds__(kWG) void k_all_gather_elem(Ptrs<64> p, int P, int64_t m) {
+    using E = typename std::conditional<ES == 2, uint16_t, uint32_t>::type;
+    const int64_t total = m * P;
+    for (int64_t i = blockIdx.x * static_cast<int64_t>(kWG) + threadIdx.x; i < total;
+         i += static_cast<int64_t>(gridDim.x) * kWG) {
+        const int64_t r = i / m;
+        const int64_t j = i - r * m;
+        const E* src = reinterpret_cast<const E*>(p.in[r]);
+        const E v = src[j];
+        for (int d = 0; d < P; ++d) {
+            E* dst = reinterpret_cast<E*>(p.out[d]) + r * m;
+            if (dst != src) dst[j] = v;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- all-to-all
+
+// Descriptor of one row copy: source rank, source token, destination rank,
+// destination row.
+template <int MAXP, int UNROLL>
+__global__ __launch_bounds__(kWG) void k_all_to_all(Ptrs<MAXP> p, const int4* __restrict__ desc, int64_t rowvec,
+                                                    Place pl) {
+    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
+    for (int64_t w = it.first; w < it.end; w += it.stride) {
+        const int4 d = desc[w];
+        const uint4* src = p.in[d.x] + static_cast<int64_t>(d.y) * rowvec;
+        uint4* dst = p.out[d.z] + static_cast<int64_t>(d.w) * rowvec;
+        for (int64_t v = threadIdx.x; v < rowvec; v += kWG * UNROLL) {
+            uint4 y[UNROLL];
+#pragma unroll
+            for (int u = 0; u < UNROLL; ++u)
+                if (v + u * kWG < rowvec) y[u] = src[v + u * kWG];
+#pragma unroll
+            for (int u = 0; u < UNROLL; ++u)
+                if (v + u * kWG < rowvec) dst[v + u * kWG] = y[u];
+        }
+    }
+}
+
+// Element path for rows that are not a whole number of 16-byte vectors.
+template <int ES>
+__global__ __launch_bounds__(kWG) void k_all_to_all_elem(Ptrs<64> p, const int4* __restrict__ desc, int64_t rowelems,
+                                                         Place pl) {
+    using E = typename std::conditional<ES == 2, uint16_t, uint32_t>::type;
+    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
+    for (int64_t w = it.first; w < it.end; w += it.stride) {
+        const int4 d = desc[w];
+        const E* src = reinterpret_cast<const E*>(p.in[d.x]) + static_cast<int64_t>(d.y) * rowelems;
+        E* dst = reinterpret_cast<E*>(p.out[d.z]) + static_cast<int64_t>(d.w) * rowelems;
+        for (int64_t v = threadIdx.x; v < rowelems; v += kWG) dst[v] = src[v];
+    }
+}
+
+// ---------------------------------------------------------------- probe and copy
+
+__global__ __launch_bounds__(64) void k_probe_xcc(int32_t* xcc, int32_t* hw_id) {
+    if (threadIdx.x == 0) {
+        uint32_t x, h;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(h));
+        xcc[blockIdx.x] = static_cast<int32_t>(x & 0xfu);
+        if (hw_id) hw_id[blockIdx.x] = static_cast<int32_t>(h);
+    }
+}
+
+__global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uint4* __restrict__ src, int64_t nvec,
+                                              unsigned char* __restrict__ dst_tail,
+                                              const unsigned char* __restrict__ src_tail, int tail) {
+    constexpr int U = 4;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kWG * U;
+    for (int64_t v = blockIdx.x * static_cast<int64_t>(kWG) * U + threadIdx.x; v < nvec; v += stride) {
+        uint4 y[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (v + u * kWG < nvec) y[u] = src[v + u * kWG];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (v + u * kWG < nvec) dst[v + u * kWG] = y[u];
+    }
+    if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < tail) dst_tail[threadIdx.x] = src_tail[threadIdx.x];
+}
+
+// ---------------------------------------------------------------- launch helpers
+
+int64_t cap_grid(int64_t items) {
+    const int64_t cap = max_workgroups();
+    return items < cap ? (items > 0 ? items : 1) : cap;
+}
+
+int log2_or_neg(int v) {
+    for (int k = 0; k < 31; ++k)
+        if ((1 << k) == v) return k;
+    return -1;
+}
+
+template <int PT, int MAXP, int DT, int VPT>
+void launch_ar_t(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G,
+                 hipStream_t st) {
+    Ptrs<MAXP> p = make_ptrs<MAXP>(in, out, P, P);
+    hipLaunchKernelGGL((k_allreduce<PT, MAXP, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, st, p, s, pl);
+}
+
+template <int DT, int VPT>
+void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G,
+                 hipStream_t st) {
+    switch (P) {
+        case 2: launch_ar_t<2, 2, DT, VPT>(in, out, P, s, pl, G, st); break;
+        case 4: launch_ar_t<4, 4, DT, VPT>(in, out, P, s, pl, G, st); break;
+        case 8: launch_ar_t<8, 8, DT, VPT>(in, out, P, s, pl, G, st); break;
+        case 16: launch_ar_t<16, 16, DT, VPT>(in, out, P, s, pl, G, st); break;
+        default: launch_ar_t<0, 64, DT, VPT>(in, out, P, s, pl, G, st); break;
+    }
+}
+
+template <int PT, int MAXP, int DT, int VPT>
+void launch_rs_t(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G,
+                 hipStream_t st) {
+    Ptrs<MAXP> p = make_ptrs<MAXP>(in, out, P, P);
+    hipLaunchKernelGGL((k_reduce_scatter<PT, MAXP, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, st, p, s,
+                       pl);
+}
+
+template <int DT, int VPT>
+void launch_rs_p(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G,
+                 hipStream_t st) {
+    switch (P) {
+        case 2: launch_rs_t<2, 2, DT, VPT>(in, out, P, s, pl, G, st); break;
+        case 4: launch_rs_t<4, 4, DT, VPT>(in, out, P, s, pl, G, st); break;
+        case 8: launch_rs_t<8, 8, DT, VPT>(in, out, P, s, pl, G, st); break;
+        case 16: launch_rs_t<16, 16, DT, VPT>(in, out, P, s, pl, G, st); break;
+        default: launch_rs_t<0, 64, DT, VPT>(in, out, P, s, pl, G, st); break;
+    }
+}
+
+int largest_divisor_upto(int P, int cap) {
+    for (int d = cap < P ? cap : P; d > 1; --d)
+        if (P % d == 0) return d;
+    return 1;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+
+hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size_t count, int dtype,
+                            int dest_groups, int mode, hipStream_t stream) {
+    const size_t es = dtype_size(dtype);
+    const size_t bytes = count * es;
+    ArShape s{};
+    s.nvec = static_cast<int64_t>(bytes / 16);
+    s.tail = static_cast<int32_t>((bytes % 16) / es);
+    s.P = P;
+    s.gsize = dest_groups > 1 ? dest_groups : 1;
+    s.gshift = log2_or_neg(s.gsize);
+    s.dpi = P / s.gsize;
+    int vpt = tuning().ar_vpt;
+    if (vpt != 1 && vpt != 2) vpt = (P <= 16 && s.nvec >= (int64_t(1) << 20)) ? 2 : 1;
+    const int64_t cv = static_cast<int64_t>(kWG) * vpt;
+    const int64_t groups = (s.nvec + cv - 1) / cv;
+    const int64_t G = cap_grid(groups * s.gsize);
+    const Place pl = make_place_uniform(mode, G, groups, s.gsize);
+    if (dtype == kDtF32) {
+        if (vpt == 2) launch_ar_p<kDtF32, 2>(in, out, P, s, pl, G, stream);
+        else launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, stream);
+    } else {
+        if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, stream);
+        else launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, stream);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P, size_t m, int dtype, int mode,
+                                 hipStream_t stream) {
+    const size_t es = dtype_size(dtype);
+    if ((m * es) % 16 != 0) {
+        Ptrs<64> p = make_ptrs<64>(in, out, P, P);
+        const int64_t total = static_cast<int64_t>(m) * P;
+        const int64_t G = cap_grid((total + kWG - 1) / kWG);
+        if (dtype == kDtF32)
+            hipLaunchKernelGGL((k_reduce_scatter_elem<kDtF32>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream,
+                               p, P, static_cast<int64_t>(m));
+        else
+            hipLaunchKernelGGL((k_reduce_scatter_elem<kDtBf16>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream,
+                               p, P, static_cast<int64_t>(m));
+        return hipGetLastError();
+    }
+    RsShape s{};
+    s.mv = static_cast<int64_t>(m * es / 16);
+    s.P = P;
+    const int vpt = (P <= 16 && s.mv * P >= (int64_t(1) << 20)) ? 2 : 1;
+    const int64_t cv = static_cast<int64_t>(kWG) * vpt;
+    s.wcs = (s.mv + cv - 1) / cv;
+    const int64_t G = cap_grid(s.wcs * P);
+    const Place pl = make_place_uniform(mode, G, s.wcs * P, 1);
+    if (dtype == kDtF32) {
+        if (vpt == 2) launch_rs_p<kDtF32, 2>(in, out, P, s, pl, G, stream);
+        else launch_rs_p<kDtF32, 1>(in, out, P, s, pl, G, stream);
+    } else {
+        if (vpt == 2) launch_rs_p<kDtBf16, 2>(in, out, P, s, pl, G, stream);
+        else launch_rs_p<kDtBf16, 1>(in, out, P, s, pl, G, stream);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_all_gather(const void* const* in, void* const* out, int P, size_t m, int dtype, int mode,
+                             hipStream_t stream) {
+    const size_t es = dtype_size(dtype);
+    if ((m * es) % 16 != 0) {
+        Ptrs<64> p = make_ptrs<64>(in, out, P, P);
+        const int64_t total = static_cast<int64_t>(m) * P;
+        const int64_t G = cap_grid((total + kWG - 1) / kWG);
+        if (es == 4)
+            hipLaunchKernelGGL((k_all_gather_elem<4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P,
+                               static_cast<int64_t>(m));
+        else
+            hipLaunchKernelGGL((k_all_gather_elem<2>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P,
+                               static_cast<int64_t>(m));
+        return hipGetLastError();
+    }
+    AgShape s{};
+    s.mv = static_cast<int64_t>(m * es / 16);
+    s.P = P;
+    const int vpt = s.mv * P >= (int64_t(1) << 20) ? 2 : 1;
+    const int64_t cv = static_cast<int64_t>(kWG) * vpt;
+    s.wcs = (s.mv + cv - 1) / cv;
+    // Split destinations when there are few chunks, so that more workgroups
+    // share the stores; each member re-reads its chunk (an L2 hit when the
+    // group's members sit on one XCD).
+    s.gsize = (s.wcs * P < 512) ? largest_divisor_upto(P, 8) : 1;
+    s.gshift = log2_or_neg(s.gsize);
+    s.dpi = P / s.gsize;
+    const int64_t G = cap_grid(s.wcs * P * s.gsize);
+    const Place pl = make_place_uniform(mode, G, s.wcs * P, s.gsize);
+    if (P <= 8) {
+        Ptrs<8> p = make_ptrs<8>(in, out, P, P);
+        if (vpt == 2)
+            hipLaunchKernelGGL((k_all_gather<8, 2>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, s, pl);
+        else
+            hipLaunchKernelGGL((k_all_gather<8, 1>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, s, pl);
+    } else {
+        Ptrs<64> p = make_ptrs<64>(in, out, P, P);
+        if (vpt == 2)
+            hipLaunchKernelGGL((k_all_gather<64, 2>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, s, pl);
+        else
+            hipLaunchKernelGGL((k_all_gather<64, 1>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, s, pl);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, const void* desc, int64_t nitems,
+                             const int64_t* group_start, int64_t ngroups, size_t row_bytes, int esize, int mode,
+                             hipStream_t stream) {
+    const bool vec = row_bytes % 16 == 0;
+    const int64_t rowlen = static_cast<int64_t>(vec ? row_bytes / 16 : row_bytes / esize);
+    const int64_t G = cap_grid(nitems);
+    const Place pl = make_place_groups(mode, G, group_start, ngroups);
+    const int4* d = static_cast<const int4*>(desc);
+    if (vec) {
+        if (P <= 8) {
+            Ptrs<8> p = make_ptrs<8>(send, recv, P, P);
+            hipLaunchKernelGGL((k_all_to_all<8, 4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, d, rowlen,
+                               pl);
+        } else {
+            Ptrs<64> p = make_ptrs<64>(send, recv, P, P);
+            hipLaunchKernelGGL((k_all_to_all<64, 4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, d,
+                               rowlen, pl);
+        }
+    } else {
+        Ptrs<64> p = make_ptrs<64>(send, recv, P, P);
+        if (esize == 4)
+            hipLaunchKernelGGL((k_all_to_all_elem<4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, d,
+                               rowlen, pl);
+        else
+            hipLaunchKernelGGL((k_all_to_all_elem<2>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, d,
+                               rowlen, pl);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream) {
+    hipLaunchKernelGGL(k_probe_xcc, dim3(static_cast<unsigned>(G)), dim3(64), 0, stream, xcc, hw_id);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+    const int64_t nvec = static_cast<int64_t>(bytes / 16);
+    const int tail = static_cast<int>(bytes % 16);
+    const int64_t per_wg = static_cast<int64_t>(kWG) * 4;
+    int64_t G = (nvec + per_wg - 1) / per_wg;
+    if (G > 4096) G = 4096;
+    if (G < 1) G = 1;
+    hipLaunchKernelGGL(k_copy, dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, static_cast<uint4*>(dst),
+                       static_cast<const uint4*>(src), nvec, static_cast<unsigned char*>(dst) + nvec * 16,
+                       static_cast<const unsigned char*>(src) + nvec * 16, tail);
+    return hipGetLastError();
+}
+
+}  // namespace nuna

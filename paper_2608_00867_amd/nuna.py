@@ -1,0 +1,298 @@
+"""Thin ctypes binding over ``libnuna.so`` (C ABI in ``include/nuna.h``).
+
+Argument marshalling only: every collective runs in the library's gfx950
+kernels.  Torch tensors supply device memory and the stream; nothing here
+computes on the host, and there is no fallback: if the library is missing,
+loading it raises.
+
+Two layers:
+
+* ``raw`` functions take integer device pointers and return the status code
+  (used to exercise the C ABI directly, including its argument checks);
+* tensor functions take lists of CUDA tensors (one per simulated rank),
+  enqueue on the current torch stream and raise ``NunaError`` on failure.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libnuna.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_MISALIGNED, ERR_OVERLAP, ERR_HIP = range(6)
+STATUS_NAMES = {0: "NUNA_OK", 1: "NUNA_ERR_INVALID_ARG", 2: "NUNA_ERR_UNSUPPORTED", 3: "NUNA_ERR_MISALIGNED",
+                4: "NUNA_ERR_OVERLAP", 5: "NUNA_ERR_HIP"}
+F32, BF16 = 0, 1
+LINEAR, XCD = 0, 1
+ALGO_AUTO, ALGO_ONE_SHOT, ALGO_TWO_SHOT, ALGO_ONE_SHOT_SPLIT = 0, 1, 2, 3
+
+PLACEMENTS = {"linear": LINEAR, "xcd": XCD, LINEAR: LINEAR, XCD: XCD}
+ALGOS = {"auto": ALGO_AUTO, "one_shot": ALGO_ONE_SHOT, "two_shot": ALGO_TWO_SHOT, "one_shot_split": ALGO_ONE_SHOT_SPLIT,
+         ALGO_AUTO: ALGO_AUTO, ALGO_ONE_SHOT: ALGO_ONE_SHOT, ALGO_TWO_SHOT: ALGO_TWO_SHOT,
+         ALGO_ONE_SHOT_SPLIT: ALGO_ONE_SHOT_SPLIT}
+
+_vp = ctypes.c_void_p
+_vpp = ctypes.POINTER(ctypes.c_void_p)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_i32p = ctypes.POINTER(ctypes.c_int32)
+
+# Every function the header declares, with its ctypes signature.
+SIGNATURES = {
+    "nuna_init": ([], ctypes.c_int),
+    "nuna_last_error_string": ([], ctypes.c_char_p),
+    "nuna_version": ([], ctypes.c_int),
+    "nuna_set_max_workgroups": ([ctypes.c_int], ctypes.c_int),
+    "nuna_allreduce": ([_vpp, _vpp, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp],
+                       ctypes.c_int),
+    "nuna_reduce_scatter": ([_vpp, _vpp, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp],
+                            ctypes.c_int),
+    "nuna_all_gather": ([_vpp, _vpp, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp], ctypes.c_int),
+    "nuna_a2a_layout_create": ([ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp,
+                                ctypes.POINTER(_vp)], ctypes.c_int),
+    "nuna_a2a_layout_upload": ([_vp], ctypes.c_int),
+    "nuna_a2a_layout_recv_rows": ([_vp, _i64p], ctypes.c_int),
+    "nuna_a2a_layout_recv_map": ([_vp, ctypes.c_int, _i32p, _i32p], ctypes.c_int),
+    "nuna_a2a_layout_destroy": ([_vp], None),
+    "nuna_all_to_all": ([_vpp, _vpp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp],
+                        ctypes.c_int),
+    "nuna_placement_items": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _i64p,
+                              _i64p, _i64p], ctypes.c_int),
+    "nuna_probe_xcc": ([ctypes.c_int, _vp, _vp, _vp], ctypes.c_int),
+    "nuna_copy": ([_vp, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
+}
+
+_lib = None
+
+
+class NunaError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+def lib():
+    """Load libnuna.so once.  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -c 'import __graft_entry__ as g; g.build()'`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def last_error():
+    return lib().nuna_last_error_string().decode()
+
+
+def _check(st):
+    if st != OK:
+        raise NunaError(st, last_error())
+
+
+def _ptr_array(ptrs):
+    return (ctypes.c_void_p * max(len(ptrs), 1))(*[int(p) if p is not None else None for p in ptrs])
+
+
+# ------------------------------------------------------------------ raw ABI (integer pointers)
+
+def allreduce_raw(in_ptrs, out_ptrs, P, count, dtype, algo=ALGO_AUTO, place=XCD, stream=0):
+    a = _ptr_array(in_ptrs) if in_ptrs is not None else None
+    b = _ptr_array(out_ptrs) if out_ptrs is not None else None
+    return lib().nuna_allreduce(a, b, P, count, dtype, algo, place, stream)
+
+
+def reduce_scatter_raw(in_ptrs, out_ptrs, P, recvcount, dtype, place=XCD, stream=0):
+    a = _ptr_array(in_ptrs) if in_ptrs is not None else None
+    b = _ptr_array(out_ptrs) if out_ptrs is not None else None
+    return lib().nuna_reduce_scatter(a, b, P, recvcount, dtype, place, stream)
+
+
+def all_gather_raw(in_ptrs, out_ptrs, P, sendcount, dtype, place=XCD, stream=0):
+    a = _ptr_array(in_ptrs) if in_ptrs is not None else None
+    b = _ptr_array(out_ptrs) if out_ptrs is not None else None
+    return lib().nuna_all_gather(a, b, P, sendcount, dtype, place, stream)
+
+
+def all_to_all_raw(send_ptrs, recv_ptrs, layout_handle, row_elems, recv_capacity_rows, dtype, place=XCD, stream=0):
+    a = _ptr_array(send_ptrs) if send_ptrs is not None else None
+    b = _ptr_array(recv_ptrs) if recv_ptrs is not None else None
+    return lib().nuna_all_to_all(a, b, layout_handle, row_elems, recv_capacity_rows, dtype, place, stream)
+
+
+def placement_items(place, b, G, groups, group_size):
+    """(first, end, stride) of the work items workgroup b runs (host mirror of the kernels' map)."""
+    f, e, s = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().nuna_placement_items(PLACEMENTS[place], b, G, groups, group_size, ctypes.byref(f), ctypes.byref(e),
+                                      ctypes.byref(s)))
+    return f.value, e.value, s.value
+
+
+def init():
+    _check(lib().nuna_init())
+
+
+def set_max_workgroups(n):
+    """Cap workgroups per launch (0 = default); launch shape only, never results."""
+    _check(lib().nuna_set_max_workgroups(int(n)))
+
+
+# ------------------------------------------------------------------ tensor API
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _check_ranks(ts, name):
+    if not ts:
+        raise ValueError(f"{name}: need at least one rank buffer")
+    d, n = ts[0].dtype, ts[0].numel()
+    for t in ts:
+        if not t.is_cuda or not t.is_contiguous() or t.dtype != d or t.numel() != n:
+            raise ValueError(f"{name}: rank buffers must be contiguous CUDA tensors of one dtype and size")
+    return d, n
+
+
+def allreduce(ins, outs=None, algo="auto", placement="xcd", stream=None):
+    """out[d] = sum over ranks r (ascending, fp32 accumulation) of ins[r], for every d."""
+    _, n = _check_ranks(ins, "ins")
+    if outs is None:
+        outs = [_torch().empty_like(ins[0]) for _ in ins]
+    _check_ranks(outs, "outs")
+    if outs[0].numel() != n or outs[0].dtype != ins[0].dtype:
+        raise ValueError("outs must match ins in dtype and size")
+    _check(allreduce_raw([t.data_ptr() for t in ins], [t.data_ptr() for t in outs], len(ins), n,
+                         _dtype_code(ins[0]), ALGOS[algo], PLACEMENTS[placement], _stream(stream)))
+    return outs
+
+
+def reduce_scatter(ins, outs=None, placement="xcd", stream=None):
+    """outs[r][j] = sum over q ascending of ins[q][r*m + j], m = numel / P."""
+    _, n = _check_ranks(ins, "ins")
+    P = len(ins)
+    if n % P:
+        raise ValueError("reduce-scatter input size must be a multiple of P")
+    m = n // P
+    if outs is None:
+        outs = [_torch().empty(m, dtype=ins[0].dtype, device=ins[0].device) for _ in ins]
+    _check_ranks(outs, "outs")
+    if outs[0].numel() != m:
+        raise ValueError("each output holds numel/P elements")
+    _check(reduce_scatter_raw([t.data_ptr() for t in ins], [t.data_ptr() for t in outs], P, m, _dtype_code(ins[0]),
+                              PLACEMENTS[placement], _stream(stream)))
+    return outs
+
+
+def all_gather(ins, outs=None, placement="xcd", stream=None):
+    """outs[d][r*m + j] = ins[r][j] for every d."""
+    _, m = _check_ranks(ins, "ins")
+    P = len(ins)
+    if outs is None:
+        outs = [_torch().empty(P * m, dtype=ins[0].dtype, device=ins[0].device) for _ in ins]
+    _check_ranks(outs, "outs")
+    if outs[0].numel() != P * m:
+        raise ValueError("each output holds P*m elements")
+    _check(all_gather_raw([t.data_ptr() for t in ins], [t.data_ptr() for t in outs], P, m, _dtype_code(ins[0]),
+                          PLACEMENTS[placement], _stream(stream)))
+    return outs
+
+
+class A2ALayout:
+    """Routing plan of one MoE dispatch (host planning in the library)."""
+
+    def __init__(self, topk_idx, num_experts):
+        import numpy as np
+        topk = np.ascontiguousarray(topk_idx, dtype=np.int32)
+        if topk.ndim != 3:
+            raise ValueError("topk_idx must be [P, tokens_per_rank, topk]")
+        self.P, self.T, self.k = (int(x) for x in topk.shape)
+        self.num_experts = int(num_experts)
+        self._topk = topk
+        h = ctypes.c_void_p()
+        _check(lib().nuna_a2a_layout_create(self.P, self.T, self.k, self.num_experts,
+                                            topk.ctypes.data if topk.size else None, ctypes.byref(h)))
+        self.handle = h
+
+    def upload(self):
+        _check(lib().nuna_a2a_layout_upload(self.handle))
+        return self
+
+    def recv_rows(self):
+        import numpy as np
+        rows = np.zeros(self.P, dtype=np.int64)
+        _check(lib().nuna_a2a_layout_recv_rows(self.handle, rows.ctypes.data_as(_i64p)))
+        return rows
+
+    def recv_map(self, d):
+        import numpy as np
+        n = int(self.recv_rows()[d])
+        sr = np.zeros(max(n, 1), dtype=np.int32)
+        st = np.zeros(max(n, 1), dtype=np.int32)
+        _check(lib().nuna_a2a_layout_recv_map(self.handle, d, sr.ctypes.data_as(_i32p), st.ctypes.data_as(_i32p)))
+        return sr[:n], st[:n]
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            lib().nuna_a2a_layout_destroy(self.handle)
+        self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def all_to_all(send, recv, layout, placement="xcd", stream=None):
+    """recv[d][j] = send[s][t] for the j-th row (s, t) routed to d by the layout."""
+    P = layout.P
+    if len(send) != P or len(recv) != P:
+        raise ValueError("one send and one recv buffer per rank")
+    for t in send:
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 2 or t.shape != send[0].shape:
+            raise ValueError("send buffers must be contiguous CUDA tensors [T, row]")
+    row = send[0].shape[1]
+    cap = recv[0].shape[0]
+    for t in recv:
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 2 or t.shape[1] != row or t.dtype != send[0].dtype:
+            raise ValueError("recv buffers must be contiguous CUDA tensors [capacity, row] of the send dtype")
+        cap = min(cap, t.shape[0])
+    _check(all_to_all_raw([t.data_ptr() for t in send], [t.data_ptr() for t in recv], layout.handle, row, cap,
+                          _dtype_code(send[0]), PLACEMENTS[placement], _stream(stream)))
+    return recv
+
+
+def probe_xcc(G, stream=None):
+    """Run the dispatch probe: per workgroup, the XCC id and raw HW_ID it ran on."""
+    torch = _torch()
+    xcc = torch.full((G,), -1, dtype=torch.int32, device="cuda")
+    hw = torch.full((G,), -1, dtype=torch.int32, device="cuda")
+    _check(lib().nuna_probe_xcc(G, xcc.data_ptr(), hw.data_ptr(), _stream(stream)))
+    return xcc, hw
+
+
+def copy(dst, src, stream=None):
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst too small")
+    _check(lib().nuna_copy(dst.data_ptr(), src.data_ptr(), nbytes, _stream(stream)))
+    return dst

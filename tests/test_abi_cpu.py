@@ -1,0 +1,273 @@
+"""C-ABI tests that need no GPU: exports, argument validation, host planning.
+
+Argument checks in libnuna run before any HIP call, so invalid calls are
+rejected here exactly as on a GPU machine.  Tests that pass made-up device
+pointers skip themselves when a GPU is visible, so no kernel is ever launched
+on addresses that do not exist.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_00867_amd import nuna
+from paper_2608_00867_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nuna.h")
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
+no_gpu_only = pytest.mark.skipif(_gpu_visible(), reason="uses made-up device pointers; CPU-only")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(nuna_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_expected_entry_points():
+    decl = _declared_functions()
+    for name in ("nuna_allreduce", "nuna_reduce_scatter", "nuna_all_gather", "nuna_all_to_all",
+                 "nuna_a2a_layout_create", "nuna_init", "nuna_last_error_string"):
+        assert name in decl
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(nuna.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_binding_covers_every_declared_symbol():
+    assert sorted(nuna.SIGNATURES) == _declared_functions()
+
+
+# ---------------------------------------------------------------- validation with made-up pointers
+
+BASE = 0x7F0000000000  # never dereferenced: every case below fails validation, or there is no device
+
+
+def _bufs(P, stride=1 << 20, base=BASE):
+    return [base + r * stride for r in range(P)]
+
+
+@no_gpu_only
+@pytest.mark.parametrize("case,expect", [
+    ("null_in", nuna.ERR_INVALID_ARG),
+    ("null_out", nuna.ERR_INVALID_ARG),
+    ("null_elem", nuna.ERR_INVALID_ARG),
+    ("P0", nuna.ERR_INVALID_ARG),
+    ("P65", nuna.ERR_INVALID_ARG),
+    ("bad_dtype", nuna.ERR_UNSUPPORTED),
+    ("bad_place", nuna.ERR_INVALID_ARG),
+    ("bad_algo", nuna.ERR_INVALID_ARG),
+    ("misaligned_in", nuna.ERR_MISALIGNED),
+    ("misaligned_out", nuna.ERR_MISALIGNED),
+    ("huge_count", nuna.ERR_INVALID_ARG),
+    ("outs_overlap", nuna.ERR_OVERLAP),
+    ("in_is_other_ranks_out", nuna.ERR_OVERLAP),
+    ("in_partially_overlaps_out", nuna.ERR_OVERLAP),
+])
+def test_allreduce_rejects(case, expect):
+    P, n = 8, 4096
+    ins, outs = _bufs(P), _bufs(P, base=BASE + (1 << 32))
+    dtype, place, algo = nuna.BF16, nuna.XCD, nuna.ALGO_AUTO
+    if case == "null_in":
+        ins = None
+    elif case == "null_out":
+        outs = None
+    elif case == "null_elem":
+        ins[3] = None
+    elif case == "P0":
+        P = 0
+    elif case == "P65":
+        P = 65
+        ins, outs = _bufs(P), _bufs(P, base=BASE + (1 << 32))
+    elif case == "bad_dtype":
+        dtype = 7
+    elif case == "bad_place":
+        place = 2
+    elif case == "bad_algo":
+        algo = 9
+    elif case == "misaligned_in":
+        ins[2] += 8
+    elif case == "misaligned_out":
+        outs[5] += 2
+    elif case == "huge_count":
+        n = 1 << 62
+    elif case == "outs_overlap":
+        outs[1] = outs[0] + 16
+    elif case == "in_is_other_ranks_out":
+        ins[2] = outs[3]
+    elif case == "in_partially_overlaps_out":
+        ins[4] = outs[4] + 16
+    st = nuna.allreduce_raw(ins, outs, P, n, dtype, algo, place)
+    assert st == expect, (st, nuna.last_error())
+    assert nuna.last_error()
+
+
+@no_gpu_only
+def test_zero_count_is_a_noop_without_hip():
+    assert nuna.allreduce_raw(_bufs(8), _bufs(8, base=BASE + (1 << 32)), 8, 0, nuna.BF16) == nuna.OK
+    assert nuna.reduce_scatter_raw(_bufs(8), _bufs(8, base=BASE + (1 << 32)), 8, 0, nuna.BF16) == nuna.OK
+    assert nuna.all_gather_raw(_bufs(8), _bufs(8, base=BASE + (1 << 32)), 8, 0, nuna.BF16) == nuna.OK
+
+
+@no_gpu_only
+def test_valid_call_without_device_reports_hip_error():
+    """Validation passes, then the launch fails loudly: there is no host fallback."""
+    st = nuna.allreduce_raw(_bufs(8), _bufs(8, base=BASE + (1 << 32)), 8, 4096, nuna.BF16)
+    assert st == nuna.ERR_HIP, nuna.last_error()
+    assert "HIP" in nuna.last_error()
+
+
+@no_gpu_only
+def test_in_place_forms_pass_validation():
+    P, m = 8, 4096
+    es = 2
+    outs = _bufs(P, stride=1 << 24)
+    # all-reduce in place
+    assert nuna.allreduce_raw(outs, outs, P, P * m, nuna.BF16) == nuna.ERR_HIP
+    # dest-split in place silently becomes one-shot; validation still passes
+    assert nuna.allreduce_raw(outs, outs, P, P * m, nuna.BF16, nuna.ALGO_ONE_SHOT_SPLIT) == nuna.ERR_HIP
+    # reduce-scatter: out[r] = in[r] + r*m elements
+    rs_out = [outs[r] + r * m * es for r in range(P)]
+    assert nuna.reduce_scatter_raw(outs, rs_out, P, m, nuna.BF16) == nuna.ERR_HIP
+    # all-gather: in[r] = out[r] + r*m elements
+    ag_in = [outs[r] + r * m * es for r in range(P)]
+    assert nuna.all_gather_raw(ag_in, outs, P, m, nuna.BF16) == nuna.ERR_HIP
+    # wrong in-place offsets are overlaps
+    bad = [outs[r] + ((r + 1) % P) * m * es for r in range(P)]
+    assert nuna.reduce_scatter_raw(outs, bad, P, m, nuna.BF16) == nuna.ERR_OVERLAP
+    assert nuna.all_gather_raw(bad, outs, P, m, nuna.BF16) == nuna.ERR_OVERLAP
+
+
+@no_gpu_only
+def test_copy_and_probe_validation():
+    L = nuna.lib()
+    assert L.nuna_copy(BASE, BASE + 8, 64, None) == nuna.ERR_MISALIGNED
+    assert L.nuna_copy(BASE, BASE + 16, 64, None) == nuna.ERR_OVERLAP
+    assert L.nuna_copy(None, BASE, 64, None) == nuna.ERR_INVALID_ARG
+    assert L.nuna_copy(BASE, BASE + 4096, 0, None) == nuna.OK
+    assert L.nuna_probe_xcc(0, BASE, None, None) == nuna.ERR_INVALID_ARG
+    assert L.nuna_probe_xcc(8, None, None, None) == nuna.ERR_INVALID_ARG
+
+
+def test_init_without_device_fails_cleanly():
+    if _gpu_visible():
+        pytest.skip("GPU visible")
+    assert nuna.lib().nuna_init() == nuna.ERR_HIP
+
+
+# ---------------------------------------------------------------- all-to-all planner (host, bit-exact)
+
+@pytest.mark.parametrize("P,T,k,E,seed", [(1, 4, 1, 1, 1), (2, 5, 2, 4, 2), (3, 9, 2, 6, 3), (8, 64, 8, 256, 4),
+                                          (8, 512, 8, 256, wl.seed_for(4)), (64, 16, 8, 256, 6), (4, 0, 2, 8, 7)])
+def test_a2a_planner_matches_oracle(P, T, k, E, seed):
+    topk = wl.moe_routing(P, T, k, E, seed)
+    lay = nuna.A2ALayout(topk, E)
+    rows = lay.recv_rows()
+    assert np.array_equal(rows, oracle.a2a_counts(topk, E))
+    for d in range(P):
+        sr, st = lay.recv_map(d)
+        osr, ost = oracle.a2a_map(topk, E, d)
+        assert np.array_equal(sr, osr) and np.array_equal(st, ost), d
+    lay.close()
+
+
+@pytest.mark.parametrize("case", ["bad_expert", "negative_expert", "E_not_multiple", "topk0", "P0", "T_neg"])
+def test_a2a_layout_rejects(case):
+    P, T, k, E = 4, 3, 2, 8
+    topk = np.zeros((P, T, k), dtype=np.int32)
+    if case == "bad_expert":
+        topk[1, 2, 1] = E
+    elif case == "negative_expert":
+        topk[0, 0, 0] = -1
+    elif case == "E_not_multiple":
+        E = 10
+    elif case == "topk0":
+        k = 0
+    elif case == "P0":
+        P = 0
+    elif case == "T_neg":
+        T = -1
+    h = ctypes.c_void_p()
+    st = nuna.lib().nuna_a2a_layout_create(P, T, k, E, topk.ctypes.data, ctypes.byref(h))
+    assert st == nuna.ERR_INVALID_ARG, nuna.last_error()
+    assert not h.value
+
+
+def test_a2a_requires_upload_and_capacity():
+    if _gpu_visible():
+        pytest.skip("GPU visible")
+    topk = wl.moe_routing(4, 8, 2, 8, 11)
+    lay = nuna.A2ALayout(topk, 8)
+    rows = lay.recv_rows()
+    send = _bufs(4)
+    recv = _bufs(4, base=BASE + (1 << 32))
+    assert nuna.all_to_all_raw(send, recv, lay.handle, 64, int(rows.max()), nuna.BF16) == nuna.ERR_INVALID_ARG
+    assert "upload" in nuna.last_error()
+    assert nuna.all_to_all_raw(send, recv, lay.handle, 64, int(rows.max()) - 1, nuna.BF16) == nuna.ERR_INVALID_ARG
+    assert "capacity" in nuna.last_error()
+    recv[1] = send[2] + 16
+    assert nuna.all_to_all_raw(send, recv, lay.handle, 64, int(rows.max()), nuna.BF16) == nuna.ERR_OVERLAP
+    lay.close()
+
+
+# ---------------------------------------------------------------- placement map (host mirror)
+
+def _map(place, G, groups, gsize):
+    seen = {}
+    for b in range(G):
+        f, e, s = nuna.placement_items(place, b, G, groups, gsize)
+        for w in range(f, e, s):
+            assert w not in seen, (place, G, groups, gsize, w)
+            seen[w] = b
+    return seen
+
+
+@pytest.mark.parametrize("G,groups,gsize", [(1, 1, 1), (5, 5, 1), (8, 8, 1), (13, 13, 1), (16, 64, 1), (24, 3, 8),
+                                            (64, 8, 8), (37, 11, 3), (100, 100, 1), (2048, 16384, 1), (7, 50, 2)])
+def test_placement_covers_every_item_once(G, groups, gsize):
+    W = groups * gsize
+    for place in (nuna.LINEAR, nuna.XCD):
+        seen = _map(place, G, groups, gsize)
+        assert sorted(seen) == list(range(W))
+
+
+@pytest.mark.parametrize("G,groups,gsize", [(24, 3, 8), (64, 8, 8), (37, 11, 3), (16, 64, 1), (80, 10, 8)])
+def test_xcd_mode_keeps_groups_on_one_xcd_in_contiguous_ranges(G, groups, gsize):
+    seen = _map(nuna.XCD, G, groups, gsize)
+    xcd_of_item = {w: b % 8 for w, b in seen.items()}
+    for g in range(groups):
+        assert len({xcd_of_item[g * gsize + m] for m in range(gsize)}) == 1, g
+    for x in range(8):
+        items = sorted(w for w, xx in xcd_of_item.items() if xx == x)
+        if items:
+            assert items == list(range(items[0], items[-1] + 1)), x
+    # an XCD's share of items follows its share of workgroups, to within one group
+    for x in range(8):
+        wgs = sum(1 for b in range(G) if b % 8 == x)
+        items = sum(1 for xx in xcd_of_item.values() if xx == x)
+        assert abs(items - wgs * groups * gsize / G) <= gsize, (x, items, wgs)
+
+
+def test_linear_mode_is_round_robin():
+    seen = _map(nuna.LINEAR, 16, 40, 1)
+    assert all(b == w % 16 for w, b in seen.items())
+    # a split group's members land on different XCDs in LINEAR mode
+    seen = _map(nuna.LINEAR, 64, 8, 8)
+    for g in range(8):
+        assert len({seen[g * 8 + m] % 8 for m in range(8)}) == 8

@@ -1,0 +1,360 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, element by element.
+
+Bar: bit-exact everywhere.  Reductions add ranks in ascending order with fp32
+accumulation and one rounding on both sides, copies move bytes.  The only
+relaxation is for NaN results of arithmetic (inf - inf), whose payload IEEE-754
+leaves to the implementation: there only NaN-ness is compared.
+
+Cases: the five workloads at full size (decode / prefill all-reduce, fp32
+integer all-reduce, P=64 all-reduce, MoE all-to-all dispatch), both placement
+modes, every algorithm, plus ragged and tiny sizes, in-place forms, special
+values, guard bands around every output, persistent-loop launches and HIP
+graph replay.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import assert_bitwise, assert_bitwise_nan_aware, to_dev, to_host
+from paper_2608_00867_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+PLACES = ["linear", "xcd"]
+AR_ALGOS = ["one_shot", "one_shot_split", "two_shot", "auto"]
+
+
+@pytest.fixture(scope="module")
+def nuna():
+    from paper_2608_00867_amd import nuna as n
+    n.init()
+    return n
+
+
+@pytest.fixture(autouse=True)
+def _free():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def _guarded(shape_elems, dtype, pad=256):
+    """A CUDA buffer with `pad` sentinel elements on both sides; returns (view, whole)."""
+    whole = torch.empty(shape_elems + 2 * pad, dtype=dtype, device="cuda")
+    whole.view(torch.int16 if dtype == torch.bfloat16 else torch.int32).fill_(0x5A5A)
+    return whole[pad:pad + shape_elems], whole
+
+
+def _check_guards(whole, n, pad=256):
+    w = whole.view(torch.int16 if whole.dtype == torch.bfloat16 else torch.int32).cpu().numpy()
+    assert np.all(w[:pad] == 0x5A5A) and np.all(w[pad + n:] == 0x5A5A), "write outside the output buffer"
+
+
+def run_allreduce(nuna, x, algo, place, guard=True):
+    ins = [to_dev(a) for a in x]
+    dt = ins[0].dtype
+    n = x[0].size
+    if guard:
+        pairs = [_guarded(n, dt) for _ in x]
+        outs = [p[0] for p in pairs]
+    else:
+        outs = [torch.empty_like(t) for t in ins]
+    nuna.allreduce(ins, outs, algo=algo, placement=place)
+    torch.cuda.synchronize()
+    if guard:
+        for _, whole in pairs:
+            _check_guards(whole, n)
+    return [to_host(o) for o in outs]
+
+
+# ---------------------------------------------------------------- placement proof
+
+@pytest.mark.parametrize("G", [8, 64, 1000, 4096])
+def test_probe_workgroup_b_runs_on_xcd_b_mod_8(nuna, G):
+    xcc, hw = nuna.probe_xcc(G)
+    torch.cuda.synchronize()
+    x = xcc.cpu().numpy()
+    assert np.array_equal(x, np.arange(G) % 8), np.unique(x - np.arange(G) % 8)
+
+
+# ---------------------------------------------------------------- workload 1: fp32 integers, P=8, n=2048
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("algo", AR_ALGOS)
+def test_ar_f32_int_p8(nuna, algo, place):
+    x = wl.ar_f32_int()
+    ref = oracle.allreduce(x)
+    got = run_allreduce(nuna, x, algo, place)
+    exact = np.sum(np.stack(x).astype(np.int64), axis=0)
+    for d in range(8):
+        assert_bitwise(got[d], ref[d], f"rank {d}")
+        assert np.array_equal(got[d].astype(np.int64), exact)
+
+
+# ---------------------------------------------------------------- workload 2: decode all-reduce bf16, P=8
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("algo", AR_ALGOS)
+@pytest.mark.parametrize("T", wl.DECODE_TOKENS)
+def test_ar_bf16_decode(nuna, T, algo, place):
+    x = wl.ar_bf16_decode(T)
+    ref = oracle.allreduce(x)
+    got = run_allreduce(nuna, x, algo, place)
+    for d in range(8):
+        assert_bitwise(got[d], ref[d], f"T={T} rank {d}")
+
+
+# ---------------------------------------------------------------- workload 3: prefill two-shot bf16, P=8
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("algo", ["two_shot", "one_shot"])
+@pytest.mark.parametrize("T", wl.PREFILL_TOKENS)
+def test_ar_bf16_prefill(nuna, T, algo, place):
+    x = wl.ar_bf16_prefill(T)
+    ref = oracle.allreduce(x)
+    got = run_allreduce(nuna, x, algo, place, guard=(T <= 1024))
+    for d in range(8):
+        assert_bitwise(got[d], ref[d], f"T={T} rank {d}")
+
+
+# ---------------------------------------------------------------- workload 5: P=64 bf16
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("algo", ["one_shot", "one_shot_split", "two_shot"])
+@pytest.mark.parametrize("kib", wl.P64_KIB)
+def test_ar_bf16_p64(nuna, kib, algo, place):
+    x = wl.ar_bf16_p64(kib)
+    ref = oracle.allreduce(x)
+    got = run_allreduce(nuna, x, algo, place)
+    for d in (0, 1, 31, 63):
+        assert_bitwise(got[d], ref[d], f"{kib} KiB rank {d}")
+    for d in range(64):
+        assert_bitwise(got[d], got[0], f"{kib} KiB rank {d} vs rank 0")
+
+
+# ---------------------------------------------------------------- ragged and tiny sizes
+
+RAGGED_N = [1, 3, 7, 8, 9, 255, 4095, 4096, 4097, 2048 * 3 + 5, 70001]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("P", [1, 2, 3, 5, 8, 16, 24, 64])
+def test_ar_ragged(nuna, P, dtype):
+    for n in RAGGED_N:
+        if P == 64 and n > 4097:
+            continue
+        seed = 1000 * P + n
+        x = wl.normal_f32(P, n, seed) if dtype == "f32" else wl.normal_bf16(P, n, seed)
+        ref = oracle.allreduce(x)
+        for algo in AR_ALGOS:
+            for place in PLACES:
+                got = run_allreduce(nuna, x, algo, place)
+                for d in range(P):
+                    assert_bitwise(got[d], ref[d], f"P={P} n={n} {dtype} {algo} {place} rank {d}")
+
+
+@pytest.mark.parametrize("algo", AR_ALGOS)
+def test_ar_in_place(nuna, algo):
+    for P, n, dtype in [(8, 8192 * 4, "bf16"), (8, 4097, "f32"), (64, 8192, "bf16"), (3, 999, "bf16")]:
+        x = wl.normal_bf16(P, n, 7 + P) if dtype == "bf16" else wl.normal_f32(P, n, 7 + P)
+        ref = oracle.allreduce(x)
+        for place in PLACES:
+            bufs = [to_dev(a) for a in x]
+            nuna.allreduce(bufs, bufs, algo=algo, placement=place)
+            torch.cuda.synchronize()
+            for d in range(P):
+                assert_bitwise(to_host(bufs[d]), ref[d], f"in-place P={P} n={n} {algo} {place} rank {d}")
+
+
+def test_ar_special_values(nuna):
+    """-0.0 sums, denormals, overflow to inf, inf-inf NaN, NaN inputs."""
+    P, n = 8, 4096
+    rng = np.random.default_rng(5)
+    for dt in (np.float32, np.uint16):
+        view = np.uint32 if dt == np.float32 else np.uint16
+        if dt == np.float32:
+            specials = np.array([0x80000000, 0x00000001, 0x807FFFFF, 0x7F7FFFFF, 0xFF7FFFFF, 0x7F800000, 0xFF800000,
+                                 0x7FC00000, 0x00800000, 0x3F800000], dtype=np.uint32)
+        else:
+            specials = np.array([0x8000, 0x0001, 0x807F, 0x7F7F, 0xFF7F, 0x7F80, 0xFF80, 0x7FC0, 0x0080, 0x3F80],
+                                dtype=np.uint16)
+        x = [specials[rng.integers(0, specials.size, size=n)].view(dt) for _ in range(P)]
+        x[0][:64] = np.full(64, specials[0], dtype=view).view(dt)  # some all -0 columns
+        for r in range(P):
+            x[r][:64] = np.full(64, specials[0], dtype=view).view(dt)
+        ref = oracle.allreduce(x)
+        for algo in ("one_shot", "one_shot_split", "two_shot"):
+            for place in PLACES:
+                got = run_allreduce(nuna, x, algo, place)
+                for d in range(P):
+                    assert_bitwise_nan_aware(got[d], ref[d], f"specials {dt.__name__} {algo} {place} rank {d}")
+                assert np.all(got[0].view(view)[:64] == specials[0])
+
+
+def test_ar_persistent_loop(nuna):
+    """Fewer workgroups than work items: every workgroup loops over its items."""
+    x = wl.normal_bf16(8, 8192 * 64 + 24, 77)
+    ref = oracle.allreduce(x)
+    try:
+        for cap in (1, 7, 8, 13, 64):
+            nuna.set_max_workgroups(cap)
+            for algo in AR_ALGOS:
+                for place in PLACES:
+                    got = run_allreduce(nuna, x, algo, place)
+                    for d in range(8):
+                        assert_bitwise(got[d], ref[d], f"cap={cap} {algo} {place} rank {d}")
+    finally:
+        nuna.set_max_workgroups(0)
+
+
+# ---------------------------------------------------------------- reduce-scatter / all-gather standalone
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("P,m,dtype", [(8, 65536, "bf16"), (8, 1000, "bf16"), (8, 3, "f32"), (2, 4096, "f32"),
+                                       (5, 777, "bf16"), (64, 2048, "bf16"), (1, 100, "f32"), (8, 4096 * 64, "bf16")])
+def test_reduce_scatter(nuna, P, m, dtype, place):
+    x = wl.normal_bf16(P, P * m, 3 * m + P) if dtype == "bf16" else wl.normal_f32(P, P * m, 3 * m + P)
+    ref = oracle.reduce_scatter(x)
+    ins = [to_dev(a) for a in x]
+    pairs = [_guarded(m, ins[0].dtype) for _ in range(P)]
+    outs = [p[0] for p in pairs]
+    nuna.reduce_scatter(ins, outs, placement=place)
+    torch.cuda.synchronize()
+    for r in range(P):
+        _check_guards(pairs[r][1], m)
+        assert_bitwise(to_host(outs[r]), ref[r], f"RS P={P} m={m} rank {r}")
+    # in-place form: out[r] is shard r of in[r] (the ABI needs 16-byte aligned shards)
+    bufs = [to_dev(a) for a in x]
+    shard_views = [bufs[r][r * m:(r + 1) * m] for r in range(P)]
+    if (m * bufs[0].element_size()) % 16 and P > 1:
+        with pytest.raises(nuna.NunaError) as e:
+            nuna.reduce_scatter(bufs, shard_views, placement=place)
+        assert e.value.status == nuna.ERR_MISALIGNED
+        return
+    nuna.reduce_scatter(bufs, shard_views, placement=place)
+    torch.cuda.synchronize()
+    for r in range(P):
+        assert_bitwise(to_host(shard_views[r]), ref[r], f"RS in-place P={P} m={m} rank {r}")
+
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("P,m,dtype", [(8, 65536, "bf16"), (8, 1000, "bf16"), (8, 3, "f32"), (3, 4096, "f32"),
+                                       (64, 512, "bf16"), (1, 64, "bf16"), (8, 4096 * 64, "bf16")])
+def test_all_gather(nuna, P, m, dtype, place):
+    x = wl.random_bits(P, m, np.uint16 if dtype == "bf16" else np.float32, 5 * m + P)
+    ref = oracle.all_gather(x)
+    ins = [to_dev(a) for a in x]
+    pairs = [_guarded(P * m, ins[0].dtype) for _ in range(P)]
+    outs = [p[0] for p in pairs]
+    nuna.all_gather(ins, outs, placement=place)
+    torch.cuda.synchronize()
+    for d in range(P):
+        _check_guards(pairs[d][1], P * m)
+        assert_bitwise(to_host(outs[d]), ref[d], f"AG P={P} m={m} rank {d}")
+    # in-place form: in[r] is shard r of out[r] (the ABI needs 16-byte aligned shards)
+    if (m * ins[0].element_size()) % 16 and P > 1:
+        return
+    bufs = [torch.zeros(P * m, dtype=ins[0].dtype, device="cuda") for _ in range(P)]
+    for r in range(P):
+        bufs[r][r * m:(r + 1) * m].copy_(ins[r])
+    nuna.all_gather([bufs[r][r * m:(r + 1) * m] for r in range(P)], bufs, placement=place)
+    torch.cuda.synchronize()
+    for d in range(P):
+        assert_bitwise(to_host(bufs[d]), ref[d], f"AG in-place P={P} m={m} rank {d}")
+
+
+# ---------------------------------------------------------------- workload 4: MoE all-to-all dispatch
+
+def _run_a2a(nuna, send_np, topk, E, place, guard_rows=2):
+    P = len(send_np)
+    lay = nuna.A2ALayout(topk, E).upload()
+    rows = lay.recv_rows()
+    send = [to_dev(a) for a in send_np]
+    H = send_np[0].shape[1]
+    cap = int(rows.max()) if rows.size else 0
+    cap = max(cap, 1)
+    recv_whole = [torch.full((cap + guard_rows, H), 0, dtype=send[0].dtype, device="cuda") for _ in range(P)]
+    for w in recv_whole:
+        w.view(torch.int16 if w.dtype == torch.bfloat16 else torch.int32).fill_(0x3C3C)
+    recv = [w[:cap] for w in recv_whole]
+    nuna.all_to_all(send, recv, lay, placement=place)
+    torch.cuda.synchronize()
+    out = []
+    for d in range(P):
+        whole = to_host(recv_whole[d])
+        tailbits = whole[int(rows[d]):].view(np.uint16 if whole.dtype == np.uint16 else np.uint32)
+        assert np.all(tailbits == 0x3C3C), f"rank {d}: write past its rows"
+        out.append(whole[:int(rows[d])])
+    lay.close()
+    return out
+
+
+@pytest.mark.parametrize("place", PLACES)
+def test_a2a_moe_full(nuna, place):
+    send, topk = wl.a2a_moe()
+    ref = oracle.all_to_all(send, topk, wl.MOE_EXPERTS)
+    got = _run_a2a(nuna, send, topk, wl.MOE_EXPERTS, place)
+    for d in range(8):
+        assert_bitwise(got[d], ref[d], f"a2a rank {d}")
+
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("P,T,k,E,H,dtype", [(8, 16, 8, 256, 7168, np.uint16), (2, 5, 1, 2, 8, np.uint16),
+                                             (3, 7, 2, 6, 13, np.uint16), (4, 33, 3, 16, 5, np.float32),
+                                             (64, 4, 8, 256, 64, np.uint16), (8, 1, 8, 64, 7168, np.uint16),
+                                             (1, 9, 1, 4, 256, np.float32)])
+def test_a2a_small(nuna, P, T, k, E, H, dtype, place):
+    topk = wl.moe_routing(P, T, k, E, 17 * P + T)
+    send = [a.reshape(T, H) for a in wl.random_bits(P, T * H, dtype, 19 * P + T)]
+    ref = oracle.all_to_all(send, topk, E)
+    got = _run_a2a(nuna, send, topk, E, place)
+    for d in range(P):
+        assert_bitwise(got[d], ref[d], f"a2a P={P} T={T} H={H} rank {d}")
+
+
+# ---------------------------------------------------------------- graph capture and replay
+
+def test_graph_replay_matches_eager(nuna):
+    """Calls captured into a HIP graph and replayed several times, with eager work between replays."""
+    x = wl.ar_bf16_decode(4)
+    ref = oracle.allreduce(x)
+    ins = [to_dev(a) for a in x]
+    outs = [torch.empty_like(t) for t in ins]
+    x2 = wl.ar_bf16_decode(16)
+    ref2 = oracle.allreduce(x2)
+    ins2 = [to_dev(a) for a in x2]
+    outs2 = [torch.empty_like(t) for t in ins2]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        nuna.allreduce(ins, outs, algo="one_shot_split", placement="xcd")  # warm-up outside capture
+        nuna.allreduce(ins2, outs2, algo="two_shot", placement="linear")
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        nuna.allreduce(ins, outs, algo="one_shot_split", placement="xcd")
+        nuna.allreduce(ins2, outs2, algo="two_shot", placement="linear")
+        nuna.allreduce(ins, outs, algo="one_shot", placement="linear")
+    for rep in range(4):
+        for o in outs + outs2:
+            o.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for d in range(8):
+            assert_bitwise(to_host(outs[d]), ref[d], f"replay {rep} rank {d}")
+            assert_bitwise(to_host(outs2[d]), ref2[d], f"replay {rep} rank {d} (two-shot)")
+
+
+def test_copy_kernel(nuna):
+    for nbytes in (16, 4096, 1000003, 64 << 20):
+        src = torch.randint(-2 ** 31, 2 ** 31 - 1, ((nbytes + 3) // 4,), dtype=torch.int32, device="cuda")
+        srcb = src.view(torch.uint8)[:nbytes]
+        dst = torch.zeros(nbytes + 64, dtype=torch.uint8, device="cuda")
+        nuna.lib().nuna_copy(dst.data_ptr(), srcb.data_ptr(), nbytes, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        assert torch.equal(dst[:nbytes], srcb)
+        assert int(dst[nbytes:].abs().sum()) == 0
