@@ -90,8 +90,10 @@ def time_graphs(torch, graphs, calls_per_graph, reps, warmup):
             g.replay()
     torch.cuda.synchronize()
     res = {k: [] for k in graphs}
-    for _ in range(reps):
-        for k, g in graphs.items():
+    names = list(graphs)
+    for rep in range(reps):
+        for k in (names if rep % 2 == 0 else names[::-1]):  # A/B then B/A
+            g = graphs[k]
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
             a.record()
@@ -224,8 +226,10 @@ def decode_steps_timed(nuna, torch, pool, args):
             g.replay()
     torch.cuda.synchronize()
     ev = {p: [] for p in graphs}
-    for _ in range(reps):
-        for p, g in graphs.items():
+    names = list(graphs)
+    for rep in range(reps):
+        for p in (names if rep % 2 == 0 else names[::-1]):  # A/B then B/A
+            g = graphs[p]
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
             a.record()

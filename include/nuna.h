@@ -23,11 +23,11 @@
  *   NUNA_PLACE_LINEAR  work item w runs on workgroup w (grid-stride): the
  *                      round-robin, locality-unaware baseline (UA).
  *   NUNA_PLACE_XCD     work items that touch the same data chunk form one
- *                      logical group; groups are spread over the 8 XCDs and
- *                      each XCD owns a contiguous, group-aligned range of work
- *                      items (NAP* -- aware workgroup placement, default page
- *                      placement).  Chunks are multiples of 4 KiB so no page is
- *                      shared by two XCDs' work items (Sec. 4.2, 4 kB pages).
+ *                      logical group; groups are dealt round-robin to the 8
+ *                      XCDs and a group's members run concurrently on one
+ *                      XCD, sharing its L2 (NAP* -- aware workgroup
+ *                      placement, default page placement).  A group of one
+ *                      work item is placed as LINEAR places it.
  * The mode changes which workgroup computes what, never the result.
  *
  * Buffers and ownership.  All data buffers are device memory owned by the
@@ -198,13 +198,20 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
 
 /*
  * Placement map, host mirror of what the kernels compute (for inspection and
- * tests; no HIP call).  For workgroup b of a G-workgroup launch over
- * `groups` logical groups of `group_size` work items each, returns the first
- * work item, the end (exclusive) and the stride of the items workgroup b runs.
- * Items are numbered group-major: item = group * group_size + member.
+ * tests; no HIP call).  A launch over `groups` logical groups of
+ * `group_size` work items each (items numbered group-major: item =
+ * group * group_size + member) with G workgroups: nuna_placement_items
+ * writes to items[0..capacity) the work items workgroup b runs, in the
+ * order it runs them, and sets *count to their number
+ * (NUNA_ERR_INVALID_ARG if capacity is too small; *count is still set).
+ * nuna_placement_grid gives the workgroup count a launch of that placement
+ * uses before the nuna_set_max_workgroups cap (XCD mode sizes every XCD for
+ * the longest per-XCD group list).
  */
 nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G, int64_t groups,
-                                   int64_t group_size, int64_t* first, int64_t* end, int64_t* stride);
+                                   int64_t group_size, int64_t* items, int64_t capacity, int64_t* count);
+nuna_status_t nuna_placement_grid(nuna_placement_t place, int64_t groups, int64_t group_size,
+                                  int64_t* workgroups);
 
 /*
  * Dispatch probe (verifies the workgroup -> XCD assumption behind

@@ -20,6 +20,9 @@ inline size_t dtype_size(int dt) { return dt == kDtF32 ? 4u : 2u; }
 struct Tuning {
     int max_grid = 16384;  // cap on workgroups per launch (persistent loop beyond)
     int ar_vpt = 0;        // all-reduce vectors per thread per item (0 = by size)
+    int wg_threads = 0;    // workgroup size for the streaming kernels (0 = by size)
+    int rp_min_ranks = 24; // all-reduce with at least this many ranks uses the rank-parallel kernel
+    int rp_vectors = 16;   // rank-parallel chunk: vectors per rank per work item
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
@@ -40,11 +43,11 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
                              int mode, hipStream_t stream);
 
 // All-to-all row copy driven by a descriptor table (device int4 per item:
-// src rank, src token, dst rank, dst row).  xcd_start: 9 item offsets
-// (group-aligned) used by the XCD mode; ignored by LINEAR.
+// src rank, src token, dst rank, dst row) stored in placement order.  For the
+// XCD mode, xcd_start holds the 9 offsets of the per-XCD item lists.
 hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, const void* desc,
-                             int64_t nitems, const int64_t* group_start, int64_t ngroups,
-                             size_t row_bytes, int esize, int mode, hipStream_t stream);
+                             int64_t nitems, const int64_t* xcd_start, size_t row_bytes, int esize,
+                             int mode, hipStream_t stream);
 
 hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
 

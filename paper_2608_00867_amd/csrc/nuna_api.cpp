@@ -114,6 +114,9 @@ const Tuning& tuning() {
     std::call_once(g_tuning_once, [] {
         g_tuning.max_grid = env_int("NUNA_MAX_GRID", g_tuning.max_grid);
         g_tuning.ar_vpt = env_int("NUNA_AR_VPT", g_tuning.ar_vpt);
+        g_tuning.wg_threads = env_int("NUNA_WG_THREADS", g_tuning.wg_threads);
+        g_tuning.rp_min_ranks = env_int("NUNA_RP_MIN_RANKS", g_tuning.rp_min_ranks);
+        g_tuning.rp_vectors = env_int("NUNA_RP_VECTORS", g_tuning.rp_vectors);
     });
     return g_tuning;
 }
@@ -271,8 +274,8 @@ struct nuna_a2a_layout {
     std::vector<int32_t> map_src;     // source rank of each received row, destination-major
     std::vector<int32_t> map_tok;     // source token of each received row
     std::vector<int32_t> desc_linear; // 4 ints per item, ordered by (dst, row)
-    std::vector<int32_t> desc_group;  // 4 ints per item, ordered by (src, token, dst)
-    std::vector<int64_t> group_start; // item offset of each source-row group in desc_group, + total
+    std::vector<int32_t> desc_group;  // 4 ints per item, XCD-major: source-row groups dealt round-robin to XCDs
+    int64_t xcd_start[NUNA_NUM_XCD + 1] = {};  // per-XCD list offsets into desc_group
     int64_t nitems = 0;
     void* dev_linear = nullptr;
     void* dev_group = nullptr;
@@ -318,16 +321,19 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
     L->map_src.resize(L->nitems);
     L->map_tok.resize(L->nitems);
     L->desc_linear.resize(4 * L->nitems);
-    L->desc_group.reserve(4 * L->nitems);
-    L->group_start.reserve(static_cast<size_t>(ntok) + 1);
     // Pass 2: walk tokens in (source, token) order; each destination's row
-    // counter therefore advances in receive order.
+    // counter therefore advances in receive order.  A token with at least one
+    // destination is a logical group (its copies all read the same source
+    // row); group g is dealt to XCD g mod 8 (round-robin over domains).
+    std::vector<std::vector<int32_t>> per_xcd(NUNA_NUM_XCD);
     std::vector<int64_t> next(P, 0);
+    int64_t ngroups = 0;
     for (int s = 0; s < P; ++s) {
         for (int t = 0; t < tokens_per_rank; ++t) {
             const uint64_t m = mask[static_cast<size_t>(s) * tokens_per_rank + t];
             if (!m) continue;
-            L->group_start.push_back(static_cast<int64_t>(L->desc_group.size() / 4));
+            std::vector<int32_t>& lst = per_xcd[ngroups % NUNA_NUM_XCD];
+            ++ngroups;
             for (int d = 0; d < P; ++d) {
                 if (!(m >> d & 1u)) continue;
                 const int64_t j = next[d]++;
@@ -336,11 +342,16 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
                 L->map_tok[pos] = t;
                 const int32_t q[4] = {s, t, d, static_cast<int32_t>(j)};
                 std::memcpy(&L->desc_linear[4 * pos], q, sizeof q);
-                L->desc_group.insert(L->desc_group.end(), q, q + 4);
+                lst.insert(lst.end(), q, q + 4);
             }
         }
     }
-    L->group_start.push_back(L->nitems);
+    L->desc_group.reserve(4 * L->nitems);
+    for (int x = 0; x < NUNA_NUM_XCD; ++x) {
+        L->xcd_start[x] = static_cast<int64_t>(L->desc_group.size() / 4);
+        L->desc_group.insert(L->desc_group.end(), per_xcd[x].begin(), per_xcd[x].end());
+    }
+    L->xcd_start[NUNA_NUM_XCD] = L->nitems;
     *out = L;
     return ok();
 }
@@ -433,26 +444,36 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
     if (L->nitems == 0) return ok();
     if (!L->dev_linear) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
     const void* desc = place == NUNA_PLACE_XCD ? L->dev_group : L->dev_linear;
-    hipError_t e = nuna::launch_all_to_all(send, recv, P, desc, L->nitems, L->group_start.data(),
-                                           static_cast<int64_t>(L->group_start.size()) - 1, row_bytes,
+    hipError_t e = nuna::launch_all_to_all(send, recv, P, desc, L->nitems, L->xcd_start, row_bytes,
                                            static_cast<int>(es), place, stream);
     return hip_status(e, "all-to-all launch");
 }
 
 nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G, int64_t groups, int64_t group_size,
-                                   int64_t* first, int64_t* end, int64_t* stride) {
+                                   int64_t* items, int64_t capacity, int64_t* count) {
     if (!valid_place(place)) return fail(NUNA_ERR_INVALID_ARG, "invalid placement mode %d", static_cast<int>(place));
-    if (!first || !end || !stride) return fail(NUNA_ERR_INVALID_ARG, "NULL output");
-    if (G < 1 || b < 0 || b >= G || groups < 0 || group_size < 1 || groups > (int64_t(1) << 40) ||
-        G > (int64_t(1) << 31))
+    if (!count || (capacity > 0 && !items) || capacity < 0) return fail(NUNA_ERR_INVALID_ARG, "bad output buffer");
+    if (G < 1 || b < 0 || b >= G || groups < 0 || group_size < 1 || group_size > (1 << 20) ||
+        groups > (int64_t(1) << 40) || G > (int64_t(1) << 31))
         return fail(NUNA_ERR_INVALID_ARG, "invalid geometry b=%lld G=%lld groups=%lld group_size=%lld",
                     static_cast<long long>(b), static_cast<long long>(G), static_cast<long long>(groups),
                     static_cast<long long>(group_size));
-    const nuna::Place pl = nuna::make_place_uniform(place, G, groups, group_size);
+    const nuna::Place pl = nuna::make_place_uniform(place, groups, group_size);
     const nuna::ItemRange r = nuna::items_of(pl, b, G);
-    *first = r.first;
-    *end = r.end;
-    *stride = r.stride;
+    int64_t n = 0;
+    for (int64_t i = r.first; i < r.end; i += r.stride, ++n)
+        if (n < capacity) items[n] = nuna::item_at(pl, b, G, i);
+    *count = n;
+    if (n > capacity) return fail(NUNA_ERR_INVALID_ARG, "capacity %lld < %lld items", static_cast<long long>(capacity),
+                                  static_cast<long long>(n));
+    return ok();
+}
+
+nuna_status_t nuna_placement_grid(nuna_placement_t place, int64_t groups, int64_t group_size, int64_t* workgroups) {
+    if (!valid_place(place)) return fail(NUNA_ERR_INVALID_ARG, "invalid placement mode %d", static_cast<int>(place));
+    if (!workgroups || groups < 0 || group_size < 1 || groups > (int64_t(1) << 40))
+        return fail(NUNA_ERR_INVALID_ARG, "invalid geometry");
+    *workgroups = nuna::place_grid(nuna::make_place_uniform(place, groups, group_size));
     return ok();
 }
 

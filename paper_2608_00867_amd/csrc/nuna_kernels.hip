@@ -99,6 +99,31 @@ struct Arith<kDtBf16> {
     }
 };
 
+// ---------------------------------------------------------------- memory access
+
+// Non-temporal (streaming) 16-byte accesses.  Stores: every output byte is
+// written once and consumed by a later kernel, so the writes stream towards
+// memory instead of piling up as dirty L2 lines that the end-of-kernel
+// release must write back.  Loads: used where a work item is the only reader
+// of its input chunk; work items that re-read a chunk shared by their group
+// use ordinary cached loads so the re-reads hit L2.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void store_stream(uint4* p, const uint4& v) {
+    const u32x4_t t = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(t, reinterpret_cast<u32x4_t*>(p));
+}
+
+template <bool NT>
+__device__ __forceinline__ uint4 load16(const uint4* p) {
+    if constexpr (NT) {
+        const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+        return make_uint4(t.x, t.y, t.z, t.w);
+    } else {
+        return *p;
+    }
+}
+
 // ---------------------------------------------------------------- kernel arguments
 
 template <int MAXP>
@@ -121,32 +146,33 @@ constexpr int rank_batch() {
     return PT == 0 ? 16 : (PT < 16 ? PT : 16);
 }
 
-// dst[j] = src[v0 + j*kWG] for j < VPT.  FULL: every index is in range (a
-// uniform property of the chunk), so no per-lane guard is emitted.
-template <bool FULL, int VPT>
-__device__ __forceinline__ void load_vecs(uint4 (&dst)[VPT], const uint4* src, int64_t v0, int64_t limit) {
+// A thread's vectors within a chunk are v0 + j*nt, j < VPT, where nt is the
+// workgroup size.  FULL: every index is in range (a uniform property of the
+// chunk), so no per-lane guard is emitted.
+template <bool FULL, int VPT, bool NT = false>
+__device__ __forceinline__ void load_vecs(uint4 (&dst)[VPT], const uint4* src, int64_t v0, int nt, int64_t limit) {
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
-        if (FULL || v0 + j * kWG < limit)
-            dst[j] = src[v0 + j * kWG];
+        if (FULL || v0 + j * nt < limit)
+            dst[j] = load16<NT>(src + v0 + j * nt);
         else
             dst[j] = make_uint4(0u, 0u, 0u, 0u);
     }
 }
 
 template <bool FULL, int VPT>
-__device__ __forceinline__ void store_vecs(uint4* dst, const uint4 (&y)[VPT], int64_t v0, int64_t limit) {
+__device__ __forceinline__ void store_vecs(uint4* dst, const uint4 (&y)[VPT], int64_t v0, int nt, int64_t limit) {
 #pragma unroll
     for (int j = 0; j < VPT; ++j)
-        if (FULL || v0 + j * kWG < limit) dst[v0 + j * kWG] = y[j];
+        if (FULL || v0 + j * nt < limit) store_stream(dst + v0 + j * nt, y[j]);
 }
 
 // acc[j] = sum over ranks r = 0, 1, ..., P-1 (in that order) of
-// in[r][base + v0 + j*kWG], for vectors below `limit` (relative to base).
+// in[r][base + v0 + j*nt], for vectors below `limit` (relative to base).
 // Lanes past the limit add zeros and are never stored.
-template <int PT, int DT, int VPT, bool FULL, int MAXP>
-__device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, int P, int64_t base, int64_t v0, int64_t limit,
-                                             float (&acc)[VPT][Arith<DT>::kLanes]) {
+template <int PT, int DT, int VPT, bool FULL, bool NT, int MAXP>
+__device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, int P, int64_t base, int64_t v0, int nt,
+                                             int64_t limit, float (&acc)[VPT][Arith<DT>::kLanes]) {
     using A = Arith<DT>;
     constexpr int B = rank_batch<PT>();
     if constexpr (PT > 0) {
@@ -154,7 +180,7 @@ __device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, int P, int64_t
         for (int r0 = 0; r0 < PT; r0 += B) {
             uint4 buf[B][VPT];
 #pragma unroll
-            for (int q = 0; q < B; ++q) load_vecs<FULL, VPT>(buf[q], p.in[r0 + q] + base, v0, limit);
+            for (int q = 0; q < B; ++q) load_vecs<FULL, VPT, NT>(buf[q], p.in[r0 + q] + base, v0, nt, limit);
 #pragma unroll
             for (int q = 0; q < B; ++q)
 #pragma unroll
@@ -171,7 +197,7 @@ __device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, int P, int64_t
             uint4 buf[B][VPT];
 #pragma unroll
             for (int q = 0; q < B; ++q)
-                if (r0 + q < P) load_vecs<FULL, VPT>(buf[q], p.in[r0 + q] + base, v0, limit);
+                if (r0 + q < P) load_vecs<FULL, VPT, NT>(buf[q], p.in[r0 + q] + base, v0, nt, limit);
 #pragma unroll
             for (int q = 0; q < B; ++q)
                 if (r0 + q < P) {
@@ -202,53 +228,186 @@ __device__ __forceinline__ void split_item(int64_t w, int32_t gsize, int32_t gsh
 // ---------------------------------------------------------------- all-reduce (one-shot, optional split)
 
 struct ArShape {
-    int64_t nvec;    // full 16-byte vectors per rank buffer
-    int32_t gsize;   // work items per chunk (destination groups)
-    int32_t gshift;  // log2(gsize) if a power of two, else -1
-    int32_t dpi;     // destinations per work item (P / gsize)
+    int64_t nvec;  // full 16-byte vectors per rank buffer
+    int32_t dpi;   // destinations per work item (P / group size)
     int32_t P;
-    int32_t tail;    // elements after the last full vector
+    int32_t tail;  // elements after the last full vector
     int32_t pad;
 };
 
-template <int PT, int DT, int VPT, bool FULL, int MAXP>
-__device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const ArShape& s, int P, int64_t v0, int g) {
+template <int PT, int DT, int VPT, bool FULL, bool NT, int MAXP>
+__device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const ArShape& s, int P, int64_t v0, int nt,
+                                                int g, bool all_dests) {
     using A = Arith<DT>;
     float acc[VPT][A::kLanes];
-    reduce_ranks<PT, DT, VPT, FULL>(p, P, 0, v0, s.nvec, acc);
+    reduce_ranks<PT, DT, VPT, FULL, NT>(p, P, 0, v0, nt, s.nvec, acc);
     uint4 y[VPT];
 #pragma unroll
     for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
-    if (PT > 0 && s.gsize == 1) {
+    if (PT > 0 && all_dests) {
 #pragma unroll
-        for (int d = 0; d < (PT > 0 ? PT : 1); ++d) store_vecs<FULL, VPT>(p.out[d], y, v0, s.nvec);
+        for (int d = 0; d < (PT > 0 ? PT : 1); ++d) store_vecs<FULL, VPT>(p.out[d], y, v0, nt, s.nvec);
     } else {
         const int d0 = g * s.dpi;
-        for (int d = d0; d < d0 + s.dpi; ++d) store_vecs<FULL, VPT>(p.out[d], y, v0, s.nvec);
+        for (int d = d0; d < d0 + s.dpi; ++d) store_vecs<FULL, VPT>(p.out[d], y, v0, nt, s.nvec);
     }
 }
 
 template <int PT, int MAXP, int DT, int VPT>
 __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Place pl) {
     using A = Arith<DT>;
-    constexpr int CV = kWG * VPT;
+    const int nt = blockDim.x;
+    const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int P = PT > 0 ? PT : s.P;
+    const bool all_dests = pl.gsize == 1;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t w = it.first; w < it.end; w += it.stride) {
+    for (int64_t i = it.first; i < it.end; i += it.stride) {
+        const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
         int64_t c;
         int g;
-        split_item(w, s.gsize, s.gshift, c, g);
-        const int64_t v0 = c * CV + threadIdx.x;
-        if ((c + 1) * CV <= s.nvec)
-            allreduce_chunk<PT, DT, VPT, true>(p, s, P, v0, g);
-        else
-            allreduce_chunk<PT, DT, VPT, false>(p, s, P, v0, g);
+        split_item(w, pl.gsize, pl.gshift, c, g);
+        const int64_t v0 = c * cv + threadIdx.x;
+        // A chunk read by one work item streams; a chunk shared by a group is
+        // read through L2 so the group's re-reads hit.
+        if (all_dests) {
+            if ((c + 1) * cv <= s.nvec)
+                allreduce_chunk<PT, DT, VPT, true, true>(p, s, P, v0, nt, g, all_dests);
+            else
+                allreduce_chunk<PT, DT, VPT, false, true>(p, s, P, v0, nt, g, all_dests);
+        } else {
+            if ((c + 1) * cv <= s.nvec)
+                allreduce_chunk<PT, DT, VPT, true, false>(p, s, P, v0, nt, g, all_dests);
+            else
+                allreduce_chunk<PT, DT, VPT, false, false>(p, s, P, v0, nt, g, all_dests);
+        }
     }
     if (s.tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < s.tail) {
         const int64_t i = s.nvec * (16 / A::kEsize) + threadIdx.x;
         float a = A::load1(p.in[0], i);
         for (int r = 1; r < P; ++r) a = a + A::load1(p.in[r], i);
         for (int d = 0; d < P; ++d) A::store1(p.out[d], i, a);
+    }
+}
+
+// ---------------------------------------------------------------- all-reduce, rank-parallel (many ranks)
+//
+// For many ranks and small messages the per-thread rank loop above issues its
+// loads in batches, one memory round trip per batch.  Here a work item is a
+// chunk of V <= 64 vectors of every rank, and the loads are spread over the
+// workgroup's waves by rank: wave w loads ranks w, w+NW, ... (one uniform
+// pointer per load instruction), so every load of the item is in flight at
+// once.  The tile goes to LDS; then one thread per output dword adds the P
+// ranks in ascending order from LDS (the same order and rounding as every
+// other kernel), and the waves store the result to the P outputs rank by rank.
+
+struct RpShape {
+    int64_t nvec;  // full 16-byte vectors per rank buffer
+    int32_t P;
+    int32_t V;     // vectors per rank per work item (<= 64)
+    int32_t tail;  // elements after the last full vector
+    int32_t pad;
+};
+
+template <int PT, int DT>
+__device__ __forceinline__ uint32_t rp_sum_column(const uint32_t* col, int stride, int P) {
+    // col[r * stride] is this thread's dword of rank r.
+    constexpr int U = 16;
+    if constexpr (DT == kDtF32) {
+        float a = __uint_as_float(col[0]);
+        if constexpr (PT > 0) {
+#pragma unroll
+            for (int r = 1; r < PT; ++r) a = a + __uint_as_float(col[r * stride]);
+        } else {
+            int r = 1;
+            for (; r + U <= P; r += U) {
+                uint32_t t[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) t[q] = col[(r + q) * stride];
+#pragma unroll
+                for (int q = 0; q < U; ++q) a = a + __uint_as_float(t[q]);
+            }
+            for (; r < P; ++r) a = a + __uint_as_float(col[r * stride]);
+        }
+        return __float_as_uint(a);
+    } else {
+        float lo = bf16_lo(col[0]), hi = bf16_hi(col[0]);
+        if constexpr (PT > 0) {
+#pragma unroll
+            for (int r = 1; r < PT; ++r) {
+                const uint32_t t = col[r * stride];
+                lo = lo + bf16_lo(t);
+                hi = hi + bf16_hi(t);
+            }
+        } else {
+            int r = 1;
+            for (; r + U <= P; r += U) {
+                uint32_t t[U];
+#pragma unroll
+                for (int q = 0; q < U; ++q) t[q] = col[(r + q) * stride];
+#pragma unroll
+                for (int q = 0; q < U; ++q) {
+                    lo = lo + bf16_lo(t[q]);
+                    hi = hi + bf16_hi(t[q]);
+                }
+            }
+            for (; r < P; ++r) {
+                const uint32_t t = col[r * stride];
+                lo = lo + bf16_lo(t);
+                hi = hi + bf16_hi(t);
+            }
+        }
+        return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+    }
+}
+
+template <int PT, int DT>
+__global__ __launch_bounds__(kWG) void k_allreduce_rp(Ptrs<64> p, RpShape s, Place pl) {
+    using A = Arith<DT>;
+    extern __shared__ uint4 lds[];  // [P][V] input tile, then [V] result
+    constexpr int kMaxLoads = 64 / (kWG / 64);  // ranks per wave at P = 64
+    const int P = PT > 0 ? PT : s.P;
+    const int V = s.V;
+    const int nw = blockDim.x >> 6;
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    uint4* res = lds + P * V;
+    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
+    for (int64_t i = it.first; i < it.end; i += it.stride) {
+        const int64_t c = item_at(pl, blockIdx.x, gridDim.x, i);
+        const int64_t base = c * V;
+        const int64_t left = s.nvec - base;
+        const int lim = left < V ? static_cast<int>(left) : V;
+        // phase 1: all loads of the item in flight, then into LDS
+        uint4 buf[kMaxLoads];
+#pragma unroll
+        for (int j = 0; j < kMaxLoads; ++j) {
+            const int r = wave + j * nw;
+            if (r < P && lane < lim) buf[j] = load16<true>(p.in[r] + base + lane);
+        }
+#pragma unroll
+        for (int j = 0; j < kMaxLoads; ++j) {
+            const int r = wave + j * nw;
+            if (r < P && lane < lim) lds[r * V + lane] = buf[j];
+        }
+        __syncthreads();
+        // phase 2: one thread per output dword, ranks in ascending order
+        if (static_cast<int>(threadIdx.x) < lim * 4) {
+            const uint32_t* col = reinterpret_cast<const uint32_t*>(lds) + threadIdx.x;
+            reinterpret_cast<uint32_t*>(res)[threadIdx.x] = rp_sum_column<PT, DT>(col, V * 4, P);
+        }
+        __syncthreads();
+        // phase 3: the result to every output, rank by rank
+        if (lane < lim) {
+            const uint4 y = res[lane];
+            for (int d = wave; d < P; d += nw) store_stream(p.out[d] + base + lane, y);
+        }
+        __syncthreads();
+    }
+    if (s.tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < s.tail) {
+        const int64_t e = s.nvec * (16 / A::kEsize) + threadIdx.x;
+        float a = A::load1(p.in[0], e);
+        for (int r = 1; r < P; ++r) a = a + A::load1(p.in[r], e);
+        for (int d = 0; d < P; ++d) A::store1(p.out[d], e, a);
     }
 }
 
@@ -263,29 +422,31 @@ struct RsShape {
 
 template <int PT, int DT, int VPT, bool FULL, int MAXP>
 __device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const RsShape& s, int P, int64_t r,
-                                                     int64_t v0) {
+                                                     int64_t v0, int nt) {
     using A = Arith<DT>;
     float acc[VPT][A::kLanes];
-    reduce_ranks<PT, DT, VPT, FULL>(p, P, r * s.mv, v0, s.mv, acc);
+    reduce_ranks<PT, DT, VPT, FULL, true>(p, P, r * s.mv, v0, nt, s.mv, acc);
     uint4 y[VPT];
 #pragma unroll
     for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
-    store_vecs<FULL, VPT>(p.out[r], y, v0, s.mv);
+    store_vecs<FULL, VPT>(p.out[r], y, v0, nt, s.mv);
 }
 
 template <int PT, int MAXP, int DT, int VPT>
 __global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s, Place pl) {
-    constexpr int CV = kWG * VPT;
+    const int nt = blockDim.x;
+    const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int P = PT > 0 ? PT : s.P;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t w = it.first; w < it.end; w += it.stride) {
+    for (int64_t i = it.first; i < it.end; i += it.stride) {
+        const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
         const int64_t r = w / s.wcs;
         const int64_t c = w - r * s.wcs;
-        const int64_t v0 = c * CV + threadIdx.x;
-        if ((c + 1) * CV <= s.mv)
-            reduce_scatter_chunk<PT, DT, VPT, true>(p, s, P, r, v0);
+        const int64_t v0 = c * cv + threadIdx.x;
+        if ((c + 1) * cv <= s.mv)
+            reduce_scatter_chunk<PT, DT, VPT, true>(p, s, P, r, v0, nt);
         else
-            reduce_scatter_chunk<PT, DT, VPT, false>(p, s, P, r, v0);
+            reduce_scatter_chunk<PT, DT, VPT, false>(p, s, P, r, v0, nt);
     }
 }
 
@@ -294,8 +455,8 @@ template <int DT>
 __global__ __launch_bounds__(kWG) void k_reduce_scatter_elem(Ptrs<64> p, int P, int64_t m) {
     using A = Arith<DT>;
     const int64_t total = m * P;
-    for (int64_t i = blockIdx.x * static_cast<int64_t>(kWG) + threadIdx.x; i < total;
-         i += static_cast<int64_t>(gridDim.x) * kWG) {
+    for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < total;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const int64_t r = i / m;
         float a = A::load1(p.in[0], i);
         for (int q = 1; q < P; ++q) a = a + A::load1(p.in[q], i);
@@ -306,43 +467,50 @@ __global__ __launch_bounds__(kWG) void k_reduce_scatter_elem(Ptrs<64> p, int P, 
 // ---------------------------------------------------------------- all-gather
 
 struct AgShape {
-    int64_t mv;     // vectors per shard
-    int64_t wcs;    // chunks per shard
+    int64_t mv;   // vectors per shard
+    int64_t wcs;  // chunks per shard
     int32_t P;
-    int32_t gsize;  // destination groups per chunk
-    int32_t gshift;
-    int32_t dpi;    // destinations per item
+    int32_t dpi;  // destinations per item
 };
 
-template <int VPT, bool FULL, int MAXP>
+template <int VPT, bool FULL, bool NT, int MAXP>
 __device__ __forceinline__ void all_gather_chunk(const Ptrs<MAXP>& p, const AgShape& s, int64_t r, int64_t v0,
-                                                 int g) {
+                                                 int nt, int g) {
     const uint4* src = p.in[r];
     uint4 y[VPT];
-    load_vecs<FULL, VPT>(y, src, v0, s.mv);
+    load_vecs<FULL, VPT, NT>(y, src, v0, nt, s.mv);
     const int d0 = g * s.dpi;
     for (int d = d0; d < d0 + s.dpi; ++d) {
         uint4* dst = p.out[d] + r * s.mv;
         if (dst == src) continue;  // in-place shard
-        store_vecs<FULL, VPT>(dst, y, v0, s.mv);
+        store_vecs<FULL, VPT>(dst, y, v0, nt, s.mv);
     }
 }
 
 template <int MAXP, int VPT>
 __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Place pl) {
-    constexpr int CV = kWG * VPT;
+    const int nt = blockDim.x;
+    const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t w = it.first; w < it.end; w += it.stride) {
+    for (int64_t i = it.first; i < it.end; i += it.stride) {
+        const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
         int64_t grp;
         int g;
-        split_item(w, s.gsize, s.gshift, grp, g);
+        split_item(w, pl.gsize, pl.gshift, grp, g);
         const int64_t r = grp / s.wcs;
         const int64_t c = grp - r * s.wcs;
-        const int64_t v0 = c * CV + threadIdx.x;
-        if ((c + 1) * CV <= s.mv)
-            all_gather_chunk<VPT, true>(p, s, r, v0, g);
-        else
-            all_gather_chunk<VPT, false>(p, s, r, v0, g);
+        const int64_t v0 = c * cv + threadIdx.x;
+        if (pl.gsize == 1) {
+            if ((c + 1) * cv <= s.mv)
+                all_gather_chunk<VPT, true, true>(p, s, r, v0, nt, g);
+            else
+                all_gather_chunk<VPT, false, true>(p, s, r, v0, nt, g);
+        } else {
+            if ((c + 1) * cv <= s.mv)
+                all_gather_chunk<VPT, true, false>(p, s, r, v0, nt, g);
+            else
+                all_gather_chunk<VPT, false, false>(p, s, r, v0, nt, g);
+        }
     }
 }
 
@@ -350,8 +518,8 @@ template <int ES>
 __global__ __launch_bounds__(kWG) void k_all_gather_elem(Ptrs<64> p, int P, int64_t m) {
     using E = typename std::conditional<ES == 2, uint16_t, uint32_t>::type;
     const int64_t total = m * P;
-    for (int64_t i = blockIdx.x * static_cast<int64_t>(kWG) + threadIdx.x; i < total;
-         i += static_cast<int64_t>(gridDim.x) * kWG) {
+    for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < total;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const int64_t r = i / m;
         const int64_t j = i - r * m;
         const E* src = reinterpret_cast<const E*>(p.in[r]);
@@ -365,24 +533,25 @@ __global__ __launch_bounds__(kWG) void k_all_gather_elem(Ptrs<64> p, int P, int6
 
 // ---------------------------------------------------------------- all-to-all
 
-// Descriptor of one row copy: source rank, source token, destination rank,
-// destination row.
+// One descriptor per row copy, stored in placement order: source rank,
+// source token, destination rank, destination row.
 template <int MAXP, int UNROLL>
 __global__ __launch_bounds__(kWG) void k_all_to_all(Ptrs<MAXP> p, const int4* __restrict__ desc, int64_t rowvec,
                                                     Place pl) {
+    const int nt = blockDim.x;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t w = it.first; w < it.end; w += it.stride) {
-        const int4 d = desc[w];
+    for (int64_t i = it.first; i < it.end; i += it.stride) {
+        const int4 d = desc[i];
         const uint4* src = p.in[d.x] + static_cast<int64_t>(d.y) * rowvec;
         uint4* dst = p.out[d.z] + static_cast<int64_t>(d.w) * rowvec;
-        for (int64_t v = threadIdx.x; v < rowvec; v += kWG * UNROLL) {
+        for (int64_t v = threadIdx.x; v < rowvec; v += static_cast<int64_t>(nt) * UNROLL) {
             uint4 y[UNROLL];
 #pragma unroll
             for (int u = 0; u < UNROLL; ++u)
-                if (v + u * kWG < rowvec) y[u] = src[v + u * kWG];
+                if (v + u * nt < rowvec) y[u] = src[v + u * nt];
 #pragma unroll
             for (int u = 0; u < UNROLL; ++u)
-                if (v + u * kWG < rowvec) dst[v + u * kWG] = y[u];
+                if (v + u * nt < rowvec) store_stream(dst + v + u * nt, y[u]);
         }
     }
 }
@@ -393,11 +562,11 @@ __global__ __launch_bounds__(kWG) void k_all_to_all_elem(Ptrs<64> p, const int4*
                                                          Place pl) {
     using E = typename std::conditional<ES == 2, uint16_t, uint32_t>::type;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t w = it.first; w < it.end; w += it.stride) {
-        const int4 d = desc[w];
+    for (int64_t i = it.first; i < it.end; i += it.stride) {
+        const int4 d = desc[i];
         const E* src = reinterpret_cast<const E*>(p.in[d.x]) + static_cast<int64_t>(d.y) * rowelems;
         E* dst = reinterpret_cast<E*>(p.out[d.z]) + static_cast<int64_t>(d.w) * rowelems;
-        for (int64_t v = threadIdx.x; v < rowelems; v += kWG) dst[v] = src[v];
+        for (int64_t v = threadIdx.x; v < rowelems; v += blockDim.x) dst[v] = src[v];
     }
 }
 
@@ -432,53 +601,47 @@ __global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uin
 
 // ---------------------------------------------------------------- launch helpers
 
-int64_t cap_grid(int64_t items) {
+int64_t cap_grid(int64_t wgs) {
     const int64_t cap = max_workgroups();
-    return items < cap ? (items > 0 ? items : 1) : cap;
-}
-
-int log2_or_neg(int v) {
-    for (int k = 0; k < 31; ++k)
-        if ((1 << k) == v) return k;
-    return -1;
+    return wgs < cap ? (wgs > 0 ? wgs : 1) : cap;
 }
 
 template <int PT, int MAXP, int DT, int VPT>
-void launch_ar_t(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G,
+void launch_ar_t(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G, int nt,
                  hipStream_t st) {
     Ptrs<MAXP> p = make_ptrs<MAXP>(in, out, P, P);
-    hipLaunchKernelGGL((k_allreduce<PT, MAXP, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, st, p, s, pl);
+    hipLaunchKernelGGL((k_allreduce<PT, MAXP, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p, s, pl);
 }
 
 template <int DT, int VPT>
-void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G,
+void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G, int nt,
                  hipStream_t st) {
     switch (P) {
-        case 2: launch_ar_t<2, 2, DT, VPT>(in, out, P, s, pl, G, st); break;
-        case 4: launch_ar_t<4, 4, DT, VPT>(in, out, P, s, pl, G, st); break;
-        case 8: launch_ar_t<8, 8, DT, VPT>(in, out, P, s, pl, G, st); break;
-        case 16: launch_ar_t<16, 16, DT, VPT>(in, out, P, s, pl, G, st); break;
-        default: launch_ar_t<0, 64, DT, VPT>(in, out, P, s, pl, G, st); break;
+        case 2: launch_ar_t<2, 2, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 4: launch_ar_t<4, 4, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 8: launch_ar_t<8, 8, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 16: launch_ar_t<16, 16, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        default: launch_ar_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
     }
 }
 
 template <int PT, int MAXP, int DT, int VPT>
-void launch_rs_t(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G,
+void launch_rs_t(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G, int nt,
                  hipStream_t st) {
     Ptrs<MAXP> p = make_ptrs<MAXP>(in, out, P, P);
-    hipLaunchKernelGGL((k_reduce_scatter<PT, MAXP, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, st, p, s,
+    hipLaunchKernelGGL((k_reduce_scatter<PT, MAXP, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p, s,
                        pl);
 }
 
 template <int DT, int VPT>
-void launch_rs_p(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G,
+void launch_rs_p(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G, int nt,
                  hipStream_t st) {
     switch (P) {
-        case 2: launch_rs_t<2, 2, DT, VPT>(in, out, P, s, pl, G, st); break;
-        case 4: launch_rs_t<4, 4, DT, VPT>(in, out, P, s, pl, G, st); break;
-        case 8: launch_rs_t<8, 8, DT, VPT>(in, out, P, s, pl, G, st); break;
-        case 16: launch_rs_t<16, 16, DT, VPT>(in, out, P, s, pl, G, st); break;
-        default: launch_rs_t<0, 64, DT, VPT>(in, out, P, s, pl, G, st); break;
+        case 2: launch_rs_t<2, 2, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 4: launch_rs_t<4, 4, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 8: launch_rs_t<8, 8, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 16: launch_rs_t<16, 16, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        default: launch_rs_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
     }
 }
 
@@ -488,33 +651,81 @@ int largest_divisor_upto(int P, int cap) {
     return 1;
 }
 
+// Workgroup size: small messages use one-wavefront workgroups so that their
+// few vectors spread over more compute units.
+int pick_threads(int64_t vectors_total) {
+    const int forced = tuning().wg_threads;
+    if (forced == 64 || forced == 128 || forced == 256) return forced;
+    return vectors_total < (int64_t(1) << 14) ? 64 : kWG;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
+
+template <int PT, int DT>
+void launch_rp_t(const void* const* in, void* const* out, int P, const RpShape& s, const Place& pl, int64_t G,
+                 hipStream_t st) {
+    Ptrs<64> p = make_ptrs<64>(in, out, P, P);
+    const size_t lds = static_cast<size_t>(P + 1) * s.V * 16;
+    hipLaunchKernelGGL((k_allreduce_rp<PT, DT>), dim3(static_cast<unsigned>(G)), dim3(kWG), lds, st, p, s, pl);
+}
+
+template <int DT>
+void launch_rp_p(const void* const* in, void* const* out, int P, const RpShape& s, const Place& pl, int64_t G,
+                 hipStream_t st) {
+    switch (P) {
+        case 64: launch_rp_t<64, DT>(in, out, P, s, pl, G, st); break;
+        case 32: launch_rp_t<32, DT>(in, out, P, s, pl, G, st); break;
+        default: launch_rp_t<0, DT>(in, out, P, s, pl, G, st); break;
+    }
+}
+
+// Rank-parallel all-reduce: a work item is a chunk of V vectors of all ranks.
+hipError_t launch_allreduce_rp(const void* const* in, void* const* out, int P, size_t count, int dtype, int mode,
+                               hipStream_t stream) {
+    const size_t es = dtype_size(dtype);
+    const size_t bytes = count * es;
+    RpShape s{};
+    s.nvec = static_cast<int64_t>(bytes / 16);
+    s.tail = static_cast<int32_t>((bytes % 16) / es);
+    s.P = P;
+    int V = tuning().rp_vectors;
+    if (V != 4 && V != 8 && V != 16 && V != 32 && V != 64) V = 16;
+    while (V > 4 && static_cast<size_t>(P + 1) * V * 16 > 65536) V /= 2;  // LDS tile within 64 KiB
+    s.V = V;
+    const int64_t groups = (s.nvec + V - 1) / V;
+    const Place pl = make_place_uniform(mode, groups > 0 ? groups : 1, 1);
+    const int64_t G = cap_grid(place_grid(pl));
+    if (dtype == kDtF32) launch_rp_p<kDtF32>(in, out, P, s, pl, G, stream);
+    else launch_rp_p<kDtBf16>(in, out, P, s, pl, G, stream);
+    return hipGetLastError();
+}
 
 hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size_t count, int dtype,
                             int dest_groups, int mode, hipStream_t stream) {
     const size_t es = dtype_size(dtype);
     const size_t bytes = count * es;
+    if (dest_groups <= 1 && P >= tuning().rp_min_ranks) return launch_allreduce_rp(in, out, P, count, dtype, mode, stream);
     ArShape s{};
     s.nvec = static_cast<int64_t>(bytes / 16);
     s.tail = static_cast<int32_t>((bytes % 16) / es);
     s.P = P;
-    s.gsize = dest_groups > 1 ? dest_groups : 1;
-    s.gshift = log2_or_neg(s.gsize);
-    s.dpi = P / s.gsize;
+    const int gsize = dest_groups > 1 ? dest_groups : 1;
+    s.dpi = P / gsize;
     int vpt = tuning().ar_vpt;
     if (vpt != 1 && vpt != 2) vpt = (P <= 16 && s.nvec >= (int64_t(1) << 20)) ? 2 : 1;
-    const int64_t cv = static_cast<int64_t>(kWG) * vpt;
+    const int nt = pick_threads(s.nvec);
+    const int64_t cv = static_cast<int64_t>(nt) * vpt;
     const int64_t groups = (s.nvec + cv - 1) / cv;
-    const int64_t G = cap_grid(groups * s.gsize);
-    const Place pl = make_place_uniform(mode, G, groups, s.gsize);
+    const Place pl = make_place_uniform(mode, groups > 0 ? groups : 1, gsize);
+    const int64_t G = cap_grid(place_grid(pl));
     if (dtype == kDtF32) {
-        if (vpt == 2) launch_ar_p<kDtF32, 2>(in, out, P, s, pl, G, stream);
-        else launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, stream);
+        if (vpt == 2) launch_ar_p<kDtF32, 2>(in, out, P, s, pl, G, nt, stream);
+        else launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
     } else {
-        if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, stream);
-        else launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, stream);
+        if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, stream);
+        else launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
     }
     return hipGetLastError();
 }
@@ -538,16 +749,17 @@ hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P,
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
     const int vpt = (P <= 16 && s.mv * P >= (int64_t(1) << 20)) ? 2 : 1;
-    const int64_t cv = static_cast<int64_t>(kWG) * vpt;
+    const int nt = pick_threads(s.mv * P);
+    const int64_t cv = static_cast<int64_t>(nt) * vpt;
     s.wcs = (s.mv + cv - 1) / cv;
-    const int64_t G = cap_grid(s.wcs * P);
-    const Place pl = make_place_uniform(mode, G, s.wcs * P, 1);
+    const Place pl = make_place_uniform(mode, s.wcs * P, 1);
+    const int64_t G = cap_grid(place_grid(pl));
     if (dtype == kDtF32) {
-        if (vpt == 2) launch_rs_p<kDtF32, 2>(in, out, P, s, pl, G, stream);
-        else launch_rs_p<kDtF32, 1>(in, out, P, s, pl, G, stream);
+        if (vpt == 2) launch_rs_p<kDtF32, 2>(in, out, P, s, pl, G, nt, stream);
+        else launch_rs_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
     } else {
-        if (vpt == 2) launch_rs_p<kDtBf16, 2>(in, out, P, s, pl, G, stream);
-        else launch_rs_p<kDtBf16, 1>(in, out, P, s, pl, G, stream);
+        if (vpt == 2) launch_rs_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, stream);
+        else launch_rs_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
     }
     return hipGetLastError();
 }
@@ -571,39 +783,51 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
     const int vpt = s.mv * P >= (int64_t(1) << 20) ? 2 : 1;
-    const int64_t cv = static_cast<int64_t>(kWG) * vpt;
+    const int nt = pick_threads(s.mv * P);
+    const int64_t cv = static_cast<int64_t>(nt) * vpt;
     s.wcs = (s.mv + cv - 1) / cv;
     // Split destinations when there are few chunks, so that more workgroups
     // share the stores; each member re-reads its chunk (an L2 hit when the
     // group's members sit on one XCD).
-    s.gsize = (s.wcs * P < 512) ? largest_divisor_upto(P, 8) : 1;
-    s.gshift = log2_or_neg(s.gsize);
-    s.dpi = P / s.gsize;
-    const int64_t G = cap_grid(s.wcs * P * s.gsize);
-    const Place pl = make_place_uniform(mode, G, s.wcs * P, s.gsize);
+    const int gsize = (s.wcs * P < 512) ? largest_divisor_upto(P, 8) : 1;
+    s.dpi = P / gsize;
+    const Place pl = make_place_uniform(mode, s.wcs * P, gsize);
+    const int64_t G = cap_grid(place_grid(pl));
     if (P <= 8) {
         Ptrs<8> p = make_ptrs<8>(in, out, P, P);
         if (vpt == 2)
-            hipLaunchKernelGGL((k_all_gather<8, 2>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, s, pl);
+            hipLaunchKernelGGL((k_all_gather<8, 2>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
         else
-            hipLaunchKernelGGL((k_all_gather<8, 1>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, s, pl);
+            hipLaunchKernelGGL((k_all_gather<8, 1>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
     } else {
         Ptrs<64> p = make_ptrs<64>(in, out, P, P);
         if (vpt == 2)
-            hipLaunchKernelGGL((k_all_gather<64, 2>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, s, pl);
+            hipLaunchKernelGGL((k_all_gather<64, 2>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
         else
-            hipLaunchKernelGGL((k_all_gather<64, 1>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, s, pl);
+            hipLaunchKernelGGL((k_all_gather<64, 1>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
     }
     return hipGetLastError();
 }
 
 hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, const void* desc, int64_t nitems,
-                             const int64_t* group_start, int64_t ngroups, size_t row_bytes, int esize, int mode,
-                             hipStream_t stream) {
+                             const int64_t* xcd_start, size_t row_bytes, int esize, int mode, hipStream_t stream) {
     const bool vec = row_bytes % 16 == 0;
     const int64_t rowlen = static_cast<int64_t>(vec ? row_bytes / 16 : row_bytes / esize);
-    const int64_t G = cap_grid(nitems);
-    const Place pl = make_place_groups(mode, G, group_start, ngroups);
+    Place pl{};
+    pl.mode = mode;
+    pl.gsize = 0;
+    pl.gshift = -1;
+    int64_t want = nitems;
+    if (mode == kPlaceXcd) {
+        int64_t longest = 0;
+        for (int x = 0; x <= kNumXcd; ++x) pl.start[x] = xcd_start[x];
+        for (int x = 0; x < kNumXcd; ++x)
+            longest = xcd_start[x + 1] - xcd_start[x] > longest ? xcd_start[x + 1] - xcd_start[x] : longest;
+        want = kNumXcd * longest;
+    } else {
+        pl.start[kNumXcd] = nitems;
+    }
+    const int64_t G = cap_grid(want);
     const int4* d = static_cast<const int4*>(desc);
     if (vec) {
         if (P <= 8) {

@@ -1,29 +1,28 @@
 // placement.h -- workgroup -> work-item map for the two placement modes.
 //
-// Shared by the device kernels and the host (which precomputes the per-XCD
-// table and mirrors the map for inspection).
+// Shared by the device kernels and the host (which fills the kernel-argument
+// view and mirrors the map for inspection).
 //
-// Work items are numbered group-major: item = group * group_size + member,
-// where a logical group is the set of work items that touch the same input
-// chunk (Sec. 4.2.1: threadblocks that share chunks are grouped, and a group
-// is placed as a unit).  Groups may also have variable sizes (all-to-all);
-// then the caller supplies the group start offsets.
+// Work items are numbered group-major: item = group * group_size + member.
+// A logical group is the set of work items that touch the same input chunk
+// (Sec. 4.2.1: a threadblock joins the group it shares chunks with, and
+// Algorithm 1 places each group as a unit).  Groups may also have variable
+// sizes (all-to-all); the host then lists the items in placement order.
 //
 // MI355X dispatches workgroup b of a launch to XCD (b mod 8).  With G
-// workgroups, XCD x holds Gx = ceil((G - x) / 8) of them, and the XCDs before
-// x hold S_x = sum_{x' < x} G_x' = a*x + min(x, c), where G = 8a + c.
+// workgroups, XCD x holds Gx = ceil((G - x) / 8) of them; its k-th one has
+// k = b div 8.
 //
-//  LINEAR (UA, Sec. 5.3): workgroup b runs items b, b+G, b+2G, ...  With one
-//      item per workgroup, consecutive items land on consecutive XCDs and the
-//      members of a group are spread over different XCDs.
+//  LINEAR (UA, Sec. 5.3): workgroup b runs items b, b+G, b+2G, ...  The
+//      members of a group (consecutive items) are spread over different XCDs.
 //
-//  XCD (NAP*, Sec. 5.3): XCD x owns the contiguous item range
-//      [start[x], start[x+1]), a share of the items proportional to its
-//      workgroup count S_{x+1} - S_x, cut at group boundaries so no group is
-//      split between XCDs (Algorithm 1 keeps a logical group inside one
-//      domain).  Its k-th workgroup (k = b div 8) runs items start[x] + k,
-//      start[x] + k + Gx, ...  Group members are consecutive items, so they run
-//      concurrently on neighbouring workgroups of one XCD and share its L2.
+//  XCD (NAP*, Sec. 5.3): Algorithm 1 hands logical groups round-robin to the
+//      domains (the next domain for each group) and keeps every group inside
+//      one domain.  Here the domains are the 8 XCDs: group g goes to XCD
+//      g mod 8, and XCD x runs its groups x, x+8, x+16, ... member by member
+//      on consecutive workgroups, so the members of a group run at the same
+//      time on one XCD and re-read their shared chunk from that XCD's L2.
+//      A group of one item is placed exactly as LINEAR places it.
 #pragma once
 
 #include <stdint.h>
@@ -48,64 +47,92 @@ struct ItemRange {
     int64_t stride;
 };
 
-// Kernel-argument view of a placement: for XCD mode start[0..8] are the
-// per-XCD item ranges; for both modes start[8] is the total item count.
+// Kernel-argument view of a placement.
+//  Uniform groups (gsize > 0): `groups` groups of gsize items each.
+//  Listed order (gsize == 0): the items are already stored in placement
+//      order; XCD x runs list positions [start[x], start[x+1]).
 struct Place {
+    int64_t groups;
     int64_t start[kNumXcd + 1];
     int32_t mode;
+    int32_t gsize;
+    int32_t gshift;  // log2(gsize) when a power of two, else -1
     int32_t pad;
 };
 
-// Workgroups on XCDs 0..x-1 when G workgroups are dealt round-robin over 8 XCDs.
-NUNA_HD inline int64_t wgs_before_xcd(int64_t x, int64_t G) {
-    const int64_t a = G / kNumXcd, c = G % kNumXcd;
-    return a * x + (x < c ? x : c);
+NUNA_HD inline int64_t place_items(const Place& pl) {
+    return pl.gsize > 0 ? pl.groups * pl.gsize : pl.start[kNumXcd];
 }
 
+// The linear map runs when:
+//  - the mode is LINEAR;
+//  - groups have one item each: dealing single items round-robin to the XCDs
+//    is exactly what LINEAR does, so the same code runs;
+//  - the launch has fewer than 8 workgroups and cannot reach every XCD.
+NUNA_HD inline bool linear_map(const Place& pl, int64_t G) {
+    return pl.mode == kPlaceLinear || pl.gsize == 1 || G < kNumXcd;
+}
+
+// Range of list positions workgroup b of G runs.
 NUNA_HD inline ItemRange items_of(const Place& pl, int64_t b, int64_t G) {
     ItemRange r;
-    if (pl.mode == kPlaceLinear) {
+    if (linear_map(pl, G)) {
         r.first = b;
-        r.end = pl.start[kNumXcd];
+        r.end = place_items(pl);
         r.stride = G;
         return r;
     }
     const int64_t x = b & (kNumXcd - 1);
     const int64_t k = b >> 3;
-    r.first = pl.start[x] + k;
-    r.end = pl.start[x + 1];
     r.stride = (G - x + kNumXcd - 1) >> 3;
+    if (pl.gsize > 0) {
+        const int64_t gx = pl.groups > x ? (pl.groups - x + kNumXcd - 1) >> 3 : 0;
+        r.first = k;
+        r.end = gx * pl.gsize;
+    } else {
+        r.first = pl.start[x] + k;
+        r.end = pl.start[x + 1];
+    }
     return r;
 }
 
-// Host: placement table for `groups` groups of `group_size` items.
-inline Place make_place_uniform(int mode, int64_t G, int64_t groups, int64_t group_size) {
+// Work item at list position i of workgroup b of G.
+NUNA_HD inline int64_t item_at(const Place& pl, int64_t b, int64_t G, int64_t i) {
+    if (linear_map(pl, G) || pl.gsize == 0) return i;
+    const int64_t x = b & (kNumXcd - 1);
+    int64_t q, m;
+    if (pl.gshift >= 0) {
+        q = i >> pl.gshift;
+        m = i & ((int64_t(1) << pl.gshift) - 1);
+    } else {
+        q = i / pl.gsize;
+        m = i - q * pl.gsize;
+    }
+    return (x + kNumXcd * q) * pl.gsize + m;
+}
+
+inline int log2_exact(int64_t v) {
+    for (int k = 0; k < 62; ++k)
+        if ((int64_t(1) << k) == v) return k;
+    return -1;
+}
+
+// Host: placement of `groups` uniform groups of `gsize` items.
+inline Place make_place_uniform(int mode, int64_t groups, int64_t gsize) {
     Place pl{};
     pl.mode = mode;
-    for (int x = 0; x <= kNumXcd; ++x) pl.start[x] = group_size * ((groups * wgs_before_xcd(x, G)) / G);
-    pl.start[kNumXcd] = groups * group_size;
+    pl.groups = groups;
+    pl.gsize = static_cast<int32_t>(gsize);
+    pl.gshift = log2_exact(gsize);
     return pl;
 }
 
-// Host: placement table for variable-size groups; group_start holds ngroups+1
-// item offsets (the last one is the item count).
-inline Place make_place_groups(int mode, int64_t G, const int64_t* group_start, int64_t ngroups) {
-    Place pl{};
-    pl.mode = mode;
-    const int64_t nitems = group_start[ngroups];
-    for (int x = 0; x < kNumXcd; ++x) {
-        const int64_t target = nitems * wgs_before_xcd(x, G) / G;
-        int64_t lo = 0, hi = ngroups;  // first group whose start is >= target
-        while (lo < hi) {
-            const int64_t mid = (lo + hi) / 2;
-            if (group_start[mid] < target) lo = mid + 1;
-            else hi = mid;
-        }
-        pl.start[x] = group_start[lo];
-    }
-    pl.start[0] = 0;
-    pl.start[kNumXcd] = nitems;
-    return pl;
+// Host: workgroups a launch of this placement needs so that every item gets
+// its own workgroup (before any cap).  XCD mode sizes every XCD for the
+// largest per-XCD group list; workgroups past a list's end exit at once.
+inline int64_t place_grid(const Place& pl) {
+    if (pl.mode == kPlaceLinear || pl.gsize <= 1) return place_items(pl);
+    return kNumXcd * ((pl.groups + kNumXcd - 1) / kNumXcd) * pl.gsize;
 }
 
 }  // namespace nuna

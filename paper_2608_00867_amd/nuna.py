@@ -55,7 +55,8 @@ SIGNATURES = {
     "nuna_all_to_all": ([_vpp, _vpp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp],
                         ctypes.c_int),
     "nuna_placement_items": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _i64p,
-                              _i64p, _i64p], ctypes.c_int),
+                              ctypes.c_int64, _i64p], ctypes.c_int),
+    "nuna_placement_grid": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, _i64p], ctypes.c_int),
     "nuna_probe_xcc": ([ctypes.c_int, _vp, _vp, _vp], ctypes.c_int),
     "nuna_copy": ([_vp, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
 }
@@ -124,11 +125,22 @@ def all_to_all_raw(send_ptrs, recv_ptrs, layout_handle, row_elems, recv_capacity
 
 
 def placement_items(place, b, G, groups, group_size):
-    """(first, end, stride) of the work items workgroup b runs (host mirror of the kernels' map)."""
-    f, e, s = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
-    _check(lib().nuna_placement_items(PLACEMENTS[place], b, G, groups, group_size, ctypes.byref(f), ctypes.byref(e),
-                                      ctypes.byref(s)))
-    return f.value, e.value, s.value
+    """Work items workgroup b of G runs, in order (host mirror of the kernels' map)."""
+    import numpy as np
+    cnt = ctypes.c_int64()
+    lib().nuna_placement_items(PLACEMENTS[place], b, G, groups, group_size, None, 0, ctypes.byref(cnt))
+    n = cnt.value
+    buf = np.zeros(max(n, 1), dtype=np.int64)
+    _check(lib().nuna_placement_items(PLACEMENTS[place], b, G, groups, group_size, buf.ctypes.data_as(_i64p), n,
+                                      ctypes.byref(cnt)))
+    return buf[:n].tolist()
+
+
+def placement_grid(place, groups, group_size):
+    """Workgroups a launch of this placement uses (before the cap)."""
+    g = ctypes.c_int64()
+    _check(lib().nuna_placement_grid(PLACEMENTS[place], groups, group_size, ctypes.byref(g)))
+    return g.value
 
 
 def init():

@@ -229,45 +229,57 @@ def test_a2a_requires_upload_and_capacity():
 # ---------------------------------------------------------------- placement map (host mirror)
 
 def _map(place, G, groups, gsize):
+    """item -> (workgroup, position in that workgroup's sequence)"""
     seen = {}
     for b in range(G):
-        f, e, s = nuna.placement_items(place, b, G, groups, gsize)
-        for w in range(f, e, s):
+        for pos, w in enumerate(nuna.placement_items(place, b, G, groups, gsize)):
             assert w not in seen, (place, G, groups, gsize, w)
-            seen[w] = b
+            seen[w] = (b, pos)
     return seen
 
 
-@pytest.mark.parametrize("G,groups,gsize", [(1, 1, 1), (5, 5, 1), (8, 8, 1), (13, 13, 1), (16, 64, 1), (24, 3, 8),
-                                            (64, 8, 8), (37, 11, 3), (100, 100, 1), (2048, 16384, 1), (7, 50, 2)])
-def test_placement_covers_every_item_once(G, groups, gsize):
+GEOMS = [(1, 1), (5, 1), (8, 1), (13, 1), (64, 1), (3, 8), (8, 8), (11, 3), (100, 1), (16384, 1), (50, 2), (4, 8),
+         (9, 7)]
+
+
+@pytest.mark.parametrize("groups,gsize", GEOMS)
+def test_placement_covers_every_item_once(groups, gsize):
     W = groups * gsize
     for place in (nuna.LINEAR, nuna.XCD):
-        seen = _map(place, G, groups, gsize)
-        assert sorted(seen) == list(range(W))
+        G0 = nuna.placement_grid(place, groups, gsize)
+        for G in sorted({G0, max(1, G0 // 3), 1, 7, 8}):
+            if G > 4096 and G != G0:
+                continue
+            seen = _map(place, G, groups, gsize)
+            assert sorted(seen) == list(range(W)), (place, G)
 
 
-@pytest.mark.parametrize("G,groups,gsize", [(24, 3, 8), (64, 8, 8), (37, 11, 3), (16, 64, 1), (80, 10, 8)])
-def test_xcd_mode_keeps_groups_on_one_xcd_in_contiguous_ranges(G, groups, gsize):
+@pytest.mark.parametrize("groups,gsize", [g for g in GEOMS if g[0] * g[1] <= 4096])
+def test_xcd_mode_deals_groups_round_robin_and_runs_members_together(groups, gsize):
+    G = nuna.placement_grid(nuna.XCD, groups, gsize)
+    assert G >= groups * gsize and (gsize == 1 or G % 8 == 0)
     seen = _map(nuna.XCD, G, groups, gsize)
-    xcd_of_item = {w: b % 8 for w, b in seen.items()}
     for g in range(groups):
-        assert len({xcd_of_item[g * gsize + m] for m in range(gsize)}) == 1, g
-    for x in range(8):
-        items = sorted(w for w, xx in xcd_of_item.items() if xx == x)
-        if items:
-            assert items == list(range(items[0], items[-1] + 1)), x
-    # an XCD's share of items follows its share of workgroups, to within one group
-    for x in range(8):
-        wgs = sum(1 for b in range(G) if b % 8 == x)
-        items = sum(1 for xx in xcd_of_item.values() if xx == x)
-        assert abs(items - wgs * groups * gsize / G) <= gsize, (x, items, wgs)
+        bs = [seen[g * gsize + m][0] for m in range(gsize)]
+        # group g lives on XCD g mod 8 (workgroup b runs on XCD b mod 8) ...
+        assert {b % 8 for b in bs} == {g % 8}, g
+        # ... one item per workgroup, members on consecutive workgroup slots of that XCD
+        assert all(seen[g * gsize + m][1] == 0 for m in range(gsize))
+        ks = [b // 8 for b in bs]
+        assert ks == list(range(ks[0], ks[0] + gsize)), (g, ks)
 
 
-def test_linear_mode_is_round_robin():
+def test_xcd_mode_with_single_item_groups_equals_linear():
+    for W in (8, 64, 1000):
+        G = nuna.placement_grid(nuna.XCD, W, 1)
+        lin = _map(nuna.LINEAR, G, W, 1)
+        xcd = _map(nuna.XCD, G, W, 1)
+        assert lin == xcd
+
+
+def test_linear_mode_is_round_robin_and_spreads_groups():
     seen = _map(nuna.LINEAR, 16, 40, 1)
-    assert all(b == w % 16 for w, b in seen.items())
-    # a split group's members land on different XCDs in LINEAR mode
+    assert all(b == w % 16 for w, (b, _) in seen.items())
     seen = _map(nuna.LINEAR, 64, 8, 8)
     for g in range(8):
-        assert len({seen[g * 8 + m] % 8 for m in range(8)}) == 8
+        assert len({seen[g * 8 + m][0] % 8 for m in range(8)}) == 8
