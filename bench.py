@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"))
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle timing budget (cpu_baseline)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--profile", type=int, default=0, metavar="N",
+                    help="profiling run: N cold launches each of the dominant kernel (decode all-reduce T=64, "
+                         "XCD) and of the 64 MiB reference copy, eager, then exit")
     return ap.parse_args()
 
 
@@ -411,6 +414,33 @@ def copy_case(nuna, torch, pool, args, emit):
         del s
 
 
+# ---------------------------------------------------------------------------------------------- --profile
+
+PROFILE_COPY_BYTES = 64 << 20
+
+
+def profile_run(nuna, torch, pool, n):
+    """Short eager run for rocprofv3 counter passes: the dominant kernel on cold buffers, then the
+    reference copy of PROFILE_COPY_BYTES (the calibration kernel for the traffic counters)."""
+    from paper_2608_00867_amd import workloads as wl
+    x = wl.ar_bf16_decode(64)
+    pool.off = 0
+    sets = ar_sets(torch, pool, x, min(n, pool.nbytes // ar_footprint(8, x[0].size, 2)))
+    torch.cuda.synchronize()
+    for i in range(n):
+        ins, outs = sets[i % len(sets)]
+        nuna.allreduce(ins, outs, algo="auto", placement="xcd")
+    torch.cuda.synchronize()
+    pool.off = 0
+    a = pool.take(PROFILE_COPY_BYTES)
+    b = pool.take(PROFILE_COPY_BYTES)
+    for _ in range(n):
+        nuna.copy(b, a)
+    torch.cuda.synchronize()
+    print(json.dumps({"profile": {"dominant_launches": n, "dominant_alg_bytes": 2 * 8 * x[0].size * 2,
+                                  "copy_launches": n, "copy_bytes": PROFILE_COPY_BYTES}}), flush=True)
+
+
 # ---------------------------------------------------------------------------------------------- main
 
 def main():
@@ -427,6 +457,9 @@ def main():
 
     if args.full:
         full_sweep(nuna, torch, pool, args)
+        return
+    if args.profile:
+        profile_run(nuna, torch, pool, args.profile)
         return
 
     torch.cuda.synchronize()

@@ -19,10 +19,8 @@ inline size_t dtype_size(int dt) { return dt == kDtF32 ? 4u : 2u; }
 // launch shape only, never the arithmetic).
 struct Tuning {
     int max_grid = 16384;  // cap on workgroups per launch (persistent loop beyond)
-    int ar_vpt = 0;        // all-reduce vectors per thread per item (0 = by size)
     int wg_threads = 0;    // workgroup size for the streaming kernels (0 = by size)
-    int rp_min_ranks = 24; // all-reduce with at least this many ranks uses the rank-parallel kernel
-    int rp_vectors = 16;   // rank-parallel chunk: vectors per rank per work item
+    int lpr_min_ranks = 24;  // one-shot all-reduce with at least this many ranks runs lane-per-rank
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).

@@ -113,10 +113,8 @@ namespace nuna {
 const Tuning& tuning() {
     std::call_once(g_tuning_once, [] {
         g_tuning.max_grid = env_int("NUNA_MAX_GRID", g_tuning.max_grid);
-        g_tuning.ar_vpt = env_int("NUNA_AR_VPT", g_tuning.ar_vpt);
         g_tuning.wg_threads = env_int("NUNA_WG_THREADS", g_tuning.wg_threads);
-        g_tuning.rp_min_ranks = env_int("NUNA_RP_MIN_RANKS", g_tuning.rp_min_ranks);
-        g_tuning.rp_vectors = env_int("NUNA_RP_VECTORS", g_tuning.rp_vectors);
+        g_tuning.lpr_min_ranks = env_int("NUNA_LPR_MIN_RANKS", g_tuning.lpr_min_ranks);
     });
     return g_tuning;
 }

@@ -140,10 +140,75 @@ Ptrs<MAXP> make_ptrs(const void* const* in, void* const* out, int nin, int nout)
     return p;
 }
 
+// Rank pointer table.  With a handful of ranks the kernels index the
+// kernel-argument pointer array with compile-time offsets, and the pointers
+// arrive in SGPRs with the first scalar loads.  With many ranks, or a rank
+// chosen at run time, each pointer would be a separate scalar load that the
+// dependent vector load must wait for.  Instead every wave loads the table
+// once, lane r holding rank r's input and output pointers (one vector load
+// each), and v_readlane hands any rank's pointer to the wave as a uniform
+// value with no memory round trip.  The table is loaded with all lanes
+// active, at kernel start.
+struct RankTable {
+    uint32_t in_lo, in_hi, out_lo, out_hi;
+};
+
+template <int MAXP>
+__device__ __forceinline__ RankTable load_rank_table(const Ptrs<MAXP>& p, int P) {
+    const int lane = threadIdx.x & 63;
+    RankTable t{0u, 0u, 0u, 0u};
+    (void)P;  // entries past P are null pointers and never used
+    if (lane < MAXP) {
+        const uint64_t a = reinterpret_cast<uint64_t>(p.in[lane]);
+        const uint64_t b = reinterpret_cast<uint64_t>(p.out[lane]);
+        t.in_lo = static_cast<uint32_t>(a);
+        t.in_hi = static_cast<uint32_t>(a >> 32);
+        t.out_lo = static_cast<uint32_t>(b);
+        t.out_hi = static_cast<uint32_t>(b >> 32);
+    }
+    return t;
+}
+
+__device__ __forceinline__ const uint4* rank_in(const RankTable& t, int r) {
+    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.in_lo), r));
+    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.in_hi), r));
+    return reinterpret_cast<const uint4*>((hi << 32) | lo);
+}
+
+__device__ __forceinline__ uint4* rank_out(const RankTable& t, int r) {
+    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.out_lo), r));
+    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.out_hi), r));
+    return reinterpret_cast<uint4*>((hi << 32) | lo);
+}
+
+// Pointer access: compile-time offsets for up to 16 ranks, the table beyond.
+template <int PT>
+constexpr bool use_table() {
+    return PT == 0 || PT > 16;
+}
+
+template <int PT, int MAXP>
+__device__ __forceinline__ const uint4* in_ptr(const Ptrs<MAXP>& p, const RankTable& t, int r) {
+    if constexpr (use_table<PT>())
+        return rank_in(t, r);
+    else
+        return p.in[r];
+}
+
+template <int PT, int MAXP>
+__device__ __forceinline__ uint4* out_ptr(const Ptrs<MAXP>& p, const RankTable& t, int r) {
+    if constexpr (use_table<PT>())
+        return rank_out(t, r);
+    else
+        return p.out[r];
+}
+
 // Ranks loaded per batch: all loads of a batch are issued before its adds.
+// Compile-time rank counts load every rank at once; a run-time count goes in
+// batches of 16.
 template <int PT>
 constexpr int rank_batch() {
-    return PT == 0 ? 16 : (PT < 16 ? PT : 16);
+    return PT == 0 ? 16 : PT;
 }
 
 // A thread's vectors within a chunk are v0 + j*nt, j < VPT, where nt is the
@@ -171,8 +236,8 @@ __device__ __forceinline__ void store_vecs(uint4* dst, const uint4 (&y)[VPT], in
 // in[r][base + v0 + j*nt], for vectors below `limit` (relative to base).
 // Lanes past the limit add zeros and are never stored.
 template <int PT, int DT, int VPT, bool FULL, bool NT, int MAXP>
-__device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, int P, int64_t base, int64_t v0, int nt,
-                                             int64_t limit, float (&acc)[VPT][Arith<DT>::kLanes]) {
+__device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, const RankTable& tab, int P, int64_t base, int64_t v0,
+                                             int nt, int64_t limit, float (&acc)[VPT][Arith<DT>::kLanes]) {
     using A = Arith<DT>;
     constexpr int B = rank_batch<PT>();
     if constexpr (PT > 0) {
@@ -180,7 +245,8 @@ __device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, int P, int64_t
         for (int r0 = 0; r0 < PT; r0 += B) {
             uint4 buf[B][VPT];
 #pragma unroll
-            for (int q = 0; q < B; ++q) load_vecs<FULL, VPT, NT>(buf[q], p.in[r0 + q] + base, v0, nt, limit);
+            for (int q = 0; q < B; ++q)
+                load_vecs<FULL, VPT, NT>(buf[q], in_ptr<PT>(p, tab, r0 + q) + base, v0, nt, limit);
 #pragma unroll
             for (int q = 0; q < B; ++q)
 #pragma unroll
@@ -197,7 +263,7 @@ __device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, int P, int64_t
             uint4 buf[B][VPT];
 #pragma unroll
             for (int q = 0; q < B; ++q)
-                if (r0 + q < P) load_vecs<FULL, VPT, NT>(buf[q], p.in[r0 + q] + base, v0, nt, limit);
+                if (r0 + q < P) load_vecs<FULL, VPT, NT>(buf[q], rank_in(tab, r0 + q) + base, v0, nt, limit);
 #pragma unroll
             for (int q = 0; q < B; ++q)
                 if (r0 + q < P) {
@@ -236,20 +302,20 @@ struct ArShape {
 };
 
 template <int PT, int DT, int VPT, bool FULL, bool NT, int MAXP>
-__device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const ArShape& s, int P, int64_t v0, int nt,
-                                                int g, bool all_dests) {
+__device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const RankTable& tab, const ArShape& s, int P,
+                                                int64_t v0, int nt, int g, bool all_dests) {
     using A = Arith<DT>;
     float acc[VPT][A::kLanes];
-    reduce_ranks<PT, DT, VPT, FULL, NT>(p, P, 0, v0, nt, s.nvec, acc);
+    reduce_ranks<PT, DT, VPT, FULL, NT>(p, tab, P, 0, v0, nt, s.nvec, acc);
     uint4 y[VPT];
 #pragma unroll
     for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
     if (PT > 0 && all_dests) {
 #pragma unroll
-        for (int d = 0; d < (PT > 0 ? PT : 1); ++d) store_vecs<FULL, VPT>(p.out[d], y, v0, nt, s.nvec);
+        for (int d = 0; d < (PT > 0 ? PT : 1); ++d) store_vecs<FULL, VPT>(out_ptr<PT>(p, tab, d), y, v0, nt, s.nvec);
     } else {
         const int d0 = g * s.dpi;
-        for (int d = d0; d < d0 + s.dpi; ++d) store_vecs<FULL, VPT>(p.out[d], y, v0, nt, s.nvec);
+        for (int d = d0; d < d0 + s.dpi; ++d) store_vecs<FULL, VPT>(out_ptr<PT>(p, tab, d), y, v0, nt, s.nvec);
     }
 }
 
@@ -260,6 +326,7 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int P = PT > 0 ? PT : s.P;
     const bool all_dests = pl.gsize == 1;
+    const RankTable tab = use_table<PT>() ? load_rank_table(p, P) : RankTable{0u, 0u, 0u, 0u};
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
@@ -271,14 +338,14 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
         // read through L2 so the group's re-reads hit.
         if (all_dests) {
             if ((c + 1) * cv <= s.nvec)
-                allreduce_chunk<PT, DT, VPT, true, true>(p, s, P, v0, nt, g, all_dests);
+                allreduce_chunk<PT, DT, VPT, true, true>(p, tab, s, P, v0, nt, g, all_dests);
             else
-                allreduce_chunk<PT, DT, VPT, false, true>(p, s, P, v0, nt, g, all_dests);
+                allreduce_chunk<PT, DT, VPT, false, true>(p, tab, s, P, v0, nt, g, all_dests);
         } else {
             if ((c + 1) * cv <= s.nvec)
-                allreduce_chunk<PT, DT, VPT, true, false>(p, s, P, v0, nt, g, all_dests);
+                allreduce_chunk<PT, DT, VPT, true, false>(p, tab, s, P, v0, nt, g, all_dests);
             else
-                allreduce_chunk<PT, DT, VPT, false, false>(p, s, P, v0, nt, g, all_dests);
+                allreduce_chunk<PT, DT, VPT, false, false>(p, tab, s, P, v0, nt, g, all_dests);
         }
     }
     if (s.tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < s.tail) {
@@ -289,87 +356,90 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
     }
 }
 
-// ---------------------------------------------------------------- all-reduce, rank-parallel (many ranks)
+// ---------------------------------------------------------------- all-reduce, lane per rank (many ranks)
 //
-// For many ranks and small messages the per-thread rank loop above issues its
-// loads in batches, one memory round trip per batch.  Here a work item is a
-// chunk of V <= 64 vectors of every rank, and the loads are spread over the
-// workgroup's waves by rank: wave w loads ranks w, w+NW, ... (one uniform
-// pointer per load instruction), so every load of the item is in flight at
-// once.  The tile goes to LDS; then one thread per output dword adds the P
-// ranks in ascending order from LDS (the same order and rounding as every
-// other kernel), and the waves store the result to the P outputs rank by rank.
+// With many ranks a thread that owns one vector position must issue P loads
+// and P stores, so small messages run on few workgroups with long
+// per-thread instruction streams.  Here thread t of a workgroup owns slot
+// (rank t mod P, vector t div P) of a chunk of V = 256 / P vectors: it loads
+// one vector of its rank with that rank's own pointer (fetched from the lane
+// holding it in the rank table), writes it to an LDS tile [P][V], and after
+// the barrier one thread per output dword adds the P ranks in ascending
+// order (same order and rounding as every other kernel).  After a second
+// barrier thread t stores the result vector to its rank's output.  A message
+// of 16 KiB per rank at P=64 thus spreads over 256 workgroups.
 
-struct RpShape {
+struct LprShape {
     int64_t nvec;  // full 16-byte vectors per rank buffer
     int32_t P;
-    int32_t V;     // vectors per rank per work item (<= 64)
+    int32_t V;     // vectors per rank per work item; P * V <= kWG
     int32_t tail;  // elements after the last full vector
     int32_t pad;
 };
 
+// Sum column `col` of the LDS tile over ranks 0..P-1 in order; the dword of
+// rank r is col[r * stride].
 template <int PT, int DT>
-__device__ __forceinline__ uint32_t rp_sum_column(const uint32_t* col, int stride, int P) {
-    // col[r * stride] is this thread's dword of rank r.
+__device__ __forceinline__ uint32_t lpr_sum_column(const uint32_t* col, int stride, int P) {
     constexpr int U = 16;
+    float lo, hi;
     if constexpr (DT == kDtF32) {
-        float a = __uint_as_float(col[0]);
-        if constexpr (PT > 0) {
-#pragma unroll
-            for (int r = 1; r < PT; ++r) a = a + __uint_as_float(col[r * stride]);
-        } else {
-            int r = 1;
-            for (; r + U <= P; r += U) {
-                uint32_t t[U];
-#pragma unroll
-                for (int q = 0; q < U; ++q) t[q] = col[(r + q) * stride];
-#pragma unroll
-                for (int q = 0; q < U; ++q) a = a + __uint_as_float(t[q]);
-            }
-            for (; r < P; ++r) a = a + __uint_as_float(col[r * stride]);
-        }
-        return __float_as_uint(a);
+        lo = __uint_as_float(col[0]);
+        hi = 0.0f;
     } else {
-        float lo = bf16_lo(col[0]), hi = bf16_hi(col[0]);
-        if constexpr (PT > 0) {
-#pragma unroll
-            for (int r = 1; r < PT; ++r) {
-                const uint32_t t = col[r * stride];
-                lo = lo + bf16_lo(t);
-                hi = hi + bf16_hi(t);
-            }
-        } else {
-            int r = 1;
-            for (; r + U <= P; r += U) {
-                uint32_t t[U];
-#pragma unroll
-                for (int q = 0; q < U; ++q) t[q] = col[(r + q) * stride];
-#pragma unroll
-                for (int q = 0; q < U; ++q) {
-                    lo = lo + bf16_lo(t[q]);
-                    hi = hi + bf16_hi(t[q]);
-                }
-            }
-            for (; r < P; ++r) {
-                const uint32_t t = col[r * stride];
-                lo = lo + bf16_lo(t);
-                hi = hi + bf16_hi(t);
-            }
-        }
-        return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
+        lo = bf16_lo(col[0]);
+        hi = bf16_hi(col[0]);
     }
+    auto add = [&](uint32_t v) {
+        if constexpr (DT == kDtF32) {
+            lo = lo + __uint_as_float(v);
+        } else {
+            lo = lo + bf16_lo(v);
+            hi = hi + bf16_hi(v);
+        }
+    };
+    if constexpr (PT > 0) {
+        uint32_t t[PT];
+#pragma unroll
+        for (int r = 1; r < PT; ++r) t[r] = col[r * stride];
+#pragma unroll
+        for (int r = 1; r < PT; ++r) add(t[r]);
+    } else {
+        int r = 1;
+        for (; r + U <= P; r += U) {
+            uint32_t t[U];
+#pragma unroll
+            for (int q = 0; q < U; ++q) t[q] = col[(r + q) * stride];
+#pragma unroll
+            for (int q = 0; q < U; ++q) add(t[q]);
+        }
+        for (; r < P; ++r) add(col[r * stride]);
+    }
+    if constexpr (DT == kDtF32)
+        return __float_as_uint(lo);
+    else
+        return f32_to_bf16(lo) | (f32_to_bf16(hi) << 16);
 }
 
 template <int PT, int DT>
-__global__ __launch_bounds__(kWG) void k_allreduce_rp(Ptrs<64> p, RpShape s, Place pl) {
+__global__ __launch_bounds__(kWG) void k_allreduce_lpr(Ptrs<64> p, LprShape s, Place pl) {
     using A = Arith<DT>;
-    extern __shared__ uint4 lds[];  // [P][V] input tile, then [V] result
-    constexpr int kMaxLoads = 64 / (kWG / 64);  // ranks per wave at P = 64
+    extern __shared__ uint4 lds[];  // [P][V] tile, then [V] results
     const int P = PT > 0 ? PT : s.P;
     const int V = s.V;
-    const int nw = blockDim.x >> 6;
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
+    const int t = threadIdx.x;
+    const RankTable tab = load_rank_table(p, P);
+    // This thread's slot and its rank's pointers, fetched from lane `rank`.
+    const int rank = t % P;
+    const int vec = t / P;
+    const bool active = vec < V;
+    const int src_lane = rank * 4;
+    const uint64_t in_lo = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src_lane, static_cast<int>(tab.in_lo)));
+    const uint64_t in_hi = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src_lane, static_cast<int>(tab.in_hi)));
+    const uint64_t out_lo = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src_lane, static_cast<int>(tab.out_lo)));
+    const uint64_t out_hi = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src_lane, static_cast<int>(tab.out_hi)));
+    const uint4* my_in = reinterpret_cast<const uint4*>((in_hi << 32) | in_lo);
+    uint4* my_out = reinterpret_cast<uint4*>((out_hi << 32) | out_lo);
     uint4* res = lds + P * V;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
@@ -377,34 +447,18 @@ __global__ __launch_bounds__(kWG) void k_allreduce_rp(Ptrs<64> p, RpShape s, Pla
         const int64_t base = c * V;
         const int64_t left = s.nvec - base;
         const int lim = left < V ? static_cast<int>(left) : V;
-        // phase 1: all loads of the item in flight, then into LDS
-        uint4 buf[kMaxLoads];
-#pragma unroll
-        for (int j = 0; j < kMaxLoads; ++j) {
-            const int r = wave + j * nw;
-            if (r < P && lane < lim) buf[j] = load16<true>(p.in[r] + base + lane);
-        }
-#pragma unroll
-        for (int j = 0; j < kMaxLoads; ++j) {
-            const int r = wave + j * nw;
-            if (r < P && lane < lim) lds[r * V + lane] = buf[j];
+        if (active && vec < lim) lds[rank * V + vec] = load16<true>(my_in + base + vec);
+        __syncthreads();
+        if (t < lim * 4) {
+            const uint32_t* col = reinterpret_cast<const uint32_t*>(lds) + t;
+            reinterpret_cast<uint32_t*>(res)[t] = lpr_sum_column<PT, DT>(col, V * 4, P);
         }
         __syncthreads();
-        // phase 2: one thread per output dword, ranks in ascending order
-        if (static_cast<int>(threadIdx.x) < lim * 4) {
-            const uint32_t* col = reinterpret_cast<const uint32_t*>(lds) + threadIdx.x;
-            reinterpret_cast<uint32_t*>(res)[threadIdx.x] = rp_sum_column<PT, DT>(col, V * 4, P);
-        }
-        __syncthreads();
-        // phase 3: the result to every output, rank by rank
-        if (lane < lim) {
-            const uint4 y = res[lane];
-            for (int d = wave; d < P; d += nw) store_stream(p.out[d] + base + lane, y);
-        }
+        if (active && vec < lim) store_stream(my_out + base + vec, res[vec]);
         __syncthreads();
     }
-    if (s.tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < s.tail) {
-        const int64_t e = s.nvec * (16 / A::kEsize) + threadIdx.x;
+    if (s.tail > 0 && blockIdx.x == 0 && t < s.tail) {
+        const int64_t e = s.nvec * (16 / A::kEsize) + t;
         float a = A::load1(p.in[0], e);
         for (int r = 1; r < P; ++r) a = a + A::load1(p.in[r], e);
         for (int d = 0; d < P; ++d) A::store1(p.out[d], e, a);
@@ -421,15 +475,15 @@ struct RsShape {
 };
 
 template <int PT, int DT, int VPT, bool FULL, int MAXP>
-__device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const RsShape& s, int P, int64_t r,
-                                                     int64_t v0, int nt) {
+__device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const RankTable& tab, const RsShape& s,
+                                                     int P, int64_t r, int64_t v0, int nt) {
     using A = Arith<DT>;
     float acc[VPT][A::kLanes];
-    reduce_ranks<PT, DT, VPT, FULL, true>(p, P, r * s.mv, v0, nt, s.mv, acc);
+    reduce_ranks<PT, DT, VPT, FULL, true>(p, tab, P, r * s.mv, v0, nt, s.mv, acc);
     uint4 y[VPT];
 #pragma unroll
     for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
-    store_vecs<FULL, VPT>(p.out[r], y, v0, nt, s.mv);
+    store_vecs<FULL, VPT>(use_table<PT>() ? rank_out(tab, static_cast<int>(r)) : p.out[r], y, v0, nt, s.mv);
 }
 
 template <int PT, int MAXP, int DT, int VPT>
@@ -437,6 +491,7 @@ __global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s,
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int P = PT > 0 ? PT : s.P;
+    const RankTable tab = use_table<PT>() ? load_rank_table(p, P) : RankTable{0u, 0u, 0u, 0u};
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
@@ -444,9 +499,9 @@ __global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s,
         const int64_t c = w - r * s.wcs;
         const int64_t v0 = c * cv + threadIdx.x;
         if ((c + 1) * cv <= s.mv)
-            reduce_scatter_chunk<PT, DT, VPT, true>(p, s, P, r, v0, nt);
+            reduce_scatter_chunk<PT, DT, VPT, true>(p, tab, s, P, r, v0, nt);
         else
-            reduce_scatter_chunk<PT, DT, VPT, false>(p, s, P, r, v0, nt);
+            reduce_scatter_chunk<PT, DT, VPT, false>(p, tab, s, P, r, v0, nt);
     }
 }
 
@@ -473,15 +528,15 @@ struct AgShape {
     int32_t dpi;  // destinations per item
 };
 
-template <int VPT, bool FULL, bool NT, int MAXP>
-__device__ __forceinline__ void all_gather_chunk(const Ptrs<MAXP>& p, const AgShape& s, int64_t r, int64_t v0,
-                                                 int nt, int g) {
-    const uint4* src = p.in[r];
+template <int VPT, bool FULL, bool NT>
+__device__ __forceinline__ void all_gather_chunk(const RankTable& tab, const AgShape& s, int64_t r, int64_t v0, int nt,
+                                                 int g) {
+    const uint4* src = rank_in(tab, static_cast<int>(r));
     uint4 y[VPT];
     load_vecs<FULL, VPT, NT>(y, src, v0, nt, s.mv);
     const int d0 = g * s.dpi;
     for (int d = d0; d < d0 + s.dpi; ++d) {
-        uint4* dst = p.out[d] + r * s.mv;
+        uint4* dst = rank_out(tab, d) + r * s.mv;
         if (dst == src) continue;  // in-place shard
         store_vecs<FULL, VPT>(dst, y, v0, nt, s.mv);
     }
@@ -491,6 +546,7 @@ template <int MAXP, int VPT>
 __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Place pl) {
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
+    const RankTable tab = load_rank_table(p, s.P);
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
@@ -502,14 +558,14 @@ __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Pla
         const int64_t v0 = c * cv + threadIdx.x;
         if (pl.gsize == 1) {
             if ((c + 1) * cv <= s.mv)
-                all_gather_chunk<VPT, true, true>(p, s, r, v0, nt, g);
+                all_gather_chunk<VPT, true, true>(tab, s, r, v0, nt, g);
             else
-                all_gather_chunk<VPT, false, true>(p, s, r, v0, nt, g);
+                all_gather_chunk<VPT, false, true>(tab, s, r, v0, nt, g);
         } else {
             if ((c + 1) * cv <= s.mv)
-                all_gather_chunk<VPT, true, false>(p, s, r, v0, nt, g);
+                all_gather_chunk<VPT, true, false>(tab, s, r, v0, nt, g);
             else
-                all_gather_chunk<VPT, false, false>(p, s, r, v0, nt, g);
+                all_gather_chunk<VPT, false, false>(tab, s, r, v0, nt, g);
         }
     }
 }
@@ -536,14 +592,15 @@ __global__ __launch_bounds__(kWG) void k_all_gather_elem(Ptrs<64> p, int P, int6
 // One descriptor per row copy, stored in placement order: source rank,
 // source token, destination rank, destination row.
 template <int MAXP, int UNROLL>
-__global__ __launch_bounds__(kWG) void k_all_to_all(Ptrs<MAXP> p, const int4* __restrict__ desc, int64_t rowvec,
-                                                    Place pl) {
+__global__ __launch_bounds__(kWG) void k_all_to_all(Ptrs<MAXP> p, int P, const int4* __restrict__ desc,
+                                                    int64_t rowvec, Place pl) {
     const int nt = blockDim.x;
+    const RankTable tab = load_rank_table(p, P);
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         const int4 d = desc[i];
-        const uint4* src = p.in[d.x] + static_cast<int64_t>(d.y) * rowvec;
-        uint4* dst = p.out[d.z] + static_cast<int64_t>(d.w) * rowvec;
+        const uint4* src = rank_in(tab, d.x) + static_cast<int64_t>(d.y) * rowvec;
+        uint4* dst = rank_out(tab, d.z) + static_cast<int64_t>(d.w) * rowvec;
         for (int64_t v = threadIdx.x; v < rowvec; v += static_cast<int64_t>(nt) * UNROLL) {
             uint4 y[UNROLL];
 #pragma unroll
@@ -621,6 +678,8 @@ void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& 
         case 4: launch_ar_t<4, 4, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         case 8: launch_ar_t<8, 8, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         case 16: launch_ar_t<16, 16, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 32: launch_ar_t<32, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 64: launch_ar_t<64, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         default: launch_ar_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
     }
 }
@@ -641,6 +700,8 @@ void launch_rs_p(const void* const* in, void* const* out, int P, const RsShape& 
         case 4: launch_rs_t<4, 4, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         case 8: launch_rs_t<8, 8, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         case 16: launch_rs_t<16, 16, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 32: launch_rs_t<32, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 64: launch_rs_t<64, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         default: launch_rs_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
     }
 }
@@ -664,41 +725,42 @@ int pick_threads(int64_t vectors_total) {
 // ---------------------------------------------------------------- launchers
 
 template <int PT, int DT>
-void launch_rp_t(const void* const* in, void* const* out, int P, const RpShape& s, const Place& pl, int64_t G,
-                 hipStream_t st) {
+void launch_lpr_t(const void* const* in, void* const* out, int P, const LprShape& s, const Place& pl, int64_t G,
+                  hipStream_t st) {
     Ptrs<64> p = make_ptrs<64>(in, out, P, P);
     const size_t lds = static_cast<size_t>(P + 1) * s.V * 16;
-    hipLaunchKernelGGL((k_allreduce_rp<PT, DT>), dim3(static_cast<unsigned>(G)), dim3(kWG), lds, st, p, s, pl);
+    hipLaunchKernelGGL((k_allreduce_lpr<PT, DT>), dim3(static_cast<unsigned>(G)), dim3(kWG), lds, st, p, s, pl);
 }
 
 template <int DT>
-void launch_rp_p(const void* const* in, void* const* out, int P, const RpShape& s, const Place& pl, int64_t G,
-                 hipStream_t st) {
+void launch_lpr_p(const void* const* in, void* const* out, int P, const LprShape& s, const Place& pl, int64_t G,
+                  hipStream_t st) {
     switch (P) {
-        case 64: launch_rp_t<64, DT>(in, out, P, s, pl, G, st); break;
-        case 32: launch_rp_t<32, DT>(in, out, P, s, pl, G, st); break;
-        default: launch_rp_t<0, DT>(in, out, P, s, pl, G, st); break;
+        case 16: launch_lpr_t<16, DT>(in, out, P, s, pl, G, st); break;
+        case 32: launch_lpr_t<32, DT>(in, out, P, s, pl, G, st); break;
+        case 64: launch_lpr_t<64, DT>(in, out, P, s, pl, G, st); break;
+        default: launch_lpr_t<0, DT>(in, out, P, s, pl, G, st); break;
     }
 }
 
-// Rank-parallel all-reduce: a work item is a chunk of V vectors of all ranks.
-hipError_t launch_allreduce_rp(const void* const* in, void* const* out, int P, size_t count, int dtype, int mode,
-                               hipStream_t stream) {
+// Lane-per-rank all-reduce: a work item is a chunk of V = 256 / P vectors of
+// every rank.
+hipError_t launch_allreduce_lpr(const void* const* in, void* const* out, int P, size_t count, int dtype, int mode,
+                                hipStream_t stream) {
     const size_t es = dtype_size(dtype);
     const size_t bytes = count * es;
-    RpShape s{};
+    LprShape s{};
     s.nvec = static_cast<int64_t>(bytes / 16);
     s.tail = static_cast<int32_t>((bytes % 16) / es);
     s.P = P;
-    int V = tuning().rp_vectors;
-    if (V != 4 && V != 8 && V != 16 && V != 32 && V != 64) V = 16;
-    while (V > 4 && static_cast<size_t>(P + 1) * V * 16 > 65536) V /= 2;  // LDS tile within 64 KiB
-    s.V = V;
-    const int64_t groups = (s.nvec + V - 1) / V;
+    s.V = kWG / P;
+    const int64_t groups = (s.nvec + s.V - 1) / s.V;
     const Place pl = make_place_uniform(mode, groups > 0 ? groups : 1, 1);
     const int64_t G = cap_grid(place_grid(pl));
-    if (dtype == kDtF32) launch_rp_p<kDtF32>(in, out, P, s, pl, G, stream);
-    else launch_rp_p<kDtBf16>(in, out, P, s, pl, G, stream);
+    if (dtype == kDtF32)
+        launch_lpr_p<kDtF32>(in, out, P, s, pl, G, stream);
+    else
+        launch_lpr_p<kDtBf16>(in, out, P, s, pl, G, stream);
     return hipGetLastError();
 }
 
@@ -706,27 +768,22 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
                             int dest_groups, int mode, hipStream_t stream) {
     const size_t es = dtype_size(dtype);
     const size_t bytes = count * es;
-    if (dest_groups <= 1 && P >= tuning().rp_min_ranks) return launch_allreduce_rp(in, out, P, count, dtype, mode, stream);
+    if (dest_groups <= 1 && P >= tuning().lpr_min_ranks) return launch_allreduce_lpr(in, out, P, count, dtype, mode, stream);
     ArShape s{};
     s.nvec = static_cast<int64_t>(bytes / 16);
     s.tail = static_cast<int32_t>((bytes % 16) / es);
     s.P = P;
     const int gsize = dest_groups > 1 ? dest_groups : 1;
     s.dpi = P / gsize;
-    int vpt = tuning().ar_vpt;
-    if (vpt != 1 && vpt != 2) vpt = (P <= 16 && s.nvec >= (int64_t(1) << 20)) ? 2 : 1;
     const int nt = pick_threads(s.nvec);
-    const int64_t cv = static_cast<int64_t>(nt) * vpt;
+    const int64_t cv = nt;
     const int64_t groups = (s.nvec + cv - 1) / cv;
     const Place pl = make_place_uniform(mode, groups > 0 ? groups : 1, gsize);
     const int64_t G = cap_grid(place_grid(pl));
-    if (dtype == kDtF32) {
-        if (vpt == 2) launch_ar_p<kDtF32, 2>(in, out, P, s, pl, G, nt, stream);
-        else launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
-    } else {
-        if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, stream);
-        else launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
-    }
+    if (dtype == kDtF32)
+        launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
+    else
+        launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
     return hipGetLastError();
 }
 
@@ -748,19 +805,15 @@ hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P,
     RsShape s{};
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
-    const int vpt = (P <= 16 && s.mv * P >= (int64_t(1) << 20)) ? 2 : 1;
     const int nt = pick_threads(s.mv * P);
-    const int64_t cv = static_cast<int64_t>(nt) * vpt;
+    const int64_t cv = nt;
     s.wcs = (s.mv + cv - 1) / cv;
     const Place pl = make_place_uniform(mode, s.wcs * P, 1);
     const int64_t G = cap_grid(place_grid(pl));
-    if (dtype == kDtF32) {
-        if (vpt == 2) launch_rs_p<kDtF32, 2>(in, out, P, s, pl, G, nt, stream);
-        else launch_rs_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
-    } else {
-        if (vpt == 2) launch_rs_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, stream);
-        else launch_rs_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
-    }
+    if (dtype == kDtF32)
+        launch_rs_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
+    else
+        launch_rs_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
     return hipGetLastError();
 }
 
@@ -782,7 +835,7 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     AgShape s{};
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
-    const int vpt = s.mv * P >= (int64_t(1) << 20) ? 2 : 1;
+    const int vpt = 1;
     const int nt = pick_threads(s.mv * P);
     const int64_t cv = static_cast<int64_t>(nt) * vpt;
     s.wcs = (s.mv + cv - 1) / cv;
@@ -795,16 +848,10 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     const int64_t G = cap_grid(place_grid(pl));
     if (P <= 8) {
         Ptrs<8> p = make_ptrs<8>(in, out, P, P);
-        if (vpt == 2)
-            hipLaunchKernelGGL((k_all_gather<8, 2>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
-        else
-            hipLaunchKernelGGL((k_all_gather<8, 1>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
+        hipLaunchKernelGGL((k_all_gather<8, 1>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
     } else {
         Ptrs<64> p = make_ptrs<64>(in, out, P, P);
-        if (vpt == 2)
-            hipLaunchKernelGGL((k_all_gather<64, 2>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
-        else
-            hipLaunchKernelGGL((k_all_gather<64, 1>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
+        hipLaunchKernelGGL((k_all_gather<64, 1>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
     }
     return hipGetLastError();
 }
@@ -832,11 +879,11 @@ hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, 
     if (vec) {
         if (P <= 8) {
             Ptrs<8> p = make_ptrs<8>(send, recv, P, P);
-            hipLaunchKernelGGL((k_all_to_all<8, 4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, d, rowlen,
-                               pl);
+            hipLaunchKernelGGL((k_all_to_all<8, 4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P, d,
+                               rowlen, pl);
         } else {
             Ptrs<64> p = make_ptrs<64>(send, recv, P, P);
-            hipLaunchKernelGGL((k_all_to_all<64, 4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, d,
+            hipLaunchKernelGGL((k_all_to_all<64, 4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P, d,
                                rowlen, pl);
         }
     } else {
