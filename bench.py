@@ -47,6 +47,12 @@ def parse():
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"))
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle timing budget (cpu_baseline)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV", default=None,
+                    help="print a markdown summary of a rocprofv3 --kernel-trace CSV (per kernel and grid)")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"), default=None,
+                    help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --profile into HBM traffic "
+                         "per launch of the dominant kernel, scaled by the reference copy; writes "
+                         "profiles/dominant_traffic.json and prints markdown")
     ap.add_argument("--profile", type=int, default=0, metavar="N",
                     help="profiling run: N cold launches each of the dominant kernel (decode all-reduce T=64, "
                          "XCD) and of the 64 MiB reference copy, eager, then exit")
@@ -275,7 +281,7 @@ def roofline_dominant(sweep):
     us = row["xcd_us"]["median"]
     achieved = row["alg_bytes"] / (us * 1e-6) / 1e9
     return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(),
             "kernel": "k_allreduce<P=8,bf16,VPT=1> one-shot, [64,8192] bf16 per rank, XCD placement",
             "alg_bytes_per_launch": row["alg_bytes"], "avg_launch_us": us}
 
@@ -441,10 +447,97 @@ def profile_run(nuna, torch, pool, n):
                                   "copy_launches": n, "copy_bytes": PROFILE_COPY_BYTES}}), flush=True)
 
 
+# ---------------------------------------------------------------------------------------------- rocprofv3 summaries
+
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "dominant_traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_00867_amd", "csrc", "nuna_kernels.hip")
+
+
+def kernel_source_sha():
+    import hashlib
+    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+
+
+def _short(name):
+    name = name.replace("nuna::(anonymous namespace)::", "")
+    name = name[5:] if name.startswith("void ") else name
+    return name.split("(")[0] if "(" in name else name
+
+
+def summarize_trace(path):
+    import csv
+    import collections
+    by = collections.defaultdict(list)
+    for r in csv.DictReader(open(path)):
+        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        by[(_short(r["Kernel_Name"]), int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))].append(dur)
+    print("| kernel | grid (threads) | workgroup | dispatches | avg µs | median µs | p10 µs | p90 µs |")
+    print("|---|---|---|---|---|---|---|---|")
+    for (k, g, w), v in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+        v = sorted(v)
+        print(f"| `{k}` | {g} | {w} | {len(v)} | {statistics.mean(v):.3f} | {statistics.median(v):.3f} | "
+              f"{v[len(v) // 10]:.3f} | {v[(9 * len(v)) // 10]:.3f} |")
+
+
+def summarize_traffic(fetch_csv, write_csv):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the --profile run.  The reference copy moves
+    PROFILE_COPY_BYTES each way; its readings give the scale factor of each counter."""
+    import csv
+    import collections
+
+    def read(path):
+        by = collections.defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            by[(_short(r["Kernel_Name"]), int(r["Grid_Size"]))].append(float(r["Counter_Value"]))
+        return by
+
+    f, w = read(fetch_csv), read(write_csv)
+    dom = [k for k in f if k[0].startswith("k_allreduce")]
+    cpy = [k for k in f if k[0].startswith("k_copy")]
+    assert len(dom) == 1 and len(cpy) == 1, (dom, cpy)
+    kib = PROFILE_COPY_BYTES / 1024
+    ff = kib / statistics.median(f[cpy[0]])
+    wf = kib / statistics.median(w[cpy[0]])
+    fetch = statistics.median(f[dom[0]]) * ff * 1024
+    write = statistics.median(w[dom[0]]) * wf * 1024
+    alg = 2 * 8 * 64 * 8192 * 2
+    rec = {"kernel": dom[0][0], "grid": dom[0][1], "fetch_bytes": round(fetch), "write_bytes": round(write),
+           "traffic_bytes": round(fetch + write), "alg_bytes": alg, "fetch_scale": round(ff, 4),
+           "write_scale": round(wf, 4), "kernel_source_sha256": kernel_source_sha()}
+    os.makedirs(os.path.dirname(TRAFFIC_JSON), exist_ok=True)
+    json.dump(rec, open(TRAFFIC_JSON, "w"), indent=1)
+    print("| counter | reference copy (KiB/dispatch, moves %d KiB each way) | scale | dominant kernel (KiB/dispatch) | "
+          "scaled bytes |" % kib)
+    print("|---|---|---|---|---|")
+    print(f"| FETCH_SIZE | {statistics.median(f[cpy[0]]):.1f} | {ff:.4f} | {statistics.median(f[dom[0]]):.1f} | "
+          f"{fetch:.0f} |")
+    print(f"| WRITE_SIZE | {statistics.median(w[cpy[0]]):.1f} | {wf:.4f} | {statistics.median(w[dom[0]]):.1f} | "
+          f"{write:.0f} |")
+    print(f"\nTraffic per launch {fetch + write:.0f} B vs algorithmic {alg} B: ratio {(fetch + write) / alg:.4f}.")
+
+
+def measured_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed counter summary, or None when the
+    kernel source has changed since the counters were taken."""
+    try:
+        rec = json.load(open(TRAFFIC_JSON))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_sha():
+        return None
+    return rec["traffic_bytes"]
+
+
 # ---------------------------------------------------------------------------------------------- main
 
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace)
+        return
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path runs all P "
               f"simulated ranks on one GPU, and no figure across GPUs is produced).", file=sys.stderr)
