@@ -20,7 +20,9 @@ inline size_t dtype_size(int dt) { return dt == kDtF32 ? 4u : 2u; }
 struct Tuning {
     int max_grid = 16384;  // cap on workgroups per launch (persistent loop beyond)
     int wg_threads = 0;    // workgroup size for the streaming kernels (0 = by size)
-    int lpr_min_ranks = 24;  // one-shot all-reduce with at least this many ranks runs lane-per-rank
+    int vpt = 0;           // bf16 all-reduce vectors per thread per work item (0 = by size)
+    int lpr_min_ranks = 16;           // lane-per-rank all-reduce: at least this many ranks ...
+    int64_t lpr_max_vectors = 131072;  // ... and at most this many input vectors in total (2 MiB)
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
@@ -32,13 +34,16 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
                             int dest_groups, int mode, hipStream_t stream);
 
 // Reduce-scatter: in[q] holds P*m elements; out[r][j] = sum_q in[q][r*m+j].
+// keep_output: store the shards through the caches (they are read right
+// after, by the all-gather phase of a two-shot all-reduce).
 hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P, size_t m, int dtype,
-                                 int mode, hipStream_t stream);
+                                 int mode, bool keep_output, hipStream_t stream);
 
 // All-gather: out[d][r*m + j] = in[r][j]; a destination whose shard region
-// is the source itself (in-place form) is skipped.
+// is the source itself (in-place form) is skipped.  src_cached: read the
+// sources through the caches (they were just written).
 hipError_t launch_all_gather(const void* const* in, void* const* out, int P, size_t m, int dtype,
-                             int mode, hipStream_t stream);
+                             int mode, bool src_cached, hipStream_t stream);
 
 // All-to-all row copy driven by a descriptor table (device int4 per item:
 // src rank, src token, dst rank, dst row) stored in placement order.  For the

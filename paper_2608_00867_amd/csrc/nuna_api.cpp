@@ -114,7 +114,9 @@ const Tuning& tuning() {
     std::call_once(g_tuning_once, [] {
         g_tuning.max_grid = env_int("NUNA_MAX_GRID", g_tuning.max_grid);
         g_tuning.wg_threads = env_int("NUNA_WG_THREADS", g_tuning.wg_threads);
+        g_tuning.vpt = env_int("NUNA_VPT", g_tuning.vpt);
         g_tuning.lpr_min_ranks = env_int("NUNA_LPR_MIN_RANKS", g_tuning.lpr_min_ranks);
+        g_tuning.lpr_max_vectors = env_int("NUNA_LPR_MAX_VECTORS", static_cast<int>(g_tuning.lpr_max_vectors));
     });
     return g_tuning;
 }
@@ -199,9 +201,9 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
             shard_out[r] = static_cast<char*>(out[r]) + static_cast<size_t>(r) * m * es;
             shard_in[r] = shard_out[r];
         }
-        e = nuna::launch_reduce_scatter(in, shard_out, P, m, dtype, place, stream);
+        e = nuna::launch_reduce_scatter(in, shard_out, P, m, dtype, place, true, stream);
         if (e != hipSuccess) return hip_status(e, "reduce-scatter phase launch");
-        e = nuna::launch_all_gather(shard_in, out, P, m, dtype, place, stream);
+        e = nuna::launch_all_gather(shard_in, out, P, m, dtype, place, true, stream);
         return hip_status(e, "all-gather phase launch");
     }
     int groups = 1;
@@ -236,7 +238,7 @@ nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P
         return i.rank == o.rank && o.lo == i.lo + static_cast<uintptr_t>(o.rank) * mb;
     });
     if (st) return st;
-    return hip_status(nuna::launch_reduce_scatter(in, out, P, recvcount, dtype, place, stream),
+    return hip_status(nuna::launch_reduce_scatter(in, out, P, recvcount, dtype, place, false, stream),
                       "reduce-scatter launch");
 }
 
@@ -260,7 +262,7 @@ nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, si
         return i.rank == o.rank && i.lo == o.lo + static_cast<uintptr_t>(i.rank) * mb;
     });
     if (st) return st;
-    return hip_status(nuna::launch_all_gather(in, out, P, sendcount, dtype, place, stream), "all-gather launch");
+    return hip_status(nuna::launch_all_gather(in, out, P, sendcount, dtype, place, false, stream), "all-gather launch");
 }
 
 // ------------------------------------------------------------ all-to-all layout

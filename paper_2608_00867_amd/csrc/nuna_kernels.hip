@@ -225,11 +225,17 @@ __device__ __forceinline__ void load_vecs(uint4 (&dst)[VPT], const uint4* src, i
     }
 }
 
-template <bool FULL, int VPT>
+template <bool FULL, int VPT, bool NT = true>
 __device__ __forceinline__ void store_vecs(uint4* dst, const uint4 (&y)[VPT], int64_t v0, int nt, int64_t limit) {
 #pragma unroll
-    for (int j = 0; j < VPT; ++j)
-        if (FULL || v0 + j * nt < limit) store_stream(dst + v0 + j * nt, y[j]);
+    for (int j = 0; j < VPT; ++j) {
+        if (FULL || v0 + j * nt < limit) {
+            if constexpr (NT)
+                store_stream(dst + v0 + j * nt, y[j]);
+            else
+                dst[v0 + j * nt] = y[j];
+        }
+    }
 }
 
 // acc[j] = sum over ranks r = 0, 1, ..., P-1 (in that order) of
@@ -474,7 +480,7 @@ struct RsShape {
     int32_t pad;
 };
 
-template <int PT, int DT, int VPT, bool FULL, int MAXP>
+template <int PT, int DT, int VPT, bool FULL, bool KEEP, int MAXP>
 __device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const RankTable& tab, const RsShape& s,
                                                      int P, int64_t r, int64_t v0, int nt) {
     using A = Arith<DT>;
@@ -483,10 +489,12 @@ __device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const 
     uint4 y[VPT];
 #pragma unroll
     for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
-    store_vecs<FULL, VPT>(use_table<PT>() ? rank_out(tab, static_cast<int>(r)) : p.out[r], y, v0, nt, s.mv);
+    store_vecs<FULL, VPT, !KEEP>(use_table<PT>() ? rank_out(tab, static_cast<int>(r)) : p.out[r], y, v0, nt, s.mv);
 }
 
-template <int PT, int MAXP, int DT, int VPT>
+// KEEP: the shard is read again right away (the all-gather phase of a two-shot
+// all-reduce), so it is stored through the caches instead of streamed.
+template <int PT, int MAXP, int DT, int VPT, bool KEEP>
 __global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s, Place pl) {
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
@@ -499,9 +507,9 @@ __global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s,
         const int64_t c = w - r * s.wcs;
         const int64_t v0 = c * cv + threadIdx.x;
         if ((c + 1) * cv <= s.mv)
-            reduce_scatter_chunk<PT, DT, VPT, true>(p, tab, s, P, r, v0, nt);
+            reduce_scatter_chunk<PT, DT, VPT, true, KEEP>(p, tab, s, P, r, v0, nt);
         else
-            reduce_scatter_chunk<PT, DT, VPT, false>(p, tab, s, P, r, v0, nt);
+            reduce_scatter_chunk<PT, DT, VPT, false, KEEP>(p, tab, s, P, r, v0, nt);
     }
 }
 
@@ -542,7 +550,9 @@ __device__ __forceinline__ void all_gather_chunk(const RankTable& tab, const AgS
     }
 }
 
-template <int MAXP, int VPT>
+// CACHED: the sources were just written (two-shot all-gather phase) and may
+// still sit in L2 or the Infinity Cache, so they are read through the caches.
+template <int MAXP, int VPT, bool CACHED>
 __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Place pl) {
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
@@ -556,7 +566,7 @@ __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Pla
         const int64_t r = grp / s.wcs;
         const int64_t c = grp - r * s.wcs;
         const int64_t v0 = c * cv + threadIdx.x;
-        if (pl.gsize == 1) {
+        if (pl.gsize == 1 && !CACHED) {
             if ((c + 1) * cv <= s.mv)
                 all_gather_chunk<VPT, true, true>(tab, s, r, v0, nt, g);
             else
@@ -678,32 +688,52 @@ void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& 
         case 4: launch_ar_t<4, 4, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         case 8: launch_ar_t<8, 8, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         case 16: launch_ar_t<16, 16, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        case 32: launch_ar_t<32, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        case 64: launch_ar_t<64, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        default: launch_ar_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        default:
+            if constexpr (VPT == 1) {
+                if (P == 32) launch_ar_t<32, 64, DT, 1>(in, out, P, s, pl, G, nt, st);
+                else if (P == 64) launch_ar_t<64, 64, DT, 1>(in, out, P, s, pl, G, nt, st);
+                else launch_ar_t<0, 64, DT, 1>(in, out, P, s, pl, G, nt, st);
+            } else {
+                launch_ar_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st);  // not reached: pick_vpt gives 1
+            }
+            break;
     }
 }
 
-template <int PT, int MAXP, int DT, int VPT>
+template <int PT, int MAXP, int DT, int VPT, bool KEEP>
 void launch_rs_t(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G, int nt,
                  hipStream_t st) {
     Ptrs<MAXP> p = make_ptrs<MAXP>(in, out, P, P);
-    hipLaunchKernelGGL((k_reduce_scatter<PT, MAXP, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p, s,
-                       pl);
+    hipLaunchKernelGGL((k_reduce_scatter<PT, MAXP, DT, VPT, KEEP>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p,
+                       s, pl);
 }
 
-template <int DT, int VPT>
+template <int DT, int VPT, bool KEEP>
 void launch_rs_p(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G, int nt,
                  hipStream_t st) {
     switch (P) {
-        case 2: launch_rs_t<2, 2, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        case 4: launch_rs_t<4, 4, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        case 8: launch_rs_t<8, 8, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        case 16: launch_rs_t<16, 16, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        case 32: launch_rs_t<32, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        case 64: launch_rs_t<64, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        default: launch_rs_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 2: launch_rs_t<2, 2, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
+        case 4: launch_rs_t<4, 4, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
+        case 8: launch_rs_t<8, 8, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
+        case 16: launch_rs_t<16, 16, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
+        case 32: launch_rs_t<32, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
+        case 64: launch_rs_t<64, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
+        default: launch_rs_t<0, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
     }
+}
+
+// Vectors per thread per work item for bf16 all-reduce with up to 16 ranks,
+// by message size (measured on MI355X, cold): 4 at 4 MiB per rank, 2 at
+// 16 MiB, 1 at 64 MiB and above and for every smaller (latency-bound)
+// message, where more workgroups win.
+int pick_vpt(int64_t vectors_per_rank, int P) {
+    if (P > 16) return 1;
+    const int forced = tuning().vpt;
+    if (forced == 1 || forced == 2 || forced == 4) return forced;
+    if (vectors_per_rank >= (int64_t(1) << 22)) return 1;
+    if (vectors_per_rank >= (int64_t(1) << 20)) return 2;
+    if (vectors_per_rank >= (int64_t(1) << 18)) return 4;
+    return 1;
 }
 
 int largest_divisor_upto(int P, int cap) {
@@ -712,12 +742,14 @@ int largest_divisor_upto(int P, int cap) {
     return 1;
 }
 
-// Workgroup size: small messages use one-wavefront workgroups so that their
-// few vectors spread over more compute units.
-int pick_threads(int64_t vectors_total) {
+// Workgroup size: one-wavefront workgroups spread small messages, and the
+// long per-thread rank loops of many-rank reductions, over more compute
+// units; 256-thread workgroups stream large few-rank messages.
+int pick_threads(int64_t vectors_per_rank, int P) {
     const int forced = tuning().wg_threads;
     if (forced == 64 || forced == 128 || forced == 256) return forced;
-    return vectors_total < (int64_t(1) << 14) ? 64 : kWG;
+    if (P > 16) return 64;
+    return vectors_per_rank < (int64_t(1) << 14) ? 64 : kWG;
 }
 
 }  // namespace
@@ -768,27 +800,35 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
                             int dest_groups, int mode, hipStream_t stream) {
     const size_t es = dtype_size(dtype);
     const size_t bytes = count * es;
-    if (dest_groups <= 1 && P >= tuning().lpr_min_ranks) return launch_allreduce_lpr(in, out, P, count, dtype, mode, stream);
+    // Many ranks, small total input: the lane-per-rank kernel spreads the work
+    // over the most workgroups.
+    if (dest_groups <= 1 && P >= tuning().lpr_min_ranks &&
+        static_cast<int64_t>(bytes / 16) * P <= tuning().lpr_max_vectors)
+        return launch_allreduce_lpr(in, out, P, count, dtype, mode, stream);
     ArShape s{};
     s.nvec = static_cast<int64_t>(bytes / 16);
     s.tail = static_cast<int32_t>((bytes % 16) / es);
     s.P = P;
     const int gsize = dest_groups > 1 ? dest_groups : 1;
     s.dpi = P / gsize;
-    const int nt = pick_threads(s.nvec);
-    const int64_t cv = nt;
+    const int nt = pick_threads(s.nvec, P);
+    const int vpt = pick_vpt(s.nvec, P);
+    const int64_t cv = static_cast<int64_t>(nt) * vpt;
     const int64_t groups = (s.nvec + cv - 1) / cv;
     const Place pl = make_place_uniform(mode, groups > 0 ? groups : 1, gsize);
     const int64_t G = cap_grid(place_grid(pl));
-    if (dtype == kDtF32)
+    if (dtype == kDtF32) {
         launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
-    else
-        launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
+    } else {
+        if (vpt == 4) launch_ar_p<kDtBf16, 4>(in, out, P, s, pl, G, nt, stream);
+        else if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, stream);
+        else launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P, size_t m, int dtype, int mode,
-                                 hipStream_t stream) {
+                                 bool keep_output, hipStream_t stream) {
     const size_t es = dtype_size(dtype);
     if ((m * es) % 16 != 0) {
         Ptrs<64> p = make_ptrs<64>(in, out, P, P);
@@ -805,20 +845,23 @@ hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P,
     RsShape s{};
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
-    const int nt = pick_threads(s.mv * P);
+    const int nt = pick_threads(s.mv, P);
     const int64_t cv = nt;
     s.wcs = (s.mv + cv - 1) / cv;
     const Place pl = make_place_uniform(mode, s.wcs * P, 1);
     const int64_t G = cap_grid(place_grid(pl));
-    if (dtype == kDtF32)
-        launch_rs_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
-    else
-        launch_rs_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
+    if (dtype == kDtF32) {
+        if (keep_output) launch_rs_p<kDtF32, 1, true>(in, out, P, s, pl, G, nt, stream);
+        else launch_rs_p<kDtF32, 1, false>(in, out, P, s, pl, G, nt, stream);
+    } else {
+        if (keep_output) launch_rs_p<kDtBf16, 1, true>(in, out, P, s, pl, G, nt, stream);
+        else launch_rs_p<kDtBf16, 1, false>(in, out, P, s, pl, G, nt, stream);
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_all_gather(const void* const* in, void* const* out, int P, size_t m, int dtype, int mode,
-                             hipStream_t stream) {
+                             bool src_cached, hipStream_t stream) {
     const size_t es = dtype_size(dtype);
     if ((m * es) % 16 != 0) {
         Ptrs<64> p = make_ptrs<64>(in, out, P, P);
@@ -836,7 +879,7 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
     const int vpt = 1;
-    const int nt = pick_threads(s.mv * P);
+    const int nt = pick_threads(s.mv, P);
     const int64_t cv = static_cast<int64_t>(nt) * vpt;
     s.wcs = (s.mv + cv - 1) / cv;
     // Split destinations when there are few chunks, so that more workgroups
@@ -848,10 +891,19 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     const int64_t G = cap_grid(place_grid(pl));
     if (P <= 8) {
         Ptrs<8> p = make_ptrs<8>(in, out, P, P);
-        hipLaunchKernelGGL((k_all_gather<8, 1>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
+        if (src_cached)
+            hipLaunchKernelGGL((k_all_gather<8, 1, true>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
+        else
+            hipLaunchKernelGGL((k_all_gather<8, 1, false>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s,
+                               pl);
     } else {
         Ptrs<64> p = make_ptrs<64>(in, out, P, P);
-        hipLaunchKernelGGL((k_all_gather<64, 1>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
+        if (src_cached)
+            hipLaunchKernelGGL((k_all_gather<64, 1, true>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s,
+                               pl);
+        else
+            hipLaunchKernelGGL((k_all_gather<64, 1, false>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s,
+                               pl);
     }
     return hipGetLastError();
 }

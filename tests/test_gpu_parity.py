@@ -155,6 +155,27 @@ def test_ar_ragged(nuna, P, dtype):
                     assert_bitwise(got[d], ref[d], f"P={P} n={n} {dtype} {algo} {place} rank {d}")
 
 
+@pytest.mark.parametrize("P", [2, 4, 8, 16])
+def test_ar_large_ragged(nuna, P):
+    """Messages of 4-16 MiB per rank use several vectors per thread; ragged sizes end in a partial
+    chunk and a scalar tail.  Also under a workgroup cap (persistent loop)."""
+    for n, seed in ((2 ** 21 + 8 * 3 + 5, 1), (2 ** 23 + 8 * 1000 + 3, 2)):
+        if P == 16 and n > 2 ** 22:
+            continue
+        x = wl.normal_bf16(P, n, 900 + P + seed)
+        ref = oracle.allreduce(x)
+        try:
+            for cap in (0, 100):
+                nuna.set_max_workgroups(cap)
+                for algo in ("one_shot", "two_shot"):
+                    for place in PLACES:
+                        got = run_allreduce(nuna, x, algo, place, guard=True)
+                        for d in range(P):
+                            assert_bitwise(got[d], ref[d], f"P={P} n={n} cap={cap} {algo} {place} rank {d}")
+        finally:
+            nuna.set_max_workgroups(0)
+
+
 @pytest.mark.parametrize("algo", AR_ALGOS)
 def test_ar_in_place(nuna, algo):
     for P, n, dtype in [(8, 8192 * 4, "bf16"), (8, 4097, "f32"), (64, 8192, "bf16"), (3, 999, "bf16")]:
