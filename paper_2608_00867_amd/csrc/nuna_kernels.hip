@@ -716,9 +716,15 @@ void launch_rs_p(const void* const* in, void* const* out, int P, const RsShape& 
         case 4: launch_rs_t<4, 4, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
         case 8: launch_rs_t<8, 8, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
         case 16: launch_rs_t<16, 16, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
-        case 32: launch_rs_t<32, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
-        case 64: launch_rs_t<64, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
-        default: launch_rs_t<0, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st); break;
+        default:
+            if constexpr (VPT == 1) {
+                if (P == 32) launch_rs_t<32, 64, DT, 1, KEEP>(in, out, P, s, pl, G, nt, st);
+                else if (P == 64) launch_rs_t<64, 64, DT, 1, KEEP>(in, out, P, s, pl, G, nt, st);
+                else launch_rs_t<0, 64, DT, 1, KEEP>(in, out, P, s, pl, G, nt, st);
+            } else {
+                launch_rs_t<0, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st);  // not reached: pick_vpt gives 1
+            }
+            break;
     }
 }
 
@@ -744,12 +750,15 @@ int largest_divisor_upto(int P, int cap) {
 
 // Workgroup size: one-wavefront workgroups spread small messages, and the
 // long per-thread rank loops of many-rank reductions, over more compute
-// units; 256-thread workgroups stream large few-rank messages.
+// units; 256-thread workgroups stream large few-rank messages, except at
+// 4 MiB per rank where 128 threads with 4 vectors each measured best.
 int pick_threads(int64_t vectors_per_rank, int P) {
     const int forced = tuning().wg_threads;
     if (forced == 64 || forced == 128 || forced == 256) return forced;
     if (P > 16) return 64;
-    return vectors_per_rank < (int64_t(1) << 14) ? 64 : kWG;
+    if (vectors_per_rank < (int64_t(1) << 14)) return 64;
+    if (vectors_per_rank >= (int64_t(1) << 18) && vectors_per_rank < (int64_t(1) << 20)) return 128;
+    return kWG;
 }
 
 }  // namespace
@@ -845,14 +854,22 @@ hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P,
     RsShape s{};
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
-    const int nt = pick_threads(s.mv, P);
-    const int64_t cv = nt;
+    // Shape by the vectors each input rank holds (P shards of mv vectors).
+    const int nt = pick_threads(s.mv * P, P);
+    const int vpt = dtype == kDtBf16 ? pick_vpt(s.mv * P, P) : 1;
+    const int64_t cv = static_cast<int64_t>(nt) * vpt;
     s.wcs = (s.mv + cv - 1) / cv;
     const Place pl = make_place_uniform(mode, s.wcs * P, 1);
     const int64_t G = cap_grid(place_grid(pl));
     if (dtype == kDtF32) {
         if (keep_output) launch_rs_p<kDtF32, 1, true>(in, out, P, s, pl, G, nt, stream);
         else launch_rs_p<kDtF32, 1, false>(in, out, P, s, pl, G, nt, stream);
+    } else if (vpt == 4) {
+        if (keep_output) launch_rs_p<kDtBf16, 4, true>(in, out, P, s, pl, G, nt, stream);
+        else launch_rs_p<kDtBf16, 4, false>(in, out, P, s, pl, G, nt, stream);
+    } else if (vpt == 2) {
+        if (keep_output) launch_rs_p<kDtBf16, 2, true>(in, out, P, s, pl, G, nt, stream);
+        else launch_rs_p<kDtBf16, 2, false>(in, out, P, s, pl, G, nt, stream);
     } else {
         if (keep_output) launch_rs_p<kDtBf16, 1, true>(in, out, P, s, pl, G, nt, stream);
         else launch_rs_p<kDtBf16, 1, false>(in, out, P, s, pl, G, nt, stream);
@@ -878,8 +895,9 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     AgShape s{};
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
-    const int vpt = 1;
-    const int nt = pick_threads(s.mv, P);
+    // Shape by the vectors each output rank receives (P shards of mv vectors).
+    const int nt = pick_threads(s.mv * P, P);
+    const int vpt = pick_vpt(s.mv * P, P);
     const int64_t cv = static_cast<int64_t>(nt) * vpt;
     s.wcs = (s.mv + cv - 1) / cv;
     // Split destinations when there are few chunks, so that more workgroups
@@ -891,19 +909,28 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     const int64_t G = cap_grid(place_grid(pl));
     if (P <= 8) {
         Ptrs<8> p = make_ptrs<8>(in, out, P, P);
-        if (src_cached)
-            hipLaunchKernelGGL((k_all_gather<8, 1, true>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s, pl);
-        else
-            hipLaunchKernelGGL((k_all_gather<8, 1, false>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s,
-                               pl);
+        const dim3 g(static_cast<unsigned>(G)), b(nt);
+        if (src_cached) {
+            if (vpt == 4) hipLaunchKernelGGL((k_all_gather<8, 4, true>), g, b, 0, stream, p, s, pl);
+            else if (vpt == 2) hipLaunchKernelGGL((k_all_gather<8, 2, true>), g, b, 0, stream, p, s, pl);
+            else hipLaunchKernelGGL((k_all_gather<8, 1, true>), g, b, 0, stream, p, s, pl);
+        } else {
+            if (vpt == 4) hipLaunchKernelGGL((k_all_gather<8, 4, false>), g, b, 0, stream, p, s, pl);
+            else if (vpt == 2) hipLaunchKernelGGL((k_all_gather<8, 2, false>), g, b, 0, stream, p, s, pl);
+            else hipLaunchKernelGGL((k_all_gather<8, 1, false>), g, b, 0, stream, p, s, pl);
+        }
     } else {
         Ptrs<64> p = make_ptrs<64>(in, out, P, P);
-        if (src_cached)
-            hipLaunchKernelGGL((k_all_gather<64, 1, true>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s,
-                               pl);
-        else
-            hipLaunchKernelGGL((k_all_gather<64, 1, false>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, stream, p, s,
-                               pl);
+        const dim3 g(static_cast<unsigned>(G)), b(nt);
+        if (src_cached) {
+            if (vpt == 4) hipLaunchKernelGGL((k_all_gather<64, 4, true>), g, b, 0, stream, p, s, pl);
+            else if (vpt == 2) hipLaunchKernelGGL((k_all_gather<64, 2, true>), g, b, 0, stream, p, s, pl);
+            else hipLaunchKernelGGL((k_all_gather<64, 1, true>), g, b, 0, stream, p, s, pl);
+        } else {
+            if (vpt == 4) hipLaunchKernelGGL((k_all_gather<64, 4, false>), g, b, 0, stream, p, s, pl);
+            else if (vpt == 2) hipLaunchKernelGGL((k_all_gather<64, 2, false>), g, b, 0, stream, p, s, pl);
+            else hipLaunchKernelGGL((k_all_gather<64, 1, false>), g, b, 0, stream, p, s, pl);
+        }
     }
     return hipGetLastError();
 }

@@ -234,7 +234,8 @@ def test_ar_persistent_loop(nuna):
 
 @pytest.mark.parametrize("place", PLACES)
 @pytest.mark.parametrize("P,m,dtype", [(8, 65536, "bf16"), (8, 1000, "bf16"), (8, 3, "f32"), (2, 4096, "f32"),
-                                       (5, 777, "bf16"), (64, 2048, "bf16"), (1, 100, "f32"), (8, 4096 * 64, "bf16")])
+                                       (5, 777, "bf16"), (64, 2048, "bf16"), (1, 100, "f32"), (8, 4096 * 64, "bf16"),
+                                       (8, 2 ** 17 + 1024 + 8, "bf16"), (4, 2 ** 18 + 8, "bf16")])
 def test_reduce_scatter(nuna, P, m, dtype, place):
     x = wl.normal_bf16(P, P * m, 3 * m + P) if dtype == "bf16" else wl.normal_f32(P, P * m, 3 * m + P)
     ref = oracle.reduce_scatter(x)
@@ -262,7 +263,8 @@ def test_reduce_scatter(nuna, P, m, dtype, place):
 
 @pytest.mark.parametrize("place", PLACES)
 @pytest.mark.parametrize("P,m,dtype", [(8, 65536, "bf16"), (8, 1000, "bf16"), (8, 3, "f32"), (3, 4096, "f32"),
-                                       (64, 512, "bf16"), (1, 64, "bf16"), (8, 4096 * 64, "bf16")])
+                                       (64, 512, "bf16"), (1, 64, "bf16"), (8, 4096 * 64, "bf16"),
+                                       (8, 2 ** 17 + 1024 + 8, "bf16")])
 def test_all_gather(nuna, P, m, dtype, place):
     x = wl.random_bits(P, m, np.uint16 if dtype == "bf16" else np.float32, 5 * m + P)
     ref = oracle.all_gather(x)
