@@ -222,6 +222,23 @@ nuna_status_t nuna_placement_grid(nuna_placement_t place, int64_t groups, int64_
 nuna_status_t nuna_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
 
 /*
+ * Load-latency probe: the one-GPU counterpart of the paper's measurement of
+ * how remote-access latency varies with the CU and the target address
+ * (Sec. 3.2).  A single lane on XCD `xcd` walks the nbytes / stride blocks
+ * of `buf` (device memory) in order; for block i it first loads another
+ * 128-byte line of the block (warming the address translation), then times
+ * one load of the word at i*stride + line_offset.  cycles[i] (device
+ * uint32 array, nbytes / stride entries) receives that latency in shader
+ * clock cycles.  The loads should be cold: the caller evicts the caches
+ * beforehand (for instance by streaming over more than the 256 MB Infinity
+ * Cache).  Runs serially, about half a microsecond per block.  Requires
+ * 4-byte aligned buf and cycles, stride and line_offset multiples of 4,
+ * line_offset + 4 <= stride.
+ */
+nuna_status_t nuna_probe_load_latency(const void* buf, size_t nbytes, size_t stride, size_t line_offset, int xcd,
+                                      uint32_t* cycles, hipStream_t stream);
+
+/*
  * Plain device copy of `bytes` bytes (16-byte aligned pointers, no overlap):
  * the reference streaming kernel used to calibrate memory-traffic counters
  * and the copy-bandwidth ceiling.

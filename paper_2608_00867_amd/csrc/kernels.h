@@ -56,4 +56,8 @@ hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t str
 
 hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
 
+// Serial load-latency probe from XCD `xcd` (warm_off < 0: no translation warm-up).
+hipError_t launch_probe_latency(const void* buf, int64_t nblocks, int64_t stride, int64_t line_off, int64_t warm_off,
+                                int xcd, uint32_t* cycles, hipStream_t stream);
+
 }  // namespace nuna

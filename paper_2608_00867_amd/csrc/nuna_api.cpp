@@ -485,6 +485,26 @@ nuna_status_t nuna_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t st
     return hip_status(nuna::launch_probe_xcc(G, xcc, hw_id, stream), "probe launch");
 }
 
+nuna_status_t nuna_probe_load_latency(const void* buf, size_t nbytes, size_t stride, size_t line_offset, int xcd,
+                                      uint32_t* cycles, hipStream_t stream) {
+    if (!buf || !cycles) return fail(NUNA_ERR_INVALID_ARG, "NULL pointer");
+    if ((reinterpret_cast<uintptr_t>(buf) & 3u) || (reinterpret_cast<uintptr_t>(cycles) & 3u))
+        return fail(NUNA_ERR_MISALIGNED, "probe buffers must be 4-byte aligned");
+    if (stride < 4 || stride % 4 || line_offset % 4 || line_offset + 4 > stride)
+        return fail(NUNA_ERR_INVALID_ARG, "need stride >= 4, stride and line_offset multiples of 4, line_offset + 4 <= stride");
+    if (xcd < 0 || xcd >= NUNA_NUM_XCD) return fail(NUNA_ERR_INVALID_ARG, "xcd %d outside [0, %d)", xcd, NUNA_NUM_XCD);
+    if (nbytes > kMaxBytes) return fail(NUNA_ERR_INVALID_ARG, "nbytes too large");
+    const int64_t nblocks = static_cast<int64_t>(nbytes / stride);
+    if (nblocks < 1) return fail(NUNA_ERR_INVALID_ARG, "buffer holds no whole block");
+    // Warm-up line: the 128-byte line half a block away from the probed one,
+    // when the block is large enough for the two to be different lines.
+    int64_t warm = -1;
+    if (stride >= 256) warm = static_cast<int64_t>(((line_offset / 128 + stride / 256) * 128) % stride);
+    return hip_status(nuna::launch_probe_latency(buf, nblocks, static_cast<int64_t>(stride),
+                                                 static_cast<int64_t>(line_offset), warm, xcd, cycles, stream),
+                      "latency probe launch");
+}
+
 nuna_status_t nuna_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
     if (!dst || !src) return fail(NUNA_ERR_INVALID_ARG, "NULL pointer");
     if (!aligned16(dst) || !aligned16(src)) return fail(NUNA_ERR_MISALIGNED, "copy pointers must be 16-byte aligned");

@@ -59,6 +59,8 @@ SIGNATURES = {
     "nuna_placement_grid": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, _i64p], ctypes.c_int),
     "nuna_probe_xcc": ([ctypes.c_int, _vp, _vp, _vp], ctypes.c_int),
     "nuna_copy": ([_vp, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
+    "nuna_probe_load_latency": ([_vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, _vp, _vp],
+                                ctypes.c_int),
 }
 
 _lib = None
@@ -308,3 +310,32 @@ def copy(dst, src, stream=None):
         raise ValueError("dst too small")
     _check(lib().nuna_copy(dst.data_ptr(), src.data_ptr(), nbytes, _stream(stream)))
     return dst
+
+
+def probe_load_latency(buf, stride, line_offset, xcd, stream=None):
+    """Cold-load latency (shader cycles) of each stride-sized block of `buf` (a CUDA tensor) seen from
+    XCD `xcd`.  The caller evicts the caches first.  Returns an int64 CPU tensor."""
+    torch = _torch()
+    nbytes = buf.numel() * buf.element_size()
+    cyc = torch.zeros(nbytes // stride, dtype=torch.int32, device=buf.device)
+    _check(lib().nuna_probe_load_latency(buf.data_ptr(), nbytes, stride, line_offset, xcd, cyc.data_ptr(),
+                                         _stream(stream)))
+    torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+    return cyc.cpu().to(torch.int64)
+
+
+def memory_affinity(buf, stride=8192, line_offset=256, xcds=(0, 4), evict_bytes=1 << 30):
+    """Near XCD group of each block of `buf`: probe it cold from one XCD of each group and return
+    (latencies [len(xcds), nblocks] int64, near index per block).  Eviction between passes streams
+    `evict_bytes` through a scratch tensor (plumbing on the host side of the call)."""
+    torch = _torch()
+    ev = torch.empty(evict_bytes // 4, dtype=torch.int32, device=buf.device)
+    lats = []
+    for j, x in enumerate(xcds):
+        ev.fill_(j)
+        torch.cuda.synchronize()
+        lats.append(probe_load_latency(buf, stride, line_offset, x))
+    del ev
+    lat = torch.stack(lats)
+    return lat, lat.argmin(dim=0)
+
