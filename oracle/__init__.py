@@ -20,6 +20,9 @@ path):
 * all-gather:     out[d][r*m + j] = in[r][j]   (byte copy)
 * all-to-all:     recv[d] = rows send[s][t] with d among the owner ranks of
                   token (s, t)'s top-k experts, ordered by (s, t) ascending.
+* combine:        out[s][t] = narrow(sum over destination ranks d ascending of
+                  y[d][j(s, t, d)]), the reverse of the dispatch (MoE result
+                  collection).
 """
 import ctypes
 import os
@@ -62,6 +65,8 @@ class Oracle:
         lib.oracle_a2a_map.restype = ctypes.c_int64
         lib.oracle_all_to_all.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_size_t,
                                                                 _c_vpp, _c_vpp]
+        lib.oracle_a2a_combine.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, _c_vpp,
+                                                                 _c_vpp]
         lib.oracle_f32_to_bf16_array.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t]
         lib.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
         lib.oracle_f32_to_bf16.restype = ctypes.c_uint16
@@ -152,6 +157,24 @@ class Oracle:
         assert rc == 0
         return recv
 
+    def combine(self, y, topk, num_experts):
+        """y: list of P arrays [rows_d, row] (one result row per received row); returns list of P
+        arrays [T, row] with each token's results summed over its destination ranks (ascending)."""
+        topk = np.ascontiguousarray(topk, dtype=np.int32)
+        P, T, k = topk.shape
+        if len(y) != P:
+            raise ValueError("one result buffer per rank")
+        row = y[0].shape[1]
+        for a in y:
+            if a.ndim != 2 or a.shape[1] != row or a.dtype != y[0].dtype or not a.flags.c_contiguous:
+                raise ValueError("result buffers must be contiguous [rows, row] of one dtype")
+        dt = _dtype_code(y[0])
+        out = [np.zeros((T, row), dtype=y[0].dtype) for _ in range(P)]
+        ys = [a if a.size else np.zeros((1, row), dtype=a.dtype) for a in y]
+        rc = self.lib.oracle_a2a_combine(P, T, k, num_experts, topk.ctypes.data, row, dt, _ptrs(ys), _ptrs(out))
+        assert rc == 0
+        return out
+
     # -- rounding ---------------------------------------------------------
     def f32_to_bf16(self, x):
         x = np.ascontiguousarray(x, dtype=np.float32)
@@ -199,6 +222,10 @@ def a2a_map(topk, num_experts, d):
 
 def all_to_all(send, topk, num_experts):
     return get().all_to_all(send, topk, num_experts)
+
+
+def combine(y, topk, num_experts):
+    return get().combine(y, topk, num_experts)
 
 
 def f32_to_bf16(x):

@@ -223,3 +223,48 @@ int oracle_all_to_all(int P, int T, int k, int E, const int32_t* topk, size_t ro
     }
     return 0;
 }
+
+/* ---- all-to-all combine (MoE result collection) ------------------------- */
+
+/* The reverse of the dispatch above: rank d holds one result row y[d][j]
+ * for the j-th row it received.  Token t of source rank s collects the
+ * results of every rank it was sent to:
+ *     out[s][t, :] = narrow(sum over d ascending, d a destination of (s, t),
+ *                           of y[d][j(s, t, d), :])
+ * with the same fp32 accumulation and single rounding as the all-reduce
+ * (the first term starts the sum).  j(s, t, d) is the receive position the
+ * dispatch gave token (s, t) at rank d.  Every token has at least one
+ * destination (k >= 1), so every output row is written. */
+int oracle_a2a_combine(int P, int T, int k, int E, const int32_t* topk, size_t row_elems, int dtype,
+                       const void* const* y, void* const* out)
+{
+    if (P < 1 || T < 0 || k < 1 || E < P || E % P != 0 || (dtype != ORC_F32 && dtype != ORC_BF16)) return 1;
+    int64_t* pos = (int64_t*)malloc(sizeof(int64_t) * (size_t)P * (size_t)(T > 0 ? T : 1) * (size_t)P);
+    int64_t* next = (int64_t*)calloc((size_t)P, sizeof(int64_t));
+    if (!pos || !next) { free(pos); free(next); return 2; }
+    /* receive position of (s, t) at each destination, -1 when not sent there */
+    for (int s = 0; s < P; ++s)
+        for (int t = 0; t < T; ++t)
+            for (int d = 0; d < P; ++d) {
+                size_t idx = ((size_t)s * T + t) * P + d;
+                pos[idx] = orc_token_goes_to(topk, P, T, k, E, s, t, d) ? next[d]++ : -1;
+            }
+    for (int s = 0; s < P; ++s)
+        for (int t = 0; t < T; ++t)
+            for (size_t h = 0; h < row_elems; ++h) {
+                int have = 0;
+                float acc = 0.0f;
+                for (int d = 0; d < P; ++d) {
+                    int64_t j = pos[((size_t)s * T + t) * P + d];
+                    if (j < 0) continue;
+                    float v = orc_load(y[d], dtype, (size_t)j * row_elems + h);
+                    acc = have ? acc + v : v;
+                    have = 1;
+                }
+                orc_store(out[s], dtype, (size_t)t * row_elems + h, acc);
+            }
+    free(pos);
+    free(next);
+    return 0;
+}
+

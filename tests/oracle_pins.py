@@ -405,4 +405,76 @@ def pin_a2a_conservation(orc):
     assert rows.sum() == total
 
 
+# ---------------------------------------------------------------- combine pins
+
+def pin_combine_k1_inverts_dispatch(orc):
+    """With one expert per token, combine(dispatch(x)) returns x bit for bit (one term per token)."""
+    for dt in (np.uint16, np.float32):
+        P, T, E, H = 4, 9, 8, 24
+        topk = wl.moe_routing(P, T, 1, E, 301)
+        x = [a.reshape(T, H) for a in (wl.normal_bf16(P, T * H, 302) if dt == np.uint16 else wl.normal_f32(P, T * H, 302))]
+        back = orc.combine(orc.all_to_all(x, topk, E), topk, E)
+        view = np.uint16 if dt == np.uint16 else np.uint32
+        for s in range(P):
+            assert np.array_equal(back[s].view(view), x[s].view(view)), (dt, s)
+
+
+def pin_combine_identity_experts_count_destinations(orc):
+    """Identity experts on integer rows: each token comes back multiplied by its number of distinct
+    destination ranks (exact: small integers)."""
+    P, T, k, E, H = 8, 40, 8, 256, 16
+    topk = wl.moe_routing(P, T, k, E, 311)
+    ints = [np.random.default_rng(312 + s).integers(-8, 8, size=(T, H), endpoint=True) for s in range(P)]
+    x = [wl.f32_to_bf16_bits(a.astype(np.float32)).reshape(T, H) for a in ints]
+    back = orc.combine(orc.all_to_all(x, topk, E), topk, E)
+    per = E // P
+    for s in range(P):
+        c = np.array([len({int(e) // per for e in topk[s, t]}) for t in range(T)])
+        got = _bf16_to_f32_torch(back[s].ravel()).reshape(T, H)
+        assert np.array_equal(got, (ints[s] * c[:, None]).astype(np.float32)), s
+
+
+def pin_combine_sequential_sum(orc):
+    """Combine equals, per token, numpy's sequential accumulate over its results in ascending
+    destination order (rows located by a brute-force routing enumeration), then torch's rounding.
+    The fp32 case draws results of mixed magnitude so that a different summation order changes
+    the rounded sum."""
+    P, T, k, E, H = 4, 12, 3, 16, 8
+    topk = wl.moe_routing(P, T, k, E, 321)
+    lists = _a2a_brute(topk, E)
+    for dt in ("bf16", "f32"):
+        if dt == "bf16":
+            y = [wl.normal_bf16(1, len(lists[d]) * H, 330 + d)[0].reshape(len(lists[d]), H) for d in range(P)]
+        else:
+            y = []
+            for d in range(P):
+                g = np.random.default_rng(340 + d)
+                v = g.standard_normal((len(lists[d]), H)) * np.exp2(g.integers(-12, 12, size=(len(lists[d]), H)))
+                y.append(v.astype(np.float32))
+        out = orc.combine(y, topk, E)
+        for s in range(P):
+            for t in range(T):
+                dests = [d for d in range(P) if (s, t) in lists[d]]
+                rows = [y[d][lists[d].index((s, t))] for d in dests]
+                if dt == "bf16":
+                    terms = np.stack([_bf16_to_f32_torch(r) for r in rows])
+                    ref = _f32_to_bf16_torch(np.add.accumulate(terms, axis=0, dtype=np.float32)[-1])
+                    assert np.array_equal(out[s][t], ref), (dt, s, t)
+                else:
+                    ref = np.add.accumulate(np.stack(rows), axis=0, dtype=np.float32)[-1]
+                    assert np.array_equal(out[s][t].view(np.uint32), ref.view(np.uint32)), (dt, s, t)
+
+
+def pin_combine_conserves_integer_totals(orc):
+    """Integer results: the grand total over all output rows equals the total over all result rows."""
+    P, T, k, E, H = 8, 30, 8, 256, 4
+    topk = wl.moe_routing(P, T, k, E, 341)
+    rows = orc.a2a_counts(topk, E)
+    ys = [np.random.default_rng(342 + d).integers(-4, 4, size=(int(rows[d]), H), endpoint=True) for d in range(P)]
+    y = [wl.f32_to_bf16_bits(a.astype(np.float32)).reshape(-1, H) for a in ys]
+    out = orc.combine(y, topk, E)
+    tot_out = sum(int(_bf16_to_f32_torch(o.ravel()).astype(np.int64).sum()) for o in out)
+    assert tot_out == sum(int(a.sum()) for a in ys)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

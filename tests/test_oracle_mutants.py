@@ -41,6 +41,12 @@ MUTANTS = {
     "a2a_token_major_order": (
         "int64_t j = 0;\n    for (int s = 0; s < P; ++s)\n        for (int t = 0; t < T; ++t)\n            if (orc_token_goes_to(topk, P, T, k, E, s, t, d)) {\n                src_rank[j] = s;",
         "int64_t j = 0;\n    for (int t = 0; t < T; ++t)\n        for (int s = 0; s < P; ++s)\n            if (orc_token_goes_to(topk, P, T, k, E, s, t, d)) {\n                src_rank[j] = s;"),
+    "combine_descending_ranks": ("for (int d = 0; d < P; ++d) {\n                    int64_t j = pos[",
+                                 "for (int d = P - 1; d >= 0; --d) {\n                    int64_t j = pos["),
+    "combine_drops_last_rank": ("for (int d = 0; d < P; ++d) {\n                    int64_t j = pos[",
+                                "for (int d = 0; d < P - 1; ++d) {\n                    int64_t j = pos["),
+    "combine_wrong_row": ("float v = orc_load(y[d], dtype, (size_t)j * row_elems + h);",
+                          "float v = orc_load(y[d], dtype, (size_t)(j > 0 ? j - 1 : 0) * row_elems + h);"),
     "a2a_row_offset": ("unsigned char* dst = (unsigned char*)recv[d] + (size_t)j * row_bytes;",
                        "unsigned char* dst = (unsigned char*)recv[d] + (size_t)(j > 0 ? j - 1 : 0) * row_bytes;"),
 }
