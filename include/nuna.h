@@ -159,11 +159,13 @@ nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, si
  * nuna_a2a_layout_create: host-only planning, no HIP call.
  *   topk_idx  HOST int32 array [P][tokens_per_rank][topk], read during the
  *             call; every entry in [0, num_experts).
- *   Requires 1 <= P <= 64, tokens_per_rank >= 0, 1 <= topk <= num_experts,
- *   num_experts % P == 0.  *out receives a layout owned by the caller.
+ *   Requires 1 <= P <= 64, tokens_per_rank >= 0, P * tokens_per_rank <=
+ *   INT32_MAX, 1 <= topk <= num_experts, num_experts % P == 0.  *out
+ *   receives a layout owned by the caller.
  * nuna_a2a_layout_upload: copies the layout's descriptor tables to the
  *   current device (allocates device memory; synchronous; not capturable).
- *   A layout must be uploaded before nuna_all_to_all uses it.
+ *   A layout must be uploaded before nuna_all_to_all or
+ *   nuna_all_to_all_combine uses it.
  * nuna_a2a_layout_recv_rows: rows_per_rank[d] = rows rank d receives (HOST
  *   int64 array of P).
  * nuna_a2a_layout_recv_map: for destination d, the source rank and token of
@@ -195,6 +197,30 @@ void nuna_a2a_layout_destroy(nuna_a2a_layout_t* layout);
 nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const nuna_a2a_layout_t* layout,
                               size_t row_elems, size_t recv_capacity_rows, nuna_dtype_t dtype,
                               nuna_placement_t place, hipStream_t stream);
+
+/*
+ * All-to-all combine: the result-collection step of MoE expert parallelism
+ * (Sec. 2.1: the all-to-all that sends tokens to their experts also brings
+ * the expert outputs back).  It reverses a dispatch made with the same
+ * layout: row j of y[d] is the result for the j-th row rank d received, and
+ *   out[s][t, :] = y[d0][j0, :] + y[d1][j1, :] + ...
+ * over the distinct ranks d0 < d1 < ... that token t of rank s was sent to
+ * (j_i its receive row there).  Addition runs in that rank order in fp32,
+ * starting from the first row, with one rounding to dtype at the end (bf16:
+ * round to nearest even; NaN stays NaN).  Every output row is written.
+ *   y[d]    P device pointers, each with room for y_capacity_rows rows of
+ *           row_elems; rows beyond rows_per_rank[d] are not read.
+ *   out[s]  P device pointers, each [tokens_per_rank][row_elems] of dtype.
+ *   The placement argument is accepted for symmetry with the dispatch; a
+ *   combine work item shares no input with any other, so both modes run the
+ *   same map.
+ *   Returns NUNA_ERR_INVALID_ARG if the layout is not uploaded or any
+ *   rows_per_rank[d] exceeds y_capacity_rows.  Result and output buffers
+ *   must not overlap (NUNA_ERR_OVERLAP).  A layout with no tokens is a no-op.
+ */
+nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, const nuna_a2a_layout_t* layout,
+                                      size_t row_elems, size_t y_capacity_rows, nuna_dtype_t dtype,
+                                      nuna_placement_t place, hipStream_t stream);
 
 /*
  * Placement map, host mirror of what the kernels compute (for inspection and

@@ -23,6 +23,7 @@ struct Tuning {
     int vpt = 0;           // bf16 all-reduce vectors per thread per work item (0 = by size)
     int lpr_min_ranks = 16;           // lane-per-rank all-reduce: at least this many ranks ...
     int64_t lpr_max_vectors = 131072;  // ... and at most this many input vectors in total (2 MiB)
+    int combine_vpt = 0;               // combine vectors per thread per pass (0 = default)
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
@@ -51,6 +52,12 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
 hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, const void* desc,
                              int64_t nitems, const int64_t* xcd_start, size_t row_bytes, int esize,
                              int mode, hipStream_t stream);
+
+// MoE combine: out[s][t] = sum over the token's entries (rank d, row j), in
+// list order, of y[d][j].  off: device int64[P*T + 1]; ent: device int32
+// pairs (rank, row).
+hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, const void* off, const void* ent,
+                          size_t row_bytes, int dtype, int mode, hipStream_t stream);
 
 hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
 

@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cstdarg>
+#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -117,6 +118,7 @@ const Tuning& tuning() {
         g_tuning.vpt = env_int("NUNA_VPT", g_tuning.vpt);
         g_tuning.lpr_min_ranks = env_int("NUNA_LPR_MIN_RANKS", g_tuning.lpr_min_ranks);
         g_tuning.lpr_max_vectors = env_int("NUNA_LPR_MAX_VECTORS", static_cast<int>(g_tuning.lpr_max_vectors));
+        g_tuning.combine_vpt = env_int("NUNA_COMBINE_VPT", g_tuning.combine_vpt);
     });
     return g_tuning;
 }
@@ -277,8 +279,15 @@ struct nuna_a2a_layout {
     std::vector<int32_t> desc_group;  // 4 ints per item, XCD-major: source-row groups dealt round-robin to XCDs
     int64_t xcd_start[NUNA_NUM_XCD + 1] = {};  // per-XCD list offsets into desc_group
     int64_t nitems = 0;
+    // Combine tables: token i = s*T + t owns entries [comb_off[i], comb_off[i+1]),
+    // each a (destination rank, receive row) pair, destinations ascending.
+    std::vector<int64_t> comb_off;
+    std::vector<int32_t> comb_ent;
+    void* dev_base = nullptr;  // one allocation holding every device table
     void* dev_linear = nullptr;
     void* dev_group = nullptr;
+    void* dev_comb_off = nullptr;
+    void* dev_comb_ent = nullptr;
     int device = -1;
 };
 
@@ -295,6 +304,9 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
     if (tokens_per_rank > 0 && !topk_idx) return fail(NUNA_ERR_INVALID_ARG, "topk_idx is NULL");
     const int per = num_experts / P;
     const int64_t ntok = static_cast<int64_t>(P) * tokens_per_rank;
+    // Receive rows and token indices are stored as int32.
+    if (ntok > INT32_MAX)
+        return fail(NUNA_ERR_INVALID_ARG, "P*tokens_per_rank=%lld exceeds %d", static_cast<long long>(ntok), INT32_MAX);
     for (int64_t i = 0; i < ntok * topk; ++i)
         if (topk_idx[i] < 0 || topk_idx[i] >= num_experts)
             return fail(NUNA_ERR_INVALID_ARG, "topk_idx[%lld]=%d outside [0, %d)", static_cast<long long>(i),
@@ -325,12 +337,18 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
     // counter therefore advances in receive order.  A token with at least one
     // destination is a logical group (its copies all read the same source
     // row); group g is dealt to XCD g mod 8 (round-robin over domains).
+    // The same walk lists, per token, the (destination, receive row) pairs
+    // the combine reads back, destinations ascending.
     std::vector<std::vector<int32_t>> per_xcd(NUNA_NUM_XCD);
     std::vector<int64_t> next(P, 0);
     int64_t ngroups = 0;
+    L->comb_off.assign(static_cast<size_t>(ntok) + 1, 0);
+    L->comb_ent.reserve(2 * L->nitems);
     for (int s = 0; s < P; ++s) {
         for (int t = 0; t < tokens_per_rank; ++t) {
-            const uint64_t m = mask[static_cast<size_t>(s) * tokens_per_rank + t];
+            const size_t tok = static_cast<size_t>(s) * tokens_per_rank + t;
+            const uint64_t m = mask[tok];
+            L->comb_off[tok + 1] = L->comb_off[tok] + __builtin_popcountll(m);
             if (!m) continue;
             std::vector<int32_t>& lst = per_xcd[ngroups % NUNA_NUM_XCD];
             ++ngroups;
@@ -343,6 +361,8 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
                 const int32_t q[4] = {s, t, d, static_cast<int32_t>(j)};
                 std::memcpy(&L->desc_linear[4 * pos], q, sizeof q);
                 lst.insert(lst.end(), q, q + 4);
+                L->comb_ent.push_back(d);
+                L->comb_ent.push_back(static_cast<int32_t>(j));
             }
         }
     }
@@ -361,32 +381,42 @@ nuna_status_t nuna_a2a_layout_upload(nuna_a2a_layout_t* L) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_status(e, "hipGetDevice");
-    if (L->dev_linear) {
+    if (L->device >= 0) {
         if (L->device == dev) return ok();
         return fail(NUNA_ERR_INVALID_ARG, "layout already uploaded to device %d (current %d)", L->device, dev);
     }
-    const size_t bytes = static_cast<size_t>(L->nitems) * 16;
-    if (bytes == 0) {
-        L->device = dev;
-        L->dev_linear = L->dev_group = nullptr;
+    if (L->nitems == 0) {  // nothing routed: no tables, every collective on it is a no-op
         L->device = dev;
         return ok();
     }
-    void* a = nullptr;
-    void* b = nullptr;
-    if ((e = hipMalloc(&a, bytes)) != hipSuccess) return hip_status(e, "hipMalloc (a2a descriptors)");
-    if ((e = hipMalloc(&b, bytes)) != hipSuccess) {
-        (void)hipFree(a);
-        return hip_status(e, "hipMalloc (a2a descriptors)");
+    // One allocation: dispatch descriptors (linear, then XCD-major), combine
+    // offsets, combine entries.  Every part starts 16-byte aligned.
+    const size_t n_desc = static_cast<size_t>(L->nitems) * 16;
+    const size_t n_off = (L->comb_off.size() * sizeof(int64_t) + 15) & ~size_t(15);
+    const size_t n_ent = L->comb_ent.size() * sizeof(int32_t);
+    const size_t bytes = 2 * n_desc + n_off + n_ent;
+    void* base = nullptr;
+    if ((e = hipMalloc(&base, bytes)) != hipSuccess) return hip_status(e, "hipMalloc (a2a tables)");
+    char* b = static_cast<char*>(base);
+    const struct {
+        size_t at;
+        const void* src;
+        size_t n;
+    } parts[4] = {{0, L->desc_linear.data(), n_desc},
+                  {n_desc, L->desc_group.data(), n_desc},
+                  {2 * n_desc, L->comb_off.data(), L->comb_off.size() * sizeof(int64_t)},
+                  {2 * n_desc + n_off, L->comb_ent.data(), n_ent}};
+    for (const auto& q : parts) {
+        if ((e = hipMemcpy(b + q.at, q.src, q.n, hipMemcpyHostToDevice)) != hipSuccess) {
+            (void)hipFree(base);
+            return hip_status(e, "hipMemcpy (a2a tables)");
+        }
     }
-    if ((e = hipMemcpy(a, L->desc_linear.data(), bytes, hipMemcpyHostToDevice)) != hipSuccess ||
-        (e = hipMemcpy(b, L->desc_group.data(), bytes, hipMemcpyHostToDevice)) != hipSuccess) {
-        (void)hipFree(a);
-        (void)hipFree(b);
-        return hip_status(e, "hipMemcpy (a2a descriptors)");
-    }
-    L->dev_linear = a;
-    L->dev_group = b;
+    L->dev_base = base;
+    L->dev_linear = b;
+    L->dev_group = b + n_desc;
+    L->dev_comb_off = b + 2 * n_desc;
+    L->dev_comb_ent = b + 2 * n_desc + n_off;
     L->device = dev;
     return ok();
 }
@@ -409,8 +439,7 @@ nuna_status_t nuna_a2a_layout_recv_map(const nuna_a2a_layout_t* L, int d, int32_
 
 void nuna_a2a_layout_destroy(nuna_a2a_layout_t* L) {
     if (!L) return;
-    if (L->dev_linear) (void)hipFree(L->dev_linear);
-    if (L->dev_group) (void)hipFree(L->dev_group);
+    if (L->dev_base) (void)hipFree(L->dev_base);
     delete L;
 }
 
@@ -442,11 +471,45 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
     st = check_overlaps(ss, rs, [](const Span&, const Span&) { return false; });
     if (st) return st;
     if (L->nitems == 0) return ok();
-    if (!L->dev_linear) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
+    if (L->device < 0) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
     const void* desc = place == NUNA_PLACE_XCD ? L->dev_group : L->dev_linear;
     hipError_t e = nuna::launch_all_to_all(send, recv, P, desc, L->nitems, L->xcd_start, row_bytes,
                                            static_cast<int>(es), place, stream);
     return hip_status(e, "all-to-all launch");
+}
+
+nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, const nuna_a2a_layout_t* L,
+                                      size_t row_elems, size_t y_capacity_rows, nuna_dtype_t dtype,
+                                      nuna_placement_t place, hipStream_t stream) {
+    if (!L) return fail(NUNA_ERR_INVALID_ARG, "layout is NULL");
+    const int P = L->P;
+    nuna_status_t st = check_common(P, dtype, place);
+    if (st) return st;
+    if ((st = check_ptr_array(y, P, "y"))) return st;
+    if ((st = check_ptr_array(const_cast<const void* const*>(out), P, "out"))) return st;
+    const size_t es = nuna::dtype_size(dtype);
+    if (row_elems == 0) return fail(NUNA_ERR_INVALID_ARG, "row_elems is 0");
+    if (row_elems > kMaxBytes / es) return fail(NUNA_ERR_INVALID_ARG, "row_elems %zu too large", row_elems);
+    const size_t row_bytes = row_elems * es;
+    for (int d = 0; d < P; ++d)
+        if (static_cast<size_t>(L->rows[d]) > y_capacity_rows)
+            return fail(NUNA_ERR_INVALID_ARG, "rank %d holds %lld result rows, capacity is %zu", d,
+                        static_cast<long long>(L->rows[d]), y_capacity_rows);
+    if (static_cast<size_t>(L->T) > kMaxBytes / row_bytes || y_capacity_rows > kMaxBytes / row_bytes)
+        return fail(NUNA_ERR_INVALID_ARG, "buffer sizes too large");
+    std::vector<Span> ys(P), os(P);
+    for (int r = 0; r < P; ++r) {
+        ys[r] = {reinterpret_cast<uintptr_t>(y[r]), reinterpret_cast<uintptr_t>(y[r]) + row_bytes * y_capacity_rows,
+                 r};
+        os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + row_bytes * L->T, r};
+    }
+    st = check_overlaps(ys, os, [](const Span&, const Span&) { return false; });
+    if (st) return st;
+    if (L->nitems == 0) return ok();
+    if (L->device < 0) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
+    hipError_t e = nuna::launch_combine(y, out, P, L->T, L->dev_comb_off, L->dev_comb_ent, row_bytes,
+                                        static_cast<int>(dtype), place, stream);
+    return hip_status(e, "all-to-all combine launch");
 }
 
 nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G, int64_t groups, int64_t group_size,

@@ -54,6 +54,8 @@ SIGNATURES = {
     "nuna_a2a_layout_destroy": ([_vp], None),
     "nuna_all_to_all": ([_vpp, _vpp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp],
                         ctypes.c_int),
+    "nuna_all_to_all_combine": ([_vpp, _vpp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.c_int,
+                                 _vp], ctypes.c_int),
     "nuna_placement_items": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _i64p,
                               ctypes.c_int64, _i64p], ctypes.c_int),
     "nuna_placement_grid": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, _i64p], ctypes.c_int),
@@ -124,6 +126,12 @@ def all_to_all_raw(send_ptrs, recv_ptrs, layout_handle, row_elems, recv_capacity
     a = _ptr_array(send_ptrs) if send_ptrs is not None else None
     b = _ptr_array(recv_ptrs) if recv_ptrs is not None else None
     return lib().nuna_all_to_all(a, b, layout_handle, row_elems, recv_capacity_rows, dtype, place, stream)
+
+
+def all_to_all_combine_raw(y_ptrs, out_ptrs, layout_handle, row_elems, y_capacity_rows, dtype, place=XCD, stream=0):
+    a = _ptr_array(y_ptrs) if y_ptrs is not None else None
+    b = _ptr_array(out_ptrs) if out_ptrs is not None else None
+    return lib().nuna_all_to_all_combine(a, b, layout_handle, row_elems, y_capacity_rows, dtype, place, stream)
 
 
 def placement_items(place, b, G, groups, group_size):
@@ -293,6 +301,25 @@ def all_to_all(send, recv, layout, placement="xcd", stream=None):
     _check(all_to_all_raw([t.data_ptr() for t in send], [t.data_ptr() for t in recv], layout.handle, row, cap,
                           _dtype_code(send[0]), PLACEMENTS[placement], _stream(stream)))
     return recv
+
+
+def all_to_all_combine(y, out, layout, placement="xcd", stream=None):
+    """out[s][t] = sum over the ranks d that token (s, t) was sent to (ascending) of its result row in y[d]."""
+    P = layout.P
+    if len(y) != P or len(out) != P:
+        raise ValueError("one result and one output buffer per rank")
+    for t in out:
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 2 or t.shape != out[0].shape:
+            raise ValueError("output buffers must be contiguous CUDA tensors [T, row]")
+    row = out[0].shape[1]
+    cap = y[0].shape[0]
+    for t in y:
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 2 or t.shape[1] != row or t.dtype != out[0].dtype:
+            raise ValueError("result buffers must be contiguous CUDA tensors [capacity, row] of the output dtype")
+        cap = min(cap, t.shape[0])
+    _check(all_to_all_combine_raw([t.data_ptr() for t in y], [t.data_ptr() for t in out], layout.handle, row, cap,
+                                  _dtype_code(out[0]), PLACEMENTS[placement], _stream(stream)))
+    return out
 
 
 def probe_xcc(G, stream=None):

@@ -22,6 +22,8 @@ Sec. 5.2):
                     top-8 distinct experts of 256 chosen uniformly, 32 experts
                     per rank.
 * ``ar_bf16_p64``  one-shot all-reduce bf16, P=64, {16..256} KiB per rank.
+* ``a2a_moe`` combine: the same routing, with N(0,1) bf16 result rows in
+                    place of the expert outputs (``result_rows``).
 """
 import numpy as np
 
@@ -106,6 +108,22 @@ def moe_rows(P, T, hidden, seed):
     g = _rng(seed)
     return [f32_to_bf16_bits(g.standard_normal(T * hidden, dtype=np.float32)).reshape(T, hidden)
             for _ in range(P)]
+
+
+def result_rows(rows, hidden, dtype, seed):
+    """One buffer per rank of N(0,1) result rows, rows[d] x hidden (expert outputs to combine).
+    fp32 values are scaled by 2^u, u uniform in [-12, 12], so that the order in which a
+    token's results are added changes the rounded sum."""
+    g = _rng(seed)
+    out = []
+    for r in rows:
+        n = int(r) * hidden
+        if dtype == np.uint16:
+            out.append(f32_to_bf16_bits(g.standard_normal(n, dtype=np.float32)).reshape(int(r), hidden))
+        else:
+            v = g.standard_normal(n) * np.exp2(g.integers(-12, 12, size=n, endpoint=True))
+            out.append(v.astype(np.float32).reshape(int(r), hidden))
+    return out
 
 
 # ---- named workloads ------------------------------------------------------

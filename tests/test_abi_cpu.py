@@ -226,6 +226,52 @@ def test_a2a_requires_upload_and_capacity():
     lay.close()
 
 
+def test_combine_requires_upload_capacity_and_disjoint_buffers():
+    if _gpu_visible():
+        pytest.skip("GPU visible")
+    topk = wl.moe_routing(4, 8, 2, 8, 12)
+    lay = nuna.A2ALayout(topk, 8)
+    rows = lay.recv_rows()
+    y = _bufs(4)
+    out = _bufs(4, base=BASE + (1 << 32))
+    cap = int(rows.max())
+    assert nuna.all_to_all_combine_raw(y, out, lay.handle, 64, cap, nuna.BF16) == nuna.ERR_INVALID_ARG
+    assert "upload" in nuna.last_error()
+    assert nuna.all_to_all_combine_raw(y, out, lay.handle, 64, cap - 1, nuna.BF16) == nuna.ERR_INVALID_ARG
+    assert "capacity" in nuna.last_error()
+    assert nuna.all_to_all_combine_raw(y, out, lay.handle, 0, cap, nuna.BF16) == nuna.ERR_INVALID_ARG
+    assert nuna.all_to_all_combine_raw(y, out, lay.handle, 64, cap, 7) == nuna.ERR_UNSUPPORTED
+    assert nuna.all_to_all_combine_raw(y, out, lay.handle, 64, cap, nuna.BF16, place=5) == nuna.ERR_INVALID_ARG
+    bad = list(y)
+    bad[2] = y[2] + 2
+    assert nuna.all_to_all_combine_raw(bad, out, lay.handle, 64, cap, nuna.BF16) == nuna.ERR_MISALIGNED
+    bad[2] = 0
+    assert nuna.all_to_all_combine_raw(bad, out, lay.handle, 64, cap, nuna.BF16) == nuna.ERR_INVALID_ARG
+    clash = list(out)
+    clash[3] = y[1] + 16
+    assert nuna.all_to_all_combine_raw(y, clash, lay.handle, 64, cap, nuna.BF16) == nuna.ERR_OVERLAP
+    clash = list(out)
+    clash[3] = out[0] + 16
+    assert nuna.all_to_all_combine_raw(y, clash, lay.handle, 64, cap, nuna.BF16) == nuna.ERR_OVERLAP
+    assert nuna.all_to_all_combine_raw(y, out, None, 64, cap, nuna.BF16) == nuna.ERR_INVALID_ARG
+    lay.close()
+
+
+def test_combine_on_empty_layout_is_a_noop():
+    lay = nuna.A2ALayout(np.zeros((4, 0, 2), dtype=np.int32), 8)
+    assert nuna.all_to_all_combine_raw(_bufs(4), _bufs(4, base=BASE + (1 << 32)), lay.handle, 64, 0,
+                                       nuna.BF16) == nuna.OK
+    lay.close()
+
+
+def test_a2a_layout_rejects_more_than_int32_tokens():
+    topk = np.zeros((1, 1, 1), dtype=np.int32)  # not read: the size check comes first
+    h = ctypes.c_void_p()
+    st = nuna.lib().nuna_a2a_layout_create(64, (1 << 31) // 64, 1, 64, topk.ctypes.data, ctypes.byref(h))
+    assert st == nuna.ERR_INVALID_ARG and "exceeds" in nuna.last_error()
+    assert not h.value
+
+
 # ---------------------------------------------------------------- placement map (host mirror)
 
 def _map(place, G, groups, gsize):

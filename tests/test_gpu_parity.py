@@ -6,7 +6,8 @@ relaxation is for NaN results of arithmetic (inf - inf), whose payload IEEE-754
 leaves to the implementation: there only NaN-ness is compared.
 
 Cases: the five workloads at full size (decode / prefill all-reduce, fp32
-integer all-reduce, P=64 all-reduce, MoE all-to-all dispatch), both placement
+integer all-reduce, P=64 all-reduce, MoE all-to-all dispatch) and the MoE
+combine that reverses the dispatch, both placement
 modes, every algorithm, plus ragged and tiny sizes, in-place forms, special
 values, guard bands around every output, persistent-loop launches and HIP
 graph replay.
@@ -335,6 +336,117 @@ def test_a2a_small(nuna, P, T, k, E, H, dtype, place):
     got = _run_a2a(nuna, send, topk, E, place)
     for d in range(P):
         assert_bitwise(got[d], ref[d], f"a2a P={P} T={T} H={H} rank {d}")
+
+
+# ---------------------------------------------------------------- MoE combine (result collection)
+
+def _run_combine(nuna, y_np, topk, E, place, pad=64):
+    """Combine on the GPU.  Result buffers are padded past each rank's rows with NaN rows, so a
+    read of a wrong row shows in the output; outputs have `pad` guard elements on both sides
+    (64 elements keep the output 16-byte aligned)."""
+    P, T = int(topk.shape[0]), int(topk.shape[1])
+    lay = nuna.A2ALayout(topk, E).upload()
+    rows = lay.recv_rows()
+    H = y_np[0].shape[1]
+    tdt = torch.bfloat16 if y_np[0].dtype == np.uint16 else torch.float32
+    ibits = torch.int16 if tdt == torch.bfloat16 else torch.int32
+    nan = 0x7FC1 if tdt == torch.bfloat16 else 0x7FC00001
+    cap = max(int(rows.max()), 1) + 1
+    y = []
+    for d in range(P):
+        buf = torch.empty((cap, H), dtype=tdt, device="cuda")
+        buf.view(ibits).fill_(nan)
+        buf[:int(rows[d])] = to_dev(y_np[d])
+        y.append(buf)
+    out_whole = [torch.empty(T * H + 2 * pad, dtype=tdt, device="cuda") for _ in range(P)]
+    for w in out_whole:
+        w.view(ibits).fill_(0x3C3C)
+    out = [w[pad:pad + T * H].view(T, H) for w in out_whole]
+    nuna.all_to_all_combine(y, out, lay, placement=place)
+    torch.cuda.synchronize()
+    got = []
+    for s in range(P):
+        whole = to_host(out_whole[s])
+        band = np.concatenate([whole[:pad], whole[pad + T * H:]])
+        assert np.all(band.view(np.uint16 if whole.dtype == np.uint16 else np.uint32) == 0x3C3C), \
+            f"rank {s}: write outside its output rows"
+        got.append(whole[pad:pad + T * H].reshape(T, H))
+    lay.close()
+    return got
+
+
+@pytest.mark.parametrize("place", PLACES)
+def test_combine_moe_full(nuna, place):
+    _, topk = wl.a2a_moe()
+    rows = oracle.a2a_counts(topk, wl.MOE_EXPERTS)
+    y = wl.result_rows(rows, wl.HIDDEN_MOE, np.uint16, wl.seed_for(4, 7))
+    ref = oracle.combine(y, topk, wl.MOE_EXPERTS)
+    got = _run_combine(nuna, y, topk, wl.MOE_EXPERTS, place)
+    for s in range(8):
+        assert_bitwise(got[s], ref[s], f"combine rank {s}")
+
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("P,T,k,E,H,dtype", [(2, 5, 2, 4, 24, np.float32), (3, 9, 2, 6, 10, np.uint16),
+                                             (4, 33, 3, 16, 5, np.float32), (16, 32, 4, 64, 64, np.float32),
+                                             (64, 16, 8, 256, 128, np.uint16), (64, 4, 64, 64, 256, np.float32),
+                                             (8, 1, 8, 256, 7168, np.uint16), (8, 3, 8, 256, 7176, np.uint16),
+                                             (1, 9, 1, 4, 256, np.float32), (8, 40, 8, 256, 1000, np.float32)])
+def test_combine_small(nuna, P, T, k, E, H, dtype, place):
+    topk = wl.moe_routing(P, T, k, E, 23 * P + T)
+    y = wl.result_rows(oracle.a2a_counts(topk, E), H, dtype, 29 * P + T)
+    ref = oracle.combine(y, topk, E)
+    got = _run_combine(nuna, y, topk, E, place)
+    for s in range(P):
+        assert_bitwise(got[s], ref[s], f"combine P={P} T={T} k={k} H={H} rank {s}")
+
+
+def test_combine_special_values(nuna):
+    """inf, -inf, NaN payloads, signed zeros and denormals among the results."""
+    P, T, k, E, H = 8, 24, 8, 64, 256
+    topk = wl.moe_routing(P, T, k, E, 31)
+    rows = oracle.a2a_counts(topk, E)
+    for dtype in (np.uint16, np.float32):
+        y = [wl.random_bits(1, int(r) * H, dtype, 37 + d)[0].reshape(int(r), H) for d, r in enumerate(rows)]
+        ref = oracle.combine(y, topk, E)
+        got = _run_combine(nuna, y, topk, E, "xcd")
+        for s in range(P):
+            assert_bitwise_nan_aware(got[s], ref[s], f"combine specials {dtype.__name__} rank {s}")
+
+
+def test_combine_inverts_dispatch(nuna):
+    """With one expert per token, dispatch followed by combine returns every token row unchanged."""
+    P, T, E, H = 8, 64, 64, wl.HIDDEN_MOE
+    topk = wl.moe_routing(P, T, 1, E, 41)
+    send = wl.moe_rows(P, T, H, 43)
+    lay = nuna.A2ALayout(topk, E).upload()
+    cap = int(lay.recv_rows().max())
+    sd = [to_dev(a) for a in send]
+    recv = [torch.empty((cap, H), dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+    back = [torch.empty((T, H), dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+    nuna.all_to_all(sd, recv, lay, placement="xcd")
+    nuna.all_to_all_combine(recv, back, lay, placement="xcd")
+    torch.cuda.synchronize()
+    for s in range(P):
+        assert_bitwise(to_host(back[s]), send[s], f"round trip rank {s}")
+    lay.close()
+
+
+@pytest.mark.parametrize("cap", [1, 5, 13])
+def test_combine_persistent_loop(nuna, cap):
+    """Fewer workgroups than work items: every workgroup loops over its items."""
+    P, T, k, E, H = 8, 20, 8, 256, 1024
+    topk = wl.moe_routing(P, T, k, E, 47)
+    y = wl.result_rows(oracle.a2a_counts(topk, E), H, np.uint16, 53)
+    ref = oracle.combine(y, topk, E)
+    nuna.set_max_workgroups(cap)
+    try:
+        for place in PLACES:
+            got = _run_combine(nuna, y, topk, E, place)
+            for s in range(P):
+                assert_bitwise(got[s], ref[s], f"combine cap={cap} {place} rank {s}")
+    finally:
+        nuna.set_max_workgroups(0)
 
 
 # ---------------------------------------------------------------- graph capture and replay
