@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--reps", type=int, default=15, help="timed replays per size in the sweeps")
     ap.add_argument("--full", action="store_true", help="sweep every workload and write JSONL")
     ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"))
+    ap.add_argument("--only", default=None, metavar="PREFIX",
+                    help="with --full: only the workloads whose name starts with PREFIX")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle timing budget (cpu_baseline)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--summarize-trace", metavar="KERNEL_TRACE_CSV", default=None,
@@ -321,7 +323,13 @@ def full_sweep(nuna, torch, pool, args):
         f.flush()
         print(json.dumps(rec), flush=True)
 
-    def ar_case(name, x, algos):
+    def want(name):
+        return args.only is None or name.startswith(args.only)
+
+    def ar_case(name, make, algos):
+        if not want(name):
+            return
+        x = make()
         P, n = len(x), x[0].size
         es = 2 if x[0].dtype == np.uint16 else 4
         for algo in algos:
@@ -336,15 +344,20 @@ def full_sweep(nuna, torch, pool, args):
                       **{f"{p}_frac_hbm": round(res[p]["gbps"] / HBM_PEAK_GBPS, 4) for p in res},
                       "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
 
-    ar_case("ar_f32_int_p8", wl.ar_f32_int(), ["one_shot", "one_shot_split", "two_shot"])
+    ar_case("ar_f32_int_p8", wl.ar_f32_int, ["one_shot", "one_shot_split", "two_shot"])
     for T in wl.DECODE_TOKENS:
-        ar_case(f"ar_bf16_decode_T{T}", wl.ar_bf16_decode(T), ["one_shot", "one_shot_split", "two_shot"])
+        ar_case(f"ar_bf16_decode_T{T}", lambda T=T: wl.ar_bf16_decode(T), ["one_shot", "one_shot_split", "two_shot"])
     for T in wl.PREFILL_TOKENS:
-        ar_case(f"ar_bf16_prefill_T{T}", wl.ar_bf16_prefill(T), ["two_shot", "one_shot"])
+        ar_case(f"ar_bf16_prefill_T{T}", lambda T=T: wl.ar_bf16_prefill(T), ["two_shot", "one_shot"])
     for kib in wl.P64_KIB:
-        ar_case(f"ar_bf16_p64_{kib}KiB", wl.ar_bf16_p64(kib), ["one_shot", "one_shot_split", "two_shot"])
-    a2a_case(nuna, torch, pool, args, emit)
-    copy_case(nuna, torch, pool, args, emit)
+        ar_case(f"ar_bf16_p64_{kib}KiB", lambda kib=kib: wl.ar_bf16_p64(kib), ["one_shot", "one_shot_split",
+                                                                             "two_shot"])
+    if want("a2a_moe_dispatch"):
+        a2a_case(nuna, torch, pool, args, emit)
+    if want("a2a_moe_combine"):
+        combine_case(nuna, torch, pool, args, emit)
+    if want("copy_reference"):
+        copy_case(nuna, torch, pool, args, emit)
     f.close()
 
 
@@ -388,6 +401,59 @@ def a2a_case(nuna, torch, pool, args, emit):
         res = {p: stats(t[p]) for p in t}
         emit({"workload": "a2a_moe_dispatch_bf16_p8", "P": P, "tokens_per_rank": T, "hidden": H,
               "rows_received": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
+              "calls_per_graph": calls, "parity": bool(ok),
+              **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
+              **{f"{p}_gbps": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9, 1) for p in res},
+              **{f"{p}_frac_hbm": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+                 for p in res},
+              "linear_over_xcd_time": round(res["linear"]["median"] / res["xcd"]["median"], 4)})
+        del graphs, sets
+    lay.close()
+
+
+def combine_case(nuna, torch, pool, args, emit):
+    """MoE combine at the dispatch's shape: every received row comes back as a result row and is
+    summed into its token (reads: all result rows; writes: every token row once)."""
+    import oracle
+    from paper_2608_00867_amd import workloads as wl
+    _, topk = wl.a2a_moe()
+    E, H = wl.MOE_EXPERTS, wl.HIDDEN_MOE
+    P, T = int(topk.shape[0]), int(topk.shape[1])
+    lay = nuna.A2ALayout(topk, E).upload()
+    rows = lay.recv_rows()
+    cap = int(rows.max())
+    rb = H * 2
+    alg_bytes = int(rows.sum() * rb + P * T * rb)
+    set_bytes = P * cap * rb + P * T * rb
+    y_np = wl.result_rows(rows, H, np.uint16, wl.seed_for(4, 7))
+    src = [dev_copy_of(torch, a.reshape(-1)) for a in y_np]
+    ref = oracle.combine(y_np, topk, E)
+    for cold in (True, False):
+        nsets = max(1, min(pool.nbytes // (set_bytes + 16 * ALIGN), math.ceil(COLD_SPAN / set_bytes) + 1)) \
+            if cold else 1
+        pool.off = 0
+        sets = []
+        for _ in range(nsets):
+            y = [pool.take(cap * rb).view(torch.bfloat16).view(cap, H) for _ in range(P)]
+            out = [pool.take(T * rb).view(torch.bfloat16).view(T, H) for _ in range(P)]
+            for d in range(P):
+                y[d][:int(rows[d])].view(-1).copy_(src[d])
+            sets.append((y, out))
+        calls = max(4, nsets)
+        ok = True
+        for p in ("linear", "xcd"):
+            nuna.all_to_all_combine(sets[0][0], sets[0][1], lay, placement=p)
+            torch.cuda.synchronize()
+            for d in range(P):
+                g = sets[0][1][d].cpu().view(torch.int16).numpy().view(np.uint16)
+                ok = ok and np.array_equal(g, ref[d])
+        graphs = {p: capture(torch, lambda i, p=p: nuna.all_to_all_combine(sets[i % nsets][0], sets[i % nsets][1],
+                                                                            lay, placement=p), calls)
+                  for p in ("linear", "xcd")}
+        t = time_graphs(torch, graphs, calls, args.reps, args.warmup)
+        res = {p: stats(t[p]) for p in t}
+        emit({"workload": "a2a_moe_combine_bf16_p8", "P": P, "tokens_per_rank": T, "hidden": H,
+              "result_rows": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
               "calls_per_graph": calls, "parity": bool(ok),
               **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
               **{f"{p}_gbps": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9, 1) for p in res},
@@ -443,19 +509,70 @@ def profile_run(nuna, torch, pool, n):
     for _ in range(n):
         nuna.copy(b, a)
     torch.cuda.synchronize()
+    moe = profile_moe(nuna, torch, pool, n)
     print(json.dumps({"profile": {"dominant_launches": n, "dominant_alg_bytes": 2 * 8 * x[0].size * 2,
-                                  "copy_launches": n, "copy_bytes": PROFILE_COPY_BYTES}}), flush=True)
+                                  "copy_launches": n, "copy_bytes": PROFILE_COPY_BYTES, **moe}}), flush=True)
+
+
+def moe_alg_bytes():
+    """Algorithmic bytes of one MoE dispatch and of one combine at the full shape (equal: every
+    received row is read or written once, every token row written or read once)."""
+    import oracle
+    from paper_2608_00867_amd import workloads as wl
+    _, topk = wl.a2a_moe()
+    rows = oracle.a2a_counts(topk, wl.MOE_EXPERTS)
+    rb = wl.HIDDEN_MOE * 2
+    return int(rows.sum() * rb + topk.shape[0] * topk.shape[1] * rb)
+
+
+def profile_moe(nuna, torch, pool, n):
+    """`n` dispatches then `n` combines at the MoE shape (XCD placement), rotating over buffer sets
+    that together exceed the caches."""
+    from paper_2608_00867_amd import workloads as wl
+    send_np, topk = wl.a2a_moe()
+    E, H = wl.MOE_EXPERTS, wl.HIDDEN_MOE
+    P, T = int(topk.shape[0]), int(topk.shape[1])
+    lay = nuna.A2ALayout(topk, E).upload()
+    cap = int(lay.recv_rows().max())
+    rb = H * 2
+    set_bytes = P * T * rb + P * cap * rb
+    nsets = max(1, min(3, pool.nbytes // (set_bytes + 16 * ALIGN)))
+    pool.off = 0
+    sets = []
+    for _ in range(nsets):
+        tok = [pool.take(T * rb).view(torch.bfloat16).view(T, H) for _ in range(P)]
+        rec = [pool.take(cap * rb).view(torch.bfloat16).view(cap, H) for _ in range(P)]
+        for t, a in zip(tok, send_np):
+            t.copy_(dev_copy_of(torch, a))
+        sets.append((tok, rec))
+    torch.cuda.synchronize()
+    for i in range(n):
+        tok, rec = sets[i % nsets]
+        nuna.all_to_all(tok, rec, lay, placement="xcd")
+    torch.cuda.synchronize()
+    for i in range(n):
+        tok, rec = sets[i % nsets]
+        nuna.all_to_all_combine(rec, tok, lay, placement="xcd")
+    torch.cuda.synchronize()
+    lay.close()
+    return {"moe_launches": n, "moe_alg_bytes": moe_alg_bytes()}
 
 
 # ---------------------------------------------------------------------------------------------- rocprofv3 summaries
 
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "dominant_traffic.json")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_00867_amd", "csrc", "nuna_kernels.hip")
+# Sources the dominant kernel is compiled from (its kernel file and the headers it includes).
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_00867_amd", "csrc", f)
+                  for f in ("nuna_kernels.hip", "device_common.h", "placement.h", "kernels.h")]
 
 
 def kernel_source_sha():
     import hashlib
-    return hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        h.update(os.path.basename(path).encode() + b"\0")
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
 
 
 def _short(name):
@@ -514,6 +631,17 @@ def summarize_traffic(fetch_csv, write_csv):
     print(f"| WRITE_SIZE | {statistics.median(w[cpy[0]]):.1f} | {wf:.4f} | {statistics.median(w[dom[0]]):.1f} | "
           f"{write:.0f} |")
     print(f"\nTraffic per launch {fetch + write:.0f} B vs algorithmic {alg} B: ratio {(fetch + write) / alg:.4f}.")
+    moe = [k for k in f if k[0].startswith("k_all_to_all") or k[0].startswith("k_combine")]
+    if moe:
+        malg = moe_alg_bytes()
+        print("\nMoE kernels of the same runs (8 ranks, 512 tokens x 7168 bf16 per rank, top-8 of 256 experts; "
+              f"algorithmic bytes per launch {malg}):\n")
+        print("| kernel | FETCH_SIZE (KiB) | WRITE_SIZE (KiB) | scaled fetch B | scaled write B | traffic / algorithmic |")
+        print("|---|---|---|---|---|---|")
+        for k in sorted(moe):
+            fk, wk = statistics.median(f[k]), statistics.median(w.get(k, [0.0]))
+            fb, wb = fk * ff * 1024, wk * wf * 1024
+            print(f"| `{k[0]}` | {fk:.1f} | {wk:.1f} | {fb:.0f} | {wb:.0f} | {(fb + wb) / malg:.4f} |")
 
 
 def measured_traffic():

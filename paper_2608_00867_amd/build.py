@@ -8,8 +8,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libnuna.so")
 
-SOURCES = [os.path.join(CSRC, "nuna_kernels.hip"), os.path.join(CSRC, "nuna_probe.hip"),
-           os.path.join(CSRC, "nuna_api.cpp")]
+SOURCES = [os.path.join(CSRC, "nuna_kernels.hip"), os.path.join(CSRC, "nuna_moe.hip"),
+           os.path.join(CSRC, "nuna_probe.hip"), os.path.join(CSRC, "nuna_api.cpp")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

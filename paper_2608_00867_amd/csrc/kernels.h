@@ -24,6 +24,7 @@ struct Tuning {
     int lpr_min_ranks = 16;           // lane-per-rank all-reduce: at least this many ranks ...
     int64_t lpr_max_vectors = 131072;  // ... and at most this many input vectors in total (2 MiB)
     int combine_vpt = 0;               // combine vectors per thread per pass (0 = default)
+    int combine_chunks = 0;            // combine column chunks per token (0 = by size)
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).

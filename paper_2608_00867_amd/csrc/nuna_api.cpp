@@ -119,6 +119,7 @@ const Tuning& tuning() {
         g_tuning.lpr_min_ranks = env_int("NUNA_LPR_MIN_RANKS", g_tuning.lpr_min_ranks);
         g_tuning.lpr_max_vectors = env_int("NUNA_LPR_MAX_VECTORS", static_cast<int>(g_tuning.lpr_max_vectors));
         g_tuning.combine_vpt = env_int("NUNA_COMBINE_VPT", g_tuning.combine_vpt);
+        g_tuning.combine_chunks = env_int("NUNA_COMBINE_CHUNKS", g_tuning.combine_chunks);
     });
     return g_tuning;
 }

@@ -1,4 +1,6 @@
-// nuna_kernels.hip -- gfx950 kernels of the collective copy/reduce path.
+// nuna_kernels.hip -- gfx950 kernels of the collective copy/reduce path:
+// all-reduce (one-shot, split, lane-per-rank), reduce-scatter, all-gather,
+// the dispatch probe and the reference copy.
 //
 // Memory-bound streaming kernels: every lane moves 16-byte vectors
 // (global_load/store_dwordx4), so one wavefront instruction touches 1 KiB of
@@ -9,293 +11,10 @@
 // below any compute roof.
 //
 // Workgroup -> work item mapping comes from placement.h (LINEAR / XCD modes).
-#include <hip/hip_runtime.h>
-
-#include <type_traits>
-
-#include "kernels.h"
-#include "placement.h"
+#include "device_common.h"
 
 namespace nuna {
 namespace {
-
-constexpr int kWG = 256;  // 4 wavefronts of 64 lanes
-
-// ---------------------------------------------------------------- numerics
-
-__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
-
-// fp32 -> bf16 round-to-nearest-even.  NaN keeps its sign and upper payload
-// and is made quiet; overflow rounds to infinity.
-__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
-template <int DT>
-struct Arith;
-
-template <>
-struct Arith<kDtF32> {
-    static constexpr int kLanes = 4;
-    static constexpr int kEsize = 4;
-    __device__ static __forceinline__ void init(float (&a)[4], const uint4& v) {
-        a[0] = __uint_as_float(v.x);
-        a[1] = __uint_as_float(v.y);
-        a[2] = __uint_as_float(v.z);
-        a[3] = __uint_as_float(v.w);
-    }
-    __device__ static __forceinline__ void add(float (&a)[4], const uint4& v) {
-        a[0] = a[0] + __uint_as_float(v.x);
-        a[1] = a[1] + __uint_as_float(v.y);
-        a[2] = a[2] + __uint_as_float(v.z);
-        a[3] = a[3] + __uint_as_float(v.w);
-    }
-    __device__ static __forceinline__ uint4 narrow(const float (&a)[4]) {
-        return make_uint4(__float_as_uint(a[0]), __float_as_uint(a[1]), __float_as_uint(a[2]),
-                          __float_as_uint(a[3]));
-    }
-    __device__ static __forceinline__ float load1(const void* p, int64_t i) {
-        return static_cast<const float*>(p)[i];
-    }
-    __device__ static __forceinline__ void store1(void* p, int64_t i, float v) { static_cast<float*>(p)[i] = v; }
-};
-
-template <>
-struct Arith<kDtBf16> {
-    static constexpr int kLanes = 8;
-    static constexpr int kEsize = 2;
-    __device__ static __forceinline__ void init(float (&a)[8], const uint4& v) {
-        a[0] = bf16_lo(v.x);
-        a[1] = bf16_hi(v.x);
-        a[2] = bf16_lo(v.y);
-        a[3] = bf16_hi(v.y);
-        a[4] = bf16_lo(v.z);
-        a[5] = bf16_hi(v.z);
-        a[6] = bf16_lo(v.w);
-        a[7] = bf16_hi(v.w);
-    }
-    __device__ static __forceinline__ void add(float (&a)[8], const uint4& v) {
-        a[0] = a[0] + bf16_lo(v.x);
-        a[1] = a[1] + bf16_hi(v.x);
-        a[2] = a[2] + bf16_lo(v.y);
-        a[3] = a[3] + bf16_hi(v.y);
-        a[4] = a[4] + bf16_lo(v.z);
-        a[5] = a[5] + bf16_hi(v.z);
-        a[6] = a[6] + bf16_lo(v.w);
-        a[7] = a[7] + bf16_hi(v.w);
-    }
-    __device__ static __forceinline__ uint4 narrow(const float (&a)[8]) {
-        return make_uint4(f32_to_bf16(a[0]) | (f32_to_bf16(a[1]) << 16), f32_to_bf16(a[2]) | (f32_to_bf16(a[3]) << 16),
-                          f32_to_bf16(a[4]) | (f32_to_bf16(a[5]) << 16), f32_to_bf16(a[6]) | (f32_to_bf16(a[7]) << 16));
-    }
-    __device__ static __forceinline__ float load1(const void* p, int64_t i) {
-        return bf16_lo(static_cast<const uint16_t*>(p)[i]);
-    }
-    __device__ static __forceinline__ void store1(void* p, int64_t i, float v) {
-        static_cast<uint16_t*>(p)[i] = static_cast<uint16_t>(f32_to_bf16(v));
-    }
-};
-
-// ---------------------------------------------------------------- memory access
-
-// Non-temporal (streaming) 16-byte accesses.  Stores: every output byte is
-// written once and consumed by a later kernel, so the writes stream towards
-// memory instead of piling up as dirty L2 lines that the end-of-kernel
-// release must write back.  Loads: used where a work item is the only reader
-// of its input chunk; work items that re-read a chunk shared by their group
-// use ordinary cached loads so the re-reads hit L2.
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ void store_stream(uint4* p, const uint4& v) {
-    const u32x4_t t = {v.x, v.y, v.z, v.w};
-    __builtin_nontemporal_store(t, reinterpret_cast<u32x4_t*>(p));
-}
-
-template <bool NT>
-__device__ __forceinline__ uint4 load16(const uint4* p) {
-    if constexpr (NT) {
-        const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
-        return make_uint4(t.x, t.y, t.z, t.w);
-    } else {
-        return *p;
-    }
-}
-
-// ---------------------------------------------------------------- kernel arguments
-
-template <int MAXP>
-struct Ptrs {
-    const uint4* in[MAXP];
-    uint4* out[MAXP];
-};
-
-template <int MAXP>
-Ptrs<MAXP> make_ptrs(const void* const* in, void* const* out, int nin, int nout) {
-    Ptrs<MAXP> p{};
-    for (int r = 0; r < nin; ++r) p.in[r] = static_cast<const uint4*>(in[r]);
-    for (int r = 0; r < nout; ++r) p.out[r] = static_cast<uint4*>(out[r]);
-    return p;
-}
-
-// Rank pointer table.  With a handful of ranks the kernels index the
-// kernel-argument pointer array with compile-time offsets, and the pointers
-// arrive in SGPRs with the first scalar loads.  With many ranks, or a rank
-// chosen at run time, each pointer would be a separate scalar load that the
-// dependent vector load must wait for.  Instead every wave loads the table
-// once, lane r holding rank r's input and output pointers (one vector load
-// each), and v_readlane hands any rank's pointer to the wave as a uniform
-// value with no memory round trip.  The table is loaded with all lanes
-// active, at kernel start.
-struct RankTable {
-    uint32_t in_lo, in_hi, out_lo, out_hi;
-};
-
-template <int MAXP>
-__device__ __forceinline__ RankTable load_rank_table(const Ptrs<MAXP>& p, int P) {
-    const int lane = threadIdx.x & 63;
-    RankTable t{0u, 0u, 0u, 0u};
-    (void)P;  // entries past P are null pointers and never used
-    if (lane < MAXP) {
-        const uint64_t a = reinterpret_cast<uint64_t>(p.in[lane]);
-        const uint64_t b = reinterpret_cast<uint64_t>(p.out[lane]);
-        t.in_lo = static_cast<uint32_t>(a);
-        t.in_hi = static_cast<uint32_t>(a >> 32);
-        t.out_lo = static_cast<uint32_t>(b);
-        t.out_hi = static_cast<uint32_t>(b >> 32);
-    }
-    return t;
-}
-
-__device__ __forceinline__ const uint4* rank_in(const RankTable& t, int r) {
-    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.in_lo), r));
-    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.in_hi), r));
-    return reinterpret_cast<const uint4*>((hi << 32) | lo);
-}
-
-__device__ __forceinline__ uint4* rank_out(const RankTable& t, int r) {
-    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.out_lo), r));
-    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.out_hi), r));
-    return reinterpret_cast<uint4*>((hi << 32) | lo);
-}
-
-// Pointer access: compile-time offsets for up to 16 ranks, the table beyond.
-template <int PT>
-constexpr bool use_table() {
-    return PT == 0 || PT > 16;
-}
-
-template <int PT, int MAXP>
-__device__ __forceinline__ const uint4* in_ptr(const Ptrs<MAXP>& p, const RankTable& t, int r) {
-    if constexpr (use_table<PT>())
-        return rank_in(t, r);
-    else
-        return p.in[r];
-}
-
-template <int PT, int MAXP>
-__device__ __forceinline__ uint4* out_ptr(const Ptrs<MAXP>& p, const RankTable& t, int r) {
-    if constexpr (use_table<PT>())
-        return rank_out(t, r);
-    else
-        return p.out[r];
-}
-
-// Ranks loaded per batch: all loads of a batch are issued before its adds.
-// Compile-time rank counts load every rank at once; a run-time count goes in
-// batches of 16.
-template <int PT>
-constexpr int rank_batch() {
-    return PT == 0 ? 16 : PT;
-}
-
-// A thread's vectors within a chunk are v0 + j*nt, j < VPT, where nt is the
-// workgroup size.  FULL: every index is in range (a uniform property of the
-// chunk), so no per-lane guard is emitted.
-template <bool FULL, int VPT, bool NT = false>
-__device__ __forceinline__ void load_vecs(uint4 (&dst)[VPT], const uint4* src, int64_t v0, int nt, int64_t limit) {
-#pragma unroll
-    for (int j = 0; j < VPT; ++j) {
-        if (FULL || v0 + j * nt < limit)
-            dst[j] = load16<NT>(src + v0 + j * nt);
-        else
-            dst[j] = make_uint4(0u, 0u, 0u, 0u);
-    }
-}
-
-template <bool FULL, int VPT, bool NT = true>
-__device__ __forceinline__ void store_vecs(uint4* dst, const uint4 (&y)[VPT], int64_t v0, int nt, int64_t limit) {
-#pragma unroll
-    for (int j = 0; j < VPT; ++j) {
-        if (FULL || v0 + j * nt < limit) {
-            if constexpr (NT)
-                store_stream(dst + v0 + j * nt, y[j]);
-            else
-                dst[v0 + j * nt] = y[j];
-        }
-    }
-}
-
-// acc[j] = sum over ranks r = 0, 1, ..., P-1 (in that order) of
-// in[r][base + v0 + j*nt], for vectors below `limit` (relative to base).
-// Lanes past the limit add zeros and are never stored.
-template <int PT, int DT, int VPT, bool FULL, bool NT, int MAXP>
-__device__ __forceinline__ void reduce_ranks(const Ptrs<MAXP>& p, const RankTable& tab, int P, int64_t base, int64_t v0,
-                                             int nt, int64_t limit, float (&acc)[VPT][Arith<DT>::kLanes]) {
-    using A = Arith<DT>;
-    constexpr int B = rank_batch<PT>();
-    if constexpr (PT > 0) {
-#pragma unroll
-        for (int r0 = 0; r0 < PT; r0 += B) {
-            uint4 buf[B][VPT];
-#pragma unroll
-            for (int q = 0; q < B; ++q)
-                load_vecs<FULL, VPT, NT>(buf[q], in_ptr<PT>(p, tab, r0 + q) + base, v0, nt, limit);
-#pragma unroll
-            for (int q = 0; q < B; ++q)
-#pragma unroll
-                for (int j = 0; j < VPT; ++j) {
-                    if (r0 + q == 0)
-                        A::init(acc[j], buf[q][j]);
-                    else
-                        A::add(acc[j], buf[q][j]);
-                }
-        }
-    } else {
-        // Runtime P: batches of B ranks; the last batch may be partial.
-        for (int r0 = 0; r0 < P; r0 += B) {
-            uint4 buf[B][VPT];
-#pragma unroll
-            for (int q = 0; q < B; ++q)
-                if (r0 + q < P) load_vecs<FULL, VPT, NT>(buf[q], rank_in(tab, r0 + q) + base, v0, nt, limit);
-#pragma unroll
-            for (int q = 0; q < B; ++q)
-                if (r0 + q < P) {
-#pragma unroll
-                    for (int j = 0; j < VPT; ++j) {
-                        if (r0 + q == 0)
-                            A::init(acc[j], buf[q][j]);
-                        else
-                            A::add(acc[j], buf[q][j]);
-                    }
-                }
-        }
-    }
-}
-
-// Split a work item into (group, member): shift when the group size is a
-// power of two, divide otherwise.
-__device__ __forceinline__ void split_item(int64_t w, int32_t gsize, int32_t gshift, int64_t& grp, int& member) {
-    if (gshift >= 0) {
-        grp = w >> gshift;
-        member = static_cast<int>(w & ((int64_t(1) << gshift) - 1));
-    } else {
-        grp = w / gsize;
-        member = static_cast<int>(w - grp * gsize);
-    }
-}
 
 // ---------------------------------------------------------------- all-reduce (one-shot, optional split)
 
@@ -597,144 +316,6 @@ __global__ __launch_bounds__(kWG) void k_all_gather_elem(Ptrs<64> p, int P, int6
     }
 }
 
-// ---------------------------------------------------------------- all-to-all
-
-// One descriptor per row copy, stored in placement order: source rank,
-// source token, destination rank, destination row.
-template <int MAXP, int UNROLL>
-__global__ __launch_bounds__(kWG) void k_all_to_all(Ptrs<MAXP> p, int P, const int4* __restrict__ desc,
-                                                    int64_t rowvec, Place pl) {
-    const int nt = blockDim.x;
-    const RankTable tab = load_rank_table(p, P);
-    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t i = it.first; i < it.end; i += it.stride) {
-        const int4 d = desc[i];
-        const uint4* src = rank_in(tab, d.x) + static_cast<int64_t>(d.y) * rowvec;
-        uint4* dst = rank_out(tab, d.z) + static_cast<int64_t>(d.w) * rowvec;
-        for (int64_t v = threadIdx.x; v < rowvec; v += static_cast<int64_t>(nt) * UNROLL) {
-            uint4 y[UNROLL];
-#pragma unroll
-            for (int u = 0; u < UNROLL; ++u)
-                if (v + u * nt < rowvec) y[u] = src[v + u * nt];
-#pragma unroll
-            for (int u = 0; u < UNROLL; ++u)
-                if (v + u * nt < rowvec) store_stream(dst + v + u * nt, y[u]);
-        }
-    }
-}
-
-// Element path for rows that are not a whole number of 16-byte vectors.
-template <int ES>
-__global__ __launch_bounds__(kWG) void k_all_to_all_elem(Ptrs<64> p, const int4* __restrict__ desc, int64_t rowelems,
-                                                         Place pl) {
-    using E = typename std::conditional<ES == 2, uint16_t, uint32_t>::type;
-    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t i = it.first; i < it.end; i += it.stride) {
-        const int4 d = desc[i];
-        const E* src = reinterpret_cast<const E*>(p.in[d.x]) + static_cast<int64_t>(d.y) * rowelems;
-        E* dst = reinterpret_cast<E*>(p.out[d.z]) + static_cast<int64_t>(d.w) * rowelems;
-        for (int64_t v = threadIdx.x; v < rowelems; v += blockDim.x) dst[v] = src[v];
-    }
-}
-
-// ---------------------------------------------------------------- all-to-all combine
-
-// MoE result collection, the reverse of the dispatch: every token gets back
-// one result row from each distinct rank it was sent to, and the rows are
-// summed.  Work item w is token w >> cshift, column chunk w & (2^cshift - 1)
-// of `cw` vectors; token i = s*T + t writes output row t of rank s.  The
-// token's (rank, row) entries come in ascending rank order; the sum follows
-// that order in fp32 and is rounded once.  Each result row is read by one
-// work item only, so the loads stream past the caches.
-struct CombShape {
-    int64_t rowvec;  // 16-byte vectors per row
-    int64_t cw;      // vectors per column chunk
-    uint32_t T;      // tokens per rank
-    int32_t cshift;  // log2(column chunks per token)
-    int32_t P;
-    int32_t pad;
-};
-
-template <int MAXP, int DT, int VPT>
-__global__ __launch_bounds__(kWG) void k_combine(Ptrs<MAXP> p, const int64_t* __restrict__ off,
-                                                 const int2* __restrict__ ent, CombShape s, Place pl) {
-    using A = Arith<DT>;
-    constexpr int B = 8;  // result rows loaded per batch
-    const int nt = blockDim.x;
-    const RankTable tab = load_rank_table(p, s.P);
-    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    const int64_t cmask = (int64_t(1) << s.cshift) - 1;
-    for (int64_t i = it.first; i < it.end; i += it.stride) {
-        const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
-        const uint32_t tok = static_cast<uint32_t>(w >> s.cshift);
-        const int64_t lo = (w & cmask) * s.cw;
-        const int64_t hi = lo + s.cw < s.rowvec ? lo + s.cw : s.rowvec;
-        const uint32_t src = tok / s.T;
-        const uint32_t t = tok - src * s.T;
-        const int64_t e0 = off[tok];
-        const int c = static_cast<int>(off[tok + 1] - e0);
-        uint4* dst = rank_out(tab, static_cast<int>(src)) + static_cast<int64_t>(t) * s.rowvec;
-        // Uniform trip count (rank pointers come from v_readlane); lanes past
-        // `hi` are masked inside the loads and stores.
-        for (int64_t v0 = lo; v0 < hi; v0 += static_cast<int64_t>(nt) * VPT) {
-            const int64_t v = v0 + threadIdx.x;
-            float acc[VPT][A::kLanes];
-            for (int q0 = 0; q0 < c; q0 += B) {
-                uint4 buf[B][VPT];
-#pragma unroll
-                for (int q = 0; q < B; ++q) {
-                    if (q0 + q < c) {
-                        const int2 e = ent[e0 + q0 + q];
-                        const uint4* row = rank_in(tab, e.x) + static_cast<int64_t>(e.y) * s.rowvec;
-                        load_vecs<false, VPT, true>(buf[q], row, v, nt, hi);
-                    }
-                }
-#pragma unroll
-                for (int q = 0; q < B; ++q) {
-                    if (q0 + q < c) {
-#pragma unroll
-                        for (int j = 0; j < VPT; ++j) {
-                            if (q0 + q == 0)
-                                A::init(acc[j], buf[q][j]);
-                            else
-                                A::add(acc[j], buf[q][j]);
-                        }
-                    }
-                }
-            }
-            uint4 y[VPT];
-#pragma unroll
-            for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
-            store_vecs<false, VPT>(dst, y, v, nt, hi);
-        }
-    }
-}
-
-// Element path for rows that are not a whole number of 16-byte vectors.
-template <int DT>
-__global__ __launch_bounds__(kWG) void k_combine_elem(Ptrs<64> p, const int64_t* __restrict__ off,
-                                                      const int2* __restrict__ ent, int64_t rowelems, uint32_t T,
-                                                      Place pl) {
-    using A = Arith<DT>;
-    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t i = it.first; i < it.end; i += it.stride) {
-        const uint32_t tok = static_cast<uint32_t>(item_at(pl, blockIdx.x, gridDim.x, i));
-        const uint32_t src = tok / T;
-        const int64_t obase = static_cast<int64_t>(tok - src * T) * rowelems;
-        const int64_t e0 = off[tok];
-        const int64_t e1 = off[tok + 1];
-        for (int64_t h = threadIdx.x; h < rowelems; h += blockDim.x) {
-            float acc = 0.0f;
-            for (int64_t e = e0; e < e1; ++e) {
-                const int2 q = ent[e];
-                const float v = A::load1(p.in[q.x], static_cast<int64_t>(q.y) * rowelems + h);
-                acc = e == e0 ? v : acc + v;
-            }
-            A::store1(p.out[src], obase + h, acc);
-        }
-    }
-}
-
 // ---------------------------------------------------------------- probe and copy
 
 __global__ __launch_bounds__(64) void k_probe_xcc(int32_t* xcc, int32_t* hw_id) {
@@ -765,11 +346,6 @@ __global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uin
 }
 
 // ---------------------------------------------------------------- launch helpers
-
-int64_t cap_grid(int64_t wgs) {
-    const int64_t cap = max_workgroups();
-    return wgs < cap ? (wgs > 0 ? wgs : 1) : cap;
-}
 
 template <int PT, int MAXP, int DT, int VPT>
 void launch_ar_t(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G, int nt,
@@ -1029,109 +605,6 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
             else if (vpt == 2) hipLaunchKernelGGL((k_all_gather<64, 2, false>), g, b, 0, stream, p, s, pl);
             else hipLaunchKernelGGL((k_all_gather<64, 1, false>), g, b, 0, stream, p, s, pl);
         }
-    }
-    return hipGetLastError();
-}
-
-hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, const void* desc, int64_t nitems,
-                             const int64_t* xcd_start, size_t row_bytes, int esize, int mode, hipStream_t stream) {
-    const bool vec = row_bytes % 16 == 0;
-    const int64_t rowlen = static_cast<int64_t>(vec ? row_bytes / 16 : row_bytes / esize);
-    Place pl{};
-    pl.mode = mode;
-    pl.gsize = 0;
-    pl.gshift = -1;
-    int64_t want = nitems;
-    if (mode == kPlaceXcd) {
-        int64_t longest = 0;
-        for (int x = 0; x <= kNumXcd; ++x) pl.start[x] = xcd_start[x];
-        for (int x = 0; x < kNumXcd; ++x)
-            longest = xcd_start[x + 1] - xcd_start[x] > longest ? xcd_start[x + 1] - xcd_start[x] : longest;
-        want = kNumXcd * longest;
-    } else {
-        pl.start[kNumXcd] = nitems;
-    }
-    const int64_t G = cap_grid(want);
-    const int4* d = static_cast<const int4*>(desc);
-    if (vec) {
-        if (P <= 8) {
-            Ptrs<8> p = make_ptrs<8>(send, recv, P, P);
-            hipLaunchKernelGGL((k_all_to_all<8, 4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P, d,
-                               rowlen, pl);
-        } else {
-            Ptrs<64> p = make_ptrs<64>(send, recv, P, P);
-            hipLaunchKernelGGL((k_all_to_all<64, 4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P, d,
-                               rowlen, pl);
-        }
-    } else {
-        Ptrs<64> p = make_ptrs<64>(send, recv, P, P);
-        if (esize == 4)
-            hipLaunchKernelGGL((k_all_to_all_elem<4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, d,
-                               rowlen, pl);
-        else
-            hipLaunchKernelGGL((k_all_to_all_elem<2>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, d,
-                               rowlen, pl);
-    }
-    return hipGetLastError();
-}
-
-// Column chunks per token: split rows while the launch has fewer than 2048
-// work items and each chunk still gives every thread of a workgroup at least
-// one vector.
-int pick_combine_shift(int64_t ntok, int64_t rowvec, int nt) {
-    int sh = 0;
-    while ((ntok << (sh + 1)) <= 2048 && (rowvec >> (sh + 1)) >= nt) ++sh;
-    return sh;
-}
-
-template <int MAXP, int DT>
-void launch_combine_t(const void* const* y, void* const* out, int P, const int64_t* off, const int2* ent,
-                      const CombShape& s, const Place& pl, int64_t G, int nt, int vpt, hipStream_t st) {
-    Ptrs<MAXP> p = make_ptrs<MAXP>(y, out, P, P);
-    const dim3 g(static_cast<unsigned>(G)), b(static_cast<unsigned>(nt));
-    if (vpt == 4) hipLaunchKernelGGL((k_combine<MAXP, DT, 4>), g, b, 0, st, p, off, ent, s, pl);
-    else if (vpt == 1) hipLaunchKernelGGL((k_combine<MAXP, DT, 1>), g, b, 0, st, p, off, ent, s, pl);
-    else hipLaunchKernelGGL((k_combine<MAXP, DT, 2>), g, b, 0, st, p, off, ent, s, pl);
-}
-
-hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, const void* off, const void* ent,
-                          size_t row_bytes, int dtype, int mode, hipStream_t stream) {
-    const int64_t ntok = static_cast<int64_t>(P) * T;
-    const int64_t* o = static_cast<const int64_t*>(off);
-    const int2* e = static_cast<const int2*>(ent);
-    if (row_bytes % 16 == 0) {
-        CombShape s{};
-        s.rowvec = static_cast<int64_t>(row_bytes / 16);
-        s.T = static_cast<uint32_t>(T);
-        s.P = P;
-        const int forced = tuning().wg_threads;
-        const int nt = forced == 64 || forced == 128 || forced == 256 ? forced : 256;
-        const int fv = tuning().combine_vpt;
-        const int vpt = fv == 1 || fv == 2 || fv == 4 ? fv : 2;
-        s.cshift = pick_combine_shift(ntok, s.rowvec, nt);
-        s.cw = (s.rowvec + (int64_t(1) << s.cshift) - 1) >> s.cshift;
-        // A work item touches no data another item reads: groups of one.
-        const Place pl = make_place_uniform(mode, ntok << s.cshift, 1);
-        const int64_t G = cap_grid(place_grid(pl));
-        if (P <= 8) {
-            if (dtype == kDtF32) launch_combine_t<8, kDtF32>(y, out, P, o, e, s, pl, G, nt, vpt, stream);
-            else launch_combine_t<8, kDtBf16>(y, out, P, o, e, s, pl, G, nt, vpt, stream);
-        } else {
-            if (dtype == kDtF32) launch_combine_t<64, kDtF32>(y, out, P, o, e, s, pl, G, nt, vpt, stream);
-            else launch_combine_t<64, kDtBf16>(y, out, P, o, e, s, pl, G, nt, vpt, stream);
-        }
-    } else {
-        const Place pl = make_place_uniform(mode, ntok, 1);
-        const int64_t G = cap_grid(ntok);
-        Ptrs<64> p = make_ptrs<64>(y, out, P, P);
-        const int64_t esz = static_cast<int64_t>(dtype_size(dtype));
-        const int64_t rowelems = static_cast<int64_t>(row_bytes) / esz;
-        if (dtype == kDtF32)
-            hipLaunchKernelGGL((k_combine_elem<kDtF32>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, o,
-                               e, rowelems, static_cast<uint32_t>(T), pl);
-        else
-            hipLaunchKernelGGL((k_combine_elem<kDtBf16>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, o,
-                               e, rowelems, static_cast<uint32_t>(T), pl);
     }
     return hipGetLastError();
 }
