@@ -27,7 +27,11 @@
  *                      XCDs and a group's members run concurrently on one
  *                      XCD, sharing its L2 (NAP* -- aware workgroup
  *                      placement, default page placement).  A group of one
- *                      work item is placed as LINEAR places it.
+ *                      work item is placed as LINEAR places it.  Groups
+ *                      stay together only where the members' L2 re-reads
+ *                      are at least a quarter of the group's traffic and,
+ *                      for the split all-reduce, the launch moves more than
+ *                      256 KiB; elsewhere XCD runs the linear map.
  * The mode changes which workgroup computes what, never the result.
  *
  * Buffers and ownership.  All data buffers are device memory owned by the
