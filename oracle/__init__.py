@@ -22,7 +22,8 @@ path):
                   token (s, t)'s top-k experts, ordered by (s, t) ascending.
 * combine:        out[s][t] = narrow(sum over destination ranks d ascending of
                   y[d][j(s, t, d)]), the reverse of the dispatch (MoE result
-                  collection).
+                  collection); optionally each term is first scaled by
+                  weights[s][t][d] (fp32 product, rounded once).
 """
 import ctypes
 import os
@@ -65,8 +66,8 @@ class Oracle:
         lib.oracle_a2a_map.restype = ctypes.c_int64
         lib.oracle_all_to_all.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_size_t,
                                                                 _c_vpp, _c_vpp]
-        lib.oracle_a2a_combine.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, _c_vpp,
-                                                                 _c_vpp]
+        lib.oracle_a2a_combine.argtypes = [ctypes.c_int] * 4 + [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int,
+                                                                 ctypes.c_void_p, _c_vpp, _c_vpp]
         lib.oracle_f32_to_bf16_array.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t]
         lib.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
         lib.oracle_f32_to_bf16.restype = ctypes.c_uint16
@@ -157,11 +158,16 @@ class Oracle:
         assert rc == 0
         return recv
 
-    def combine(self, y, topk, num_experts):
+    def combine(self, y, topk, num_experts, weights=None):
         """y: list of P arrays [rows_d, row] (one result row per received row); returns list of P
-        arrays [T, row] with each token's results summed over its destination ranks (ascending)."""
+        arrays [T, row] with each token's results summed over its destination ranks (ascending).
+        weights: optional float32 [P, T, P]; weights[s, t, d] scales rank d's row for token (s, t)."""
         topk = np.ascontiguousarray(topk, dtype=np.int32)
         P, T, k = topk.shape
+        if weights is not None:
+            weights = np.ascontiguousarray(weights, dtype=np.float32)
+            if weights.shape != (P, T, P):
+                raise ValueError("weights must be [P, T, P]")
         if len(y) != P:
             raise ValueError("one result buffer per rank")
         row = y[0].shape[1]
@@ -171,7 +177,8 @@ class Oracle:
         dt = _dtype_code(y[0])
         out = [np.zeros((T, row), dtype=y[0].dtype) for _ in range(P)]
         ys = [a if a.size else np.zeros((1, row), dtype=a.dtype) for a in y]
-        rc = self.lib.oracle_a2a_combine(P, T, k, num_experts, topk.ctypes.data, row, dt, _ptrs(ys), _ptrs(out))
+        wp = weights.ctypes.data if weights is not None and weights.size else None
+        rc = self.lib.oracle_a2a_combine(P, T, k, num_experts, topk.ctypes.data, row, dt, wp, _ptrs(ys), _ptrs(out))
         assert rc == 0
         return out
 
@@ -224,8 +231,8 @@ def all_to_all(send, topk, num_experts):
     return get().all_to_all(send, topk, num_experts)
 
 
-def combine(y, topk, num_experts):
-    return get().combine(y, topk, num_experts)
+def combine(y, topk, num_experts, weights=None):
+    return get().combine(y, topk, num_experts, weights)
 
 
 def f32_to_bf16(x):

@@ -234,9 +234,15 @@ int oracle_all_to_all(int P, int T, int k, int E, const int32_t* topk, size_t ro
  * with the same fp32 accumulation and single rounding as the all-reduce
  * (the first term starts the sum).  j(s, t, d) is the receive position the
  * dispatch gave token (s, t) at rank d.  Every token has at least one
- * destination (k >= 1), so every output row is written. */
+ * destination (k >= 1), so every output row is written.
+ *
+ * Weighted form (the top-k weighted sum that gives a MoE layer its output):
+ * when `weights` is not NULL it holds P*T*P floats, weights[(s*T + t)*P + d]
+ * scaling the row rank d returns for token (s, t); each term is then the
+ * fp32 product w * y (rounded once) before it joins the sum.  With one
+ * expert per rank (E == P) these are the router's gate weights. */
 int oracle_a2a_combine(int P, int T, int k, int E, const int32_t* topk, size_t row_elems, int dtype,
-                       const void* const* y, void* const* out)
+                       const float* weights, const void* const* y, void* const* out)
 {
     if (P < 1 || T < 0 || k < 1 || E < P || E % P != 0 || (dtype != ORC_F32 && dtype != ORC_BF16)) return 1;
     int64_t* pos = (int64_t*)malloc(sizeof(int64_t) * (size_t)P * (size_t)(T > 0 ? T : 1) * (size_t)P);
@@ -258,6 +264,7 @@ int oracle_a2a_combine(int P, int T, int k, int E, const int32_t* topk, size_t r
                     int64_t j = pos[((size_t)s * T + t) * P + d];
                     if (j < 0) continue;
                     float v = orc_load(y[d], dtype, (size_t)j * row_elems + h);
+                    if (weights) v = weights[((size_t)s * T + t) * P + d] * v;
                     acc = have ? acc + v : v;
                     have = 1;
                 }

@@ -477,4 +477,64 @@ def pin_combine_conserves_integer_totals(orc):
     assert tot_out == sum(int(a.sum()) for a in ys)
 
 
+def pin_combine_unit_weights_change_nothing(orc):
+    """Weights of 1.0 leave every term as it is: the weighted combine equals the unweighted one."""
+    P, T, k, E, H = 8, 20, 8, 64, 24
+    topk = wl.moe_routing(P, T, k, E, 351)
+    rows = orc.a2a_counts(topk, E)
+    for dt in (np.uint16, np.float32):
+        y = wl.result_rows(rows, H, dt, 352)
+        a = orc.combine(y, topk, E)
+        b = orc.combine(y, topk, E, np.ones((P, T, P), dtype=np.float32))
+        for s in range(P):
+            assert np.array_equal(a[s].view(np.uint8), b[s].view(np.uint8)), (dt, s)
+
+
+def pin_combine_power_of_two_weights_scale_exactly(orc):
+    """One expert per token and weights 2^j: each token row comes back multiplied by 2^j exactly
+    (N(0,1) values: no overflow or underflow)."""
+    P, T, E, H = 4, 16, 8, 32
+    topk = wl.moe_routing(P, T, 1, E, 361)
+    x = wl.result_rows(orc.a2a_counts(topk, E), H, np.uint16, 362)
+    g = np.random.default_rng(363)
+    w = np.exp2(g.integers(-4, 4, size=(P, T, P), endpoint=True)).astype(np.float32)
+    out = orc.combine(x, topk, E, w)
+    per = E // P
+    for s in range(P):
+        for t in range(T):
+            d = int(topk[s, t, 0]) // per
+            j = [(ss, tt) for ss in range(P) for tt in range(T) if int(topk[ss, tt, 0]) // per == d].index((s, t))
+            ref = _f32_to_bf16_torch(_bf16_to_f32_torch(x[d][j]) * w[s, t, d])
+            assert np.array_equal(out[s][t], ref), (s, t)
+
+
+def pin_combine_gate_weighted_sum(orc):
+    """One expert per rank (E == P): the combine is the MoE layer's top-k weighted sum.  Per token:
+    fp32 products gate * result, added one by one in ascending expert order (numpy float32 arithmetic,
+    rows located by brute-force enumeration)."""
+    P, T, k, H = 8, 12, 3, 16
+    E = P
+    topk = wl.moe_routing(P, T, k, E, 371)
+    lists = _a2a_brute(topk, E)
+    g = np.random.default_rng(372)
+    gates = g.random((P, T, k)).astype(np.float32)
+    w = np.zeros((P, T, P), dtype=np.float32)
+    for s in range(P):
+        for t in range(T):
+            for q in range(k):
+                w[s, t, int(topk[s, t, q])] = gates[s, t, q]
+    y = []
+    for d in range(P):
+        v = g.standard_normal((len(lists[d]), H)) * np.exp2(g.integers(-12, 12, size=(len(lists[d]), H)))
+        y.append(v.astype(np.float32))
+    out = orc.combine(y, topk, E, w)
+    for s in range(P):
+        for t in range(T):
+            order = sorted(range(k), key=lambda q: int(topk[s, t, q]))
+            terms = [np.float32(gates[s, t, q]) * y[int(topk[s, t, q])][lists[int(topk[s, t, q])].index((s, t))]
+                     for q in order]
+            ref = np.add.accumulate(np.stack(terms).astype(np.float32), axis=0, dtype=np.float32)[-1]
+            assert np.array_equal(out[s][t].view(np.uint32), ref.view(np.uint32)), (s, t)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

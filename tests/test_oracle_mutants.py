@@ -47,6 +47,10 @@ MUTANTS = {
                                 "for (int d = 0; d < P - 1; ++d) {\n                    int64_t j = pos["),
     "combine_wrong_row": ("float v = orc_load(y[d], dtype, (size_t)j * row_elems + h);",
                           "float v = orc_load(y[d], dtype, (size_t)(j > 0 ? j - 1 : 0) * row_elems + h);"),
+    "combine_weight_transposed": ("if (weights) v = weights[((size_t)s * T + t) * P + d] * v;",
+                                  "if (weights) v = weights[((size_t)d * T + t) * P + s] * v;"),
+    "combine_weight_ignored": ("if (weights) v = weights[((size_t)s * T + t) * P + d] * v;",
+                               "if (weights) v = v;"),
     "a2a_row_offset": ("unsigned char* dst = (unsigned char*)recv[d] + (size_t)j * row_bytes;",
                        "unsigned char* dst = (unsigned char*)recv[d] + (size_t)(j > 0 ? j - 1 : 0) * row_bytes;"),
 }
