@@ -212,19 +212,30 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
  * (j_i its receive row there).  Addition runs in that rank order in fp32,
  * starting from the first row, with one rounding to dtype at the end (bf16:
  * round to nearest even; NaN stays NaN).  Every output row is written.
+ * Weighted form: with weights not NULL each term is first scaled,
+ *   out[s][t, :] = w[s][t][d0] * y[d0][j0, :] + w[s][t][d1] * y[d1][j1, :] + ...
+ * each product an fp32 multiply rounded once (no fused multiply-add).  With
+ * one expert per rank (num_experts == P) w holds the router's gate weights
+ * and this is the top-k weighted sum of a MoE layer; with several experts
+ * per rank, ranks usually return their local weighted sums and weights is
+ * NULL.
  *   y[d]    P device pointers, each with room for y_capacity_rows rows of
  *           row_elems; rows beyond rows_per_rank[d] are not read.
  *   out[s]  P device pointers, each [tokens_per_rank][row_elems] of dtype.
+ *   weights NULL, or a device fp32 array [P][tokens_per_rank][P] (source
+ *           rank, token, destination rank), 4-byte aligned; entries for
+ *           ranks a token was not sent to are not read.
  *   The placement argument is accepted for symmetry with the dispatch; a
  *   combine work item shares no input with any other, so both modes run the
  *   same map.
  *   Returns NUNA_ERR_INVALID_ARG if the layout is not uploaded or any
- *   rows_per_rank[d] exceeds y_capacity_rows.  Result and output buffers
- *   must not overlap (NUNA_ERR_OVERLAP).  A layout with no tokens is a no-op.
+ *   rows_per_rank[d] exceeds y_capacity_rows.  Result, weight and output
+ *   buffers must not overlap (NUNA_ERR_OVERLAP).  A layout with no tokens is
+ *   a no-op.
  */
 nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, const nuna_a2a_layout_t* layout,
-                                      size_t row_elems, size_t y_capacity_rows, nuna_dtype_t dtype,
-                                      nuna_placement_t place, hipStream_t stream);
+                                      const float* weights, size_t row_elems, size_t y_capacity_rows,
+                                      nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream);
 
 /*
  * Placement map, host mirror of what the kernels compute (for inspection and

@@ -55,10 +55,11 @@ hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, 
                              int mode, hipStream_t stream);
 
 // MoE combine: out[s][t] = sum over the token's entries (rank d, row j), in
-// list order, of y[d][j].  off: device int64[P*T + 1]; ent: device int32
-// pairs (rank, row).
+// list order, of y[d][j], each scaled by weights[(s*T + t)*P + d] when
+// weights is not null.  off: device int64[P*T + 1]; ent: device int32 pairs
+// (rank, row).
 hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, const void* off, const void* ent,
-                          size_t row_bytes, int dtype, int mode, hipStream_t stream);
+                          const float* weights, size_t row_bytes, int dtype, int mode, hipStream_t stream);
 
 hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
 

@@ -480,8 +480,8 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
 }
 
 nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, const nuna_a2a_layout_t* L,
-                                      size_t row_elems, size_t y_capacity_rows, nuna_dtype_t dtype,
-                                      nuna_placement_t place, hipStream_t stream) {
+                                      const float* weights, size_t row_elems, size_t y_capacity_rows,
+                                      nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream) {
     if (!L) return fail(NUNA_ERR_INVALID_ARG, "layout is NULL");
     const int P = L->P;
     nuna_status_t st = check_common(P, dtype, place);
@@ -498,17 +498,23 @@ nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, co
                         static_cast<long long>(L->rows[d]), y_capacity_rows);
     if (static_cast<size_t>(L->T) > kMaxBytes / row_bytes || y_capacity_rows > kMaxBytes / row_bytes)
         return fail(NUNA_ERR_INVALID_ARG, "buffer sizes too large");
+    if (weights && (reinterpret_cast<uintptr_t>(weights) & 3u) != 0)
+        return fail(NUNA_ERR_MISALIGNED, "weights is not 4-byte aligned");
     std::vector<Span> ys(P), os(P);
     for (int r = 0; r < P; ++r) {
         ys[r] = {reinterpret_cast<uintptr_t>(y[r]), reinterpret_cast<uintptr_t>(y[r]) + row_bytes * y_capacity_rows,
                  r};
         os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + row_bytes * L->T, r};
     }
+    if (weights) {
+        const uintptr_t w0 = reinterpret_cast<uintptr_t>(weights);
+        ys.push_back({w0, w0 + sizeof(float) * static_cast<size_t>(P) * static_cast<size_t>(L->T) * P, -1});
+    }
     st = check_overlaps(ys, os, [](const Span&, const Span&) { return false; });
     if (st) return st;
     if (L->nitems == 0) return ok();
     if (L->device < 0) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
-    hipError_t e = nuna::launch_combine(y, out, P, L->T, L->dev_comb_off, L->dev_comb_ent, row_bytes,
+    hipError_t e = nuna::launch_combine(y, out, P, L->T, L->dev_comb_off, L->dev_comb_ent, weights, row_bytes,
                                         static_cast<int>(dtype), place, stream);
     return hip_status(e, "all-to-all combine launch");
 }

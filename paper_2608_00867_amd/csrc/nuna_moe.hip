@@ -68,9 +68,12 @@ struct CombShape {
     int32_t pad;
 };
 
-template <int MAXP, int DT, int VPT>
+// WT: each term is first scaled by the fp32 weight w[tok * P + rank] (the
+// product is rounded once; no fused multiply-add).
+template <int MAXP, int DT, int VPT, bool WT>
 __global__ __launch_bounds__(kWG) void k_combine(Ptrs<MAXP> p, const int64_t* __restrict__ off,
-                                                 const int2* __restrict__ ent, CombShape s, Place pl) {
+                                                 const int2* __restrict__ ent, const float* __restrict__ wts,
+                                                 CombShape s, Place pl) {
     using A = Arith<DT>;
     constexpr int B = 8;  // result rows loaded per batch
     const int nt = blockDim.x;
@@ -93,12 +96,14 @@ __global__ __launch_bounds__(kWG) void k_combine(Ptrs<MAXP> p, const int64_t* __
             float acc[VPT][A::kLanes];
             for (int q0 = 0; q0 < c; q0 += B) {
                 uint4 buf[B][VPT];
+                float wq[B];
 #pragma unroll
                 for (int q = 0; q < B; ++q) {
                     if (q0 + q < c) {
                         const int2 e = ent[e0 + q0 + q];
                         const uint4* row = rank_in(tab, e.x) + static_cast<int64_t>(e.y) * s.rowvec;
                         load_vecs<false, VPT, true>(buf[q], row, v, nt, hi);
+                        if constexpr (WT) wq[q] = wts[static_cast<int64_t>(tok) * s.P + e.x];
                     }
                 }
 #pragma unroll
@@ -106,10 +111,20 @@ __global__ __launch_bounds__(kWG) void k_combine(Ptrs<MAXP> p, const int64_t* __
                     if (q0 + q < c) {
 #pragma unroll
                         for (int j = 0; j < VPT; ++j) {
-                            if (q0 + q == 0)
-                                A::init(acc[j], buf[q][j]);
-                            else
-                                A::add(acc[j], buf[q][j]);
+                            if constexpr (WT) {
+                                float t[A::kLanes];
+                                A::init(t, buf[q][j]);
+#pragma unroll
+                                for (int l = 0; l < A::kLanes; ++l) {
+                                    const float term = wq[q] * t[l];
+                                    acc[j][l] = q0 + q == 0 ? term : acc[j][l] + term;
+                                }
+                            } else {
+                                if (q0 + q == 0)
+                                    A::init(acc[j], buf[q][j]);
+                                else
+                                    A::add(acc[j], buf[q][j]);
+                            }
                         }
                     }
                 }
@@ -125,8 +140,8 @@ __global__ __launch_bounds__(kWG) void k_combine(Ptrs<MAXP> p, const int64_t* __
 // Element path for rows that are not a whole number of 16-byte vectors.
 template <int DT>
 __global__ __launch_bounds__(kWG) void k_combine_elem(Ptrs<64> p, const int64_t* __restrict__ off,
-                                                      const int2* __restrict__ ent, int64_t rowelems, uint32_t T,
-                                                      Place pl) {
+                                                      const int2* __restrict__ ent, const float* __restrict__ wts,
+                                                      int P, int64_t rowelems, uint32_t T, Place pl) {
     using A = Arith<DT>;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
@@ -139,7 +154,8 @@ __global__ __launch_bounds__(kWG) void k_combine_elem(Ptrs<64> p, const int64_t*
             float acc = 0.0f;
             for (int64_t e = e0; e < e1; ++e) {
                 const int2 q = ent[e];
-                const float v = A::load1(p.in[q.x], static_cast<int64_t>(q.y) * rowelems + h);
+                float v = A::load1(p.in[q.x], static_cast<int64_t>(q.y) * rowelems + h);
+                if (wts) v = wts[static_cast<int64_t>(tok) * P + q.x] * v;
                 acc = e == e0 ? v : acc + v;
             }
             A::store1(p.out[src], obase + h, acc);
@@ -162,14 +178,23 @@ uint32_t pick_combine_chunks(int64_t ntok, int64_t rowvec, int nt) {
     return c;
 }
 
-template <int MAXP, int DT>
+template <int MAXP, int DT, bool WT>
 void launch_combine_t(const void* const* y, void* const* out, int P, const int64_t* off, const int2* ent,
-                      const CombShape& s, const Place& pl, int64_t G, int nt, int vpt, hipStream_t st) {
+                      const float* w, const CombShape& s, const Place& pl, int64_t G, int nt, int vpt,
+                      hipStream_t st) {
     Ptrs<MAXP> p = make_ptrs<MAXP>(y, out, P, P);
     const dim3 g(static_cast<unsigned>(G)), b(static_cast<unsigned>(nt));
-    if (vpt == 4) hipLaunchKernelGGL((k_combine<MAXP, DT, 4>), g, b, 0, st, p, off, ent, s, pl);
-    else if (vpt == 1) hipLaunchKernelGGL((k_combine<MAXP, DT, 1>), g, b, 0, st, p, off, ent, s, pl);
-    else hipLaunchKernelGGL((k_combine<MAXP, DT, 2>), g, b, 0, st, p, off, ent, s, pl);
+    if (vpt == 4) hipLaunchKernelGGL((k_combine<MAXP, DT, 4, WT>), g, b, 0, st, p, off, ent, w, s, pl);
+    else if (vpt == 1) hipLaunchKernelGGL((k_combine<MAXP, DT, 1, WT>), g, b, 0, st, p, off, ent, w, s, pl);
+    else hipLaunchKernelGGL((k_combine<MAXP, DT, 2, WT>), g, b, 0, st, p, off, ent, w, s, pl);
+}
+
+template <int MAXP, int DT>
+void launch_combine_w(const void* const* y, void* const* out, int P, const int64_t* off, const int2* ent,
+                      const float* w, const CombShape& s, const Place& pl, int64_t G, int nt, int vpt,
+                      hipStream_t st) {
+    if (w) launch_combine_t<MAXP, DT, true>(y, out, P, off, ent, w, s, pl, G, nt, vpt, st);
+    else launch_combine_t<MAXP, DT, false>(y, out, P, off, ent, w, s, pl, G, nt, vpt, st);
 }
 
 }  // namespace
@@ -217,7 +242,7 @@ hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, 
 }
 
 hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, const void* off, const void* ent,
-                          size_t row_bytes, int dtype, int mode, hipStream_t stream) {
+                          const float* weights, size_t row_bytes, int dtype, int mode, hipStream_t stream) {
     const int64_t ntok = static_cast<int64_t>(P) * T;
     const int64_t* o = static_cast<const int64_t*>(off);
     const int2* e = static_cast<const int2*>(ent);
@@ -236,11 +261,11 @@ hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, 
         const Place pl = make_place_uniform(mode, ntok * s.chunks, 1);
         const int64_t G = cap_grid(place_grid(pl));
         if (P <= 8) {
-            if (dtype == kDtF32) launch_combine_t<8, kDtF32>(y, out, P, o, e, s, pl, G, nt, vpt, stream);
-            else launch_combine_t<8, kDtBf16>(y, out, P, o, e, s, pl, G, nt, vpt, stream);
+            if (dtype == kDtF32) launch_combine_w<8, kDtF32>(y, out, P, o, e, weights, s, pl, G, nt, vpt, stream);
+            else launch_combine_w<8, kDtBf16>(y, out, P, o, e, weights, s, pl, G, nt, vpt, stream);
         } else {
-            if (dtype == kDtF32) launch_combine_t<64, kDtF32>(y, out, P, o, e, s, pl, G, nt, vpt, stream);
-            else launch_combine_t<64, kDtBf16>(y, out, P, o, e, s, pl, G, nt, vpt, stream);
+            if (dtype == kDtF32) launch_combine_w<64, kDtF32>(y, out, P, o, e, weights, s, pl, G, nt, vpt, stream);
+            else launch_combine_w<64, kDtBf16>(y, out, P, o, e, weights, s, pl, G, nt, vpt, stream);
         }
     } else {
         const Place pl = make_place_uniform(mode, ntok, 1);
@@ -250,10 +275,10 @@ hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, 
         const int64_t rowelems = static_cast<int64_t>(row_bytes) / esz;
         if (dtype == kDtF32)
             hipLaunchKernelGGL((k_combine_elem<kDtF32>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, o,
-                               e, rowelems, static_cast<uint32_t>(T), pl);
+                               e, weights, P, rowelems, static_cast<uint32_t>(T), pl);
         else
             hipLaunchKernelGGL((k_combine_elem<kDtBf16>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, o,
-                               e, rowelems, static_cast<uint32_t>(T), pl);
+                               e, weights, P, rowelems, static_cast<uint32_t>(T), pl);
     }
     return hipGetLastError();
 }

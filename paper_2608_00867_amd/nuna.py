@@ -54,8 +54,8 @@ SIGNATURES = {
     "nuna_a2a_layout_destroy": ([_vp], None),
     "nuna_all_to_all": ([_vpp, _vpp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp],
                         ctypes.c_int),
-    "nuna_all_to_all_combine": ([_vpp, _vpp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.c_int,
-                                 _vp], ctypes.c_int),
+    "nuna_all_to_all_combine": ([_vpp, _vpp, _vp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int,
+                                 ctypes.c_int, _vp], ctypes.c_int),
     "nuna_placement_items": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _i64p,
                               ctypes.c_int64, _i64p], ctypes.c_int),
     "nuna_placement_grid": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, _i64p], ctypes.c_int),
@@ -128,10 +128,12 @@ def all_to_all_raw(send_ptrs, recv_ptrs, layout_handle, row_elems, recv_capacity
     return lib().nuna_all_to_all(a, b, layout_handle, row_elems, recv_capacity_rows, dtype, place, stream)
 
 
-def all_to_all_combine_raw(y_ptrs, out_ptrs, layout_handle, row_elems, y_capacity_rows, dtype, place=XCD, stream=0):
+def all_to_all_combine_raw(y_ptrs, out_ptrs, layout_handle, row_elems, y_capacity_rows, dtype, place=XCD, stream=0,
+                           weights_ptr=None):
     a = _ptr_array(y_ptrs) if y_ptrs is not None else None
     b = _ptr_array(out_ptrs) if out_ptrs is not None else None
-    return lib().nuna_all_to_all_combine(a, b, layout_handle, row_elems, y_capacity_rows, dtype, place, stream)
+    return lib().nuna_all_to_all_combine(a, b, layout_handle, weights_ptr, row_elems, y_capacity_rows, dtype, place,
+                                         stream)
 
 
 def placement_items(place, b, G, groups, group_size):
@@ -303,9 +305,16 @@ def all_to_all(send, recv, layout, placement="xcd", stream=None):
     return recv
 
 
-def all_to_all_combine(y, out, layout, placement="xcd", stream=None):
-    """out[s][t] = sum over the ranks d that token (s, t) was sent to (ascending) of its result row in y[d]."""
+def all_to_all_combine(y, out, layout, placement="xcd", stream=None, weights=None):
+    """out[s][t] = sum over the ranks d that token (s, t) was sent to (ascending) of its result row in y[d],
+    each first scaled by weights[s, t, d] when weights (float32 CUDA tensor [P, T, P]) is given."""
     P = layout.P
+    wp = None
+    if weights is not None:
+        if (not weights.is_cuda or weights.dtype != _torch().float32 or not weights.is_contiguous()
+                or tuple(weights.shape) != (P, layout.T, P)):
+            raise ValueError("weights must be a contiguous float32 CUDA tensor [P, T, P]")
+        wp = weights.data_ptr()
     if len(y) != P or len(out) != P:
         raise ValueError("one result and one output buffer per rank")
     for t in out:
@@ -318,7 +327,7 @@ def all_to_all_combine(y, out, layout, placement="xcd", stream=None):
             raise ValueError("result buffers must be contiguous CUDA tensors [capacity, row] of the output dtype")
         cap = min(cap, t.shape[0])
     _check(all_to_all_combine_raw([t.data_ptr() for t in y], [t.data_ptr() for t in out], layout.handle, row, cap,
-                                  _dtype_code(out[0]), PLACEMENTS[placement], _stream(stream)))
+                                  _dtype_code(out[0]), PLACEMENTS[placement], _stream(stream), wp))
     return out
 
 

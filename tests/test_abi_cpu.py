@@ -254,6 +254,15 @@ def test_combine_requires_upload_capacity_and_disjoint_buffers():
     clash[3] = out[0] + 16
     assert nuna.all_to_all_combine_raw(y, clash, lay.handle, 64, cap, nuna.BF16) == nuna.ERR_OVERLAP
     assert nuna.all_to_all_combine_raw(y, out, None, 64, cap, nuna.BF16) == nuna.ERR_INVALID_ARG
+    w0 = BASE + (2 << 32)
+    assert nuna.all_to_all_combine_raw(y, out, lay.handle, 64, cap, nuna.BF16, weights_ptr=w0 + 2) == \
+        nuna.ERR_MISALIGNED
+    assert "weights" in nuna.last_error()
+    assert nuna.all_to_all_combine_raw(y, out, lay.handle, 64, cap, nuna.BF16, weights_ptr=out[2] + 64) == \
+        nuna.ERR_OVERLAP
+    assert nuna.all_to_all_combine_raw(y, out, lay.handle, 64, cap, nuna.BF16, weights_ptr=w0) == \
+        nuna.ERR_INVALID_ARG  # valid weights: still not uploaded
+    assert "upload" in nuna.last_error()
     lay.close()
 
 

@@ -340,7 +340,7 @@ def test_a2a_small(nuna, P, T, k, E, H, dtype, place):
 
 # ---------------------------------------------------------------- MoE combine (result collection)
 
-def _run_combine(nuna, y_np, topk, E, place, pad=64):
+def _run_combine(nuna, y_np, topk, E, place, pad=64, weights=None):
     """Combine on the GPU.  Result buffers are padded past each rank's rows with NaN rows, so a
     read of a wrong row shows in the output; outputs have `pad` guard elements on both sides
     (64 elements keep the output 16-byte aligned)."""
@@ -362,7 +362,8 @@ def _run_combine(nuna, y_np, topk, E, place, pad=64):
     for w in out_whole:
         w.view(ibits).fill_(0x3C3C)
     out = [w[pad:pad + T * H].view(T, H) for w in out_whole]
-    nuna.all_to_all_combine(y, out, lay, placement=place)
+    w = to_dev(weights) if weights is not None else None
+    nuna.all_to_all_combine(y, out, lay, placement=place, weights=w)
     torch.cuda.synchronize()
     got = []
     for s in range(P):
@@ -399,6 +400,35 @@ def test_combine_small(nuna, P, T, k, E, H, dtype, place):
     got = _run_combine(nuna, y, topk, E, place)
     for s in range(P):
         assert_bitwise(got[s], ref[s], f"combine P={P} T={T} k={k} H={H} rank {s}")
+
+
+def _gate_weights(topk, E, seed):
+    """Dense [P, T, P] weights: with E == P the router's gate of the token's expert on rank d,
+    otherwise any positive weight per destination rank."""
+    P, T, k = topk.shape
+    g = np.random.default_rng(seed)
+    w = np.zeros((P, T, P), dtype=np.float32)
+    per = E // P
+    for s in range(P):
+        for t in range(T):
+            for q in range(k):
+                w[s, t, int(topk[s, t, q]) // per] = np.float32(g.random())
+    return w
+
+
+@pytest.mark.parametrize("place", PLACES)
+@pytest.mark.parametrize("P,T,k,E,H,dtype", [(8, 64, 4, 8, 7168, np.uint16), (8, 64, 4, 8, 7168, np.float32),
+                                             (8, 40, 8, 256, 1000, np.float32), (3, 9, 2, 6, 10, np.uint16),
+                                             (64, 4, 64, 64, 256, np.float32), (64, 16, 8, 256, 128, np.uint16)])
+def test_combine_weighted(nuna, P, T, k, E, H, dtype, place):
+    """Top-k weighted combine: each rank's result row scaled by its weight before the ascending sum."""
+    topk = wl.moe_routing(P, T, k, E, 59 * P + T)
+    y = wl.result_rows(oracle.a2a_counts(topk, E), H, dtype, 61 * P + T)
+    w = _gate_weights(topk, E, 67 * P + T)
+    ref = oracle.combine(y, topk, E, w)
+    got = _run_combine(nuna, y, topk, E, place, weights=w)
+    for s in range(P):
+        assert_bitwise(got[s], ref[s], f"weighted combine P={P} T={T} k={k} E={E} H={H} rank {s}")
 
 
 def test_combine_special_values(nuna):
