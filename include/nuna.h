@@ -238,6 +238,69 @@ nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, co
                                       nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream);
 
 /*
+ * NUNA-aware placement planner: Algorithm 1 of the paper (Sec. 4.2.2,
+ * logical allocation then physical placement), host-only, no HIP call.
+ *
+ * Workload: num_tb threadblocks in the order the plan lists them;
+ * threadblock t touches the chunks chunk_ids[chunk_offsets[t] ..
+ * chunk_offsets[t+1]) (any 64-bit ids; a chunk touched by several
+ * threadblocks appears once per threadblock) and is charged tb_bytes[t]
+ * against the CU and stack budgets.  chunk_pages (same length as chunk_ids,
+ * or NULL) gives each entry's page id; a chunk must carry the same page in
+ * every entry.
+ *
+ * Logical allocation: a threadblock none of whose chunks belongs to a group
+ * starts a new group; otherwise it joins the group it shares the most chunks
+ * with (ties: the group created first), and its unassigned chunks join too.
+ * Groups are then ordered by decreasing number of threadblocks, creation
+ * order among equals.
+ * Physical placement: the i-th group of that order goes to NAR domain
+ * i mod nar_max, which spans the physical domains [n*D/nar_max,
+ * (n+1)*D/nar_max) (D = topo->num_domains; nar_max must divide D).  Each of
+ * its threadblocks takes the first CU of the domain whose remaining budget
+ * covers tb_bytes (none: the first CU with the most budget left), and the
+ * first stack in its physical domain's preference order whose remaining
+ * budget covers them (none: the most preferred stack); both budgets are
+ * charged.  A chunk lives on the stack of the first threadblock placed that
+ * touches it; with pages, a page's stack is fixed by its first chunk.
+ *
+ * Outputs (HOST arrays, caller-owned): tb_group[num_tb] (group index in
+ * creation order), tb_domain[num_tb] (NAR domain), tb_cu[num_tb] (physical
+ * domain * cus_per_domain + CU index), entry_stack[chunk_offsets[num_tb]]
+ * (stack of each entry's chunk), *num_groups.  Any output pointer may be
+ * NULL.  Invalid topology, nar_max, offsets or negative bytes:
+ * NUNA_ERR_INVALID_ARG.
+ *
+ * On MI355X the kernels realise the domain part of the plan (workgroup b runs
+ * on XCD b mod 8); the CU within an XCD is the hardware's choice, and stacks
+ * cannot be chosen per page in NPS1, so tb_cu and entry_stack describe the
+ * plan rather than what the hardware is told.
+ */
+#define NUNA_NAP_MAX_DOMAINS 16
+#define NUNA_NAP_MAX_STACKS 16
+
+typedef struct {
+    int32_t num_domains;    /* physical domains (MI355X: 8 XCDs) */
+    int32_t cus_per_domain; /* CUs per physical domain (MI355X: 32) */
+    int32_t num_stacks;     /* HBM stacks (MI355X: 8) */
+    int32_t reserved;
+    int64_t cu_budget;      /* R_max of a CU, in the units of tb_bytes */
+    int64_t stack_budget;   /* R_max of a stack */
+    int32_t stack_pref[NUNA_NAP_MAX_DOMAINS][NUNA_NAP_MAX_STACKS]; /* per physical domain: all stacks,
+                                                                      most preferred first */
+} nuna_nap_topology_t;
+
+/* MI355X: 8 XCDs x 32 CUs, 8 stacks; XCDs and stacks 0-3 on one I/O die,
+ * 4-7 on the other; XCD x prefers stack x, then its die's other stacks, then
+ * the far die's (index order); CU budget 700 x 128 B, stack budget 1 MiB. */
+nuna_status_t nuna_nap_topology_mi355x(nuna_nap_topology_t* topo);
+
+nuna_status_t nuna_nap_plan(const nuna_nap_topology_t* topo, int nar_max, int64_t num_tb,
+                            const int64_t* chunk_offsets, const int64_t* chunk_ids, const int64_t* tb_bytes,
+                            const int64_t* chunk_pages, int64_t* tb_group, int32_t* tb_domain, int32_t* tb_cu,
+                            int32_t* entry_stack, int64_t* num_groups);
+
+/*
  * Placement map, host mirror of what the kernels compute (for inspection and
  * tests; no HIP call).  A launch over `groups` logical groups of
  * `group_size` work items each (items numbered group-major: item =

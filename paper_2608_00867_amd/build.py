@@ -9,7 +9,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libnuna.so")
 
 SOURCES = [os.path.join(CSRC, "nuna_kernels.hip"), os.path.join(CSRC, "nuna_moe.hip"),
-           os.path.join(CSRC, "nuna_probe.hip"), os.path.join(CSRC, "nuna_api.cpp")]
+           os.path.join(CSRC, "nuna_probe.hip"), os.path.join(CSRC, "nap_planner.cpp"),
+           os.path.join(CSRC, "nuna_api.cpp")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

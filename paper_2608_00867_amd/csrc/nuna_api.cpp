@@ -17,6 +17,7 @@
 #include <vector>
 
 #include "kernels.h"
+#include "nap_planner.h"
 #include "nuna.h"
 #include "placement.h"
 
@@ -335,24 +336,23 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
     L->map_tok.resize(L->nitems);
     L->desc_linear.resize(4 * L->nitems);
     // Pass 2: walk tokens in (source, token) order; each destination's row
-    // counter therefore advances in receive order.  A token with at least one
-    // destination is a logical group (its copies all read the same source
-    // row); group g is dealt to XCD g mod 8 (round-robin over domains).
-    // The same walk lists, per token, the (destination, receive row) pairs
-    // the combine reads back, destinations ascending.
-    std::vector<std::vector<int32_t>> per_xcd(NUNA_NUM_XCD);
+    // counter therefore advances in receive order.  The same walk lists, per
+    // token, the (destination, receive row) pairs the combine reads back,
+    // destinations ascending.
     std::vector<int64_t> next(P, 0);
-    int64_t ngroups = 0;
     L->comb_off.assign(static_cast<size_t>(ntok) + 1, 0);
     L->comb_ent.reserve(2 * L->nitems);
+    // Placement workload for the XCD mode: one threadblock per row copy, in
+    // walk order, touching its source row and its destination row.
+    std::vector<int64_t> tb_off(static_cast<size_t>(L->nitems) + 1, 0);
+    std::vector<int64_t> tb_chunk(2 * static_cast<size_t>(L->nitems));
+    std::vector<int32_t> walk_desc(4 * static_cast<size_t>(L->nitems));
+    int64_t w = 0;
     for (int s = 0; s < P; ++s) {
         for (int t = 0; t < tokens_per_rank; ++t) {
             const size_t tok = static_cast<size_t>(s) * tokens_per_rank + t;
             const uint64_t m = mask[tok];
             L->comb_off[tok + 1] = L->comb_off[tok] + __builtin_popcountll(m);
-            if (!m) continue;
-            std::vector<int32_t>& lst = per_xcd[ngroups % NUNA_NUM_XCD];
-            ++ngroups;
             for (int d = 0; d < P; ++d) {
                 if (!(m >> d & 1u)) continue;
                 const int64_t j = next[d]++;
@@ -361,11 +361,33 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
                 L->map_tok[pos] = t;
                 const int32_t q[4] = {s, t, d, static_cast<int32_t>(j)};
                 std::memcpy(&L->desc_linear[4 * pos], q, sizeof q);
-                lst.insert(lst.end(), q, q + 4);
+                std::memcpy(&walk_desc[4 * static_cast<size_t>(w)], q, sizeof q);
+                tb_chunk[2 * static_cast<size_t>(w)] = static_cast<int64_t>(tok);        // source row
+                tb_chunk[2 * static_cast<size_t>(w) + 1] = ntok + pos;                    // destination row
+                tb_off[static_cast<size_t>(w) + 1] = 2 * (w + 1);
+                ++w;
                 L->comb_ent.push_back(d);
                 L->comb_ent.push_back(static_cast<int32_t>(j));
             }
         }
+    }
+    // XCD assignment from the placement planner (Algorithm 1): the copies of
+    // one token share its source row and form one logical group; groups go to
+    // the 8 XCDs round-robin in decreasing size order, which evens out the
+    // copies per XCD.  Every copy is charged the same, so the budgets never
+    // bind and only the domain choice matters.  The algorithm fixes where a
+    // group runs, not when: each XCD runs its groups in token order, which
+    // keeps its source-row reads in address order (dealing them in size order
+    // measured 4 % slower on MI355X).
+    const std::vector<int64_t> unit(static_cast<size_t>(L->nitems), 1);
+    const nuna::NapPlan plan = nuna::nap_plan(nuna::nap_topology_mi355x(), NUNA_NUM_XCD, L->nitems, tb_off.data(),
+                                              tb_chunk.data(), unit.data(), nullptr);
+    std::vector<std::vector<int32_t>> per_xcd(NUNA_NUM_XCD);
+    for (size_t g = 0; g < plan.groups.size(); ++g) {
+        const std::vector<int64_t>& members = plan.groups[g];
+        std::vector<int32_t>& lst = per_xcd[static_cast<size_t>(plan.tb_domain[static_cast<size_t>(members[0])])];
+        for (int64_t tb : members)
+            lst.insert(lst.end(), &walk_desc[4 * static_cast<size_t>(tb)], &walk_desc[4 * static_cast<size_t>(tb)] + 4);
     }
     L->desc_group.reserve(4 * L->nitems);
     for (int x = 0; x < NUNA_NUM_XCD; ++x) {
@@ -517,6 +539,73 @@ nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, co
     hipError_t e = nuna::launch_combine(y, out, P, L->T, L->dev_comb_off, L->dev_comb_ent, weights, row_bytes,
                                         static_cast<int>(dtype), place, stream);
     return hip_status(e, "all-to-all combine launch");
+}
+
+static_assert(NUNA_NAP_MAX_DOMAINS == nuna::kNapMaxDomains && NUNA_NAP_MAX_STACKS == nuna::kNapMaxStacks,
+              "planner limits");
+
+nuna_status_t nuna_nap_topology_mi355x(nuna_nap_topology_t* topo) {
+    if (!topo) return fail(NUNA_ERR_INVALID_ARG, "topo is NULL");
+    const nuna::NapTopology t = nuna::nap_topology_mi355x();
+    std::memset(topo, 0, sizeof *topo);
+    topo->num_domains = t.domains;
+    topo->cus_per_domain = t.cus_per_domain;
+    topo->num_stacks = t.stacks;
+    topo->cu_budget = t.cu_budget;
+    topo->stack_budget = t.stack_budget;
+    std::memcpy(topo->stack_pref, t.stack_pref, sizeof t.stack_pref);
+    return ok();
+}
+
+nuna_status_t nuna_nap_plan(const nuna_nap_topology_t* topo, int nar_max, int64_t num_tb,
+                            const int64_t* chunk_offsets, const int64_t* chunk_ids, const int64_t* tb_bytes,
+                            const int64_t* chunk_pages, int64_t* tb_group, int32_t* tb_domain, int32_t* tb_cu,
+                            int32_t* entry_stack, int64_t* num_groups) {
+    if (!topo) return fail(NUNA_ERR_INVALID_ARG, "topo is NULL");
+    if (topo->num_domains < 1 || topo->num_domains > NUNA_NAP_MAX_DOMAINS || topo->cus_per_domain < 1 ||
+        topo->cus_per_domain > (1 << 16) || topo->num_stacks < 1 || topo->num_stacks > NUNA_NAP_MAX_STACKS)
+        return fail(NUNA_ERR_INVALID_ARG, "invalid topology (domains %d, CUs per domain %d, stacks %d)",
+                    topo->num_domains, topo->cus_per_domain, topo->num_stacks);
+    for (int d = 0; d < topo->num_domains; ++d) {
+        uint32_t seen = 0;
+        for (int k = 0; k < topo->num_stacks; ++k) {
+            const int s = topo->stack_pref[d][k];
+            if (s < 0 || s >= topo->num_stacks || (seen >> s & 1u))
+                return fail(NUNA_ERR_INVALID_ARG, "stack_pref[%d] is not a permutation of the %d stacks", d,
+                            topo->num_stacks);
+            seen |= 1u << s;
+        }
+    }
+    if (nar_max < 1 || topo->num_domains % nar_max != 0)
+        return fail(NUNA_ERR_INVALID_ARG, "nar_max=%d does not divide the %d domains", nar_max, topo->num_domains);
+    if (num_tb < 0 || num_tb > (int64_t(1) << 40)) return fail(NUNA_ERR_INVALID_ARG, "num_tb=%lld", (long long)num_tb);
+    if (num_tb > 0) {
+        if (!chunk_offsets || !tb_bytes) return fail(NUNA_ERR_INVALID_ARG, "chunk_offsets or tb_bytes is NULL");
+        if (chunk_offsets[0] != 0) return fail(NUNA_ERR_INVALID_ARG, "chunk_offsets[0] != 0");
+        for (int64_t t = 0; t < num_tb; ++t) {
+            if (chunk_offsets[t + 1] < chunk_offsets[t])
+                return fail(NUNA_ERR_INVALID_ARG, "chunk_offsets decrease at %lld", (long long)t);
+            if (tb_bytes[t] < 0) return fail(NUNA_ERR_INVALID_ARG, "tb_bytes[%lld] < 0", (long long)t);
+        }
+        if (chunk_offsets[num_tb] > 0 && !chunk_ids) return fail(NUNA_ERR_INVALID_ARG, "chunk_ids is NULL");
+    }
+    nuna::NapTopology t{};
+    t.domains = topo->num_domains;
+    t.cus_per_domain = topo->cus_per_domain;
+    t.stacks = topo->num_stacks;
+    t.cu_budget = topo->cu_budget;
+    t.stack_budget = topo->stack_budget;
+    std::memcpy(t.stack_pref, topo->stack_pref, sizeof t.stack_pref);
+    const nuna::NapPlan p = nuna::nap_plan(t, nar_max, num_tb, chunk_offsets, chunk_ids, tb_bytes, chunk_pages);
+    for (int64_t i = 0; i < num_tb; ++i) {
+        if (tb_group) tb_group[i] = p.tb_group[static_cast<size_t>(i)];
+        if (tb_domain) tb_domain[i] = p.tb_domain[static_cast<size_t>(i)];
+        if (tb_cu) tb_cu[i] = p.tb_cu[static_cast<size_t>(i)];
+    }
+    if (entry_stack)
+        for (size_t e = 0; e < p.entry_stack.size(); ++e) entry_stack[e] = p.entry_stack[e];
+    if (num_groups) *num_groups = static_cast<int64_t>(p.groups.size());
+    return ok();
 }
 
 nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G, int64_t groups, int64_t group_size,

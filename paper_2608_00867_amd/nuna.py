@@ -35,6 +35,17 @@ _vpp = ctypes.POINTER(ctypes.c_void_p)
 _i64p = ctypes.POINTER(ctypes.c_int64)
 _i32p = ctypes.POINTER(ctypes.c_int32)
 
+NAP_MAX_DOMAINS = 16
+NAP_MAX_STACKS = 16
+
+
+class NapTopology(ctypes.Structure):
+    """Mirror of nuna_nap_topology_t."""
+    _fields_ = [("num_domains", ctypes.c_int32), ("cus_per_domain", ctypes.c_int32),
+                ("num_stacks", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("cu_budget", ctypes.c_int64), ("stack_budget", ctypes.c_int64),
+                ("stack_pref", (ctypes.c_int32 * NAP_MAX_STACKS) * NAP_MAX_DOMAINS)]
+
 # Every function the header declares, with its ctypes signature.
 SIGNATURES = {
     "nuna_init": ([], ctypes.c_int),
@@ -61,6 +72,9 @@ SIGNATURES = {
     "nuna_placement_grid": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, _i64p], ctypes.c_int),
     "nuna_probe_xcc": ([ctypes.c_int, _vp, _vp, _vp], ctypes.c_int),
     "nuna_copy": ([_vp, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
+    "nuna_nap_topology_mi355x": ([ctypes.POINTER(NapTopology)], ctypes.c_int),
+    "nuna_nap_plan": ([ctypes.POINTER(NapTopology), ctypes.c_int, ctypes.c_int64, _i64p, _i64p, _i64p, _i64p,
+                       _i64p, _i32p, _i32p, _i32p, _i64p], ctypes.c_int),
     "nuna_probe_load_latency": ([_vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, _vp, _vp],
                                 ctypes.c_int),
 }
@@ -153,6 +167,41 @@ def placement_grid(place, groups, group_size):
     g = ctypes.c_int64()
     _check(lib().nuna_placement_grid(PLACEMENTS[place], groups, group_size, ctypes.byref(g)))
     return g.value
+
+
+def nap_topology_mi355x(cu_budget=None, stack_budget=None):
+    """The library's MI355X topology for the placement planner, budgets optionally replaced."""
+    t = NapTopology()
+    _check(lib().nuna_nap_topology_mi355x(ctypes.byref(t)))
+    if cu_budget is not None:
+        t.cu_budget = int(cu_budget)
+    if stack_budget is not None:
+        t.stack_budget = int(stack_budget)
+    return t
+
+
+def nap_plan(tb_chunks, tb_bytes, nar_max, topo=None, entry_pages=None):
+    """Algorithm 1 in the library: tb_chunks is a list of chunk-id lists (one per threadblock),
+    tb_bytes the charge of each.  Returns numpy arrays tb_group, tb_domain, tb_cu, entry_stack
+    (aligned with the flattened chunk lists) and the group count."""
+    import numpy as np
+    topo = nap_topology_mi355x() if topo is None else topo
+    n = len(tb_chunks)
+    off = np.zeros(n + 1, dtype=np.int64)
+    off[1:] = np.cumsum([len(c) for c in tb_chunks])
+    ids = np.array([c for cs in tb_chunks for c in cs], dtype=np.int64)
+    cs = np.ascontiguousarray(tb_bytes, dtype=np.int64)
+    pages = None if entry_pages is None else np.ascontiguousarray(entry_pages, dtype=np.int64)
+    g = np.zeros(n, dtype=np.int64)
+    d = np.zeros(n, dtype=np.int32)
+    cu = np.zeros(n, dtype=np.int32)
+    st = np.zeros(max(1, ids.size), dtype=np.int32)
+    ng = ctypes.c_int64()
+    ptr = lambda a, t: a.ctypes.data_as(t) if a is not None and a.size else None  # noqa: E731
+    _check(lib().nuna_nap_plan(ctypes.byref(topo), int(nar_max), n, ptr(off, _i64p), ptr(ids, _i64p),
+                               ptr(cs, _i64p), ptr(pages, _i64p), ptr(g, _i64p), ptr(d, _i32p), ptr(cu, _i32p),
+                               ptr(st, _i32p), ctypes.byref(ng)))
+    return {"tb_group": g, "tb_domain": d, "tb_cu": cu, "entry_stack": st[:ids.size], "num_groups": ng.value}
 
 
 def init():
