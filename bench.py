@@ -55,6 +55,9 @@ def parse():
                     help="turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --profile into HBM traffic "
                          "per launch of the dominant kernel, scaled by the reference copy; writes "
                          "profiles/dominant_traffic.json and prints markdown")
+    ap.add_argument("--interference", action="store_true",
+                    help="all-gather (P=8, 1 MiB per output) timed while a hipBLASLt GEMM with about 100 output "
+                         "tiles runs on another stream, K swept, LINEAR vs XCD; writes JSONL to --out")
     ap.add_argument("--profile", type=int, default=0, metavar="N",
                     help="profiling run: N cold launches each of the dominant kernel (decode all-reduce T=64, "
                          "XCD) and of the 64 MiB reference copy, eager, then exit")
@@ -209,6 +212,56 @@ def bench_allreduce(nuna, torch, pool, x_np, algo, reps, warmup, cold=True, plac
     return alg_bytes, out, calls
 
 
+def bench_rs_ag(nuna, torch, pool, kind, x_np, reps, warmup, cold=True, places=("linear", "xcd")):
+    """Standalone reduce-scatter (kind "rs": in[r] holds P*m elements, out[r] m) or all-gather
+    (kind "ag": in[r] holds m, out[d] P*m), timed like the all-reduce.  Returns algorithmic bytes
+    (P inputs read + P outputs written), per-placement results, calls per graph and parity."""
+    import oracle
+    P, n_in = len(x_np), x_np[0].size
+    es = 2 if x_np[0].dtype == np.uint16 else 4
+    dt = torch.bfloat16 if es == 2 else torch.float32
+    n_out = n_in // P if kind == "rs" else n_in * P
+    per_in = (n_in * es + ALIGN - 1) // ALIGN * ALIGN
+    per_out = (n_out * es + ALIGN - 1) // ALIGN * ALIGN
+    fp = P * (per_in + per_out)
+    calls = calls_for(fp, cold)
+    nsets = max(1, min(calls, pool.nbytes // fp)) if cold else 1
+    pool.off = 0
+    src = [dev_copy_of(torch, a) for a in x_np]
+    sets = []
+    for _ in range(nsets):
+        region = pool.take(fp)
+        ins = [region[r * per_in:r * per_in + n_in * es].view(dt) for r in range(P)]
+        base = P * per_in
+        outs = [region[base + r * per_out:base + r * per_out + n_out * es].view(dt) for r in range(P)]
+        for a, b in zip(ins, src):
+            a.copy_(b)
+        sets.append((ins, outs))
+    op = nuna.reduce_scatter if kind == "rs" else nuna.all_gather
+    ref = oracle.reduce_scatter(x_np) if kind == "rs" else oracle.all_gather(x_np)
+    ok = True
+    for place in places:
+        op(sets[0][0], sets[0][1], placement=place)
+        torch.cuda.synchronize()
+        for d in range(P):
+            g = sets[0][1][d].cpu()
+            g = g.view(torch.int16).numpy().view(np.uint16) if es == 2 else g.numpy()
+            ok = ok and np.array_equal(g, ref[d])
+    graphs = {p: capture(torch, lambda i, p=p: op(sets[i % nsets][0], sets[i % nsets][1], placement=p), calls)
+              for p in places}
+    t = time_graphs(torch, graphs, calls, reps, warmup)
+    alg_bytes = P * (n_in + n_out) * es
+    out = {}
+    for place in places:
+        st = stats(t[place])
+        out[place] = {"us": st, "gbps": alg_bytes / (st["median"] * 1e-6) / 1e9}
+    del graphs, sets
+    return alg_bytes, out, calls, ok
+
+
+RS_AG_KIB = (16, 128, 1024, 8192)  # bytes per rank of the all-gather input / reduce-scatter output
+
+
 # ---------------------------------------------------------------------------------------------- main line
 
 DECODE_STEPS_PER_GRAPH = 64
@@ -352,6 +405,21 @@ def full_sweep(nuna, torch, pool, args):
     for kib in wl.P64_KIB:
         ar_case(f"ar_bf16_p64_{kib}KiB", lambda kib=kib: wl.ar_bf16_p64(kib), ["one_shot", "one_shot_split",
                                                                              "two_shot"])
+    for kind in ("rs", "ag"):
+        for kib in RS_AG_KIB:
+            name = f"{kind}_bf16_p8_{kib}KiB"
+            if not want(name):
+                continue
+            m = kib * 1024 // 2
+            x = wl.normal_bf16(8, 8 * m if kind == "rs" else m, wl.seed_for(7 if kind == "rs" else 8, kib))
+            for cold in (True, False):
+                nb, res, calls, ok = bench_rs_ag(nuna, torch, pool, kind, x, args.reps, args.warmup, cold=cold)
+                emit({"workload": name, "P": 8, "shard_bytes": kib * 1024, "algo": "standalone",
+                      "cache": "cold" if cold else "warm", "alg_bytes": nb, "calls_per_graph": calls, "parity": ok,
+                      **{f"{p}_us": {k: round(v, 3) for k, v in res[p]["us"].items()} for p in res},
+                      **{f"{p}_gbps": round(res[p]["gbps"], 1) for p in res},
+                      **{f"{p}_frac_hbm": round(res[p]["gbps"] / HBM_PEAK_GBPS, 4) for p in res},
+                      "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
     if want("a2a_moe_dispatch"):
         a2a_case(nuna, torch, pool, args, emit)
     if want("a2a_moe_combine"):
@@ -484,6 +552,105 @@ def copy_case(nuna, torch, pool, args, emit):
               "gbps_read_plus_write": round(2 * nb / (t["median"] * 1e-6) / 1e9, 1)})
         del g, pairs
         del s
+
+
+# ---------------------------------------------------------------------------------------------- --interference
+
+INTERF_M = 2560                      # M = N: about 100 output tiles of 256 x 256
+INTERF_K = (0, 2048, 8192, 32768, 131072)
+INTERF_AG_ELEMS = 65536              # bf16 per rank: 128 KiB in, 1 MiB out per rank with P = 8
+INTERF_CALLS = 200
+
+
+def interference(nuna, torch, args):
+    """The collective beside an unrelated GEMM (the paper's concurrent-GEMM experiment): per K, the
+    all-gather's per-call time from a graph of INTERF_CALLS calls replayed on its own stream while
+    GEMMs keep the other stream busy for the whole window; LINEAR and XCD interleaved A/B.  Both
+    streams have the default priority.  After the timed runs every output is checked bit for bit
+    against the oracle."""
+    import oracle
+    from paper_2608_00867_amd import workloads as wl
+    os.makedirs(os.path.dirname(args.out), exist_ok=True)
+    f = open(args.out, "w")
+    P, m = 8, INTERF_AG_ELEMS
+    x = wl.normal_bf16(P, m, wl.seed_for(6))
+    ref = oracle.all_gather(x)
+    ins = [dev_copy_of(torch, a) for a in x]
+    outs = {p: [torch.empty(P * m, dtype=torch.bfloat16, device="cuda") for _ in range(P)] for p in ("linear", "xcd")}
+    s_coll, s_gemm = torch.cuda.Stream(), torch.cuda.Stream()
+    graphs = {}
+    for p in ("linear", "xcd"):
+        with torch.cuda.stream(s_coll):
+            nuna.all_gather(ins, outs[p], placement=p)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s_coll):
+            for _ in range(INTERF_CALLS):
+                nuna.all_gather(ins, outs[p], placement=p)
+        graphs[p] = g
+    torch.cuda.synchronize()
+    alone = {}
+    for K in INTERF_K:
+        gemm_us = None
+        if K:
+            a = torch.randn(INTERF_M, K, dtype=torch.bfloat16, device="cuda")
+            b = torch.randn(K, INTERF_M, dtype=torch.bfloat16, device="cuda")
+            c = torch.empty(INTERF_M, INTERF_M, dtype=torch.bfloat16, device="cuda")
+            with torch.cuda.stream(s_gemm):
+                for _ in range(2):
+                    torch.matmul(a, b, out=c)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(5):
+                    torch.matmul(a, b, out=c)
+                e1.record()
+            torch.cuda.synchronize()
+            gemm_us = e0.elapsed_time(e1) * 1e3 / 5
+        res = {p: [] for p in graphs}
+        gemm_conc = []
+        for rep in range(args.reps):
+            for p in (("linear", "xcd") if rep % 2 == 0 else ("xcd", "linear")):
+                torch.cuda.synchronize()
+                ngemm = 0
+                if K:
+                    window = 2.0 * INTERF_CALLS * 10.0 + 50.0  # us: generous bound on the graph's duration
+                    ngemm = max(2, math.ceil(window / gemm_us))
+                    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    with torch.cuda.stream(s_gemm):
+                        g0.record()
+                        for _ in range(ngemm):
+                            torch.matmul(a, b, out=c)
+                        g1.record()
+                c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                with torch.cuda.stream(s_coll):
+                    c0.record()
+                    graphs[p].replay()
+                    c1.record()
+                torch.cuda.synchronize()
+                res[p].append(c0.elapsed_time(c1) * 1e3 / INTERF_CALLS)
+                if K:
+                    gemm_conc.append(g0.elapsed_time(g1) * 1e3 / ngemm)
+        ok = True
+        for p in outs:
+            for d in range(P):
+                got = outs[p][d].cpu().view(torch.int16).numpy().view(np.uint16)
+                ok = ok and np.array_equal(got, ref[d])
+        st = {p: stats(res[p]) for p in res}
+        if not K:
+            alone = {p: st[p]["median"] for p in st}
+        rec = {"workload": "all_gather_bf16_p8_1MiB_beside_gemm", "gemm_m": INTERF_M, "gemm_n": INTERF_M,
+               "gemm_k": K, "gemm_us_alone": None if gemm_us is None else round(gemm_us, 1),
+               "gemm_us_beside_collective": round(statistics.median(gemm_conc), 1) if gemm_conc else None,
+               "calls": INTERF_CALLS, "parity": bool(ok),
+               **{f"{p}_us": {k: round(v, 3) for k, v in st[p].items()} for p in st},
+               **{f"{p}_slowdown": round(st[p]["median"] / alone[p], 3) for p in st},
+               "linear_over_xcd_time": round(st["linear"]["median"] / st["xcd"]["median"], 4)}
+        f.write(json.dumps(rec) + "\n")
+        f.flush()
+        print(json.dumps(rec), flush=True)
+        if K:
+            del a, b, c
+    f.close()
 
 
 # ---------------------------------------------------------------------------------------------- --profile
@@ -681,6 +848,11 @@ def main():
         return
     if args.profile:
         profile_run(nuna, torch, pool, args.profile)
+        return
+    if args.interference:
+        if args.out == os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"):
+            args.out = os.path.join(ROOT, "gpurun_out", "interference.jsonl")
+        interference(nuna, torch, args)
         return
 
     torch.cuda.synchronize()

@@ -514,6 +514,30 @@ def test_graph_replay_matches_eager(nuna):
             assert_bitwise(to_host(outs2[d]), ref2[d], f"replay {rep} rank {d} (two-shot)")
 
 
+def test_all_gather_beside_gemm(nuna):
+    """Collectives on one stream while a library GEMM runs on another: results stay bit-exact."""
+    P, m = 8, 65536
+    x = wl.normal_bf16(P, m, 71)
+    ref = oracle.all_gather(x)
+    ins = [to_dev(a) for a in x]
+    outs = {p: [torch.empty(P * m, dtype=torch.bfloat16, device="cuda") for _ in range(P)] for p in PLACES}
+    a = torch.randn(2560, 8192, dtype=torch.bfloat16, device="cuda")
+    b = torch.randn(8192, 2560, dtype=torch.bfloat16, device="cuda")
+    s_gemm, s_coll = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s_gemm):
+        for _ in range(8):
+            c = torch.matmul(a, b)
+    with torch.cuda.stream(s_coll):
+        for _ in range(50):
+            for p in PLACES:
+                nuna.all_gather(ins, outs[p], placement=p)
+    torch.cuda.synchronize()
+    assert torch.isfinite(c.float()).all()
+    for p in PLACES:
+        for d in range(P):
+            assert_bitwise(to_host(outs[p][d]), ref[d], f"AG beside GEMM {p} rank {d}")
+
+
 def test_copy_kernel(nuna):
     for nbytes in (16, 4096, 1000003, 64 << 20):
         src = torch.randint(-2 ** 31, 2 ** 31 - 1, ((nbytes + 3) // 4,), dtype=torch.int32, device="cuda")
