@@ -106,6 +106,25 @@ int nuna_version(void);
  * for concurrent kernels.  Returns NUNA_ERR_INVALID_ARG for values < 0. */
 nuna_status_t nuna_set_max_workgroups(int max_workgroups);
 
+/* Launch-shape tunables, by the name of the environment variable that also
+ * sets them at load time.  They choose workgroup sizes, vectors per thread,
+ * kernel variants and grid caps; they never change results.  A setting
+ * applies to later calls of the process; it must not race with other calls
+ * into the library.
+ *   NUNA_MAX_GRID         default workgroup cap, 0..INT32_MAX (0: 16384)
+ *   NUNA_WG_THREADS       0 (by size), 64, 128, 256
+ *   NUNA_VPT              bf16 all-reduce vectors per thread: 0 (by size), 1, 2, 4
+ *   NUNA_LPR_MIN_RANKS    many-rank all-reduce kernels from this many ranks, 1..65 (16)
+ *   NUNA_LPR_MAX_VECTORS  lane-per-rank all-reduce up to this many input vectors in
+ *                         total, 0..2^40 (0: never)
+ *   NUNA_COMBINE_VPT      combine vectors per thread: 0 (default), 1, 2, 4
+ *   NUNA_COMBINE_CHUNKS   combine column chunks per token, 0 (by size)..INT32_MAX
+ *   NUNA_TILE_V           rank-major tile all-reduce width: 0 (16 up to 256 KiB per
+ *                         rank, else off), 16, 32, 64
+ * Unknown names and values outside these sets: NUNA_ERR_INVALID_ARG. */
+nuna_status_t nuna_set_tunable(const char* name, int64_t value);
+nuna_status_t nuna_get_tunable(const char* name, int64_t* value);
+
 /*
  * All-reduce (sum).  Sec. 2.1 (all-reduce of gradients / partial
  * activations); direct algorithm as in Sec. 5.1.

@@ -21,10 +21,11 @@ struct Tuning {
     int max_grid = 16384;  // cap on workgroups per launch (persistent loop beyond)
     int wg_threads = 0;    // workgroup size for the streaming kernels (0 = by size)
     int vpt = 0;           // bf16 all-reduce vectors per thread per work item (0 = by size)
-    int lpr_min_ranks = 16;           // lane-per-rank all-reduce: at least this many ranks ...
-    int64_t lpr_max_vectors = 131072;  // ... and at most this many input vectors in total (2 MiB)
+    int lpr_min_ranks = 16;           // many-rank all-reduce kernels (tile, lane per rank) from this many ranks
+    int64_t lpr_max_vectors = 0;       // lane-per-rank all-reduce up to this many input vectors in total (0: off)
     int combine_vpt = 0;               // combine vectors per thread per pass (0 = default)
     int combine_chunks = 0;            // combine column chunks per token (0 = by size)
+    int tile_v = 0;                    // rank-major tile all-reduce width (16/32/64; 0 = by size)
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).

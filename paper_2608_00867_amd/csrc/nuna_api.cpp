@@ -121,6 +121,7 @@ const Tuning& tuning() {
         g_tuning.lpr_max_vectors = env_int("NUNA_LPR_MAX_VECTORS", static_cast<int>(g_tuning.lpr_max_vectors));
         g_tuning.combine_vpt = env_int("NUNA_COMBINE_VPT", g_tuning.combine_vpt);
         g_tuning.combine_chunks = env_int("NUNA_COMBINE_CHUNKS", g_tuning.combine_chunks);
+        g_tuning.tile_v = env_int("NUNA_TILE_V", g_tuning.tile_v);
     });
     return g_tuning;
 }
@@ -145,6 +146,71 @@ int nuna_version(void) { return 100; }
 nuna_status_t nuna_set_max_workgroups(int max_workgroups) {
     if (max_workgroups < 0) return fail(NUNA_ERR_INVALID_ARG, "max_workgroups=%d < 0", max_workgroups);
     nuna::g_max_workgroups.store(max_workgroups, std::memory_order_relaxed);
+    return ok();
+}
+
+namespace {
+
+// Launch-shape tunables settable at run time: the environment variable's
+// name, the field it sets, and the values it accepts (an explicit list, or
+// the range [lo, hi] when the list is empty).
+struct TunableDef {
+    const char* name;
+    int64_t nuna::Tuning::*wide;  // int64 field, or null
+    int nuna::Tuning::*narrow;    // int field, or null
+    int64_t lo, hi;
+    int nvals;
+    int64_t vals[5];
+    int64_t get(const nuna::Tuning& t) const { return wide ? t.*wide : t.*narrow; }
+    void set(nuna::Tuning& t, int64_t v) const {
+        if (wide)
+            t.*wide = v;
+        else
+            t.*narrow = static_cast<int>(v);
+    }
+    bool accepts(int64_t v) const {
+        if (nvals == 0) return v >= lo && v <= hi;
+        for (int i = 0; i < nvals; ++i)
+            if (vals[i] == v) return true;
+        return false;
+    }
+};
+
+const TunableDef kTunables[] = {
+    {"NUNA_MAX_GRID", nullptr, &nuna::Tuning::max_grid, 0, INT32_MAX, 0, {}},
+    {"NUNA_WG_THREADS", nullptr, &nuna::Tuning::wg_threads, 0, 0, 4, {0, 64, 128, 256}},
+    {"NUNA_VPT", nullptr, &nuna::Tuning::vpt, 0, 0, 4, {0, 1, 2, 4}},
+    {"NUNA_LPR_MIN_RANKS", nullptr, &nuna::Tuning::lpr_min_ranks, 1, NUNA_MAX_RANKS + 1, 0, {}},
+    {"NUNA_LPR_MAX_VECTORS", &nuna::Tuning::lpr_max_vectors, nullptr, 0, int64_t(1) << 40, 0, {}},
+    {"NUNA_COMBINE_VPT", nullptr, &nuna::Tuning::combine_vpt, 0, 0, 4, {0, 1, 2, 4}},
+    {"NUNA_COMBINE_CHUNKS", nullptr, &nuna::Tuning::combine_chunks, 0, INT32_MAX, 0, {}},
+    {"NUNA_TILE_V", nullptr, &nuna::Tuning::tile_v, 0, 0, 4, {0, 16, 32, 64}},
+};
+
+const TunableDef* find_tunable(const char* name) {
+    if (!name) return nullptr;
+    for (const TunableDef& d : kTunables)
+        if (std::strcmp(d.name, name) == 0) return &d;
+    return nullptr;
+}
+
+}  // namespace
+
+nuna_status_t nuna_set_tunable(const char* name, int64_t value) {
+    const TunableDef* d = find_tunable(name);
+    if (!d) return fail(NUNA_ERR_INVALID_ARG, "unknown tunable %s", name ? name : "(null)");
+    if (!d->accepts(value))
+        return fail(NUNA_ERR_INVALID_ARG, "%s does not accept %lld", d->name, static_cast<long long>(value));
+    (void)nuna::tuning();  // environment read first, so a later read cannot undo this setting
+    d->set(g_tuning, value);
+    return ok();
+}
+
+nuna_status_t nuna_get_tunable(const char* name, int64_t* value) {
+    const TunableDef* d = find_tunable(name);
+    if (!d) return fail(NUNA_ERR_INVALID_ARG, "unknown tunable %s", name ? name : "(null)");
+    if (!value) return fail(NUNA_ERR_INVALID_ARG, "value is NULL");
+    *value = d->get(nuna::tuning());
     return ok();
 }
 

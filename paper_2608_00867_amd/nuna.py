@@ -52,6 +52,8 @@ SIGNATURES = {
     "nuna_last_error_string": ([], ctypes.c_char_p),
     "nuna_version": ([], ctypes.c_int),
     "nuna_set_max_workgroups": ([ctypes.c_int], ctypes.c_int),
+    "nuna_set_tunable": ([ctypes.c_char_p, ctypes.c_int64], ctypes.c_int),
+    "nuna_get_tunable": ([ctypes.c_char_p, _i64p], ctypes.c_int),
     "nuna_allreduce": ([_vpp, _vpp, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, ctypes.c_int, _vp],
                        ctypes.c_int),
     "nuna_reduce_scatter": ([_vpp, _vpp, ctypes.c_int, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp],
@@ -202,6 +204,36 @@ def nap_plan(tb_chunks, tb_bytes, nar_max, topo=None, entry_pages=None):
                                ptr(cs, _i64p), ptr(pages, _i64p), ptr(g, _i64p), ptr(d, _i32p), ptr(cu, _i32p),
                                ptr(st, _i32p), ctypes.byref(ng)))
     return {"tb_group": g, "tb_domain": d, "tb_cu": cu, "entry_stack": st[:ids.size], "num_groups": ng.value}
+
+
+def set_tunable(name, value):
+    """Set a launch-shape tunable (NUNA_* name) for later calls; never changes results."""
+    _check(lib().nuna_set_tunable(name.encode(), int(value)))
+
+
+def get_tunable(name):
+    v = ctypes.c_int64()
+    _check(lib().nuna_get_tunable(name.encode(), ctypes.byref(v)))
+    return v.value
+
+
+class tunables:
+    """Context manager: set tunables on entry, restore the previous values on exit."""
+
+    def __init__(self, **values):
+        self.values = values
+        self.saved = {}
+
+    def __enter__(self):
+        for k, v in self.values.items():
+            self.saved[k] = get_tunable(k)
+            set_tunable(k, v)
+        return self
+
+    def __exit__(self, *exc):
+        for k, v in self.saved.items():
+            set_tunable(k, v)
+        return False
 
 
 def init():

@@ -338,6 +338,43 @@ def test_a2a_small(nuna, P, T, k, E, H, dtype, place):
         assert_bitwise(got[d], ref[d], f"a2a P={P} T={T} H={H} rank {d}")
 
 
+# ---------------------------------------------------------------- launch-shape variants (tunables)
+
+def _ar_vs_oracle(nuna, x, what):
+    ref = oracle.allreduce(x)
+    got = run_allreduce(nuna, x, "one_shot", "xcd")
+    for d in range(len(x)):
+        assert_bitwise(got[d], ref[d], f"{what} rank {d}")
+
+
+@pytest.mark.parametrize("dtype", [np.float32, np.uint16])
+@pytest.mark.parametrize("V", [16, 32, 64])
+def test_tile_allreduce_variants(nuna, V, dtype):
+    """Rank-major tile all-reduce at every width, any rank count and ragged sizes."""
+    with nuna.tunables(NUNA_TILE_V=V, NUNA_LPR_MAX_VECTORS=0, NUNA_LPR_MIN_RANKS=1):
+        for P in (2, 3, 8, 16, 24, 64):
+            for n in (7, 9, 1000, 4097, 70001):
+                x = wl.random_bits(P, n, dtype, 97 * P + n) if n < 100 else \
+                    (wl.normal_bf16(P, n, 89 * P + n) if dtype == np.uint16 else wl.normal_f32(P, n, 89 * P + n))
+                if n < 100:
+                    ref = oracle.allreduce(x)
+                    got = run_allreduce(nuna, x, "one_shot", "linear")
+                    for d in range(P):
+                        assert_bitwise_nan_aware(got[d], ref[d], f"tile V={V} P={P} n={n} rank {d}")
+                else:
+                    _ar_vs_oracle(nuna, x, f"tile V={V} P={P} n={n}")
+
+
+@pytest.mark.parametrize("cfg", [dict(NUNA_VPT=v, NUNA_WG_THREADS=t) for v in (1, 2, 4) for t in (64, 128, 256)] +
+                         [dict(NUNA_LPR_MIN_RANKS=1, NUNA_LPR_MAX_VECTORS=1 << 30)],  # lane per rank, P >= 1
+                         ids=lambda c: ",".join(f"{k[5:]}={v}" for k, v in c.items()))
+def test_launch_shape_variants(nuna, cfg):
+    """Every forced launch shape gives the oracle's bits (P = 1 to 64; ragged and multi-chunk sizes)."""
+    with nuna.tunables(**cfg):
+        for P, n in ((1, 5003), (2, 70001), (3, 7001), (8, 4097), (8, 262144 + 24), (16, 70001), (64, 9000)):
+            _ar_vs_oracle(nuna, wl.normal_bf16(P, n, 31 * P + n), f"{cfg} P={P} n={n}")
+
+
 # ---------------------------------------------------------------- MoE combine (result collection)
 
 def _run_combine(nuna, y_np, topk, E, place, pad=64, weights=None):
