@@ -565,9 +565,10 @@ INTERF_CALLS = 200
 def interference(nuna, torch, args):
     """The collective beside an unrelated GEMM (the paper's concurrent-GEMM experiment): per K, the
     all-gather's per-call time from a graph of INTERF_CALLS calls replayed on its own stream while
-    GEMMs keep the other stream busy for the whole window; LINEAR and XCD interleaved A/B.  Both
-    streams have the default priority.  After the timed runs every output is checked bit for bit
-    against the oracle."""
+    GEMMs keep the other stream busy for the whole window; LINEAR and XCD interleaved A/B.  Two cache
+    states: warm (one buffer set gathered over and over) and cold (the calls rotate over buffer sets
+    whose total exceeds the Infinity Cache).  Both streams have the default priority.  After the timed
+    runs every output is checked bit for bit against the oracle."""
     import oracle
     from paper_2608_00867_amd import workloads as wl
     os.makedirs(os.path.dirname(args.out), exist_ok=True)
@@ -575,81 +576,94 @@ def interference(nuna, torch, args):
     P, m = 8, INTERF_AG_ELEMS
     x = wl.normal_bf16(P, m, wl.seed_for(6))
     ref = oracle.all_gather(x)
-    ins = [dev_copy_of(torch, a) for a in x]
-    outs = {p: [torch.empty(P * m, dtype=torch.bfloat16, device="cuda") for _ in range(P)] for p in ("linear", "xcd")}
+    src = [dev_copy_of(torch, a) for a in x]
+    set_bytes = P * (m + P * m) * 2
     s_coll, s_gemm = torch.cuda.Stream(), torch.cuda.Stream()
-    graphs = {}
-    for p in ("linear", "xcd"):
-        with torch.cuda.stream(s_coll):
-            nuna.all_gather(ins, outs[p], placement=p)
-        torch.cuda.synchronize()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=s_coll):
-            for _ in range(INTERF_CALLS):
-                nuna.all_gather(ins, outs[p], placement=p)
-        graphs[p] = g
-    torch.cuda.synchronize()
-    alone = {}
-    for K in INTERF_K:
-        gemm_us = None
-        if K:
-            a = torch.randn(INTERF_M, K, dtype=torch.bfloat16, device="cuda")
-            b = torch.randn(K, INTERF_M, dtype=torch.bfloat16, device="cuda")
-            c = torch.empty(INTERF_M, INTERF_M, dtype=torch.bfloat16, device="cuda")
-            with torch.cuda.stream(s_gemm):
-                for _ in range(2):
-                    torch.matmul(a, b, out=c)
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record()
-                for _ in range(5):
-                    torch.matmul(a, b, out=c)
-                e1.record()
+    for cache in ("warm", "cold"):
+        nsets = 1 if cache == "warm" else math.ceil(COLD_SPAN / set_bytes) + 1
+        sets = {}
+        for p in ("linear", "xcd"):
+            sets[p] = []
+            for _ in range(nsets):
+                ins = [torch.empty(m, dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+                for a, b in zip(ins, src):
+                    a.copy_(b)
+                sets[p].append((ins, [torch.empty(P * m, dtype=torch.bfloat16, device="cuda") for _ in range(P)]))
+        graphs = {}
+        for p in ("linear", "xcd"):
+            with torch.cuda.stream(s_coll):
+                nuna.all_gather(sets[p][0][0], sets[p][0][1], placement=p)
             torch.cuda.synchronize()
-            gemm_us = e0.elapsed_time(e1) * 1e3 / 5
-        res = {p: [] for p in graphs}
-        gemm_conc = []
-        for rep in range(args.reps):
-            for p in (("linear", "xcd") if rep % 2 == 0 else ("xcd", "linear")):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=s_coll):
+                for i in range(INTERF_CALLS):
+                    ins, outs = sets[p][i % nsets]
+                    nuna.all_gather(ins, outs, placement=p)
+            graphs[p] = g
+        torch.cuda.synchronize()
+        alone = {}
+        for K in INTERF_K:
+            gemm_us = None
+            if K:
+                a = torch.randn(INTERF_M, K, dtype=torch.bfloat16, device="cuda")
+                b = torch.randn(K, INTERF_M, dtype=torch.bfloat16, device="cuda")
+                c = torch.empty(INTERF_M, INTERF_M, dtype=torch.bfloat16, device="cuda")
+                with torch.cuda.stream(s_gemm):
+                    for _ in range(2):
+                        torch.matmul(a, b, out=c)
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    for _ in range(5):
+                        torch.matmul(a, b, out=c)
+                    e1.record()
                 torch.cuda.synchronize()
-                ngemm = 0
-                if K:
-                    window = 2.0 * INTERF_CALLS * 10.0 + 50.0  # us: generous bound on the graph's duration
-                    ngemm = max(2, math.ceil(window / gemm_us))
-                    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    with torch.cuda.stream(s_gemm):
-                        g0.record()
-                        for _ in range(ngemm):
-                            torch.matmul(a, b, out=c)
-                        g1.record()
-                c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                with torch.cuda.stream(s_coll):
-                    c0.record()
-                    graphs[p].replay()
-                    c1.record()
-                torch.cuda.synchronize()
-                res[p].append(c0.elapsed_time(c1) * 1e3 / INTERF_CALLS)
-                if K:
-                    gemm_conc.append(g0.elapsed_time(g1) * 1e3 / ngemm)
-        ok = True
-        for p in outs:
-            for d in range(P):
-                got = outs[p][d].cpu().view(torch.int16).numpy().view(np.uint16)
-                ok = ok and np.array_equal(got, ref[d])
-        st = {p: stats(res[p]) for p in res}
-        if not K:
-            alone = {p: st[p]["median"] for p in st}
-        rec = {"workload": "all_gather_bf16_p8_1MiB_beside_gemm", "gemm_m": INTERF_M, "gemm_n": INTERF_M,
-               "gemm_k": K, "gemm_us_alone": None if gemm_us is None else round(gemm_us, 1),
-               "gemm_us_beside_collective": round(statistics.median(gemm_conc), 1) if gemm_conc else None,
-               "calls": INTERF_CALLS, "parity": bool(ok),
-               **{f"{p}_us": {k: round(v, 3) for k, v in st[p].items()} for p in st},
-               **{f"{p}_slowdown": round(st[p]["median"] / alone[p], 3) for p in st},
-               "linear_over_xcd_time": round(st["linear"]["median"] / st["xcd"]["median"], 4)}
-        f.write(json.dumps(rec) + "\n")
-        f.flush()
-        print(json.dumps(rec), flush=True)
-        if K:
-            del a, b, c
+                gemm_us = e0.elapsed_time(e1) * 1e3 / 5
+            res = {p: [] for p in graphs}
+            gemm_conc = []
+            for rep in range(args.reps):
+                for p in (("linear", "xcd") if rep % 2 == 0 else ("xcd", "linear")):
+                    torch.cuda.synchronize()
+                    if K:
+                        window = 2.0 * INTERF_CALLS * 10.0 + 50.0  # us: generous bound on the graph's duration
+                        ngemm = max(2, math.ceil(window / gemm_us))
+                        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                        with torch.cuda.stream(s_gemm):
+                            g0.record()
+                            for _ in range(ngemm):
+                                torch.matmul(a, b, out=c)
+                            g1.record()
+                    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    with torch.cuda.stream(s_coll):
+                        c0.record()
+                        graphs[p].replay()
+                        c1.record()
+                    torch.cuda.synchronize()
+                    res[p].append(c0.elapsed_time(c1) * 1e3 / INTERF_CALLS)
+                    if K:
+                        gemm_conc.append(g0.elapsed_time(g1) * 1e3 / ngemm)
+            ok = True
+            for p in sets:
+                for _, outs in sets[p][:2]:
+                    for d in range(P):
+                        got = outs[d].cpu().view(torch.int16).numpy().view(np.uint16)
+                        ok = ok and np.array_equal(got, ref[d])
+            st = {p: stats(res[p]) for p in res}
+            if not K:
+                alone = {p: st[p]["median"] for p in st}
+            rec = {"workload": "all_gather_bf16_p8_1MiB_beside_gemm", "cache": cache, "gemm_m": INTERF_M,
+                   "gemm_n": INTERF_M, "gemm_k": K, "gemm_us_alone": None if gemm_us is None else round(gemm_us, 1),
+                   "gemm_us_beside_collective": round(statistics.median(gemm_conc), 1) if gemm_conc else None,
+                   "calls": INTERF_CALLS, "buffer_sets": nsets, "parity": bool(ok),
+                   **{f"{p}_us": {k: round(v, 3) for k, v in st[p].items()} for p in st},
+                   **{f"{p}_slowdown": round(st[p]["median"] / alone[p], 3) for p in st},
+                   "linear_over_xcd_time": round(st["linear"]["median"] / st["xcd"]["median"], 4)}
+            f.write(json.dumps(rec) + "\n")
+            f.flush()
+            print(json.dumps(rec), flush=True)
+            if K:
+                del a, b, c
+        del graphs, sets
+        torch.cuda.empty_cache()
     f.close()
 
 
