@@ -415,6 +415,9 @@ __global__ __launch_bounds__(64) void k_probe_xcc(int32_t* xcc, int32_t* hw_id) 
     }
 }
 
+// Reference copy.  It streams past the caches the way the collectives do
+// (non-temporal 16-byte loads and stores), so its traffic-counter readings
+// calibrate theirs and its speed is the ceiling a plain read+write reaches.
 __global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uint4* __restrict__ src, int64_t nvec,
                                               unsigned char* __restrict__ dst_tail,
                                               const unsigned char* __restrict__ src_tail, int tail) {
@@ -424,10 +427,10 @@ __global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uin
         uint4 y[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (v + u * kWG < nvec) y[u] = src[v + u * kWG];
+            if (v + u * kWG < nvec) y[u] = load16<true>(src + v + u * kWG);
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (v + u * kWG < nvec) dst[v + u * kWG] = y[u];
+            if (v + u * kWG < nvec) store_stream(dst + v + u * kWG, y[u]);
     }
     if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < tail) dst_tail[threadIdx.x] = src_tail[threadIdx.x];
 }
