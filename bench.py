@@ -60,7 +60,12 @@ def parse():
                          "tiles runs on another stream, K swept, LINEAR vs XCD; writes JSONL to --out")
     ap.add_argument("--profile", type=int, default=0, metavar="N",
                     help="profiling run: N cold launches each of the dominant kernel (decode all-reduce T=64, "
-                         "XCD) and of the 64 MiB reference copy, eager, then exit")
+                         "XCD), the 64 MiB reference copy, the split all-reduce (T=64), the MoE dispatch and "
+                         "combine, eager, then exit")
+    ap.add_argument("--summarize-l2", nargs=2, metavar=("LINEAR_CSV", "XCD_CSV"), default=None,
+                    help="markdown table of TCC_HIT_sum / TCC_MISS_sum from two --profile runs (LINEAR, XCD)")
+    ap.add_argument("--profile-place", choices=("linear", "xcd"), default="xcd",
+                    help="placement of the split all-reduce and MoE kernels in --profile")
     return ap.parse_args()
 
 
@@ -672,9 +677,11 @@ def interference(nuna, torch, args):
 PROFILE_COPY_BYTES = 64 << 20
 
 
-def profile_run(nuna, torch, pool, n):
-    """Short eager run for rocprofv3 counter passes: the dominant kernel on cold buffers, then the
-    reference copy of PROFILE_COPY_BYTES (the calibration kernel for the traffic counters)."""
+def profile_run(nuna, torch, pool, n, place="xcd"):
+    """Short eager run for rocprofv3 counter passes: the dominant kernel on cold buffers, the
+    reference copy of PROFILE_COPY_BYTES (the calibration kernel for the traffic counters), then the
+    kernels whose map the placement changes (split all-reduce, MoE dispatch; the combine too) in
+    placement `place`."""
     from paper_2608_00867_amd import workloads as wl
     x = wl.ar_bf16_decode(64)
     pool.off = 0
@@ -690,9 +697,18 @@ def profile_run(nuna, torch, pool, n):
     for _ in range(n):
         nuna.copy(b, a)
     torch.cuda.synchronize()
-    moe = profile_moe(nuna, torch, pool, n)
-    print(json.dumps({"profile": {"dominant_launches": n, "dominant_alg_bytes": 2 * 8 * x[0].size * 2,
-                                  "copy_launches": n, "copy_bytes": PROFILE_COPY_BYTES, **moe}}), flush=True)
+    # The split all-reduce: 8 destination groups per chunk, the placement under study.
+    pool.off = 0
+    sets = ar_sets(torch, pool, x, min(n, pool.nbytes // ar_footprint(8, x[0].size, 2)))
+    torch.cuda.synchronize()
+    for i in range(n):
+        ins, outs = sets[i % len(sets)]
+        nuna.allreduce(ins, outs, algo="one_shot_split", placement=place)
+    torch.cuda.synchronize()
+    moe = profile_moe(nuna, torch, pool, n, place)
+    print(json.dumps({"profile": {"place": place, "dominant_launches": n,
+                                  "dominant_alg_bytes": 2 * 8 * x[0].size * 2, "copy_launches": n,
+                                  "copy_bytes": PROFILE_COPY_BYTES, **moe}}), flush=True)
 
 
 def moe_alg_bytes():
@@ -706,9 +722,9 @@ def moe_alg_bytes():
     return int(rows.sum() * rb + topk.shape[0] * topk.shape[1] * rb)
 
 
-def profile_moe(nuna, torch, pool, n):
-    """`n` dispatches then `n` combines at the MoE shape (XCD placement), rotating over buffer sets
-    that together exceed the caches."""
+def profile_moe(nuna, torch, pool, n, place="xcd"):
+    """`n` dispatches then `n` combines at the MoE shape, rotating over buffer sets that together
+    exceed the caches."""
     from paper_2608_00867_amd import workloads as wl
     send_np, topk = wl.a2a_moe()
     E, H = wl.MOE_EXPERTS, wl.HIDDEN_MOE
@@ -729,11 +745,11 @@ def profile_moe(nuna, torch, pool, n):
     torch.cuda.synchronize()
     for i in range(n):
         tok, rec = sets[i % nsets]
-        nuna.all_to_all(tok, rec, lay, placement="xcd")
+        nuna.all_to_all(tok, rec, lay, placement=place)
     torch.cuda.synchronize()
     for i in range(n):
         tok, rec = sets[i % nsets]
-        nuna.all_to_all_combine(rec, tok, lay, placement="xcd")
+        nuna.all_to_all_combine(rec, tok, lay, placement=place)
     torch.cuda.synchronize()
     lay.close()
     return {"moe_launches": n, "moe_alg_bytes": moe_alg_bytes()}
@@ -790,7 +806,7 @@ def summarize_traffic(fetch_csv, write_csv):
         return by
 
     f, w = read(fetch_csv), read(write_csv)
-    dom = [k for k in f if k[0].startswith("k_allreduce")]
+    dom = [k for k in f if k[0].startswith("k_allreduce")][:1]  # dispatched first: the dominant kernel
     cpy = [k for k in f if k[0].startswith("k_copy")]
     assert len(dom) == 1 and len(cpy) == 1, (dom, cpy)
     kib = PROFILE_COPY_BYTES / 1024
@@ -812,17 +828,46 @@ def summarize_traffic(fetch_csv, write_csv):
     print(f"| WRITE_SIZE | {statistics.median(w[cpy[0]]):.1f} | {wf:.4f} | {statistics.median(w[dom[0]]):.1f} | "
           f"{write:.0f} |")
     print(f"\nTraffic per launch {fetch + write:.0f} B vs algorithmic {alg} B: ratio {(fetch + write) / alg:.4f}.")
-    moe = [k for k in f if k[0].startswith("k_all_to_all") or k[0].startswith("k_combine")]
-    if moe:
+    others = [k for k in f if k not in dom and (k[0].startswith("k_allreduce") or k[0].startswith("k_all_to_all")
+                                                 or k[0].startswith("k_combine"))]
+    if others:
         malg = moe_alg_bytes()
-        print("\nMoE kernels of the same runs (8 ranks, 512 tokens x 7168 bf16 per rank, top-8 of 256 experts; "
+        print("\nOther kernels of the same runs: the split all-reduce (same message, 8 destination groups per "
+              "chunk) and the MoE kernels (8 ranks, 512 tokens x 7168 bf16 per rank, top-8 of 256 experts; "
               f"algorithmic bytes per launch {malg}):\n")
-        print("| kernel | FETCH_SIZE (KiB) | WRITE_SIZE (KiB) | scaled fetch B | scaled write B | traffic / algorithmic |")
-        print("|---|---|---|---|---|---|")
-        for k in sorted(moe):
+        print("| kernel | grid (threads) | FETCH_SIZE (KiB) | WRITE_SIZE (KiB) | scaled fetch B | scaled write B | "
+              "traffic / algorithmic |")
+        print("|---|---|---|---|---|---|---|")
+        for k in others:
+            a = alg if k[0].startswith("k_allreduce") else malg
             fk, wk = statistics.median(f[k]), statistics.median(w.get(k, [0.0]))
             fb, wb = fk * ff * 1024, wk * wf * 1024
-            print(f"| `{k[0]}` | {fk:.1f} | {wk:.1f} | {fb:.0f} | {wb:.0f} | {(fb + wb) / malg:.4f} |")
+            print(f"| `{k[0]}` | {k[1]} | {fk:.1f} | {wk:.1f} | {fb:.0f} | {wb:.0f} | {(fb + wb) / a:.4f} |")
+
+
+def summarize_l2(linear_csv, xcd_csv):
+    """TCC_HIT_sum / TCC_MISS_sum (L2 requests per dispatch, summed over the 8 XCDs' L2s) of two
+    --profile runs, one per placement: the kernels whose map the placement changes."""
+    import csv
+    import collections
+
+    def read(path):
+        by = collections.defaultdict(lambda: collections.defaultdict(list))
+        for r in csv.DictReader(open(path)):
+            by[(_short(r["Kernel_Name"]), int(r["Grid_Size"]))][r["Counter_Name"]].append(float(r["Counter_Value"]))
+        return by
+
+    runs = {"LINEAR": read(linear_csv), "XCD": read(xcd_csv)}
+    keys = [k for k in runs["XCD"] if k[0].startswith(("k_allreduce", "k_all_to_all", "k_combine"))]
+    print("| kernel | grid (threads) | placement | L2 hits | L2 misses | hit rate |")
+    print("|---|---|---|---|---|---|")
+    for k in keys:
+        for mode, run in runs.items():
+            if k not in run:
+                continue
+            h = statistics.median(run[k]["TCC_HIT_sum"])
+            m = statistics.median(run[k]["TCC_MISS_sum"])
+            print(f"| `{k[0]}` | {k[1]} | {mode} | {h:.0f} | {m:.0f} | {h / (h + m):.3f} |")
 
 
 def measured_traffic():
@@ -847,6 +892,9 @@ def main():
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic)
         return
+    if args.summarize_l2:
+        summarize_l2(*args.summarize_l2)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path runs all P "
               f"simulated ranks on one GPU, and no figure across GPUs is produced).", file=sys.stderr)
@@ -861,7 +909,7 @@ def main():
         full_sweep(nuna, torch, pool, args)
         return
     if args.profile:
-        profile_run(nuna, torch, pool, args.profile)
+        profile_run(nuna, torch, pool, args.profile, args.profile_place)
         return
     if args.interference:
         if args.out == os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"):
