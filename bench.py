@@ -58,6 +58,10 @@ def parse():
     ap.add_argument("--interference", action="store_true",
                     help="all-gather (P=8, 1 MiB per output) timed while a hipBLASLt GEMM with about 100 output "
                          "tiles runs on another stream, K swept, LINEAR vs XCD; writes JSONL to --out")
+    ap.add_argument("--affinity", action="store_true",
+                    help="probe which die (XCDs 0-3 or 4-7) is near each 8 KiB block of an all-reduce's 16 rank "
+                         "buffers (decode T=64 and prefill T=1024 layouts of the pool) and print how well the "
+                         "buffers agree offset by offset")
     ap.add_argument("--profile", type=int, default=0, metavar="N",
                     help="profiling run: N cold launches each of the dominant kernel (decode all-reduce T=64, "
                          "XCD), the 64 MiB reference copy, the split all-reduce (T=64), the MoE dispatch and "
@@ -672,6 +676,31 @@ def interference(nuna, torch, args):
     f.close()
 
 
+# ---------------------------------------------------------------------------------------------- --affinity
+
+def affinity(nuna, torch, pool):
+    """Memory-side NUNA across an all-reduce's buffers.  For the first buffer set of a layout, every
+    8 KiB block's near die is probed twice (from XCD 0 and XCD 4, caches evicted between passes);
+    each rank buffer's labels are compared with rank 0's input at equal offsets."""
+    for T in (64, 1024):
+        P, n = 8, T * 8192
+        fp = ar_footprint(P, n, 2)
+        pool.off = 0
+        region = pool.take(fp)
+        per = (n * 2 + ALIGN - 1) // ALIGN * ALIGN
+        words = region.view(torch.int32)
+        passes = [nuna.memory_affinity(words, stride=8192, xcds=(0, 4))[1].cpu().numpy() for _ in range(2)]
+        nb = per // 8192
+        lab = np.stack([passes[0][v * nb:(v + 1) * nb] for v in range(2 * P)])
+        maj = (lab.mean(axis=0) >= 0.5).astype(int)
+        print(json.dumps({"layout": f"all-reduce bf16 P=8 [{T},8192]: 16 buffers of {per >> 10} KiB",
+                          "blocks_per_buffer": nb, "probe_repeatability": round(float(np.mean(passes[0] == passes[1])), 3),
+                          "agreement_with_rank0_input": [round(float(np.mean(lab[v] == lab[0])), 3)
+                                                         for v in range(2 * P)],
+                          "near_fraction_on_majority_die": round(float(np.mean(lab == maj[None, :])), 3)}),
+              flush=True)
+
+
 # ---------------------------------------------------------------------------------------------- --profile
 
 PROFILE_COPY_BYTES = 64 << 20
@@ -910,6 +939,9 @@ def main():
         return
     if args.profile:
         profile_run(nuna, torch, pool, args.profile, args.profile_place)
+        return
+    if args.affinity:
+        affinity(nuna, torch, pool)
         return
     if args.interference:
         if args.out == os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"):
