@@ -414,6 +414,8 @@ def full_sweep(nuna, torch, pool, args):
     for kib in wl.P64_KIB:
         ar_case(f"ar_bf16_p64_{kib}KiB", lambda kib=kib: wl.ar_bf16_p64(kib), ["one_shot", "one_shot_split",
                                                                              "two_shot"])
+    if want("ar_bf16_decode_eager"):
+        eager_case(nuna, torch, pool, args, emit)
     for kind in ("rs", "ag"):
         for kib in RS_AG_KIB:
             name = f"{kind}_bf16_p8_{kib}KiB"
@@ -486,6 +488,50 @@ def a2a_case(nuna, torch, pool, args, emit):
               "linear_over_xcd_time": round(res["linear"]["median"] / res["xcd"]["median"], 4)})
         del graphs, sets
     lay.close()
+
+
+EAGER_CALLS = 200
+
+
+def eager_case(nuna, torch, pool, args, emit):
+    """The launch arm: decode all-reduces launched one at a time, each followed by a device
+    synchronize, timed on the host (what a caller without graphs sees per call).  Compared with the
+    graph-replay figure of the same size, the difference is the launch and synchronization cost."""
+    from paper_2608_00867_amd import workloads as wl
+    for T in wl.DECODE_TOKENS:
+        x = wl.ar_bf16_decode(T)
+        P, n = len(x), x[0].size
+        fp = ar_footprint(P, n, 2)
+        nsets = max(1, min(EAGER_CALLS, pool.nbytes // fp))
+        pool.off = 0
+        sets = ar_sets(torch, pool, x, nsets)
+        res = {}
+        for place in ("linear", "xcd"):
+            for i in range(10):
+                nuna.allreduce(sets[i % nsets][0], sets[i % nsets][1], algo="auto", placement=place)
+            torch.cuda.synchronize()
+        per = {"linear": [], "xcd": []}
+        for rep in range(EAGER_CALLS):
+            for place in (("linear", "xcd") if rep % 2 == 0 else ("xcd", "linear")):
+                ins, outs = sets[rep % nsets]
+                t0 = time.perf_counter()
+                nuna.allreduce(ins, outs, algo="auto", placement=place)
+                torch.cuda.synchronize()
+                per[place].append((time.perf_counter() - t0) * 1e6)
+        for place in per:
+            res[place] = stats(per[place])
+        # Host cost of one call alone: back-to-back enqueues (Python binding + C ABI + launch), no sync.
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(EAGER_CALLS):
+            nuna.allreduce(sets[i % nsets][0], sets[i % nsets][1], algo="auto", placement="xcd")
+        enqueue_us = (time.perf_counter() - t0) * 1e6 / EAGER_CALLS
+        torch.cuda.synchronize()
+        emit({"workload": "ar_bf16_decode_eager", "P": P, "tokens": T, "bytes_per_rank": n * 2,
+              "timing": "host clock per eager call + device synchronize", "calls": EAGER_CALLS,
+              **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
+              "enqueue_only_us": round(enqueue_us, 3)})
+        del sets
 
 
 def combine_case(nuna, torch, pool, args, emit):

@@ -103,57 +103,16 @@ nuna_status_t check_common(int P, int dtype, int place) {
 nuna::Tuning g_tuning;
 std::once_flag g_tuning_once;
 
-int env_int(const char* name, int dflt) {
-    const char* v = std::getenv(name);
-    if (!v || !*v) return dflt;
-    return std::atoi(v);
-}
 
 }  // namespace
 
-namespace nuna {
-const Tuning& tuning() {
-    std::call_once(g_tuning_once, [] {
-        g_tuning.max_grid = env_int("NUNA_MAX_GRID", g_tuning.max_grid);
-        g_tuning.wg_threads = env_int("NUNA_WG_THREADS", g_tuning.wg_threads);
-        g_tuning.vpt = env_int("NUNA_VPT", g_tuning.vpt);
-        g_tuning.lpr_min_ranks = env_int("NUNA_LPR_MIN_RANKS", g_tuning.lpr_min_ranks);
-        g_tuning.lpr_max_vectors = env_int("NUNA_LPR_MAX_VECTORS", static_cast<int>(g_tuning.lpr_max_vectors));
-        g_tuning.combine_vpt = env_int("NUNA_COMBINE_VPT", g_tuning.combine_vpt);
-        g_tuning.combine_chunks = env_int("NUNA_COMBINE_CHUNKS", g_tuning.combine_chunks);
-        g_tuning.tile_v = env_int("NUNA_TILE_V", g_tuning.tile_v);
-    });
-    return g_tuning;
-}
-
-std::atomic<int> g_max_workgroups{0};
-
-int max_workgroups() {
-    const int v = g_max_workgroups.load(std::memory_order_relaxed);
-    if (v > 0) return v;
-    return tuning().max_grid > 0 ? tuning().max_grid : 16384;
-}
-}  // namespace nuna
-
-// ============================================================== C ABI
-
-extern "C" {
-
-const char* nuna_last_error_string(void) { return t_err.c_str(); }
-
-int nuna_version(void) { return 100; }
-
-nuna_status_t nuna_set_max_workgroups(int max_workgroups) {
-    if (max_workgroups < 0) return fail(NUNA_ERR_INVALID_ARG, "max_workgroups=%d < 0", max_workgroups);
-    nuna::g_max_workgroups.store(max_workgroups, std::memory_order_relaxed);
-    return ok();
-}
-
 namespace {
 
-// Launch-shape tunables settable at run time: the environment variable's
-// name, the field it sets, and the values it accepts (an explicit list, or
-// the range [lo, hi] when the list is empty).
+// Launch-shape tunables: the environment variable's name (read once at first
+// use, and also the name nuna_set_tunable takes), the field it sets, and the
+// values it accepts (an explicit list, or the range [lo, hi] when the list is
+// empty).  Values outside the accepted set are ignored in the environment and
+// rejected by nuna_set_tunable.
 struct TunableDef {
     const char* name;
     int64_t nuna::Tuning::*wide;  // int64 field, or null
@@ -195,6 +154,43 @@ const TunableDef* find_tunable(const char* name) {
 }
 
 }  // namespace
+
+namespace nuna {
+const Tuning& tuning() {
+    std::call_once(g_tuning_once, [] {
+        for (const TunableDef& d : kTunables) {
+            const char* v = std::getenv(d.name);
+            if (!v || !*v) continue;
+            char* end = nullptr;
+            const long long x = std::strtoll(v, &end, 10);
+            if (end && *end == '\0' && d.accepts(x)) d.set(g_tuning, x);
+        }
+    });
+    return g_tuning;
+}
+
+std::atomic<int> g_max_workgroups{0};
+
+int max_workgroups() {
+    const int v = g_max_workgroups.load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    return tuning().max_grid > 0 ? tuning().max_grid : 16384;
+}
+}  // namespace nuna
+
+// ============================================================== C ABI
+
+extern "C" {
+
+const char* nuna_last_error_string(void) { return t_err.c_str(); }
+
+int nuna_version(void) { return 100; }
+
+nuna_status_t nuna_set_max_workgroups(int max_workgroups) {
+    if (max_workgroups < 0) return fail(NUNA_ERR_INVALID_ARG, "max_workgroups=%d < 0", max_workgroups);
+    nuna::g_max_workgroups.store(max_workgroups, std::memory_order_relaxed);
+    return ok();
+}
 
 nuna_status_t nuna_set_tunable(const char* name, int64_t value) {
     const TunableDef* d = find_tunable(name);

@@ -299,6 +299,20 @@ def test_tunables_set_get_restore_and_reject():
     assert nuna.lib().nuna_get_tunable(b"NUNA_VPT", None) == nuna.ERR_INVALID_ARG
 
 
+def test_tunables_from_environment_are_validated():
+    """The environment is read once per process (here a fresh one): accepted values apply, 64-bit values
+    parse, values outside a knob's set are ignored."""
+    import subprocess
+    import sys
+    env = dict(os.environ, NUNA_TILE_V="32", NUNA_LPR_MAX_VECTORS=str(1 << 33), NUNA_WG_THREADS="33",
+               NUNA_VPT="banana")
+    code = ("import sys; sys.path.insert(0, %r); from paper_2608_00867_amd import nuna; "
+            "print(nuna.get_tunable('NUNA_TILE_V'), nuna.get_tunable('NUNA_LPR_MAX_VECTORS'), "
+            "nuna.get_tunable('NUNA_WG_THREADS'), nuna.get_tunable('NUNA_VPT'))" % ROOT)
+    out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, check=True)
+    assert out.stdout.split() == ["32", str(1 << 33), "0", "0"]
+
+
 # ---------------------------------------------------------------- placement map (host mirror)
 
 def _map(place, G, groups, gsize):
