@@ -527,10 +527,18 @@ def eager_case(nuna, torch, pool, args, emit):
             nuna.allreduce(sets[i % nsets][0], sets[i % nsets][1], algo="auto", placement="xcd")
         enqueue_us = (time.perf_counter() - t0) * 1e6 / EAGER_CALLS
         torch.cuda.synchronize()
+        # The same with the call prepared once (no per-call Python checks or marshalling).
+        calls = [nuna.prepare_allreduce(ins, outs, algo="auto", placement="xcd") for ins, outs in sets[:16]]
+        handle = torch.cuda.current_stream().cuda_stream
+        t0 = time.perf_counter()
+        for i in range(EAGER_CALLS):
+            calls[i % len(calls)](handle)
+        prepared_us = (time.perf_counter() - t0) * 1e6 / EAGER_CALLS
+        torch.cuda.synchronize()
         emit({"workload": "ar_bf16_decode_eager", "P": P, "tokens": T, "bytes_per_rank": n * 2,
               "timing": "host clock per eager call + device synchronize", "calls": EAGER_CALLS,
               **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
-              "enqueue_only_us": round(enqueue_us, 3)})
+              "enqueue_only_us": round(enqueue_us, 3), "prepared_enqueue_only_us": round(prepared_us, 3)})
         del sets
 
 

@@ -290,6 +290,39 @@ def allreduce(ins, outs=None, algo="auto", placement="xcd", stream=None):
     return outs
 
 
+class Prepared:
+    """A collective call whose buffers were checked and whose arguments were marshalled once.
+    Calling it launches the collective again, on `stream` (a torch stream, a raw stream handle, or
+    None for torch's current stream), with no per-call Python checks.  The tensors it was built
+    from must stay alive and keep their storage; they are held by this object."""
+
+    def __init__(self, fn, args, keep):
+        self._fn = fn
+        self._args = args
+        self._keep = keep
+
+    def __call__(self, stream=None):
+        if stream is None:
+            h = _torch().cuda.current_stream().cuda_stream
+        elif isinstance(stream, int):
+            h = stream
+        else:
+            h = stream.cuda_stream
+        _check(self._fn(*self._args, h))
+
+
+def prepare_allreduce(ins, outs, algo="auto", placement="xcd"):
+    """allreduce(ins, outs, algo, placement) as a Prepared call."""
+    _, n = _check_ranks(ins, "ins")
+    _check_ranks(outs, "outs")
+    if outs[0].numel() != n or outs[0].dtype != ins[0].dtype or len(outs) != len(ins):
+        raise ValueError("outs must match ins in count, dtype and size")
+    a = _ptr_array([t.data_ptr() for t in ins])
+    b = _ptr_array([t.data_ptr() for t in outs])
+    args = (a, b, len(ins), n, _dtype_code(ins[0]), ALGOS[algo], PLACEMENTS[placement])
+    return Prepared(lib().nuna_allreduce, args, (list(ins), list(outs)))
+
+
 def reduce_scatter(ins, outs=None, placement="xcd", stream=None):
     """outs[r][j] = sum over q ascending of ins[q][r*m + j], m = numel / P."""
     _, n = _check_ranks(ins, "ins")

@@ -575,6 +575,29 @@ def test_all_gather_beside_gemm(nuna):
             assert_bitwise(to_host(outs[p][d]), ref[d], f"AG beside GEMM {p} rank {d}")
 
 
+def test_prepared_allreduce_repeats_the_call(nuna):
+    """A prepared call gives the oracle's bits every time it runs, on the current stream or a given one."""
+    x = wl.ar_bf16_decode(16)
+    ref = oracle.allreduce(x)
+    ins = [to_dev(a) for a in x]
+    outs = [torch.empty_like(t) for t in ins]
+    call = nuna.prepare_allreduce(ins, outs, algo="one_shot", placement="xcd")
+    s = torch.cuda.Stream()
+    for k in range(3):
+        for o in outs:
+            o.zero_()
+        torch.cuda.synchronize()
+        if k == 0:
+            call()
+        elif k == 1:
+            call(s)
+        else:
+            call(s.cuda_stream)
+        torch.cuda.synchronize()
+        for d in range(8):
+            assert_bitwise(to_host(outs[d]), ref[d], f"prepared call {k} rank {d}")
+
+
 def test_copy_kernel(nuna):
     for nbytes in (16, 4096, 1000003, 64 << 20):
         src = torch.randint(-2 ** 31, 2 ** 31 - 1, ((nbytes + 3) // 4,), dtype=torch.int32, device="cuda")
