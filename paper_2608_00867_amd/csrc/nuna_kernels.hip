@@ -492,10 +492,10 @@ void launch_rs_p(const void* const* in, void* const* out, int P, const RsShape& 
     }
 }
 
-// Vectors per thread per work item for bf16 all-reduce with up to 16 ranks,
-// by message size (measured on MI355X, cold): 4 at 4 MiB per rank, 2 at
-// 16 MiB, 1 at 64 MiB and above and for every smaller (latency-bound)
-// message, where more workgroups win.
+// Vectors per thread per work item for the all-reduce and reduce-scatter with
+// up to 16 ranks, by message size (measured on MI355X with bf16, cold): 4 at
+// 4 MiB per rank, 2 at 16 MiB, 1 at 64 MiB and above and for every smaller
+// (latency-bound) message, where more workgroups win.
 int pick_vpt(int64_t vectors_per_rank, int P) {
     if (P > 16) return 1;
     const int forced = tuning().vpt;
@@ -664,8 +664,11 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
                                 : mode;
     const Place pl = make_place_uniform(gmode, groups > 0 ? groups : 1, gsize);
     const int64_t G = cap_grid(place_grid(pl));
+    // The kernel's vectors per thread must be the VPT the chunks were sized with.
     if (dtype == kDtF32) {
-        launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
+        if (vpt == 4) launch_ar_p<kDtF32, 4>(in, out, P, s, pl, G, nt, stream);
+        else if (vpt == 2) launch_ar_p<kDtF32, 2>(in, out, P, s, pl, G, nt, stream);
+        else launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
     } else {
         if (vpt == 4) launch_ar_p<kDtBf16, 4>(in, out, P, s, pl, G, nt, stream);
         else if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, stream);

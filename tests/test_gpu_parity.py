@@ -338,6 +338,19 @@ def test_a2a_small(nuna, P, T, k, E, H, dtype, place):
         assert_bitwise(got[d], ref[d], f"a2a P={P} T={T} H={H} rank {d}")
 
 
+@pytest.mark.parametrize("n", [(1 << 20) + 5, (1 << 22) + 3, (1 << 24) + 8])
+def test_ar_f32_large_every_algo(nuna, n):
+    """fp32 messages of 4, 16 and 64 MiB per rank at the default launch shapes (their chunk sizes use
+    4, 2 and 1 vectors per thread); every algorithm and placement."""
+    x = wl.normal_f32(8, n, 53 + n % 97)
+    ref = oracle.allreduce(x)
+    for place in PLACES:
+        for algo in AR_ALGOS:
+            got = run_allreduce(nuna, x, algo, place, guard=False)
+            for d in range(8):
+                assert_bitwise(got[d], ref[d], f"f32 n={n} {algo} {place} rank {d}")
+
+
 # ---------------------------------------------------------------- launch-shape variants (tunables)
 
 def _ar_vs_oracle(nuna, x, what):
