@@ -90,3 +90,48 @@ def test_fuzz(nuna, seed):
         torch.cuda.synchronize()
     for d in range(P):
         assert_bitwise_nan_aware(to_host(outs[d]), ref[d], f"{what} rank {d}")
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_fuzz_moe(nuna, seed):
+    """Seeded random MoE dispatch + combine (unweighted or weighted) in a random placement."""
+    g = np.random.default_rng(20000 + seed)
+    P = int(g.choice([1, 2, 3, 4, 6, 8, 16, 64]))
+    E = P * int(g.choice([1, 2, 4, 32]))
+    k = int(g.integers(1, min(E, 9) + 1))
+    T = int(g.integers(0, 70))
+    H = int(g.choice([8, 10, 64, 100, 512, 7168]))
+    dtype = np.uint16 if g.random() < 0.6 else np.float32
+    place = str(g.choice(["linear", "xcd"]))
+    weighted = bool(g.random() < 0.4)
+    what = f"seed={seed} P={P} E={E} k={k} T={T} H={H} {dtype.__name__} {place} weighted={weighted}"
+    print(what, flush=True)
+    topk = wl.moe_routing(P, T, k, E, 20000 + seed)
+    lay = nuna.A2ALayout(topk, E).upload()
+    rows = lay.recv_rows()
+    cap = max(int(rows.max()) if rows.size else 0, 1)
+    send_np = [a.reshape(T, H) for a in wl.random_bits(P, T * H, dtype, 30000 + seed)]
+    send = [to_dev(a) if T else torch.empty((0, H), dtype=torch.bfloat16 if dtype == np.uint16 else torch.float32,
+                                            device="cuda") for a in send_np]
+    recv = [torch.zeros((cap, H), dtype=send[0].dtype, device="cuda") for _ in range(P)]
+    if T:
+        nuna.all_to_all(send, recv, lay, placement=place)
+        torch.cuda.synchronize()
+        ref = oracle.all_to_all(send_np, topk, E)
+        for d in range(P):
+            got = to_host(recv[d][:int(rows[d])])
+            assert np.array_equal(got.view(np.uint8), ref[d].view(np.uint8)), f"{what} dispatch rank {d}"
+    y_np = wl.result_rows(rows, H, dtype, 40000 + seed)
+    y = [torch.zeros((cap, H), dtype=send[0].dtype, device="cuda") for _ in range(P)]
+    for d in range(P):
+        if int(rows[d]):
+            y[d][:int(rows[d])] = to_dev(y_np[d])
+    w_np = g.random((P, T, P)).astype(np.float32) if weighted else None
+    out = [torch.empty((T, H), dtype=send[0].dtype, device="cuda") for _ in range(P)]
+    if T:
+        nuna.all_to_all_combine(y, out, lay, placement=place, weights=to_dev(w_np) if weighted else None)
+        torch.cuda.synchronize()
+        ref = oracle.combine(y_np, topk, E, w_np)
+        for s in range(P):
+            assert_bitwise_nan_aware(to_host(out[s]), ref[s], f"{what} combine rank {s}")
+    lay.close()
