@@ -46,7 +46,7 @@ def _inputs(P, n, dtype, bits, seed):
     return wl.normal_bf16(P, n, seed) if dtype == np.uint16 else wl.normal_f32(P, n, seed)
 
 
-@pytest.mark.parametrize("seed", range(160))
+@pytest.mark.parametrize("seed", range(400))
 def test_fuzz(nuna, seed):
     P, n, dtype, op, algo, place, inplace, bits, variant = _case(9000 + seed)
     what = f"seed={seed} P={P} n={n} {dtype.__name__} {op} {algo} {place} inplace={inplace} {variant}"
@@ -92,7 +92,7 @@ def test_fuzz(nuna, seed):
         assert_bitwise_nan_aware(to_host(outs[d]), ref[d], f"{what} rank {d}")
 
 
-@pytest.mark.parametrize("seed", range(48))
+@pytest.mark.parametrize("seed", range(120))
 def test_fuzz_moe(nuna, seed):
     """Seeded random MoE dispatch + combine (unweighted or weighted) in a random placement."""
     g = np.random.default_rng(20000 + seed)
