@@ -1,6 +1,6 @@
 // nuna_kernels.hip -- gfx950 kernels of the collective copy/reduce path:
-// all-reduce (one-shot, split, lane-per-rank), reduce-scatter, all-gather,
-// the dispatch probe and the reference copy.
+// all-reduce (one-shot, split, rank-major tile, lane-per-rank),
+// reduce-scatter, all-gather, the dispatch probe and the reference copy.
 //
 // Memory-bound streaming kernels: every lane moves 16-byte vectors
 // (global_load/store_dwordx4), so one wavefront instruction touches 1 KiB of
@@ -92,7 +92,10 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
 // the barrier one thread per output dword adds the P ranks in ascending
 // order (same order and rounding as every other kernel).  After a second
 // barrier thread t stores the result vector to its rank's output.  A message
-// of 16 KiB per rank at P=64 thus spreads over 256 workgroups.
+// of 16 KiB per rank at P=64 thus spreads over 256 workgroups.  Each lane
+// reads a different rank, so its accesses are scattered 16-byte requests; the
+// rank-major tile kernel below measured faster at every size, and this one
+// runs only when the NUNA_LPR_MAX_VECTORS tunable asks for it.
 
 struct LprShape {
     int64_t nvec;  // full 16-byte vectors per rank buffer
