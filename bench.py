@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3, help="untimed graph replays before timing")
     ap.add_argument("--reps", type=int, default=15, help="timed replays per size in the sweeps")
     ap.add_argument("--full", action="store_true", help="sweep every workload and write JSONL")
-    ap.add_argument("--out", default=os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"))
+    ap.add_argument("--out", default=None, help="JSONL output file of --full and --interference (required there)")
     ap.add_argument("--only", default=None, metavar="PREFIX",
                     help="with --full: only the workloads whose name starts with PREFIX")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="oracle timing budget (cpu_baseline)")
@@ -978,6 +978,9 @@ def main():
     if args.summarize_l2:
         summarize_l2(*args.summarize_l2)
         return
+    if (args.full or args.interference) and not args.out:
+        print("--full and --interference need --out FILE.jsonl", file=sys.stderr)
+        sys.exit(2)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the path runs all P "
               f"simulated ranks on one GPU, and no figure across GPUs is produced).", file=sys.stderr)
@@ -998,8 +1001,6 @@ def main():
         affinity(nuna, torch, pool)
         return
     if args.interference:
-        if args.out == os.path.join(ROOT, "gpurun_out", "bench_full.jsonl"):
-            args.out = os.path.join(ROOT, "gpurun_out", "interference.jsonl")
         interference(nuna, torch, args)
         return
 
