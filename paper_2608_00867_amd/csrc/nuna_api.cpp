@@ -340,7 +340,7 @@ struct nuna_a2a_layout {
     std::vector<int32_t> map_src;     // source rank of each received row, destination-major
     std::vector<int32_t> map_tok;     // source token of each received row
     std::vector<int32_t> desc_linear; // 4 ints per item, ordered by (dst, row)
-    std::vector<int32_t> desc_group;  // 4 ints per item, XCD-major: source-row groups dealt round-robin to XCDs
+    std::vector<int32_t> desc_group;  // 4 ints per item, XCD-major: each source-row group on its planned XCD
     int64_t xcd_start[NUNA_NUM_XCD + 1] = {};  // per-XCD list offsets into desc_group
     int64_t nitems = 0;
     // Combine tables: token i = s*T + t owns entries [comb_off[i], comb_off[i+1]),
