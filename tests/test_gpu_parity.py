@@ -611,6 +611,58 @@ def test_prepared_allreduce_repeats_the_call(nuna):
             assert_bitwise(to_host(outs[d]), ref[d], f"prepared call {k} rank {d}")
 
 
+def test_graph_replay_moe_and_collectives(nuna):
+    """Dispatch, weighted combine, reduce-scatter and all-gather captured in one HIP graph and replayed
+    several times with eager work in between; every replay matches the oracle."""
+    P, T, k, E, H = 8, 32, 8, 256, 1024
+    topk = wl.moe_routing(P, T, k, E, 77)
+    send_np = wl.moe_rows(P, T, H, 78)
+    lay = nuna.A2ALayout(topk, E).upload()
+    cap = int(lay.recv_rows().max())
+    send = [to_dev(a) for a in send_np]
+    recv = [torch.empty((cap, H), dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+    back = [torch.empty((T, H), dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+    w_np = np.random.default_rng(79).random((P, T, P)).astype(np.float32)
+    w = to_dev(w_np)
+    x = wl.normal_bf16(P, P * 4096, 80)
+    ins = [to_dev(a) for a in x]
+    shards = [torch.empty(4096, dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+    gathered = [torch.empty(P * 4096, dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+    ref_recv = oracle.all_to_all(send_np, topk, E)
+    ref_back = oracle.combine(ref_recv, topk, E, w_np)
+    ref_rs = oracle.reduce_scatter(x)
+    ref_ag = oracle.all_gather(ref_rs)
+
+    def work():
+        nuna.all_to_all(send, recv, lay, placement="xcd")
+        nuna.all_to_all_combine(recv, back, lay, placement="xcd", weights=w)
+        nuna.reduce_scatter(ins, shards, placement="xcd")
+        nuna.all_gather(shards, gathered, placement="xcd")
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        work()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        work()
+    rows = lay.recv_rows()
+    for rep in range(3):
+        for t in recv + back + shards + gathered:
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for d in range(P):
+            assert_bitwise(to_host(recv[d][:int(rows[d])]), ref_recv[d], f"replay {rep} dispatch rank {d}")
+            assert_bitwise(to_host(back[d]), ref_back[d], f"replay {rep} combine rank {d}")
+            assert_bitwise(to_host(shards[d]), ref_rs[d], f"replay {rep} reduce-scatter rank {d}")
+            assert_bitwise(to_host(gathered[d]), ref_ag[d], f"replay {rep} all-gather rank {d}")
+    lay.close()
+
+
 def test_copy_kernel(nuna):
     for nbytes in (16, 4096, 1000003, 64 << 20):
         src = torch.randint(-2 ** 31, 2 ** 31 - 1, ((nbytes + 3) // 4,), dtype=torch.int32, device="cuda")
