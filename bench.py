@@ -622,111 +622,139 @@ def copy_case(nuna, torch, pool, args, emit):
 INTERF_M = 2560                      # M = N: about 100 output tiles of 256 x 256
 INTERF_K = (0, 2048, 8192, 32768, 131072)
 INTERF_AG_ELEMS = 65536              # bf16 per rank: 128 KiB in, 1 MiB out per rank with P = 8
+INTERF_AR_TOKENS = 64                # split all-reduce: [64, 8192] bf16 per rank (1 MiB)
 INTERF_CALLS = 200
+INTERF_MAX_SLOWDOWN = 30.0           # the GEMM window covers the collective's graph even this much slower
+
+
+def interference_cases(wl, oracle):
+    """The collectives run beside the GEMM.  The all-gather is the paper's setup (1 MB per output);
+    at that size its default map is the same in both placements.  The split all-reduce (each chunk's
+    8 destination groups are separate work items) is a map the placement changes."""
+    P, m = 8, INTERF_AG_ELEMS
+    x = wl.normal_bf16(P, m, wl.seed_for(6))
+    yield {"workload": "all_gather_bf16_p8_1MiB_beside_gemm", "ins": x, "out_elems": P * m,
+           "ref": oracle.all_gather(x),
+           "call": lambda nuna, ins, outs, p: nuna.all_gather(ins, outs, placement=p)}
+    x = wl.ar_bf16_decode(INTERF_AR_TOKENS)
+    yield {"workload": f"allreduce_split_bf16_p8_T{INTERF_AR_TOKENS}_beside_gemm", "ins": x,
+           "out_elems": x[0].size, "ref": oracle.allreduce(x),
+           "call": lambda nuna, ins, outs, p: nuna.allreduce(ins, outs, algo="one_shot_split", placement=p)}
 
 
 def interference(nuna, torch, args):
-    """The collective beside an unrelated GEMM (the paper's concurrent-GEMM experiment): per K, the
-    all-gather's per-call time from a graph of INTERF_CALLS calls replayed on its own stream while
+    """Each collective beside an unrelated GEMM (the paper's concurrent-GEMM experiment): per K, the
+    collective's per-call time from a graph of INTERF_CALLS calls replayed on its own stream while
     GEMMs keep the other stream busy for the whole window; LINEAR and XCD interleaved A/B.  Two cache
-    states: warm (one buffer set gathered over and over) and cold (the calls rotate over buffer sets
+    states: warm (one buffer set used over and over) and cold (the calls rotate over buffer sets
     whose total exceeds the Infinity Cache).  Both streams have the default priority.  After the timed
     runs every output is checked bit for bit against the oracle."""
     import oracle
     from paper_2608_00867_amd import workloads as wl
     os.makedirs(os.path.dirname(args.out), exist_ok=True)
     f = open(args.out, "w")
-    P, m = 8, INTERF_AG_ELEMS
-    x = wl.normal_bf16(P, m, wl.seed_for(6))
-    ref = oracle.all_gather(x)
-    src = [dev_copy_of(torch, a) for a in x]
-    set_bytes = P * (m + P * m) * 2
     s_coll, s_gemm = torch.cuda.Stream(), torch.cuda.Stream()
-    for cache in ("warm", "cold"):
-        nsets = 1 if cache == "warm" else math.ceil(COLD_SPAN / set_bytes) + 1
-        sets = {}
-        for p in ("linear", "xcd"):
-            sets[p] = []
+    for case in interference_cases(wl, oracle):
+        x, ref, call = case["ins"], case["ref"], case["call"]
+        P, m, mo = len(x), x[0].size, case["out_elems"]
+        src = [dev_copy_of(torch, a) for a in x]
+        set_bytes = P * (m + mo) * 2
+        for cache in ("warm", "cold"):
+            nsets = 1 if cache == "warm" else math.ceil(COLD_SPAN / set_bytes) + 1
+            # Both placements run on the same buffers, so that only the map differs between them.
+            sets = []
             for _ in range(nsets):
                 ins = [torch.empty(m, dtype=torch.bfloat16, device="cuda") for _ in range(P)]
                 for a, b in zip(ins, src):
                     a.copy_(b)
-                sets[p].append((ins, [torch.empty(P * m, dtype=torch.bfloat16, device="cuda") for _ in range(P)]))
-        graphs = {}
-        for p in ("linear", "xcd"):
-            with torch.cuda.stream(s_coll):
-                nuna.all_gather(sets[p][0][0], sets[p][0][1], placement=p)
-            torch.cuda.synchronize()
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g, stream=s_coll):
-                for i in range(INTERF_CALLS):
-                    ins, outs = sets[p][i % nsets]
-                    nuna.all_gather(ins, outs, placement=p)
-            graphs[p] = g
-        torch.cuda.synchronize()
-        alone = {}
-        for K in INTERF_K:
-            gemm_us = None
-            if K:
-                a = torch.randn(INTERF_M, K, dtype=torch.bfloat16, device="cuda")
-                b = torch.randn(K, INTERF_M, dtype=torch.bfloat16, device="cuda")
-                c = torch.empty(INTERF_M, INTERF_M, dtype=torch.bfloat16, device="cuda")
-                with torch.cuda.stream(s_gemm):
-                    for _ in range(2):
-                        torch.matmul(a, b, out=c)
-                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    e0.record()
-                    for _ in range(5):
-                        torch.matmul(a, b, out=c)
-                    e1.record()
+                sets.append((ins, [torch.empty(mo, dtype=torch.bfloat16, device="cuda") for _ in range(P)]))
+            graphs = {}
+            for p in ("linear", "xcd"):
+                with torch.cuda.stream(s_coll):
+                    call(nuna, sets[0][0], sets[0][1], p)
                 torch.cuda.synchronize()
-                gemm_us = e0.elapsed_time(e1) * 1e3 / 5
-            res = {p: [] for p in graphs}
-            gemm_conc = []
-            for rep in range(args.reps):
-                for p in (("linear", "xcd") if rep % 2 == 0 else ("xcd", "linear")):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=s_coll):
+                    for i in range(INTERF_CALLS):
+                        ins, outs = sets[i % nsets]
+                        call(nuna, ins, outs, p)
+                graphs[p] = g
+            torch.cuda.synchronize()
+            alone = {}
+            for K in INTERF_K:
+                gemm_us = None
+                if K:
+                    a = torch.randn(INTERF_M, K, dtype=torch.bfloat16, device="cuda")
+                    b = torch.randn(K, INTERF_M, dtype=torch.bfloat16, device="cuda")
+                    c = torch.empty(INTERF_M, INTERF_M, dtype=torch.bfloat16, device="cuda")
+                    with torch.cuda.stream(s_gemm):
+                        for _ in range(2):
+                            torch.matmul(a, b, out=c)
+                        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                        e0.record()
+                        for _ in range(5):
+                            torch.matmul(a, b, out=c)
+                        e1.record()
                     torch.cuda.synchronize()
-                    if K:
-                        window = 2.0 * INTERF_CALLS * 10.0 + 50.0  # us: generous bound on the graph's duration
-                        ngemm = max(2, math.ceil(window / gemm_us))
-                        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                        with torch.cuda.stream(s_gemm):
-                            g0.record()
-                            for _ in range(ngemm):
-                                torch.matmul(a, b, out=c)
-                            g1.record()
-                    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    with torch.cuda.stream(s_coll):
-                        c0.record()
-                        graphs[p].replay()
-                        c1.record()
+                    gemm_us = e0.elapsed_time(e1) * 1e3 / 5
+                    # us: bound on the graph's duration beside the GEMM, from the slower mode alone
+                    window = INTERF_MAX_SLOWDOWN * INTERF_CALLS * max(alone.values()) + 50.0
+                    ngemm = max(2, math.ceil(window / gemm_us))
+                res = {p: [] for p in graphs}
+                gemm_conc = []
+                covered = True
+                for rep in range(args.reps):
+                    for p in (("linear", "xcd") if rep % 2 == 0 else ("xcd", "linear")):
+                        torch.cuda.synchronize()
+                        if K:
+                            g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                            with torch.cuda.stream(s_gemm):
+                                g0.record()
+                                for _ in range(ngemm):
+                                    torch.matmul(a, b, out=c)
+                                g1.record()
+                        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                        with torch.cuda.stream(s_coll):
+                            c0.record()
+                            graphs[p].replay()
+                            c1.record()
+                        torch.cuda.synchronize()
+                        res[p].append(c0.elapsed_time(c1) * 1e3 / INTERF_CALLS)
+                        if K:
+                            gemm_conc.append(g0.elapsed_time(g1) * 1e3 / ngemm)
+                            # the GEMMs started first; they must also still run when the last call ends
+                            covered = covered and g0.elapsed_time(c1) <= g0.elapsed_time(g1)
+                ok = True
+                for p in graphs:
+                    for o in range(min(2, nsets)):
+                        for d in range(P):
+                            sets[o][1][d].zero_()
                     torch.cuda.synchronize()
-                    res[p].append(c0.elapsed_time(c1) * 1e3 / INTERF_CALLS)
-                    if K:
-                        gemm_conc.append(g0.elapsed_time(g1) * 1e3 / ngemm)
-            ok = True
-            for p in sets:
-                for _, outs in sets[p][:2]:
-                    for d in range(P):
-                        got = outs[d].cpu().view(torch.int16).numpy().view(np.uint16)
-                        ok = ok and np.array_equal(got, ref[d])
-            st = {p: stats(res[p]) for p in res}
-            if not K:
-                alone = {p: st[p]["median"] for p in st}
-            rec = {"workload": "all_gather_bf16_p8_1MiB_beside_gemm", "cache": cache, "gemm_m": INTERF_M,
-                   "gemm_n": INTERF_M, "gemm_k": K, "gemm_us_alone": None if gemm_us is None else round(gemm_us, 1),
-                   "gemm_us_beside_collective": round(statistics.median(gemm_conc), 1) if gemm_conc else None,
-                   "calls": INTERF_CALLS, "buffer_sets": nsets, "parity": bool(ok),
-                   **{f"{p}_us": {k: round(v, 3) for k, v in st[p].items()} for p in st},
-                   **{f"{p}_slowdown": round(st[p]["median"] / alone[p], 3) for p in st},
-                   "linear_over_xcd_time": round(st["linear"]["median"] / st["xcd"]["median"], 4)}
-            f.write(json.dumps(rec) + "\n")
-            f.flush()
-            print(json.dumps(rec), flush=True)
-            if K:
-                del a, b, c
-        del graphs, sets
-        torch.cuda.empty_cache()
+                    graphs[p].replay()
+                    torch.cuda.synchronize()
+                    for _, outs in sets[:2]:
+                        for d in range(P):
+                            got = outs[d].cpu().view(torch.int16).numpy().view(np.uint16)
+                            ok = ok and np.array_equal(got, ref[d])
+                st = {p: stats(res[p]) for p in res}
+                if not K:
+                    alone = {p: st[p]["median"] for p in st}
+                rec = {"workload": case["workload"], "cache": cache, "gemm_m": INTERF_M,
+                       "gemm_n": INTERF_M, "gemm_k": K,
+                       "gemm_us_alone": None if gemm_us is None else round(gemm_us, 1),
+                       "gemm_us_beside_collective": round(statistics.median(gemm_conc), 1) if gemm_conc else None,
+                       "calls": INTERF_CALLS, "buffer_sets": nsets, "parity": bool(ok),
+                       "gemm_covers_collective": bool(covered) if K else None,
+                       **{f"{p}_us": {k: round(v, 3) for k, v in st[p].items()} for p in st},
+                       **{f"{p}_slowdown": round(st[p]["median"] / alone[p], 3) for p in st},
+                       "linear_over_xcd_time": round(st["linear"]["median"] / st["xcd"]["median"], 4)}
+                f.write(json.dumps(rec) + "\n")
+                f.flush()
+                print(json.dumps(rec), flush=True)
+                if K:
+                    del a, b, c
+            del graphs, sets
+            torch.cuda.empty_cache()
     f.close()
 
 

@@ -588,6 +588,29 @@ def test_all_gather_beside_gemm(nuna):
             assert_bitwise(to_host(outs[p][d]), ref[d], f"AG beside GEMM {p} rank {d}")
 
 
+def test_split_allreduce_beside_gemm(nuna):
+    """The destination-split all-reduce (the map the placement changes) beside a GEMM on another stream."""
+    x = wl.ar_bf16_decode(64, seed=72)
+    ref = oracle.allreduce(x)
+    ins = [to_dev(a) for a in x]
+    outs = {p: [torch.empty_like(t) for t in ins] for p in PLACES}
+    a = torch.randn(2560, 8192, dtype=torch.bfloat16, device="cuda")
+    b = torch.randn(8192, 2560, dtype=torch.bfloat16, device="cuda")
+    s_gemm, s_coll = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s_gemm):
+        for _ in range(8):
+            c = torch.matmul(a, b)
+    with torch.cuda.stream(s_coll):
+        for _ in range(20):
+            for p in PLACES:
+                nuna.allreduce(ins, outs[p], algo="one_shot_split", placement=p)
+    torch.cuda.synchronize()
+    assert torch.isfinite(c.float()).all()
+    for p in PLACES:
+        for d in range(8):
+            assert_bitwise(to_host(outs[p][d]), ref[d], f"split AR beside GEMM {p} rank {d}")
+
+
 def test_prepared_allreduce_repeats_the_call(nuna):
     """A prepared call gives the oracle's bits every time it runs, on the current stream or a given one."""
     x = wl.ar_bf16_decode(16)
