@@ -596,8 +596,9 @@ def combine_case(nuna, torch, pool, args, emit):
 
 
 def copy_case(nuna, torch, pool, args, emit):
-    """Plain streaming copy: the bandwidth ceiling a read+write kernel reaches on this GPU."""
-    for mib in (16, 64, 256):
+    """Plain streaming copy: the bandwidth ceiling a read+write kernel reaches on this GPU.  32, 128
+    and 512 MiB copied move what the prefill all-reduces move at 4, 16 and 64 MiB per rank."""
+    for mib in (16, 32, 64, 128, 256, 512):
         nb = mib << 20
         nsets = max(1, min(pool.nbytes // (2 * nb), math.ceil(COLD_SPAN / (2 * nb))))
         pool.off = 0

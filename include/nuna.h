@@ -113,7 +113,9 @@ nuna_status_t nuna_set_max_workgroups(int max_workgroups);
  * into the library.
  *   NUNA_MAX_GRID         default workgroup cap, 0..INT32_MAX (0: 16384)
  *   NUNA_WG_THREADS       0 (by size), 64, 128, 256
- *   NUNA_VPT              bf16 all-reduce vectors per thread: 0 (by size), 1, 2, 4
+ *   NUNA_VPT              vectors per thread of the all-reduce, reduce-scatter and
+ *                         all-gather: 0 (by size), 1, 2, 4, 8 (8: one-shot all-reduce
+ *                         with 2, 4 or 8 ranks only; 4 elsewhere)
  *   NUNA_LPR_MIN_RANKS    many-rank all-reduce kernels from this many ranks, 1..65 (16)
  *   NUNA_LPR_MAX_VECTORS  lane-per-rank all-reduce up to this many input vectors in
  *                         total, 0..2^40 (0: never)

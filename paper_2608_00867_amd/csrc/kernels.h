@@ -20,7 +20,7 @@ inline size_t dtype_size(int dt) { return dt == kDtF32 ? 4u : 2u; }
 struct Tuning {
     int max_grid = 16384;  // cap on workgroups per launch (persistent loop beyond)
     int wg_threads = 0;    // workgroup size for the streaming kernels (0 = by size)
-    int vpt = 0;           // bf16 all-reduce vectors per thread per work item (0 = by size)
+    int vpt = 0;           // vectors per thread per work item (0 = by size; 8: one-shot all-reduce only)
     int lpr_min_ranks = 16;           // many-rank all-reduce kernels (tile, lane per rank) from this many ranks
     int64_t lpr_max_vectors = 0;       // lane-per-rank all-reduce up to this many input vectors in total (0: off)
     int combine_vpt = 0;               // combine vectors per thread per pass (0 = default)

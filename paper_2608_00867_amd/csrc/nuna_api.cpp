@@ -138,7 +138,7 @@ struct TunableDef {
 const TunableDef kTunables[] = {
     {"NUNA_MAX_GRID", nullptr, &nuna::Tuning::max_grid, 0, INT32_MAX, 0, {}},
     {"NUNA_WG_THREADS", nullptr, &nuna::Tuning::wg_threads, 0, 0, 4, {0, 64, 128, 256}},
-    {"NUNA_VPT", nullptr, &nuna::Tuning::vpt, 0, 0, 4, {0, 1, 2, 4}},
+    {"NUNA_VPT", nullptr, &nuna::Tuning::vpt, 0, 0, 5, {0, 1, 2, 4, 8}},
     {"NUNA_LPR_MIN_RANKS", nullptr, &nuna::Tuning::lpr_min_ranks, 1, NUNA_MAX_RANKS + 1, 0, {}},
     {"NUNA_LPR_MAX_VECTORS", &nuna::Tuning::lpr_max_vectors, nullptr, 0, int64_t(1) << 40, 0, {}},
     {"NUNA_COMBINE_VPT", nullptr, &nuna::Tuning::combine_vpt, 0, 0, 4, {0, 1, 2, 4}},

@@ -285,7 +285,9 @@ def test_tunables_set_get_restore_and_reject():
     names = ["NUNA_MAX_GRID", "NUNA_WG_THREADS", "NUNA_VPT", "NUNA_LPR_MIN_RANKS", "NUNA_LPR_MAX_VECTORS",
              "NUNA_COMBINE_VPT", "NUNA_COMBINE_CHUNKS", "NUNA_TILE_V"]
     before = {n: nuna.get_tunable(n) for n in names}
-    with nuna.tunables(NUNA_TILE_V=32, NUNA_WG_THREADS=128, NUNA_LPR_MAX_VECTORS=1 << 33, NUNA_COMBINE_CHUNKS=3):
+    with nuna.tunables(NUNA_TILE_V=32, NUNA_WG_THREADS=128, NUNA_LPR_MAX_VECTORS=1 << 33, NUNA_COMBINE_CHUNKS=3,
+                       NUNA_VPT=8):
+        assert nuna.get_tunable("NUNA_VPT") == 8
         assert nuna.get_tunable("NUNA_TILE_V") == 32
         assert nuna.get_tunable("NUNA_WG_THREADS") == 128
         assert nuna.get_tunable("NUNA_LPR_MAX_VECTORS") == 1 << 33

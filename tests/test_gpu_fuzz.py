@@ -15,7 +15,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 VARIANTS = [{}, dict(NUNA_MAX_GRID=7), dict(NUNA_WG_THREADS=64), dict(NUNA_WG_THREADS=128, NUNA_VPT=2),
-            dict(NUNA_VPT=4), dict(NUNA_TILE_V=32), dict(NUNA_TILE_V=64, NUNA_LPR_MIN_RANKS=2),
+            dict(NUNA_VPT=4), dict(NUNA_VPT=8), dict(NUNA_TILE_V=32), dict(NUNA_TILE_V=64, NUNA_LPR_MIN_RANKS=2),
             dict(NUNA_LPR_MIN_RANKS=1, NUNA_LPR_MAX_VECTORS=1 << 20)]
 
 

@@ -378,14 +378,57 @@ def test_tile_allreduce_variants(nuna, V, dtype):
                     _ar_vs_oracle(nuna, x, f"tile V={V} P={P} n={n}")
 
 
-@pytest.mark.parametrize("cfg", [dict(NUNA_VPT=v, NUNA_WG_THREADS=t) for v in (1, 2, 4) for t in (64, 128, 256)] +
+@pytest.mark.parametrize("cfg", [dict(NUNA_VPT=v, NUNA_WG_THREADS=t) for v in (1, 2, 4, 8) for t in (64, 128, 256)] +
                          [dict(NUNA_LPR_MIN_RANKS=1, NUNA_LPR_MAX_VECTORS=1 << 30)],  # lane per rank, P >= 1
                          ids=lambda c: ",".join(f"{k[5:]}={v}" for k, v in c.items()))
 def test_launch_shape_variants(nuna, cfg):
     """Every forced launch shape gives the oracle's bits (P = 1 to 64; ragged and multi-chunk sizes)."""
     with nuna.tunables(**cfg):
-        for P, n in ((1, 5003), (2, 70001), (3, 7001), (8, 4097), (8, 262144 + 24), (16, 70001), (64, 9000)):
+        for P, n in ((1, 5003), (2, 70001), (3, 7001), (4, 70001), (8, 4097), (8, 262144 + 24), (16, 70001),
+                     (64, 9000)):
             _ar_vs_oracle(nuna, wl.normal_bf16(P, n, 31 * P + n), f"{cfg} P={P} n={n}")
+
+
+def test_vpt8_every_collective(nuna):
+    """Eight vectors per thread exist for the all-reduce with 2, 4 or 8 ranks only; forced for every
+    collective, the others fall back to 4 and every result keeps the oracle's bits."""
+    with nuna.tunables(NUNA_VPT=8):
+        for P, n, dt in ((2, 70001, np.uint16), (4, 4097, np.float32), (8, 2 ** 17 * 8 + 40, np.uint16),
+                         (8, 100003, np.float32), (3, 7001, np.uint16), (16, 70001, np.uint16)):
+            x = wl.normal_bf16(P, n, 17 * P + n) if dt == np.uint16 else wl.normal_f32(P, n, 17 * P + n)
+            ref = oracle.allreduce(x)
+            for algo in AR_ALGOS:
+                got = run_allreduce(nuna, x, algo, "xcd")
+                for d in range(P):
+                    assert_bitwise(got[d], ref[d], f"VPT=8 {algo} P={P} n={n} rank {d}")
+            bufs = [to_dev(a) for a in x]
+            nuna.allreduce(bufs, bufs, algo="one_shot", placement="linear")
+            torch.cuda.synchronize()
+            for d in range(P):
+                assert_bitwise(to_host(bufs[d]), ref[d], f"VPT=8 in place P={P} n={n} rank {d}")
+            m = n // P
+            xs = [a[:P * m].copy() for a in x]
+            rs = nuna.reduce_scatter([to_dev(a) for a in xs], placement="xcd")
+            torch.cuda.synchronize()
+            for r, want in enumerate(oracle.reduce_scatter(xs)):
+                assert_bitwise(to_host(rs[r]), want, f"VPT=8 RS P={P} rank {r}")
+            ag_in = [a[:m].copy() for a in x]
+            ag = nuna.all_gather([to_dev(a) for a in ag_in], placement="xcd")
+            torch.cuda.synchronize()
+            for d, want in enumerate(oracle.all_gather(ag_in)):
+                assert_bitwise(to_host(ag[d]), want, f"VPT=8 AG P={P} rank {d}")
+
+
+def test_ar_eight_vector_rule_ragged(nuna):
+    """8 ranks at about 15 MiB per rank: the default shape is 8 vectors per thread (its last round
+    of workgroups is over 90 % full); the size ends in a partial chunk and a scalar tail."""
+    n = 15 * (1 << 19) + 8 * 3 + 5
+    x = wl.normal_bf16(8, n, 4242)
+    ref = oracle.allreduce(x)
+    for place in PLACES:
+        got = run_allreduce(nuna, x, "one_shot", place)
+        for d in range(8):
+            assert_bitwise(got[d], ref[d], f"15 MiB ragged {place} rank {d}")
 
 
 # ---------------------------------------------------------------- MoE combine (result collection)
