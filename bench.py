@@ -56,8 +56,9 @@ def parse():
                          "per launch of the dominant kernel, scaled by the reference copy; writes "
                          "profiles/dominant_traffic.json and prints markdown")
     ap.add_argument("--interference", action="store_true",
-                    help="all-gather (P=8, 1 MiB per output) timed while a hipBLASLt GEMM with about 100 output "
-                         "tiles runs on another stream, K swept, LINEAR vs XCD; writes JSONL to --out")
+                    help="all-gather (P=8, 1 MiB per output) and split all-reduce (P=8, [64, 8192]) timed while a "
+                         "hipBLASLt GEMM with about 100 output tiles runs on another stream, K swept, LINEAR vs XCD; "
+                         "writes JSONL to --out")
     ap.add_argument("--affinity", action="store_true",
                     help="probe which die (XCDs 0-3 or 4-7) is near each 8 KiB block of an all-reduce's 16 rank "
                          "buffers (decode T=64 and prefill T=1024 layouts of the pool) and print how well the "
@@ -351,26 +352,54 @@ def roofline_dominant(sweep):
 
 
 def cpu_baseline(seconds):
-    """The oracle (single-threaded C) on the same decode step, repeated for about `seconds`."""
+    """The oracle (single-threaded C) on the same decode step, repeated for about `seconds`; then the
+    same oracle on all host cores, each thread running it on a contiguous element range of every
+    rank buffer (each element still adds its ranks in ascending order, so the bits are the same;
+    checked).  The oracle call releases the interpreter lock while it runs."""
+    import concurrent.futures
     import oracle
     from paper_2608_00867_amd import workloads as wl
     xs = [wl.ar_bf16_decode(T) for T in wl.DECODE_TOKENS]
     step_bytes = sum(2 * len(x) * x[0].size * 2 for x in xs)
     outs = [[np.empty_like(a) for a in x] for x in xs]
     oracle.get()
-    steps = 0
-    t0 = time.perf_counter()
-    while True:
+
+    def timed(run_step, budget):
+        steps = 0
+        t0 = time.perf_counter()
+        while True:
+            run_step()
+            steps += 1
+            el = time.perf_counter() - t0
+            if el >= budget:
+                return steps, el
+
+    def single():
         for x, o in zip(xs, outs):
             oracle.allreduce(x, o)
-        steps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    return {"value": round(step_bytes * steps / el / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} decode steps (all-reduce bf16 P=8 at T=1,4,16,64) in {el:.1f} s, "
-                      f"single thread, inputs resident in host memory; host reports {os.cpu_count()} CPUs",
-            "ms_per_step": round(el / steps * 1e3, 3)}
+
+    steps, el = timed(single, seconds)
+    res = {"value": round(step_bytes * steps / el / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+           "sample": f"{steps} decode steps (all-reduce bf16 P=8 at T=1,4,16,64) in {el:.1f} s, "
+                     f"single thread, inputs resident in host memory; host reports {os.cpu_count()} CPUs",
+           "ms_per_step": round(el / steps * 1e3, 3)}
+    nthreads = max(1, min(os.cpu_count() or 1, 16))
+    outs_mt = [[np.empty_like(a) for a in x] for x in xs]
+    parts = []
+    for x, o in zip(xs, outs_mt):
+        n = x[0].size
+        bounds = [n * k // nthreads for k in range(nthreads + 1)]
+        parts += [([a[lo:hi] for a in x], [b[lo:hi] for b in o]) for lo, hi in zip(bounds, bounds[1:]) if hi > lo]
+    with concurrent.futures.ThreadPoolExecutor(nthreads) as ex:
+        def multi():
+            list(ex.map(lambda io: oracle.allreduce(io[0], io[1]), parts))
+        multi()
+        same = all(np.array_equal(a, b) for o1, o2 in zip(outs, outs_mt) for a, b in zip(o1, o2))
+        steps, el = timed(multi, seconds / 2)
+    res["all_cores"] = {"value": round(step_bytes * steps / el / 1e9, 3), "unit": "GB/s", "threads": nthreads,
+                        "same_bits_as_single": bool(same),
+                        "sample": f"{steps} decode steps in {el:.1f} s, element ranges split over {nthreads} threads"}
+    return res
 
 
 # ---------------------------------------------------------------------------------------------- --full sweep
