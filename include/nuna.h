@@ -45,10 +45,11 @@
  * return without synchronising, and make no allocation, blocking copy or
  * synchronisation, so they can be captured into a HIP graph.
  *
- * Errors.  Every call returns a status and never aborts.  All argument checks
- * run on the host before any HIP call.  On failure,
+ * Errors.  Every call returns a status and never aborts or lets an exception
+ * out.  All argument checks run on the host before any HIP call.  On failure,
  * nuna_last_error_string() describes the problem (per thread).  A launch
- * failure is NUNA_ERR_HIP.
+ * failure is NUNA_ERR_HIP; host memory exhausted while building the call's
+ * own tables (layouts, plans) is NUNA_ERR_NO_MEMORY, and nothing is leaked.
  */
 #ifndef NUNA_H
 #define NUNA_H
@@ -68,7 +69,8 @@ typedef enum {
     NUNA_ERR_UNSUPPORTED = 2, /* dtype / combination not provided */
     NUNA_ERR_MISALIGNED = 3,  /* a data pointer is not 16-byte aligned */
     NUNA_ERR_OVERLAP = 4,     /* buffers overlap other than in the documented in-place forms */
-    NUNA_ERR_HIP = 5          /* the HIP runtime reported an error (no device, launch failure, ...) */
+    NUNA_ERR_HIP = 5,         /* the HIP runtime reported an error (no device, launch failure, ...) */
+    NUNA_ERR_NO_MEMORY = 6    /* host memory for the call's own tables could not be allocated */
 } nuna_status_t;
 
 typedef enum { NUNA_F32 = 0, NUNA_BF16 = 1 } nuna_dtype_t;

@@ -12,7 +12,10 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <exception>
+#include <memory>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -38,6 +41,20 @@ nuna_status_t fail(nuna_status_t st, const char* fmt, ...) {
 nuna_status_t ok() {
     t_err.clear();
     return NUNA_OK;
+}
+
+// Called from a catch handler: turns the exception in flight into a status,
+// so that no exception crosses the C ABI.
+nuna_status_t host_exception() {
+    try {
+        throw;
+    } catch (const std::bad_alloc&) {
+        return fail(NUNA_ERR_NO_MEMORY, "host memory allocation failed");
+    } catch (const std::exception& e) {
+        return fail(NUNA_ERR_INVALID_ARG, "host exception: %s", e.what());
+    } catch (...) {
+        return fail(NUNA_ERR_INVALID_ARG, "unknown host exception");
+    }
 }
 
 nuna_status_t hip_status(hipError_t e, const char* what) {
@@ -232,7 +249,7 @@ nuna_status_t nuna_init(void) {
 }
 
 nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, size_t count, nuna_dtype_t dtype,
-                             nuna_algo_t algo, nuna_placement_t place, hipStream_t stream) {
+                             nuna_algo_t algo, nuna_placement_t place, hipStream_t stream) try {
     nuna_status_t st = check_common(P, dtype, place);
     if (st) return st;
     if (algo < NUNA_ALGO_AUTO || algo > NUNA_ALGO_ONE_SHOT_SPLIT)
@@ -282,10 +299,12 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
     }
     e = nuna::launch_allreduce(in, out, P, count, dtype, groups, place, stream);
     return hip_status(e, "all-reduce launch");
+} catch (...) {
+    return host_exception();
 }
 
 nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P, size_t recvcount,
-                                  nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream) {
+                                  nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream) try {
     nuna_status_t st = check_common(P, dtype, place);
     if (st) return st;
     if ((st = check_ptr_array(in, P, "in"))) return st;
@@ -306,10 +325,12 @@ nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P
     if (st) return st;
     return hip_status(nuna::launch_reduce_scatter(in, out, P, recvcount, dtype, place, false, stream),
                       "reduce-scatter launch");
+} catch (...) {
+    return host_exception();
 }
 
 nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, size_t sendcount, nuna_dtype_t dtype,
-                              nuna_placement_t place, hipStream_t stream) {
+                              nuna_placement_t place, hipStream_t stream) try {
     nuna_status_t st = check_common(P, dtype, place);
     if (st) return st;
     if ((st = check_ptr_array(in, P, "in"))) return st;
@@ -329,6 +350,8 @@ nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, si
     });
     if (st) return st;
     return hip_status(nuna::launch_all_gather(in, out, P, sendcount, dtype, place, false, stream), "all-gather launch");
+} catch (...) {
+    return host_exception();
 }
 
 // ------------------------------------------------------------ all-to-all layout
@@ -356,7 +379,7 @@ struct nuna_a2a_layout {
 };
 
 nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int num_experts, const int32_t* topk_idx,
-                                     nuna_a2a_layout_t** out) {
+                                     nuna_a2a_layout_t** out) try {
     if (!out) return fail(NUNA_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
     if (P < 1 || P > NUNA_MAX_RANKS) return fail(NUNA_ERR_INVALID_ARG, "P=%d outside [1, %d]", P, NUNA_MAX_RANKS);
@@ -376,7 +399,7 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
             return fail(NUNA_ERR_INVALID_ARG, "topk_idx[%lld]=%d outside [0, %d)", static_cast<long long>(i),
                         topk_idx[i], num_experts);
 
-    auto* L = new nuna_a2a_layout();
+    std::unique_ptr<nuna_a2a_layout> L(new nuna_a2a_layout());
     L->P = P;
     L->T = tokens_per_rank;
     L->k = topk;
@@ -457,8 +480,10 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
         L->desc_group.insert(L->desc_group.end(), per_xcd[x].begin(), per_xcd[x].end());
     }
     L->xcd_start[NUNA_NUM_XCD] = L->nitems;
-    *out = L;
+    *out = L.release();
     return ok();
+} catch (...) {
+    return host_exception();
 }
 
 nuna_status_t nuna_a2a_layout_upload(nuna_a2a_layout_t* L) {
@@ -530,7 +555,7 @@ void nuna_a2a_layout_destroy(nuna_a2a_layout_t* L) {
 
 nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const nuna_a2a_layout_t* L,
                               size_t row_elems, size_t recv_capacity_rows, nuna_dtype_t dtype,
-                              nuna_placement_t place, hipStream_t stream) {
+                              nuna_placement_t place, hipStream_t stream) try {
     if (!L) return fail(NUNA_ERR_INVALID_ARG, "layout is NULL");
     const int P = L->P;
     nuna_status_t st = check_common(P, dtype, place);
@@ -561,11 +586,13 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
     hipError_t e = nuna::launch_all_to_all(send, recv, P, desc, L->nitems, L->xcd_start, row_bytes,
                                            static_cast<int>(es), place, stream);
     return hip_status(e, "all-to-all launch");
+} catch (...) {
+    return host_exception();
 }
 
 nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, const nuna_a2a_layout_t* L,
                                       const float* weights, size_t row_elems, size_t y_capacity_rows,
-                                      nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream) {
+                                      nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream) try {
     if (!L) return fail(NUNA_ERR_INVALID_ARG, "layout is NULL");
     const int P = L->P;
     nuna_status_t st = check_common(P, dtype, place);
@@ -601,6 +628,8 @@ nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, co
     hipError_t e = nuna::launch_combine(y, out, P, L->T, L->dev_comb_off, L->dev_comb_ent, weights, row_bytes,
                                         static_cast<int>(dtype), place, stream);
     return hip_status(e, "all-to-all combine launch");
+} catch (...) {
+    return host_exception();
 }
 
 static_assert(NUNA_NAP_MAX_DOMAINS == nuna::kNapMaxDomains && NUNA_NAP_MAX_STACKS == nuna::kNapMaxStacks,
@@ -622,7 +651,7 @@ nuna_status_t nuna_nap_topology_mi355x(nuna_nap_topology_t* topo) {
 nuna_status_t nuna_nap_plan(const nuna_nap_topology_t* topo, int nar_max, int64_t num_tb,
                             const int64_t* chunk_offsets, const int64_t* chunk_ids, const int64_t* tb_bytes,
                             const int64_t* chunk_pages, int64_t* tb_group, int32_t* tb_domain, int32_t* tb_cu,
-                            int32_t* entry_stack, int64_t* num_groups) {
+                            int32_t* entry_stack, int64_t* num_groups) try {
     if (!topo) return fail(NUNA_ERR_INVALID_ARG, "topo is NULL");
     if (topo->num_domains < 1 || topo->num_domains > NUNA_NAP_MAX_DOMAINS || topo->cus_per_domain < 1 ||
         topo->cus_per_domain > (1 << 16) || topo->num_stacks < 1 || topo->num_stacks > NUNA_NAP_MAX_STACKS)
@@ -668,10 +697,12 @@ nuna_status_t nuna_nap_plan(const nuna_nap_topology_t* topo, int nar_max, int64_
         for (size_t e = 0; e < p.entry_stack.size(); ++e) entry_stack[e] = p.entry_stack[e];
     if (num_groups) *num_groups = static_cast<int64_t>(p.groups.size());
     return ok();
+} catch (...) {
+    return host_exception();
 }
 
 nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G, int64_t groups, int64_t group_size,
-                                   int64_t* items, int64_t capacity, int64_t* count) {
+                                   int64_t* items, int64_t capacity, int64_t* count) try {
     if (!valid_place(place)) return fail(NUNA_ERR_INVALID_ARG, "invalid placement mode %d", static_cast<int>(place));
     if (!count || (capacity > 0 && !items) || capacity < 0) return fail(NUNA_ERR_INVALID_ARG, "bad output buffer");
     if (G < 1 || b < 0 || b >= G || groups < 0 || group_size < 1 || group_size > (1 << 20) ||
@@ -688,6 +719,8 @@ nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G,
     if (n > capacity) return fail(NUNA_ERR_INVALID_ARG, "capacity %lld < %lld items", static_cast<long long>(capacity),
                                   static_cast<long long>(n));
     return ok();
+} catch (...) {
+    return host_exception();
 }
 
 nuna_status_t nuna_placement_grid(nuna_placement_t place, int64_t groups, int64_t group_size, int64_t* workgroups) {

@@ -18,9 +18,9 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libnuna.so")
 
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_MISALIGNED, ERR_OVERLAP, ERR_HIP = range(6)
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_MISALIGNED, ERR_OVERLAP, ERR_HIP, ERR_NO_MEMORY = range(7)
 STATUS_NAMES = {0: "NUNA_OK", 1: "NUNA_ERR_INVALID_ARG", 2: "NUNA_ERR_UNSUPPORTED", 3: "NUNA_ERR_MISALIGNED",
-                4: "NUNA_ERR_OVERLAP", 5: "NUNA_ERR_HIP"}
+                4: "NUNA_ERR_OVERLAP", 5: "NUNA_ERR_HIP", 6: "NUNA_ERR_NO_MEMORY"}
 F32, BF16 = 0, 1
 LINEAR, XCD = 0, 1
 ALGO_AUTO, ALGO_ONE_SHOT, ALGO_TWO_SHOT, ALGO_ONE_SHOT_SPLIT = 0, 1, 2, 3

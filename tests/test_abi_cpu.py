@@ -372,3 +372,37 @@ def test_linear_mode_is_round_robin_and_spreads_groups():
     seen = _map(nuna.LINEAR, 64, 8, 8)
     for g in range(8):
         assert len({seen[g * 8 + m][0] % 8 for m in range(8)}) == 8
+
+
+def test_status_codes_match_header():
+    """The binding's status constants are the header's enum values."""
+    text = open(os.path.join(ROOT, "include", "nuna.h")).read()
+    enum = dict((m.group(1), int(m.group(2))) for m in re.finditer(r"\b(NUNA_(?:OK|ERR_[A-Z_]+)) = (\d+)", text))
+    assert enum == {v: k for k, v in nuna.STATUS_NAMES.items()}
+    assert enum["NUNA_ERR_NO_MEMORY"] == nuna.ERR_NO_MEMORY
+
+
+def test_host_allocation_failure_is_a_status():
+    """Host tables that cannot be allocated give NUNA_ERR_NO_MEMORY: no exception leaves the C ABI and
+    the call does not end the process.  A child process caps its own address space 16 MiB above its
+    use, then asks for a routing layout whose host tables need about 64 MiB."""
+    import subprocess
+    import sys
+    code = (
+        "import ctypes, resource, sys\n"
+        "import numpy as np\n"
+        "sys.path.insert(0, %r)\n"
+        "from paper_2608_00867_amd import nuna\n"
+        "L = nuna.lib()\n"
+        "P, T = 8, 1 << 20\n"
+        "topk = np.zeros((P, T, 1), dtype=np.int32)\n"
+        "vm = int(open('/proc/self/statm').read().split()[0]) * resource.getpagesize()\n"
+        "resource.setrlimit(resource.RLIMIT_AS, (vm + (16 << 20), resource.RLIM_INFINITY))\n"
+        "h = ctypes.c_void_p()\n"
+        "st = L.nuna_a2a_layout_create(P, T, 1, 8, topk.ctypes.data, ctypes.byref(h))\n"
+        "print(st, h.value is None, nuna.last_error())\n" % ROOT)
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stderr[-2000:]
+    st, null_handle, msg = out.stdout.strip().split(" ", 2)
+    assert int(st) == nuna.ERR_NO_MEMORY and null_handle == "True", out.stdout
+    assert "allocation" in msg
