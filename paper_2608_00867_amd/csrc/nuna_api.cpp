@@ -78,20 +78,40 @@ struct Span {
 
 bool spans_overlap(const Span& a, const Span& b) { return a.lo < b.hi && b.lo < a.hi; }
 
+// The spans of one call: at most one per rank plus one extra buffer (the
+// combine's weights), held on the stack so a call allocates nothing.
+struct SpanSet {
+    Span v[NUNA_MAX_RANKS + 1];
+    int n = 0;
+    void add(const void* p, size_t bytes, int rank) {
+        const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+        v[n++] = {lo, lo + bytes, rank};
+    }
+};
+
 // Outputs must be pairwise disjoint.  An input may overlap an output only
 // when it is the documented in-place alias of that rank: input span equal to
-// `alias(rank)` exactly.  Sorting keeps the check O(P log P).
+// `alias(rank)` exactly.  Sorting the outputs (in place) keeps the check
+// O(P log P).
 template <class AllowFn>
-nuna_status_t check_overlaps(std::vector<Span> ins, std::vector<Span> outs, AllowFn allowed) {
-    std::sort(outs.begin(), outs.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
-    for (size_t i = 1; i < outs.size(); ++i)
-        if (outs[i].lo < outs[i - 1].hi)
-            return fail(NUNA_ERR_OVERLAP, "output buffers of ranks %d and %d overlap", outs[i - 1].rank, outs[i].rank);
-    for (const Span& s : ins) {
+nuna_status_t check_overlaps(const SpanSet& ins, SpanSet& outs, AllowFn allowed) {
+    Span* ob = outs.v;
+    Span* oe = outs.v + outs.n;
+    if (ob == oe) return NUNA_OK;
+    const auto by_lo = [](const Span& a, const Span& b) { return a.lo < b.lo; };
+    if (!std::is_sorted(ob, oe, by_lo)) std::sort(ob, oe, by_lo);  // callers usually pass them in order
+    for (const Span* o = ob + 1; o < oe; ++o)
+        if (o->lo < (o - 1)->hi)
+            return fail(NUNA_ERR_OVERLAP, "output buffers of ranks %d and %d overlap", (o - 1)->rank, o->rank);
+    // Sorted and disjoint: the outputs lie within [ob->lo, last->hi).
+    const uintptr_t hull_lo = ob->lo, hull_hi = (oe - 1)->hi;
+    for (int k = 0; k < ins.n; ++k) {
+        const Span& s = ins.v[k];
+        if (s.hi <= hull_lo || s.lo >= hull_hi) continue;
         // first output whose end is above s.lo
-        auto it = std::lower_bound(outs.begin(), outs.end(), s.lo,
-                                   [](const Span& o, uintptr_t lo) { return o.hi <= lo; });
-        for (; it != outs.end() && it->lo < s.hi; ++it) {
+        const Span* it = std::lower_bound(static_cast<const Span*>(ob), static_cast<const Span*>(oe), s.lo,
+                                          [](const Span& o, uintptr_t lo) { return o.hi <= lo; });
+        for (; it != oe && it->lo < s.hi; ++it) {
             if (!spans_overlap(s, *it)) continue;
             if (!allowed(s, *it))
                 return fail(NUNA_ERR_OVERLAP, "input of rank %d overlaps output of rank %d outside the in-place form",
@@ -260,11 +280,11 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
     if (count > kMaxBytes / es) return fail(NUNA_ERR_INVALID_ARG, "count %zu too large", count);
     const size_t bytes = count * es;
     if (count == 0) return ok();
-    std::vector<Span> is(P), os(P);
+    SpanSet is, os;
     bool in_place = false;
     for (int r = 0; r < P; ++r) {
-        is[r] = {reinterpret_cast<uintptr_t>(in[r]), reinterpret_cast<uintptr_t>(in[r]) + bytes, r};
-        os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + bytes, r};
+        is.add(in[r], bytes, r);
+        os.add(out[r], bytes, r);
         in_place = in_place || in[r] == out[r];
     }
     st = check_overlaps(is, os, [](const Span& i, const Span& o) { return i.rank == o.rank && i.lo == o.lo; });
@@ -314,10 +334,10 @@ nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P
         return fail(NUNA_ERR_INVALID_ARG, "recvcount %zu too large", recvcount);
     if (recvcount == 0) return ok();
     const size_t mb = recvcount * es;
-    std::vector<Span> is(P), os(P);
+    SpanSet is, os;
     for (int r = 0; r < P; ++r) {
-        is[r] = {reinterpret_cast<uintptr_t>(in[r]), reinterpret_cast<uintptr_t>(in[r]) + mb * P, r};
-        os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + mb, r};
+        is.add(in[r], mb * P, r);
+        os.add(out[r], mb, r);
     }
     st = check_overlaps(is, os, [mb](const Span& i, const Span& o) {
         return i.rank == o.rank && o.lo == i.lo + static_cast<uintptr_t>(o.rank) * mb;
@@ -340,10 +360,10 @@ nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, si
         return fail(NUNA_ERR_INVALID_ARG, "sendcount %zu too large", sendcount);
     if (sendcount == 0) return ok();
     const size_t mb = sendcount * es;
-    std::vector<Span> is(P), os(P);
+    SpanSet is, os;
     for (int r = 0; r < P; ++r) {
-        is[r] = {reinterpret_cast<uintptr_t>(in[r]), reinterpret_cast<uintptr_t>(in[r]) + mb, r};
-        os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + mb * P, r};
+        is.add(in[r], mb, r);
+        os.add(out[r], mb * P, r);
     }
     st = check_overlaps(is, os, [mb](const Span& i, const Span& o) {
         return i.rank == o.rank && i.lo == o.lo + static_cast<uintptr_t>(i.rank) * mb;
@@ -572,11 +592,10 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
                         static_cast<long long>(L->rows[d]), recv_capacity_rows);
     if (static_cast<size_t>(L->T) > kMaxBytes / row_bytes || recv_capacity_rows > kMaxBytes / row_bytes)
         return fail(NUNA_ERR_INVALID_ARG, "buffer sizes too large");
-    std::vector<Span> ss(P), rs(P);
+    SpanSet ss, rs;
     for (int r = 0; r < P; ++r) {
-        ss[r] = {reinterpret_cast<uintptr_t>(send[r]), reinterpret_cast<uintptr_t>(send[r]) + row_bytes * L->T, r};
-        rs[r] = {reinterpret_cast<uintptr_t>(recv[r]),
-                 reinterpret_cast<uintptr_t>(recv[r]) + row_bytes * recv_capacity_rows, r};
+        ss.add(send[r], row_bytes * L->T, r);
+        rs.add(recv[r], row_bytes * recv_capacity_rows, r);
     }
     st = check_overlaps(ss, rs, [](const Span&, const Span&) { return false; });
     if (st) return st;
@@ -611,16 +630,12 @@ nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, co
         return fail(NUNA_ERR_INVALID_ARG, "buffer sizes too large");
     if (weights && (reinterpret_cast<uintptr_t>(weights) & 3u) != 0)
         return fail(NUNA_ERR_MISALIGNED, "weights is not 4-byte aligned");
-    std::vector<Span> ys(P), os(P);
+    SpanSet ys, os;
     for (int r = 0; r < P; ++r) {
-        ys[r] = {reinterpret_cast<uintptr_t>(y[r]), reinterpret_cast<uintptr_t>(y[r]) + row_bytes * y_capacity_rows,
-                 r};
-        os[r] = {reinterpret_cast<uintptr_t>(out[r]), reinterpret_cast<uintptr_t>(out[r]) + row_bytes * L->T, r};
+        ys.add(y[r], row_bytes * y_capacity_rows, r);
+        os.add(out[r], row_bytes * L->T, r);
     }
-    if (weights) {
-        const uintptr_t w0 = reinterpret_cast<uintptr_t>(weights);
-        ys.push_back({w0, w0 + sizeof(float) * static_cast<size_t>(P) * static_cast<size_t>(L->T) * P, -1});
-    }
+    if (weights) ys.add(weights, sizeof(float) * static_cast<size_t>(P) * static_cast<size_t>(L->T) * P, -1);
     st = check_overlaps(ys, os, [](const Span&, const Span&) { return false; });
     if (st) return st;
     if (L->nitems == 0) return ok();
