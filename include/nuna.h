@@ -45,6 +45,12 @@
  * return without synchronising, and make no allocation, blocking copy or
  * synchronisation, so they can be captured into a HIP graph.
  *
+ * Threads.  Collective, layout and planner calls may run concurrently from
+ * several host threads; each thread keeps its own error text.  A layout is
+ * read-only once uploaded and may be shared by concurrent calls.  The
+ * setters nuna_set_max_workgroups and nuna_set_tunable change process-wide
+ * launch shapes and must not race with other calls.
+ *
  * Errors.  Every call returns a status and never aborts or lets an exception
  * out.  All argument checks run on the host before any HIP call.  On failure,
  * nuna_last_error_string() describes the problem (per thread).  A launch

@@ -406,3 +406,29 @@ def test_host_allocation_failure_is_a_status():
     st, null_handle, msg = out.stdout.strip().split(" ", 2)
     assert int(st) == nuna.ERR_NO_MEMORY and null_handle == "True", out.stdout
     assert "allocation" in msg
+
+
+def test_last_error_is_per_thread():
+    """Two threads fail with different errors at the same time; each reads back its own message."""
+    import threading
+    lib = nuna.lib()
+    results = {}
+    barrier = threading.Barrier(2)
+
+    def worker(name, P):
+        barrier.wait()
+        msgs = set()
+        for _ in range(2000):
+            st = nuna.allreduce_raw([0x1000] * P if P > 0 else [], [0x2000] * max(P, 1), P, 16, nuna.BF16)
+            msgs.add((st, lib.nuna_last_error_string().decode()))
+        results[name] = msgs
+
+    threads = [threading.Thread(target=worker, args=("bad_p", 0)), threading.Thread(target=worker, args=("bad_in", 8))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert results["bad_p"] == {(nuna.ERR_INVALID_ARG, "P=0 outside [1, 64]")}
+    assert len(results["bad_in"]) == 1
+    st, msg = next(iter(results["bad_in"]))
+    assert st == nuna.ERR_OVERLAP and "overlap" in msg

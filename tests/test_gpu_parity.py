@@ -738,3 +738,65 @@ def test_copy_kernel(nuna):
         torch.cuda.synchronize()
         assert torch.equal(dst[:nbytes], srcb)
         assert int(dst[nbytes:].abs().sum()) == 0
+
+
+def test_concurrent_host_threads(nuna):
+    """Four host threads, each on its own stream, issue all-reduces, reduce-scatters, all-gathers,
+    dispatches and combines at the same time (one layout shared by all); every result keeps the
+    oracle's bits."""
+    import threading
+    P, T, k, E, H = 8, 64, 4, 32, 256
+    topk = wl.moe_routing(P, T, k, E, 55)
+    lay = nuna.A2ALayout(topk, E).upload()
+    rows = lay.recv_rows()
+    send = wl.normal_bf16(P, T * H, 56)
+    send = [a.reshape(T, H) for a in send]
+    want_recv = oracle.all_to_all(send, topk, E)
+    want_comb = oracle.combine(want_recv, topk, E)
+    errors = []
+    barrier = threading.Barrier(4)
+
+    def worker(w):
+        try:
+            s = torch.cuda.Stream()
+            x = wl.normal_bf16(P, 4096 * (w + 1) + 8 * w, 60 + w)
+            m = x[0].size // P
+            ref_ar = oracle.allreduce(x)
+            ref_rs = oracle.reduce_scatter([a[:P * m].copy() for a in x])
+            ref_ag = oracle.all_gather([a[:m].copy() for a in x])
+            with torch.cuda.stream(s):
+                ins = [to_dev(a) for a in x]
+                rs_in = [t[:P * m] for t in ins]
+                ag_in = [t[:m] for t in ins]
+                snd = [to_dev(a) for a in send]
+                cap = int(rows.max())
+                rcv = [torch.empty((cap, H), dtype=torch.bfloat16, device="cuda") for d in range(P)]
+                out = [torch.empty((T, H), dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+                s.synchronize()
+                barrier.wait()
+                for it in range(10):
+                    place = PLACES[(w + it) % 2]
+                    ar = [torch.empty_like(t) for t in ins]
+                    nuna.allreduce(ins, ar, algo=AR_ALGOS[it % len(AR_ALGOS)], placement=place)
+                    rs = nuna.reduce_scatter(rs_in, placement=place)
+                    ag = nuna.all_gather(ag_in, placement=place)
+                    nuna.all_to_all(snd, rcv, lay, placement=place)
+                    nuna.all_to_all_combine(rcv, out, lay, placement=place)
+                s.synchronize()
+            for d in range(P):
+                assert_bitwise(to_host(ar[d]), ref_ar[d], f"thread {w} AR rank {d}")
+                assert_bitwise(to_host(rs[d]), ref_rs[d], f"thread {w} RS rank {d}")
+                assert_bitwise(to_host(ag[d]), ref_ag[d], f"thread {w} AG rank {d}")
+                assert_bitwise(to_host(rcv[d][:int(rows[d])]).reshape(-1), want_recv[d].reshape(-1),
+                               f"thread {w} A2A rank {d}")
+                assert_bitwise(to_host(out[d]).reshape(-1), want_comb[d].reshape(-1), f"thread {w} combine rank {d}")
+        except Exception as e:  # reported by the main thread
+            errors.append(f"thread {w}: {e!r}")
+
+    threads = [threading.Thread(target=worker, args=(w,)) for w in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    lay.close()
+    assert not errors, errors
