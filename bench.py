@@ -904,12 +904,25 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_00867_amd", "csrc", f)
                   for f in ("nuna_kernels.hip", "device_common.h", "placement.h", "kernels.h")]
 
 
-def kernel_source_sha():
+def kernel_source_text(text):
+    """Source text as the compiler sees it for the traffic check: comments, trailing blanks and empty
+    lines removed, so that a comment edit does not invalidate counters taken with the same code."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
+
+
+def kernel_source_sha(texts=None):
+    """SHA-256 over the dominant kernel's sources (comments and blank lines removed).  `texts` maps a
+    file name to its text; by default the files are read from the tree."""
     import hashlib
     h = hashlib.sha256()
     for path in KERNEL_SOURCES:
-        h.update(os.path.basename(path).encode() + b"\0")
-        h.update(open(path, "rb").read())
+        name = os.path.basename(path)
+        text = texts[name] if texts is not None else open(path).read()
+        h.update(name.encode() + b"\0")
+        h.update(kernel_source_text(text).encode())
     return h.hexdigest()
 
 
@@ -958,7 +971,9 @@ def summarize_traffic(fetch_csv, write_csv):
     alg = 2 * 8 * 64 * 8192 * 2
     rec = {"kernel": dom[0][0], "grid": dom[0][1], "fetch_bytes": round(fetch), "write_bytes": round(write),
            "traffic_bytes": round(fetch + write), "alg_bytes": alg, "fetch_scale": round(ff, 4),
-           "write_scale": round(wf, 4), "kernel_source_sha256": kernel_source_sha()}
+           "write_scale": round(wf, 4), "kernel_source_sha256": kernel_source_sha(),
+           "kernel_source_sha256_covers": ", ".join(os.path.basename(p) for p in KERNEL_SOURCES)
+           + " with comments and blank lines removed"}
     os.makedirs(os.path.dirname(TRAFFIC_JSON), exist_ok=True)
     json.dump(rec, open(TRAFFIC_JSON, "w"), indent=1)
     print("| counter | reference copy (KiB/dispatch, moves %d KiB each way) | scale | dominant kernel (KiB/dispatch) | "

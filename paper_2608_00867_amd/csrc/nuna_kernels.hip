@@ -471,7 +471,7 @@ void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& 
                 else if (P == 64) launch_ar_t<64, 64, DT, 1>(in, out, P, s, pl, G, nt, st);
                 else launch_ar_t<0, 64, DT, 1>(in, out, P, s, pl, G, nt, st);
             } else {
-                launch_ar_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st);  // not reached: pick_vpt gives 1
+                launch_ar_t<0, 64, DT, VPT>(in, out, P, s, pl, G, nt, st);  // other P up to 16 (above: VPT 1)
             }
             break;
     }
@@ -499,7 +499,7 @@ void launch_rs_p(const void* const* in, void* const* out, int P, const RsShape& 
                 else if (P == 64) launch_rs_t<64, 64, DT, 1, KEEP>(in, out, P, s, pl, G, nt, st);
                 else launch_rs_t<0, 64, DT, 1, KEEP>(in, out, P, s, pl, G, nt, st);
             } else {
-                launch_rs_t<0, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st);  // not reached: pick_vpt gives 1
+                launch_rs_t<0, 64, DT, VPT, KEEP>(in, out, P, s, pl, G, nt, st);  // other P up to 16 (above: VPT 1)
             }
             break;
     }
