@@ -351,6 +351,16 @@ def roofline_dominant(sweep):
             "alg_bytes_per_launch": row["alg_bytes"], "avg_launch_us": us}
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(seconds):
     """The oracle (single-threaded C) on the same decode step, repeated for about `seconds`; then the
     same oracle on all host cores, each thread running it on a contiguous element range of every
@@ -382,7 +392,7 @@ def cpu_baseline(seconds):
     res = {"value": round(step_bytes * steps / el / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
            "sample": f"{steps} decode steps (all-reduce bf16 P=8 at T=1,4,16,64) in {el:.1f} s, "
                      f"single thread, inputs resident in host memory; host reports {os.cpu_count()} CPUs",
-           "ms_per_step": round(el / steps * 1e3, 3)}
+           "cpu_model": cpu_model(), "ms_per_step": round(el / steps * 1e3, 3)}
     nthreads = max(1, min(os.cpu_count() or 1, 16))
     outs_mt = [[np.empty_like(a) for a in x] for x in xs]
     parts = []

@@ -179,9 +179,9 @@ __global__ __launch_bounds__(kWG) void k_allreduce_lpr(Ptrs<64> p, LprShape s, P
         __syncthreads();
         // 4 * lim output dwords; with fewer than 4 ranks there are more of
         // them than threads.
-        for (int c = t; c < lim * 4; c += kWG) {
-            const uint32_t* col = reinterpret_cast<const uint32_t*>(lds) + c;
-            reinterpret_cast<uint32_t*>(res)[c] = lpr_sum_column<PT, DT>(col, V * 4, P);
+        for (int dw = t; dw < lim * 4; dw += kWG) {
+            const uint32_t* col = reinterpret_cast<const uint32_t*>(lds) + dw;
+            reinterpret_cast<uint32_t*>(res)[dw] = lpr_sum_column<PT, DT>(col, V * 4, P);
         }
         __syncthreads();
         if (active && vec < lim) store_stream(my_out + base + vec, res[vec]);
