@@ -69,6 +69,12 @@ def parse():
                          "combine, eager, then exit")
     ap.add_argument("--summarize-l2", nargs=2, metavar=("LINEAR_CSV", "XCD_CSV"), default=None,
                     help="markdown table of TCC_HIT_sum / TCC_MISS_sum from two --profile runs (LINEAR, XCD)")
+    ap.add_argument("--xcc-counter-defs", metavar="YAML", default=None,
+                    help="write rocprofv3 counter definitions TCC_HIT_XCC<x> / TCC_MISS_XCC<x> (L2 hits and misses of "
+                         "one XCD, summed over its 16 channels) for `rocprofv3 -E`, then exit")
+    ap.add_argument("--summarize-l2-xcc", nargs="+", metavar="PLACE=CSV", default=None,
+                    help="markdown table of per-XCD L2 hit rates from --profile runs with the --xcc-counter-defs "
+                         "counters, e.g. linear=a.csv linear=b.csv xcd=c.csv ...")
     ap.add_argument("--profile-place", choices=("linear", "xcd"), default="xcd",
                     help="placement of the split all-reduce and MoE kernels in --profile")
     return ap.parse_args()
@@ -1036,6 +1042,58 @@ def summarize_l2(linear_csv, xcd_csv):
             print(f"| `{k[0]}` | {k[1]} | {mode} | {h:.0f} | {m:.0f} | {h / (h + m):.3f} |")
 
 
+def write_xcc_counter_defs(path):
+    """rocprofv3 extra counters: TCC_HIT and TCC_MISS of one XCC (the 16 L2 channels of that XCD)."""
+    lines = ["rocprofiler-sdk:", "  counters-schema-version: 1", "  counters:"]
+    for x in range(8):
+        for c in ("HIT", "MISS"):
+            lines += [f"  - name: TCC_{c}_XCC{x}",
+                      f"    description: TCC_{c} summed over the 16 L2 channels of XCC {x}.",
+                      "    properties: []",
+                      "    definitions:",
+                      "    - architectures:",
+                      "      - gfx950",
+                      f"      expression: reduce(select(TCC_{c},[DIMENSION_XCC=[{x}]]),sum)"]
+    d = os.path.dirname(path)
+    if d:
+        os.makedirs(d, exist_ok=True)
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def summarize_l2_xcc(specs):
+    """Per-XCD L2 hit rate (median over the dispatches of each pass) of the kernels whose map the placement
+    changes, from passes that each collected some of the TCC_HIT_XCC<x> / TCC_MISS_XCC<x> counters."""
+    import csv
+    import collections
+    vals = collections.defaultdict(list)  # (place, kernel, grid, counter) -> values
+    for spec in specs:
+        place, path = spec.split("=", 1)
+        for r in csv.DictReader(open(path)):
+            vals[(place.upper(), _short(r["Kernel_Name"]), int(r["Grid_Size"]), r["Counter_Name"])].append(
+                float(r["Counter_Value"]))
+    places = sorted({k[0] for k in vals})
+    kernels = sorted({(k[1], k[2]) for k in vals if k[1].startswith(("k_allreduce", "k_all_to_all", "k_combine"))})
+    print("| kernel | grid (threads) | placement | " + " | ".join(f"XCD {x}" for x in range(8)) + " | min–max |")
+    print("|---|---|---|" + "---|" * 9)
+    for kern, grid in kernels:
+        for place in places:
+            rates = []
+            for x in range(8):
+                h = vals.get((place, kern, grid, f"TCC_HIT_XCC{x}"))
+                m = vals.get((place, kern, grid, f"TCC_MISS_XCC{x}"))
+                if not h or not m:
+                    rates.append(None)
+                    continue
+                hh, mm = statistics.median(h), statistics.median(m)
+                rates.append(hh / (hh + mm) if hh + mm else None)
+            if all(r is None for r in rates):
+                continue
+            got = [r for r in rates if r is not None]
+            cells = " | ".join("—" if r is None else f"{r:.2f}" for r in rates)
+            print(f"| `{kern}` | {grid} | {place} | {cells} | {min(got):.2f}–{max(got):.2f} |")
+
+
 def measured_traffic():
     """HBM bytes per launch of the dominant kernel from the committed counter summary, or None when the
     kernel source has changed since the counters were taken."""
@@ -1057,6 +1115,12 @@ def main():
         return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic)
+        return
+    if args.xcc_counter_defs:
+        write_xcc_counter_defs(args.xcc_counter_defs)
+        return
+    if args.summarize_l2_xcc:
+        summarize_l2_xcc(args.summarize_l2_xcc)
         return
     if args.summarize_l2:
         summarize_l2(*args.summarize_l2)
