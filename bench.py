@@ -589,7 +589,8 @@ def eager_case(nuna, torch, pool, args, emit):
 
 def combine_case(nuna, torch, pool, args, emit):
     """MoE combine at the dispatch's shape: every received row comes back as a result row and is
-    summed into its token (reads: all result rows; writes: every token row once)."""
+    summed into its token (reads: all result rows; writes: every token row once), unweighted and with
+    one gate weight per (token, destination rank)."""
     import oracle
     from paper_2608_00867_amd import workloads as wl
     _, topk = wl.a2a_moe()
@@ -599,44 +600,49 @@ def combine_case(nuna, torch, pool, args, emit):
     rows = lay.recv_rows()
     cap = int(rows.max())
     rb = H * 2
-    alg_bytes = int(rows.sum() * rb + P * T * rb)
     set_bytes = P * cap * rb + P * T * rb
     y_np = wl.result_rows(rows, H, np.uint16, wl.seed_for(4, 7))
     src = [dev_copy_of(torch, a.reshape(-1)) for a in y_np]
-    ref = oracle.combine(y_np, topk, E)
-    for cold in (True, False):
-        nsets = max(1, min(pool.nbytes // (set_bytes + 16 * ALIGN), math.ceil(COLD_SPAN / set_bytes) + 1)) \
-            if cold else 1
-        pool.off = 0
-        sets = []
-        for _ in range(nsets):
-            y = [pool.take(cap * rb).view(torch.bfloat16).view(cap, H) for _ in range(P)]
-            out = [pool.take(T * rb).view(torch.bfloat16).view(T, H) for _ in range(P)]
-            for d in range(P):
-                y[d][:int(rows[d])].view(-1).copy_(src[d])
-            sets.append((y, out))
-        calls = max(4, nsets)
-        ok = True
-        for p in ("linear", "xcd"):
-            nuna.all_to_all_combine(sets[0][0], sets[0][1], lay, placement=p)
-            torch.cuda.synchronize()
-            for d in range(P):
-                g = sets[0][1][d].cpu().view(torch.int16).numpy().view(np.uint16)
-                ok = ok and np.array_equal(g, ref[d])
-        graphs = {p: capture(torch, lambda i, p=p: nuna.all_to_all_combine(sets[i % nsets][0], sets[i % nsets][1],
-                                                                            lay, placement=p), calls)
-                  for p in ("linear", "xcd")}
-        t = time_graphs(torch, graphs, calls, args.reps, args.warmup)
-        res = {p: stats(t[p]) for p in t}
-        emit({"workload": "a2a_moe_combine_bf16_p8", "P": P, "tokens_per_rank": T, "hidden": H,
-              "result_rows": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
-              "calls_per_graph": calls, "parity": bool(ok),
-              **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
-              **{f"{p}_gbps": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9, 1) for p in res},
-              **{f"{p}_frac_hbm": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
-                 for p in res},
-              "linear_over_xcd_time": round(res["linear"]["median"] / res["xcd"]["median"], 4)})
-        del graphs, sets
+    w_np = wl.gate_weights(topk, E, wl.seed_for(4, 8))
+    w_dev = torch.from_numpy(w_np).cuda()
+    for weighted in (False, True):
+        ref = oracle.combine(y_np, topk, E, w_np if weighted else None)
+        wt = w_dev if weighted else None
+        alg_bytes = int(rows.sum() * rb + P * T * rb + (w_np.nbytes if weighted else 0))
+        name = "a2a_moe_combine_weighted_bf16_p8" if weighted else "a2a_moe_combine_bf16_p8"
+        for cold in (True, False):
+            nsets = max(1, min(pool.nbytes // (set_bytes + 16 * ALIGN), math.ceil(COLD_SPAN / set_bytes) + 1)) \
+                if cold else 1
+            pool.off = 0
+            sets = []
+            for _ in range(nsets):
+                y = [pool.take(cap * rb).view(torch.bfloat16).view(cap, H) for _ in range(P)]
+                out = [pool.take(T * rb).view(torch.bfloat16).view(T, H) for _ in range(P)]
+                for d in range(P):
+                    y[d][:int(rows[d])].view(-1).copy_(src[d])
+                sets.append((y, out))
+            calls = max(4, nsets)
+            ok = True
+            for p in ("linear", "xcd"):
+                nuna.all_to_all_combine(sets[0][0], sets[0][1], lay, placement=p, weights=wt)
+                torch.cuda.synchronize()
+                for d in range(P):
+                    g = sets[0][1][d].cpu().view(torch.int16).numpy().view(np.uint16)
+                    ok = ok and np.array_equal(g, ref[d])
+            graphs = {p: capture(torch, lambda i, p=p: nuna.all_to_all_combine(
+                sets[i % nsets][0], sets[i % nsets][1], lay, placement=p, weights=wt), calls)
+                for p in ("linear", "xcd")}
+            t = time_graphs(torch, graphs, calls, args.reps, args.warmup)
+            res = {p: stats(t[p]) for p in t}
+            emit({"workload": name, "P": P, "tokens_per_rank": T, "hidden": H,
+                  "result_rows": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
+                  "calls_per_graph": calls, "parity": bool(ok),
+                  **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
+                  **{f"{p}_gbps": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9, 1) for p in res},
+                  **{f"{p}_frac_hbm": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+                     for p in res},
+                  "linear_over_xcd_time": round(res["linear"]["median"] / res["xcd"]["median"], 4)})
+            del graphs, sets
     lay.close()
 
 

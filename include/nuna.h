@@ -63,6 +63,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
+/* Plain C and C++ compilers other than hipcc compile this header with
+ * -D__HIP_PLATFORM_AMD__ and -I/opt/rocm/include, as HIP's own headers
+ * require; it is C99. */
 #include <hip/hip_runtime_api.h>
 
 #ifdef __cplusplus

@@ -126,6 +126,17 @@ def result_rows(rows, hidden, dtype, seed):
     return out
 
 
+def gate_weights(topk, num_experts, seed):
+    """fp32 [P, T, P] combine weights: for each token, a uniform (0, 1) weight for every destination
+    rank that owns one of its experts, 0 for the other ranks."""
+    P, T, k = topk.shape
+    g = _rng(seed)
+    w = np.zeros((P, T, P), dtype=np.float32)
+    ranks = np.asarray(topk) // (num_experts // P)
+    np.put_along_axis(w, ranks, g.random((P, T, k)).astype(np.float32), axis=2)
+    return w
+
+
 # ---- named workloads ------------------------------------------------------
 
 def ar_f32_int(seed=None, P=8, n=2048):
