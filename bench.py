@@ -420,12 +420,42 @@ def cpu_baseline(seconds):
 
 # ---------------------------------------------------------------------------------------------- --full sweep
 
+NO_SLOWER_TOL = 1.02   # XCD counts as no slower within 2 % of LINEAR's median
+TARGET_FRAC = 0.70     # of the HBM peak, for messages of 4 MiB per rank and more
+TARGET_MIN_BYTES = 4 << 20
+
+
+def message_bytes_per_rank(rec):
+    """Bytes one rank contributes to the collective: its all-reduce buffer, its reduce-scatter input
+    (P shards), its all-gather output (P shards), or its MoE token rows."""
+    if "bytes_per_rank" in rec:
+        return rec["bytes_per_rank"]
+    if "shard_bytes" in rec:
+        return rec["shard_bytes"] * rec["P"]
+    if "tokens_per_rank" in rec:
+        return rec["tokens_per_rank"] * rec["hidden"] * 2
+    return None
+
+
+def annotate_targets(rec):
+    """Per-record verdicts on the two comparative targets.  xcd_no_slower: XCD's median within 2 % of
+    LINEAR's, or the two distributions overlap (XCD's p10 at or below LINEAR's p90).  meets_70pct: at
+    4 MiB per rank and more, XCD reaches 70 % of the HBM peak."""
+    lx, xx = rec.get("linear_us"), rec.get("xcd_us")
+    if isinstance(lx, dict) and isinstance(xx, dict):
+        rec["xcd_no_slower"] = bool(xx["median"] <= NO_SLOWER_TOL * lx["median"] or xx["p10"] <= lx["p90"])
+    mb = message_bytes_per_rank(rec)
+    if mb is not None and mb >= TARGET_MIN_BYTES and "xcd_frac_hbm" in rec:
+        rec["meets_70pct"] = bool(rec["xcd_frac_hbm"] >= TARGET_FRAC)
+
+
 def full_sweep(nuna, torch, pool, args):
     from paper_2608_00867_amd import workloads as wl
     os.makedirs(os.path.dirname(args.out), exist_ok=True)
     f = open(args.out, "w")
 
     def emit(rec):
+        annotate_targets(rec)
         f.write(json.dumps(rec) + "\n")
         f.flush()
         print(json.dumps(rec), flush=True)
