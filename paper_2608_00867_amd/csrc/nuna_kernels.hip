@@ -81,6 +81,38 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
     }
 }
 
+// Direct one-shot: one work item per workgroup on the linear map, which is
+// every uncapped launch whose groups have one item.  Workgroup b reduces
+// chunk b.  All the kernel reads from its arguments sits at fixed offsets
+// (the pointers, the vector count, the tail), so one round of scalar loads
+// brings everything and the first vector loads follow at once.  The general
+// kernel above first reads its placement state and then the pointers, a chain
+// of dependent argument loads that measured about 1 us per launch at 1 MiB
+// per rank on MI355X (5.3 against 4.2 us).
+template <int PT, int DT, int VPT>
+__global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nvec, int32_t tail) {
+    using A = Arith<DT>;
+    const int nt = blockDim.x;
+    const int64_t cv = static_cast<int64_t>(nt) * VPT;
+    const int64_t c = blockIdx.x;
+    const int64_t v0 = c * cv + threadIdx.x;
+    ArShape s{};
+    s.nvec = nvec;
+    s.dpi = PT;
+    s.P = PT;
+    const RankTable tab{0u, 0u, 0u, 0u};  // compile-time rank count: pointers come from the arguments
+    if ((c + 1) * cv <= nvec)
+        allreduce_chunk<PT, DT, VPT, true, true>(p, tab, s, PT, v0, nt, 0, true);
+    else
+        allreduce_chunk<PT, DT, VPT, false, true>(p, tab, s, PT, v0, nt, 0, true);
+    if (tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < tail) {
+        const int64_t i = nvec * (16 / A::kEsize) + threadIdx.x;
+        float a = A::load1(p.in[0], i);
+        for (int r = 1; r < PT; ++r) a = a + A::load1(p.in[r], i);
+        for (int d = 0; d < PT; ++d) A::store1(p.out[d], i, a);
+    }
+}
+
 // ---------------------------------------------------------------- all-reduce, lane per rank (many ranks)
 //
 // With many ranks a thread that owns one vector position must issue P loads
@@ -477,6 +509,29 @@ void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& 
     }
 }
 
+template <int PT, int DT, int VPT>
+void launch_ar_direct_t(const void* const* in, void* const* out, const ArShape& s, int64_t G, int nt, hipStream_t st) {
+    const Ptrs<PT> p = make_ptrs<PT>(in, out, PT, PT);
+    hipLaunchKernelGGL((k_allreduce_direct<PT, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p, s.nvec,
+                       s.tail);
+}
+
+// Direct kernel for 2, 4, 8 or 16 ranks (8 vectors per thread: 2, 4 or 8 ranks).
+template <int DT, int VPT>
+void launch_ar_direct_p(const void* const* in, void* const* out, int P, const ArShape& s, int64_t G, int nt,
+                        hipStream_t st) {
+    switch (P) {
+        case 2: launch_ar_direct_t<2, DT, VPT>(in, out, s, G, nt, st); break;
+        case 4: launch_ar_direct_t<4, DT, VPT>(in, out, s, G, nt, st); break;
+        case 8: launch_ar_direct_t<8, DT, VPT>(in, out, s, G, nt, st); break;
+        default:
+            if constexpr (VPT != 8) launch_ar_direct_t<16, DT, VPT>(in, out, s, G, nt, st);
+            break;
+    }
+}
+
+bool direct_ranks(int P, int vpt) { return P == 2 || P == 4 || P == 8 || (P == 16 && vpt != 8); }
+
 template <int PT, int MAXP, int DT, int VPT, bool KEEP>
 void launch_rs_t(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G, int nt,
                  hipStream_t st) {
@@ -751,6 +806,21 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
                                 : mode;
     const Place pl = make_place_uniform(gmode, groups > 0 ? groups : 1, gsize);
     const int64_t G = cap_grid(place_grid(pl));
+    // One item per workgroup on the linear map: the direct kernel.
+    if (gsize == 1 && G == groups && direct_ranks(P, vpt)) {
+        if (dtype == kDtF32) {
+            if (vpt == 8) launch_ar_direct_p<kDtF32, 8>(in, out, P, s, G, nt, stream);
+            else if (vpt == 4) launch_ar_direct_p<kDtF32, 4>(in, out, P, s, G, nt, stream);
+            else if (vpt == 2) launch_ar_direct_p<kDtF32, 2>(in, out, P, s, G, nt, stream);
+            else launch_ar_direct_p<kDtF32, 1>(in, out, P, s, G, nt, stream);
+        } else {
+            if (vpt == 8) launch_ar_direct_p<kDtBf16, 8>(in, out, P, s, G, nt, stream);
+            else if (vpt == 4) launch_ar_direct_p<kDtBf16, 4>(in, out, P, s, G, nt, stream);
+            else if (vpt == 2) launch_ar_direct_p<kDtBf16, 2>(in, out, P, s, G, nt, stream);
+            else launch_ar_direct_p<kDtBf16, 1>(in, out, P, s, G, nt, stream);
+        }
+        return hipGetLastError();
+    }
     // The kernel's vectors per thread must be the VPT the chunks were sized with.
     if (dtype == kDtF32) {
         if (vpt == 8) launch_ar_p<kDtF32, 8>(in, out, P, s, pl, G, nt, stream);
