@@ -353,7 +353,7 @@ def roofline_dominant(sweep):
     achieved = row["alg_bytes"] / (us * 1e-6) / 1e9
     return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(),
-            "kernel": "k_allreduce<P=8,bf16,VPT=1> one-shot, [64,8192] bf16 per rank, XCD placement",
+            "kernel": "k_allreduce_direct<P=8,bf16,VPT=1> one-shot, [64,8192] bf16 per rank, XCD placement",
             "alg_bytes_per_launch": row["alg_bytes"], "avg_launch_us": us}
 
 
@@ -512,6 +512,8 @@ def full_sweep(nuna, torch, pool, args):
         combine_case(nuna, torch, pool, args, emit)
     if want("copy_reference"):
         copy_case(nuna, torch, pool, args, emit)
+    if want("launch_floor"):
+        launch_floor_case(nuna, torch, args, emit)
     f.close()
 
 
@@ -674,6 +676,23 @@ def combine_case(nuna, torch, pool, args, emit):
                   "linear_over_xcd_time": round(res["linear"]["median"] / res["xcd"]["median"], 4)})
             del graphs, sets
     lay.close()
+
+
+def launch_floor_case(nuna, torch, args, emit):
+    """Per-call time of the library's smallest kernel (the dispatch probe: one argument load and one
+    4-byte store per workgroup) in the same graph replay as the collectives: the floor that launch
+    and completion put under every call."""
+    calls = 2048
+    for G in (1, 256):
+        xcc = torch.empty(G, dtype=torch.int32, device="cuda")
+
+        def fn(i, G=G, xcc=xcc):
+            st = nuna.lib().nuna_probe_xcc(G, xcc.data_ptr(), None, torch.cuda.current_stream().cuda_stream)
+            assert st == 0, nuna.last_error()
+        g = {"probe": capture(torch, fn, calls)}
+        t = stats(time_graphs(torch, g, calls, args.reps, args.warmup)["probe"])
+        emit({"workload": "launch_floor", "kernel": "k_probe_xcc", "workgroups": G, "threads_per_workgroup": 64,
+              "calls_per_graph": calls, "us": {k: round(v, 3) for k, v in t.items()}})
 
 
 def copy_case(nuna, torch, pool, args, emit):

@@ -82,13 +82,13 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
 }
 
 // Direct one-shot: one work item per workgroup on the linear map, which is
-// every uncapped launch whose groups have one item.  Workgroup b reduces
-// chunk b.  All the kernel reads from its arguments sits at fixed offsets
-// (the pointers, the vector count, the tail), so one round of scalar loads
-// brings everything and the first vector loads follow at once.  The general
-// kernel above first reads its placement state and then the pointers, a chain
-// of dependent argument loads that measured about 1 us per launch at 1 MiB
-// per rank on MI355X (5.3 against 4.2 us).
+// every uncapped launch whose groups have one item (up to kDirectMaxGrid
+// workgroups).  Workgroup b reduces chunk b.  All the kernel reads from its
+// arguments sits at fixed offsets (the pointers, the vector count, the tail),
+// so one round of scalar loads brings everything and the first vector loads
+// follow at once.  The general kernel above first reads its placement state
+// and then the pointers, a chain of dependent argument loads that measured
+// about 1 us per launch at 1 MiB per rank on MI355X (5.3 against 4.2 us).
 template <int PT, int DT, int VPT>
 __global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nvec, int32_t tail) {
     using A = Arith<DT>;
@@ -354,6 +354,26 @@ __global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s,
     }
 }
 
+// Direct reduce-scatter: grid (chunks per shard, P), workgroup (c, r) reduces
+// chunk c of shard r; everything it reads from its arguments sits at fixed
+// offsets (see k_allreduce_direct).
+template <int PT, int DT, int VPT, bool KEEP>
+__global__ __launch_bounds__(kWG) void k_reduce_scatter_direct(Ptrs<PT> p, int64_t mv) {
+    const int nt = blockDim.x;
+    const int64_t cv = static_cast<int64_t>(nt) * VPT;
+    const int64_t c = blockIdx.x;
+    const int64_t r = blockIdx.y;
+    const int64_t v0 = c * cv + threadIdx.x;
+    RsShape s{};
+    s.mv = mv;
+    s.P = PT;
+    const RankTable tab{0u, 0u, 0u, 0u};  // compile-time rank count: pointers come from the arguments
+    if ((c + 1) * cv <= mv)
+        reduce_scatter_chunk<PT, DT, VPT, true, KEEP>(p, tab, s, PT, r, v0, nt);
+    else
+        reduce_scatter_chunk<PT, DT, VPT, false, KEEP>(p, tab, s, PT, r, v0, nt);
+}
+
 // Element-wise fallback when a shard is not a whole number of 16-byte vectors.
 template <int DT>
 __global__ __launch_bounds__(kWG) void k_reduce_scatter_elem(Ptrs<64> p, int P, int64_t m) {
@@ -418,6 +438,35 @@ __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Pla
             else
                 all_gather_chunk<VPT, false, false>(tab, s, r, v0, nt, g);
         }
+    }
+}
+
+// Direct all-gather (every destination per work item): grid (chunks per
+// shard, P), workgroup (c, r) copies chunk c of shard r to every destination.
+// The source pointer is an argument indexed by the workgroup's y index; the
+// destinations are compile-time offsets (see k_allreduce_direct).
+template <int PT, int VPT, bool CACHED>
+__global__ __launch_bounds__(kWG) void k_all_gather_direct(Ptrs<PT> p, int64_t mv) {
+    const int nt = blockDim.x;
+    const int64_t cv = static_cast<int64_t>(nt) * VPT;
+    const int64_t c = blockIdx.x;
+    const int r = static_cast<int>(blockIdx.y);
+    const int64_t v0 = c * cv + threadIdx.x;
+    const uint4* src = p.in[r];
+    uint4 y[VPT];
+    const bool full = (c + 1) * cv <= mv;
+    if (full)
+        load_vecs<true, VPT, !CACHED>(y, src, v0, nt, mv);
+    else
+        load_vecs<false, VPT, !CACHED>(y, src, v0, nt, mv);
+#pragma unroll
+    for (int d = 0; d < PT; ++d) {
+        uint4* dst = p.out[d] + r * mv;
+        if (dst == src) continue;  // in-place shard
+        if (full)
+            store_vecs<true, VPT>(dst, y, v0, nt, mv);
+        else
+            store_vecs<false, VPT>(dst, y, v0, nt, mv);
     }
 }
 
@@ -531,6 +580,13 @@ void launch_ar_direct_p(const void* const* in, void* const* out, int P, const Ar
 }
 
 bool direct_ranks(int P, int vpt) { return P == 2 || P == 4 || P == 8 || (P == 16 && vpt != 8); }
+
+// Largest grid that takes the direct kernels.  Beyond it the general kernels
+// run: at 64 MiB per rank with one vector per thread (16384 workgroups) the
+// general all-reduce measured 12 % faster than the direct one on MI355X (184
+// against 209 us), while up to 8192 workgroups the direct kernels were as fast
+// or faster at every size measured (1-64 MiB per rank, 1-4 vectors per thread).
+constexpr int64_t kDirectMaxGrid = 8192;
 
 template <int PT, int MAXP, int DT, int VPT, bool KEEP>
 void launch_rs_t(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G, int nt,
@@ -807,7 +863,7 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
     const Place pl = make_place_uniform(gmode, groups > 0 ? groups : 1, gsize);
     const int64_t G = cap_grid(place_grid(pl));
     // One item per workgroup on the linear map: the direct kernel.
-    if (gsize == 1 && G == groups && direct_ranks(P, vpt)) {
+    if (gsize == 1 && G == groups && G <= kDirectMaxGrid && direct_ranks(P, vpt)) {
         if (dtype == kDtF32) {
             if (vpt == 8) launch_ar_direct_p<kDtF32, 8>(in, out, P, s, G, nt, stream);
             else if (vpt == 4) launch_ar_direct_p<kDtF32, 4>(in, out, P, s, G, nt, stream);
@@ -832,6 +888,43 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
         else if (vpt == 4) launch_ar_p<kDtBf16, 4>(in, out, P, s, pl, G, nt, stream);
         else if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, stream);
         else launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
+    }
+    return hipGetLastError();
+}
+
+template <int PT, int DT, int VPT, bool KEEP>
+void launch_rs_direct_t(const void* const* in, void* const* out, const RsShape& s, int nt, hipStream_t st) {
+    const Ptrs<PT> p = make_ptrs<PT>(in, out, PT, PT);
+    hipLaunchKernelGGL((k_reduce_scatter_direct<PT, DT, VPT, KEEP>),
+                       dim3(static_cast<unsigned>(s.wcs), static_cast<unsigned>(PT)), dim3(nt), 0, st, p, s.mv);
+}
+
+template <int DT, int VPT, bool KEEP>
+void launch_rs_direct_p(const void* const* in, void* const* out, int P, const RsShape& s, int nt, hipStream_t st) {
+    switch (P) {
+        case 2: launch_rs_direct_t<2, DT, VPT, KEEP>(in, out, s, nt, st); break;
+        case 4: launch_rs_direct_t<4, DT, VPT, KEEP>(in, out, s, nt, st); break;
+        case 8: launch_rs_direct_t<8, DT, VPT, KEEP>(in, out, s, nt, st); break;
+        default: launch_rs_direct_t<16, DT, VPT, KEEP>(in, out, s, nt, st); break;
+    }
+}
+
+// Every uncapped reduce-scatter of 2, 4, 8 or 16 ranks (single-item groups,
+// so both placements run the linear map).
+hipError_t launch_rs_direct(const void* const* in, void* const* out, int P, const RsShape& s, int dtype, int vpt,
+                            int nt, bool keep, hipStream_t st) {
+    if (dtype == kDtF32) {
+        if (keep) launch_rs_direct_p<kDtF32, 1, true>(in, out, P, s, nt, st);
+        else launch_rs_direct_p<kDtF32, 1, false>(in, out, P, s, nt, st);
+    } else if (vpt == 4) {
+        if (keep) launch_rs_direct_p<kDtBf16, 4, true>(in, out, P, s, nt, st);
+        else launch_rs_direct_p<kDtBf16, 4, false>(in, out, P, s, nt, st);
+    } else if (vpt == 2) {
+        if (keep) launch_rs_direct_p<kDtBf16, 2, true>(in, out, P, s, nt, st);
+        else launch_rs_direct_p<kDtBf16, 2, false>(in, out, P, s, nt, st);
+    } else {
+        if (keep) launch_rs_direct_p<kDtBf16, 1, true>(in, out, P, s, nt, st);
+        else launch_rs_direct_p<kDtBf16, 1, false>(in, out, P, s, nt, st);
     }
     return hipGetLastError();
 }
@@ -861,6 +954,8 @@ hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P,
     s.wcs = (s.mv + cv - 1) / cv;
     const Place pl = make_place_uniform(mode, s.wcs * P, 1);
     const int64_t G = cap_grid(place_grid(pl));
+    if (G == s.wcs * P && G <= kDirectMaxGrid && (P == 2 || P == 4 || P == 8 || P == 16))
+        return launch_rs_direct(in, out, P, s, dtype, vpt, nt, keep_output, stream);
     if (dtype == kDtF32) {
         if (keep_output) launch_rs_p<kDtF32, 1, true>(in, out, P, s, pl, G, nt, stream);
         else launch_rs_p<kDtF32, 1, false>(in, out, P, s, pl, G, nt, stream);
@@ -875,6 +970,21 @@ hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P,
         else launch_rs_p<kDtBf16, 1, false>(in, out, P, s, pl, G, nt, stream);
     }
     return hipGetLastError();
+}
+
+template <int PT>
+void launch_ag_direct_p(const void* const* in, void* const* out, const AgShape& s, int vpt, bool cached, dim3 g,
+                        dim3 b, hipStream_t st) {
+    const Ptrs<PT> p = make_ptrs<PT>(in, out, PT, PT);
+    if (cached) {
+        if (vpt == 4) hipLaunchKernelGGL((k_all_gather_direct<PT, 4, true>), g, b, 0, st, p, s.mv);
+        else if (vpt == 2) hipLaunchKernelGGL((k_all_gather_direct<PT, 2, true>), g, b, 0, st, p, s.mv);
+        else hipLaunchKernelGGL((k_all_gather_direct<PT, 1, true>), g, b, 0, st, p, s.mv);
+    } else {
+        if (vpt == 4) hipLaunchKernelGGL((k_all_gather_direct<PT, 4, false>), g, b, 0, st, p, s.mv);
+        else if (vpt == 2) hipLaunchKernelGGL((k_all_gather_direct<PT, 2, false>), g, b, 0, st, p, s.mv);
+        else hipLaunchKernelGGL((k_all_gather_direct<PT, 1, false>), g, b, 0, st, p, s.mv);
+    }
 }
 
 hipError_t launch_all_gather(const void* const* in, void* const* out, int P, size_t m, int dtype, int mode,
@@ -912,6 +1022,15 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
                                 : mode;
     const Place pl = make_place_uniform(gmode, s.wcs * P, gsize);
     const int64_t G = cap_grid(place_grid(pl));
+    if (gsize == 1 && G == s.wcs * P && G <= kDirectMaxGrid && (P == 2 || P == 4 || P == 8)) {
+        const dim3 g(static_cast<unsigned>(s.wcs), static_cast<unsigned>(P)), b(nt);
+        switch (P) {
+            case 2: launch_ag_direct_p<2>(in, out, s, vpt, src_cached, g, b, stream); break;
+            case 4: launch_ag_direct_p<4>(in, out, s, vpt, src_cached, g, b, stream); break;
+            default: launch_ag_direct_p<8>(in, out, s, vpt, src_cached, g, b, stream); break;
+        }
+        return hipGetLastError();
+    }
     if (P <= 8) {
         Ptrs<8> p = make_ptrs<8>(in, out, P, P);
         const dim3 g(static_cast<unsigned>(G)), b(nt);
