@@ -259,57 +259,81 @@ __device__ __forceinline__ uint4* lane_rank_out(const RankTable& tab, int r) {
     return reinterpret_cast<uint4*>((hi << 32) | lo);
 }
 
+// One work item of the tile kernel: V vectors of every rank starting at `base`.
 template <int PT, int DT, int V>
-__global__ __launch_bounds__(kWG) void k_allreduce_tile(Ptrs<64> p, TileShape s, Place pl) {
-    using A = Arith<DT>;
-    static_assert(kWG % V == 0 && V * 4 <= kWG, "tile width");
+__device__ __forceinline__ void tile_item(const RankTable& tab, const TileShape& s, int P, int64_t base, uint4* lds) {
     constexpr int RPP = kWG / V;  // ranks per pass
     constexpr int kMaxPass = ((PT > 0 ? PT : 64) + RPP - 1) / RPP;
-    extern __shared__ uint4 lds[];  // [P][V]
-    const int P = PT > 0 ? PT : s.P;
     const int t = threadIdx.x;
     const int rsub = t / V;
     const int vsub = t % V;
     const int npass = (P + RPP - 1) / RPP;
-    const RankTable tab = load_rank_table(p, P);
-    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    for (int64_t i = it.first; i < it.end; i += it.stride) {
-        const int64_t base = item_at(pl, blockIdx.x, gridDim.x, i) * V;
-        const bool in_range = base + vsub < s.nvec;
-        // Every pass's load is issued before the first one is waited for.
-        uint4 buf[kMaxPass];
+    const bool in_range = base + vsub < s.nvec;
+    // Every pass's load is issued before the first one is waited for.
+    uint4 buf[kMaxPass];
 #pragma unroll
-        for (int k = 0; k < kMaxPass; ++k) {
-            const int r = k * RPP + rsub;
-            const uint4* src = lane_rank_in(tab, r < P ? r : 0);
-            if (k < npass && r < P && in_range) buf[k] = load16<true>(src + base + vsub);
-        }
-#pragma unroll
-        for (int k = 0; k < kMaxPass; ++k) {
-            const int r = k * RPP + rsub;
-            if (k < npass && r < P && in_range) lds[r * V + vsub] = buf[k];
-        }
-        __syncthreads();
-        uint32_t y = 0;
-        if (t < V * 4) y = lpr_sum_column<PT, DT>(reinterpret_cast<const uint32_t*>(lds) + t, V * 4, P);
-        __syncthreads();
-        if (t < V * 4) reinterpret_cast<uint32_t*>(lds)[t] = y;
-        __syncthreads();
-        const uint4 out = lds[vsub];
-#pragma unroll
-        for (int k = 0; k < kMaxPass; ++k) {
-            const int r = k * RPP + rsub;
-            uint4* dst = lane_rank_out(tab, r < P ? r : 0);
-            if (k < npass && r < P && in_range) store_stream(dst + base + vsub, out);
-        }
-        __syncthreads();
+    for (int k = 0; k < kMaxPass; ++k) {
+        const int r = k * RPP + rsub;
+        const uint4* src = lane_rank_in(tab, r < P ? r : 0);
+        if (k < npass && r < P && in_range) buf[k] = load16<true>(src + base + vsub);
     }
-    if (s.tail > 0 && blockIdx.x == 0 && t < s.tail) {
-        const int64_t e = s.nvec * (16 / A::kEsize) + t;
+#pragma unroll
+    for (int k = 0; k < kMaxPass; ++k) {
+        const int r = k * RPP + rsub;
+        if (k < npass && r < P && in_range) lds[r * V + vsub] = buf[k];
+    }
+    __syncthreads();
+    uint32_t y = 0;
+    if (t < V * 4) y = lpr_sum_column<PT, DT>(reinterpret_cast<const uint32_t*>(lds) + t, V * 4, P);
+    __syncthreads();
+    if (t < V * 4) reinterpret_cast<uint32_t*>(lds)[t] = y;
+    __syncthreads();
+    const uint4 out = lds[vsub];
+#pragma unroll
+    for (int k = 0; k < kMaxPass; ++k) {
+        const int r = k * RPP + rsub;
+        uint4* dst = lane_rank_out(tab, r < P ? r : 0);
+        if (k < npass && r < P && in_range) store_stream(dst + base + vsub, out);
+    }
+}
+
+// Elements after the last full vector, summed by one workgroup.
+template <int DT, int MAXP>
+__device__ __forceinline__ void tail_elements(const Ptrs<MAXP>& p, int P, int64_t nvec, int tail) {
+    using A = Arith<DT>;
+    if (tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < tail) {
+        const int64_t e = nvec * (16 / A::kEsize) + threadIdx.x;
         float a = A::load1(p.in[0], e);
         for (int r = 1; r < P; ++r) a = a + A::load1(p.in[r], e);
         for (int d = 0; d < P; ++d) A::store1(p.out[d], e, a);
     }
+}
+
+template <int PT, int DT, int V>
+__global__ __launch_bounds__(kWG) void k_allreduce_tile(Ptrs<64> p, TileShape s, Place pl) {
+    static_assert(kWG % V == 0 && V * 4 <= kWG, "tile width");
+    extern __shared__ uint4 lds[];  // [P][V]
+    const int P = PT > 0 ? PT : s.P;
+    const RankTable tab = load_rank_table(p, P);
+    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
+    for (int64_t i = it.first; i < it.end; i += it.stride) {
+        tile_item<PT, DT, V>(tab, s, P, item_at(pl, blockIdx.x, gridDim.x, i) * V, lds);
+        __syncthreads();
+    }
+    tail_elements<DT>(p, P, s.nvec, s.tail);
+}
+
+// Direct tile kernel: workgroup b takes item b (every uncapped launch of up
+// to kDirectMaxGrid workgroups; the tile kernel's groups have one item), so
+// no placement state sits between the argument loads and the data loads.
+template <int PT, int DT, int V>
+__global__ __launch_bounds__(kWG) void k_allreduce_tile_direct(Ptrs<64> p, TileShape s) {
+    static_assert(kWG % V == 0 && V * 4 <= kWG, "tile width");
+    extern __shared__ uint4 lds[];  // [P][V]
+    const int P = PT > 0 ? PT : s.P;
+    const RankTable tab = load_rank_table(p, P);
+    tile_item<PT, DT, V>(tab, s, P, static_cast<int64_t>(blockIdx.x) * V, lds);
+    tail_elements<DT>(p, P, s.nvec, s.tail);
 }
 
 // ---------------------------------------------------------------- reduce-scatter
@@ -786,20 +810,25 @@ hipError_t launch_allreduce_lpr(const void* const* in, void* const* out, int P, 
 
 template <int PT, int DT, int V>
 void launch_tile_t(const void* const* in, void* const* out, int P, const TileShape& s, const Place& pl, int64_t G,
-                   hipStream_t st) {
+                   bool direct, hipStream_t st) {
     Ptrs<64> p = make_ptrs<64>(in, out, P, P);
     const size_t lds = static_cast<size_t>(P) * V * 16;
-    hipLaunchKernelGGL((k_allreduce_tile<PT, DT, V>), dim3(static_cast<unsigned>(G)), dim3(kWG), lds, st, p, s, pl);
+    if (direct)
+        hipLaunchKernelGGL((k_allreduce_tile_direct<PT, DT, V>), dim3(static_cast<unsigned>(G)), dim3(kWG), lds, st, p,
+                           s);
+    else
+        hipLaunchKernelGGL((k_allreduce_tile<PT, DT, V>), dim3(static_cast<unsigned>(G)), dim3(kWG), lds, st, p, s,
+                           pl);
 }
 
 template <int DT, int V>
 void launch_tile_p(const void* const* in, void* const* out, int P, const TileShape& s, const Place& pl, int64_t G,
-                   hipStream_t st) {
+                   bool direct, hipStream_t st) {
     switch (P) {
-        case 16: launch_tile_t<16, DT, V>(in, out, P, s, pl, G, st); break;
-        case 32: launch_tile_t<32, DT, V>(in, out, P, s, pl, G, st); break;
-        case 64: launch_tile_t<64, DT, V>(in, out, P, s, pl, G, st); break;
-        default: launch_tile_t<0, DT, V>(in, out, P, s, pl, G, st); break;
+        case 16: launch_tile_t<16, DT, V>(in, out, P, s, pl, G, direct, st); break;
+        case 32: launch_tile_t<32, DT, V>(in, out, P, s, pl, G, direct, st); break;
+        case 64: launch_tile_t<64, DT, V>(in, out, P, s, pl, G, direct, st); break;
+        default: launch_tile_t<0, DT, V>(in, out, P, s, pl, G, direct, st); break;
     }
 }
 
@@ -815,14 +844,15 @@ hipError_t launch_allreduce_tile(const void* const* in, void* const* out, int P,
     const int64_t groups = (s.nvec + V - 1) / V;
     const Place pl = make_place_uniform(mode, groups > 0 ? groups : 1, 1);
     const int64_t G = cap_grid(place_grid(pl));
+    const bool direct = G == groups && G <= kDirectMaxGrid;  // one item per workgroup, no placement state
     if (dtype == kDtF32) {
-        if (V == 16) launch_tile_p<kDtF32, 16>(in, out, P, s, pl, G, stream);
-        else if (V == 32) launch_tile_p<kDtF32, 32>(in, out, P, s, pl, G, stream);
-        else launch_tile_p<kDtF32, 64>(in, out, P, s, pl, G, stream);
+        if (V == 16) launch_tile_p<kDtF32, 16>(in, out, P, s, pl, G, direct, stream);
+        else if (V == 32) launch_tile_p<kDtF32, 32>(in, out, P, s, pl, G, direct, stream);
+        else launch_tile_p<kDtF32, 64>(in, out, P, s, pl, G, direct, stream);
     } else {
-        if (V == 16) launch_tile_p<kDtBf16, 16>(in, out, P, s, pl, G, stream);
-        else if (V == 32) launch_tile_p<kDtBf16, 32>(in, out, P, s, pl, G, stream);
-        else launch_tile_p<kDtBf16, 64>(in, out, P, s, pl, G, stream);
+        if (V == 16) launch_tile_p<kDtBf16, 16>(in, out, P, s, pl, G, direct, stream);
+        else if (V == 32) launch_tile_p<kDtBf16, 32>(in, out, P, s, pl, G, direct, stream);
+        else launch_tile_p<kDtBf16, 64>(in, out, P, s, pl, G, direct, stream);
     }
     return hipGetLastError();
 }
