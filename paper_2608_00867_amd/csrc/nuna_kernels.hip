@@ -50,8 +50,19 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int P = PT > 0 ? PT : s.P;
+    __builtin_assume(pl.gsize > 0);  // the collectives always place uniform groups
     const bool all_dests = pl.gsize == 1;
     const RankTable tab = use_table<PT>() ? load_rank_table(p, P) : RankTable{0u, 0u, 0u, 0u};
+    if constexpr (PT == 8) {
+        // One use of every argument the item loop needs: all their loads issue together.
+        asm volatile("" ::"s"(p.in[0]), "s"(p.in[1]), "s"(p.in[2]), "s"(p.in[3]), "s"(p.in[4]), "s"(p.in[5]),
+                     "s"(p.in[6]), "s"(p.in[7]), "s"(p.out[0]), "s"(p.out[1]), "s"(p.out[2]), "s"(p.out[3]),
+                     "s"(p.out[4]), "s"(p.out[5]), "s"(p.out[6]), "s"(p.out[7]), "s"(s.nvec), "s"(s.dpi),
+                     "s"(s.tail), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize), "s"(pl.gshift), "s"(blockDim.x));
+    } else {
+        asm volatile("" ::"s"(s.nvec), "s"(s.dpi), "s"(s.tail), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize),
+                     "s"(pl.gshift), "s"(blockDim.x));
+    }
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
@@ -313,8 +324,10 @@ template <int PT, int DT, int V>
 __global__ __launch_bounds__(kWG) void k_allreduce_tile(Ptrs<64> p, TileShape s, Place pl) {
     static_assert(kWG % V == 0 && V * 4 <= kWG, "tile width");
     extern __shared__ uint4 lds[];  // [P][V]
+    __builtin_assume(pl.gsize > 0);  // the collectives always place uniform groups
     const int P = PT > 0 ? PT : s.P;
     const RankTable tab = load_rank_table(p, P);
+    asm volatile("" ::"s"(s.nvec), "s"(s.tail), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize), "s"(pl.gshift));
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         tile_item<PT, DT, V>(tab, s, P, item_at(pl, blockIdx.x, gridDim.x, i) * V, lds);
@@ -361,10 +374,20 @@ __device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const 
 // all-reduce), so it is stored through the caches instead of streamed.
 template <int PT, int MAXP, int DT, int VPT, bool KEEP>
 __global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s, Place pl) {
-    const int nt = blockDim.x;
-    const int64_t cv = static_cast<int64_t>(nt) * VPT;
+    __builtin_assume(pl.gsize > 0);  // the collectives always place uniform groups
     const int P = PT > 0 ? PT : s.P;
     const RankTable tab = use_table<PT>() ? load_rank_table(p, P) : RankTable{0u, 0u, 0u, 0u};
+    // One use of every argument the item loop needs: their loads issue together.
+    if constexpr (PT == 8)
+        asm volatile("" ::"s"(p.in[0]), "s"(p.in[1]), "s"(p.in[2]), "s"(p.in[3]), "s"(p.in[4]), "s"(p.in[5]),
+                     "s"(p.in[6]), "s"(p.in[7]), "s"(p.out[0]), "s"(p.out[1]), "s"(p.out[2]), "s"(p.out[3]),
+                     "s"(p.out[4]), "s"(p.out[5]), "s"(p.out[6]), "s"(p.out[7]), "s"(s.mv), "s"(s.wcs),
+                     "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize), "s"(pl.gshift), "s"(blockDim.x));
+    else
+        asm volatile("" ::"s"(s.mv), "s"(s.wcs), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize), "s"(pl.gshift),
+                     "s"(blockDim.x));
+    const int nt = blockDim.x;
+    const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
@@ -439,9 +462,13 @@ __device__ __forceinline__ void all_gather_chunk(const RankTable& tab, const AgS
 // still sit in L2 or the Infinity Cache, so they are read through the caches.
 template <int MAXP, int VPT, bool CACHED>
 __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Place pl) {
+    __builtin_assume(pl.gsize > 0);  // the collectives always place uniform groups
+    const RankTable tab = load_rank_table(p, s.P);
+    // One use of every scalar argument the item loop needs: their loads issue together.
+    asm volatile("" ::"s"(s.mv), "s"(s.wcs), "s"(s.dpi), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize),
+                 "s"(pl.gshift), "s"(blockDim.x));
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
-    const RankTable tab = load_rank_table(p, s.P);
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         const int64_t w = item_at(pl, blockIdx.x, gridDim.x, i);
