@@ -557,6 +557,8 @@ __global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uin
                                               unsigned char* __restrict__ dst_tail,
                                               const unsigned char* __restrict__ src_tail, int tail) {
     constexpr int U = 4;
+    // One use of every argument: their loads issue together (as in the collectives).
+    asm volatile("" ::"s"(dst), "s"(src), "s"(nvec), "s"(dst_tail), "s"(src_tail), "s"(tail));
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kWG * U;
     for (int64_t v = blockIdx.x * static_cast<int64_t>(kWG) * U + threadIdx.x; v < nvec; v += stride) {
         uint4 y[U];
