@@ -420,6 +420,7 @@ def cpu_baseline(seconds):
 
 # ---------------------------------------------------------------------------------------------- --full sweep
 
+MOE_DECODE_TOKENS = (128, 16)  # decode-shaped MoE steps beside the 512-token shape
 NO_SLOWER_TOL = 1.02   # XCD counts as no slower within 2 % of LINEAR's median
 TARGET_FRAC = 0.70     # of the HBM peak, for messages of 4 MiB per rank and more
 TARGET_MIN_BYTES = 4 << 20
@@ -507,9 +508,11 @@ def full_sweep(nuna, torch, pool, args):
                       **{f"{p}_frac_hbm": round(res[p]["gbps"] / HBM_PEAK_GBPS, 4) for p in res},
                       "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
     if want("a2a_moe_dispatch"):
-        a2a_case(nuna, torch, pool, args, emit)
+        for T_tok in (None,) + MOE_DECODE_TOKENS:
+            a2a_case(nuna, torch, pool, args, emit, T_tok)
     if want("a2a_moe_combine"):
-        combine_case(nuna, torch, pool, args, emit)
+        for T_tok in (None,) + MOE_DECODE_TOKENS:
+            combine_case(nuna, torch, pool, args, emit, T_tok)
     if want("copy_reference"):
         copy_case(nuna, torch, pool, args, emit)
     if want("launch_floor"):
@@ -517,10 +520,12 @@ def full_sweep(nuna, torch, pool, args):
     f.close()
 
 
-def a2a_case(nuna, torch, pool, args, emit):
+def a2a_case(nuna, torch, pool, args, emit, T_tokens=None):
+    """MoE dispatch at T_tokens per rank (default: the 512-token shape); decode-shaped token counts
+    measure the latency regime."""
     import oracle
     from paper_2608_00867_amd import workloads as wl
-    send_np, topk = wl.a2a_moe()
+    send_np, topk = wl.a2a_moe() if T_tokens is None else wl.a2a_moe(T=T_tokens)
     E = wl.MOE_EXPERTS
     lay = nuna.A2ALayout(topk, E).upload()
     rows = lay.recv_rows()
@@ -536,12 +541,12 @@ def a2a_case(nuna, torch, pool, args, emit):
         pool.off = 0
         sets = []
         for _ in range(nsets):
-            send = [pool.take(T * rb).view(torch.bfloat16).view(T, H) for _ in range(P)]
-            recv = [pool.take(cap * rb).view(torch.bfloat16).view(cap, H) for _ in range(P)]
+            send = [pool.take(T * rb)[:T * rb].view(torch.bfloat16).view(T, H) for _ in range(P)]
+            recv = [pool.take(cap * rb)[:cap * rb].view(torch.bfloat16).view(cap, H) for _ in range(P)]
             for a, b in zip(send, src):
                 a.view(-1).copy_(b)
             sets.append((send, recv))
-        calls = max(4, nsets)
+        calls = max(nsets, calls_for(set_bytes, cold))
         ref = oracle.all_to_all(send_np, topk, E)
         ok = True
         for p in ("linear", "xcd"):
@@ -555,7 +560,8 @@ def a2a_case(nuna, torch, pool, args, emit):
                   for p in ("linear", "xcd")}
         t = time_graphs(torch, graphs, calls, args.reps, args.warmup)
         res = {p: stats(t[p]) for p in t}
-        emit({"workload": "a2a_moe_dispatch_bf16_p8", "P": P, "tokens_per_rank": T, "hidden": H,
+        emit({"workload": "a2a_moe_dispatch_bf16_p8" + ("" if T_tokens is None else f"_T{T}"), "P": P,
+              "tokens_per_rank": T, "hidden": H,
               "rows_received": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
               "calls_per_graph": calls, "parity": bool(ok),
               **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
@@ -619,13 +625,13 @@ def eager_case(nuna, torch, pool, args, emit):
         del sets
 
 
-def combine_case(nuna, torch, pool, args, emit):
+def combine_case(nuna, torch, pool, args, emit, T_tokens=None):
     """MoE combine at the dispatch's shape: every received row comes back as a result row and is
     summed into its token (reads: all result rows; writes: every token row once), unweighted and with
     one gate weight per (token, destination rank)."""
     import oracle
     from paper_2608_00867_amd import workloads as wl
-    _, topk = wl.a2a_moe()
+    _, topk = wl.a2a_moe() if T_tokens is None else wl.a2a_moe(T=T_tokens)
     E, H = wl.MOE_EXPERTS, wl.HIDDEN_MOE
     P, T = int(topk.shape[0]), int(topk.shape[1])
     lay = nuna.A2ALayout(topk, E).upload()
@@ -641,19 +647,20 @@ def combine_case(nuna, torch, pool, args, emit):
         ref = oracle.combine(y_np, topk, E, w_np if weighted else None)
         wt = w_dev if weighted else None
         alg_bytes = int(rows.sum() * rb + P * T * rb + (w_np.nbytes if weighted else 0))
-        name = "a2a_moe_combine_weighted_bf16_p8" if weighted else "a2a_moe_combine_bf16_p8"
+        name = ("a2a_moe_combine_weighted_bf16_p8" if weighted else "a2a_moe_combine_bf16_p8") + \
+            ("" if T_tokens is None else f"_T{T}")
         for cold in (True, False):
             nsets = max(1, min(pool.nbytes // (set_bytes + 16 * ALIGN), math.ceil(COLD_SPAN / set_bytes) + 1)) \
                 if cold else 1
             pool.off = 0
             sets = []
             for _ in range(nsets):
-                y = [pool.take(cap * rb).view(torch.bfloat16).view(cap, H) for _ in range(P)]
-                out = [pool.take(T * rb).view(torch.bfloat16).view(T, H) for _ in range(P)]
+                y = [pool.take(cap * rb)[:cap * rb].view(torch.bfloat16).view(cap, H) for _ in range(P)]
+                out = [pool.take(T * rb)[:T * rb].view(torch.bfloat16).view(T, H) for _ in range(P)]
                 for d in range(P):
                     y[d][:int(rows[d])].view(-1).copy_(src[d])
                 sets.append((y, out))
-            calls = max(4, nsets)
+            calls = max(nsets, calls_for(set_bytes, cold))
             ok = True
             for p in ("linear", "xcd"):
                 nuna.all_to_all_combine(sets[0][0], sets[0][1], lay, placement=p, weights=wt)
@@ -949,8 +956,8 @@ def profile_moe(nuna, torch, pool, n, place="xcd"):
     pool.off = 0
     sets = []
     for _ in range(nsets):
-        tok = [pool.take(T * rb).view(torch.bfloat16).view(T, H) for _ in range(P)]
-        rec = [pool.take(cap * rb).view(torch.bfloat16).view(cap, H) for _ in range(P)]
+        tok = [pool.take(T * rb)[:T * rb].view(torch.bfloat16).view(T, H) for _ in range(P)]
+        rec = [pool.take(cap * rb)[:cap * rb].view(torch.bfloat16).view(cap, H) for _ in range(P)]
         for t, a in zip(tok, send_np):
             t.copy_(dev_copy_of(torch, a))
         sets.append((tok, rec))

@@ -131,7 +131,11 @@ nuna_status_t nuna_set_max_workgroups(int max_workgroups);
  *   NUNA_LPR_MAX_VECTORS  lane-per-rank all-reduce up to this many input vectors in
  *                         total, 0..2^40 (0: never)
  *   NUNA_COMBINE_VPT      combine vectors per thread: 0 (default), 1, 2, 4
- *   NUNA_COMBINE_CHUNKS   combine column chunks per token, 0 (by size)..INT32_MAX
+ *   NUNA_COMBINE_CHUNKS   combine column chunks per token, 0 (by size)..INT32_MAX; with
+ *                         up to 8 ranks raised where needed so that a chunk is at most
+ *                         (workgroup threads x combine vectors per thread) vectors
+ *   NUNA_COMBINE_LISTS    0: the combine reads per-token records with up to 8 ranks;
+ *                         1: always the offset lists
  *   NUNA_TILE_V           rank-major tile all-reduce width: 0 (16 up to 256 KiB per
  *                         rank, else off), 16, 32, 64
  * Unknown names and values outside these sets: NUNA_ERR_INVALID_ARG. */

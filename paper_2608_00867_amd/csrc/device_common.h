@@ -166,16 +166,28 @@ __device__ __forceinline__ RankTable load_rank_table(const Ptrs<MAXP>& p, int P)
     return t;
 }
 
+// The table holds global-memory addresses.  A pointer rebuilt from an
+// integer is a generic (flat) pointer, and flat instructions count in both
+// the vector-memory and the scalar/LDS wait counters: a wait for a scalar
+// load would then also wait for every flat load or store in flight.  The
+// pointers are therefore formed in the global address space and converted to
+// generic; the compiler carries the global space through to every access.
+typedef __attribute__((address_space(1))) const uint4 global_cvec;
+typedef __attribute__((address_space(1))) uint4 global_vec;
+
+__device__ __forceinline__ const uint4* global_in(uint64_t addr) { return (const uint4*)((global_cvec*)addr); }
+__device__ __forceinline__ uint4* global_out(uint64_t addr) { return (uint4*)((global_vec*)addr); }
+
 __device__ __forceinline__ const uint4* rank_in(const RankTable& t, int r) {
     const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.in_lo), r));
     const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.in_hi), r));
-    return reinterpret_cast<const uint4*>((hi << 32) | lo);
+    return global_in((hi << 32) | lo);
 }
 
 __device__ __forceinline__ uint4* rank_out(const RankTable& t, int r) {
     const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.out_lo), r));
     const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(t.out_hi), r));
-    return reinterpret_cast<uint4*>((hi << 32) | lo);
+    return global_out((hi << 32) | lo);
 }
 
 // Pointer access: compile-time offsets for up to 16 ranks, the table beyond.

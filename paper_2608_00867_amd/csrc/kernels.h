@@ -26,6 +26,7 @@ struct Tuning {
     int combine_vpt = 0;               // combine vectors per thread per pass (0 = default)
     int combine_chunks = 0;            // combine column chunks per token (0 = by size)
     int tile_v = 0;                    // rank-major tile all-reduce width (16/32/64; 0 = by size)
+    int combine_lists = 0;             // 1: combine reads the offset lists even where records exist
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
@@ -58,9 +59,12 @@ hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, 
 // MoE combine: out[s][t] = sum over the token's entries (rank d, row j), in
 // list order, of y[d][j], each scaled by weights[(s*T + t)*P + d] when
 // weights is not null.  off: device int64[P*T + 1]; ent: device int32 pairs
-// (rank, row).
+// (rank, row).  rec: null, or (P <= kCombRecRanks) the same entries as
+// kCombRecRanks words per token, (row << 3) | rank, padded with all ones.
+constexpr int kCombRecRanks = 8;
 hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, const void* off, const void* ent,
-                          const float* weights, size_t row_bytes, int dtype, int mode, hipStream_t stream);
+                          const void* rec, const float* weights, size_t row_bytes, int dtype, int mode,
+                          hipStream_t stream);
 
 hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
 

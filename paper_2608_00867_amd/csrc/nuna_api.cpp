@@ -181,6 +181,7 @@ const TunableDef kTunables[] = {
     {"NUNA_COMBINE_VPT", nullptr, &nuna::Tuning::combine_vpt, 0, 0, 4, {0, 1, 2, 4}},
     {"NUNA_COMBINE_CHUNKS", nullptr, &nuna::Tuning::combine_chunks, 0, INT32_MAX, 0, {}},
     {"NUNA_TILE_V", nullptr, &nuna::Tuning::tile_v, 0, 0, 4, {0, 16, 32, 64}},
+    {"NUNA_COMBINE_LISTS", nullptr, &nuna::Tuning::combine_lists, 0, 1, 0, {}},
 };
 
 const TunableDef* find_tunable(const char* name) {
@@ -390,11 +391,17 @@ struct nuna_a2a_layout {
     // each a (destination rank, receive row) pair, destinations ascending.
     std::vector<int64_t> comb_off;
     std::vector<int32_t> comb_ent;
+    // The same lists as fixed-size records, for up to 8 ranks: 8 words per
+    // token, word q = (receive row << 3) | rank for the token's q-th entry,
+    // all ones after its last.  Empty when P > 8 or a row index needs more
+    // than 29 bits.
+    std::vector<uint32_t> comb_rec;
     void* dev_base = nullptr;  // one allocation holding every device table
     void* dev_linear = nullptr;
     void* dev_group = nullptr;
     void* dev_comb_off = nullptr;
     void* dev_comb_ent = nullptr;
+    void* dev_comb_rec = nullptr;
     int device = -1;
 };
 
@@ -447,6 +454,9 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
     std::vector<int64_t> next(P, 0);
     L->comb_off.assign(static_cast<size_t>(ntok) + 1, 0);
     L->comb_ent.reserve(2 * L->nitems);
+    // Row indices stay below ntok < 2^29, so no entry is all ones.
+    const bool records = P <= nuna::kCombRecRanks && ntok < (int64_t(1) << 29);
+    if (records) L->comb_rec.assign(static_cast<size_t>(ntok) * nuna::kCombRecRanks, ~uint32_t(0));
     // Placement workload for the XCD mode: one threadblock per row copy, in
     // walk order, touching its source row and its destination row.
     std::vector<int64_t> tb_off(static_cast<size_t>(L->nitems) + 1, 0);
@@ -458,6 +468,7 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
             const size_t tok = static_cast<size_t>(s) * tokens_per_rank + t;
             const uint64_t m = mask[tok];
             L->comb_off[tok + 1] = L->comb_off[tok] + __builtin_popcountll(m);
+            size_t q_rec = tok * nuna::kCombRecRanks;  // the token's next record word
             for (int d = 0; d < P; ++d) {
                 if (!(m >> d & 1u)) continue;
                 const int64_t j = next[d]++;
@@ -471,6 +482,7 @@ nuna_status_t nuna_a2a_layout_create(int P, int tokens_per_rank, int topk, int n
                 tb_chunk[2 * static_cast<size_t>(w) + 1] = ntok + pos;                    // destination row
                 tb_off[static_cast<size_t>(w) + 1] = 2 * (w + 1);
                 ++w;
+                if (records) L->comb_rec[q_rec++] = static_cast<uint32_t>(j) << 3 | static_cast<uint32_t>(d);
                 L->comb_ent.push_back(d);
                 L->comb_ent.push_back(static_cast<int32_t>(j));
             }
@@ -520,11 +532,14 @@ nuna_status_t nuna_a2a_layout_upload(nuna_a2a_layout_t* L) {
         return ok();
     }
     // One allocation: dispatch descriptors (linear, then XCD-major), combine
-    // offsets, combine entries.  Every part starts 16-byte aligned.
+    // offsets, combine entries, combine records.  Every part starts 16-byte
+    // aligned; the records start 32-byte aligned (one record per 32 bytes).
     const size_t n_desc = static_cast<size_t>(L->nitems) * 16;
     const size_t n_off = (L->comb_off.size() * sizeof(int64_t) + 15) & ~size_t(15);
-    const size_t n_ent = L->comb_ent.size() * sizeof(int32_t);
-    const size_t bytes = 2 * n_desc + n_off + n_ent;
+    const size_t n_ent = (L->comb_ent.size() * sizeof(int32_t) + 31) & ~size_t(31);
+    const size_t at_rec = (2 * n_desc + n_off + n_ent + 31) & ~size_t(31);
+    const size_t n_rec = L->comb_rec.size() * sizeof(uint32_t);
+    const size_t bytes = at_rec + n_rec;
     void* base = nullptr;
     if ((e = hipMalloc(&base, bytes)) != hipSuccess) return hip_status(e, "hipMalloc (a2a tables)");
     char* b = static_cast<char*>(base);
@@ -532,11 +547,13 @@ nuna_status_t nuna_a2a_layout_upload(nuna_a2a_layout_t* L) {
         size_t at;
         const void* src;
         size_t n;
-    } parts[4] = {{0, L->desc_linear.data(), n_desc},
+    } parts[5] = {{0, L->desc_linear.data(), n_desc},
                   {n_desc, L->desc_group.data(), n_desc},
                   {2 * n_desc, L->comb_off.data(), L->comb_off.size() * sizeof(int64_t)},
-                  {2 * n_desc + n_off, L->comb_ent.data(), n_ent}};
+                  {2 * n_desc + n_off, L->comb_ent.data(), L->comb_ent.size() * sizeof(int32_t)},
+                  {at_rec, L->comb_rec.data(), n_rec}};
     for (const auto& q : parts) {
+        if (q.n == 0) continue;
         if ((e = hipMemcpy(b + q.at, q.src, q.n, hipMemcpyHostToDevice)) != hipSuccess) {
             (void)hipFree(base);
             return hip_status(e, "hipMemcpy (a2a tables)");
@@ -547,6 +564,7 @@ nuna_status_t nuna_a2a_layout_upload(nuna_a2a_layout_t* L) {
     L->dev_group = b + n_desc;
     L->dev_comb_off = b + 2 * n_desc;
     L->dev_comb_ent = b + 2 * n_desc + n_off;
+    L->dev_comb_rec = n_rec ? b + at_rec : nullptr;
     L->device = dev;
     return ok();
 }
@@ -640,8 +658,8 @@ nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, co
     if (st) return st;
     if (L->nitems == 0) return ok();
     if (L->device < 0) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
-    hipError_t e = nuna::launch_combine(y, out, P, L->T, L->dev_comb_off, L->dev_comb_ent, weights, row_bytes,
-                                        static_cast<int>(dtype), place, stream);
+    hipError_t e = nuna::launch_combine(y, out, P, L->T, L->dev_comb_off, L->dev_comb_ent, L->dev_comb_rec, weights,
+                                        row_bytes, static_cast<int>(dtype), place, stream);
     return hip_status(e, "all-to-all combine launch");
 } catch (...) {
     return host_exception();

@@ -209,8 +209,8 @@ __global__ __launch_bounds__(kWG) void k_allreduce_lpr(Ptrs<64> p, LprShape s, P
     const uint64_t in_hi = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src_lane, static_cast<int>(tab.in_hi)));
     const uint64_t out_lo = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src_lane, static_cast<int>(tab.out_lo)));
     const uint64_t out_hi = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src_lane, static_cast<int>(tab.out_hi)));
-    const uint4* my_in = reinterpret_cast<const uint4*>((in_hi << 32) | in_lo);
-    uint4* my_out = reinterpret_cast<uint4*>((out_hi << 32) | out_lo);
+    const uint4* my_in = global_in((in_hi << 32) | in_lo);
+    uint4* my_out = global_out((out_hi << 32) | out_lo);
     uint4* res = lds + P * V;
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
@@ -261,13 +261,13 @@ struct TileShape {
 __device__ __forceinline__ const uint4* lane_rank_in(const RankTable& tab, int r) {
     const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(tab.in_lo)));
     const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(tab.in_hi)));
-    return reinterpret_cast<const uint4*>((hi << 32) | lo);
+    return global_in((hi << 32) | lo);
 }
 
 __device__ __forceinline__ uint4* lane_rank_out(const RankTable& tab, int r) {
     const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(tab.out_lo)));
     const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(r * 4, static_cast<int>(tab.out_hi)));
-    return reinterpret_cast<uint4*>((hi << 32) | lo);
+    return global_out((hi << 32) | lo);
 }
 
 // One work item of the tile kernel: V vectors of every rank starting at `base`.

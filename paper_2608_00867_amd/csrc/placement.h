@@ -73,8 +73,30 @@ NUNA_HD inline bool linear_map(const Place& pl, int64_t G) {
     return pl.mode == kPlaceLinear || pl.gsize == 1 || G < kNumXcd;
 }
 
+// Range of list positions workgroup b of G runs under per-XCD item lists
+// (gsize 0): with the linear map, every b-th position of all `total`;
+// otherwise XCD x = b mod 8 runs its list [start_x, start_x1), its
+// workgroups taking every (workgroups on x)-th position.
+NUNA_HD inline ItemRange list_items(bool linear, int64_t start_x, int64_t start_x1, int64_t total, int64_t b,
+                                    int64_t G) {
+    ItemRange r;
+    if (linear) {
+        r.first = b;
+        r.end = total;
+        r.stride = G;
+        return r;
+    }
+    const int64_t x = b & (kNumXcd - 1);
+    r.first = start_x + (b >> 3);
+    r.end = start_x1;
+    r.stride = (G - x + kNumXcd - 1) >> 3;
+    return r;
+}
+
 // Range of list positions workgroup b of G runs.
 NUNA_HD inline ItemRange items_of(const Place& pl, int64_t b, int64_t G) {
+    const int64_t x = b & (kNumXcd - 1);
+    if (pl.gsize == 0) return list_items(linear_map(pl, G), pl.start[x], pl.start[x + 1], pl.start[kNumXcd], b, G);
     ItemRange r;
     if (linear_map(pl, G)) {
         r.first = b;
@@ -82,17 +104,10 @@ NUNA_HD inline ItemRange items_of(const Place& pl, int64_t b, int64_t G) {
         r.stride = G;
         return r;
     }
-    const int64_t x = b & (kNumXcd - 1);
-    const int64_t k = b >> 3;
+    const int64_t gx = pl.groups > x ? (pl.groups - x + kNumXcd - 1) >> 3 : 0;
+    r.first = b >> 3;
+    r.end = gx * pl.gsize;
     r.stride = (G - x + kNumXcd - 1) >> 3;
-    if (pl.gsize > 0) {
-        const int64_t gx = pl.groups > x ? (pl.groups - x + kNumXcd - 1) >> 3 : 0;
-        r.first = k;
-        r.end = gx * pl.gsize;
-    } else {
-        r.first = pl.start[x] + k;
-        r.end = pl.start[x + 1];
-    }
     return r;
 }
 

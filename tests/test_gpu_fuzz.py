@@ -17,6 +17,8 @@ torch = pytest.importorskip("torch")
 VARIANTS = [{}, dict(NUNA_MAX_GRID=7), dict(NUNA_WG_THREADS=64), dict(NUNA_WG_THREADS=128, NUNA_VPT=2),
             dict(NUNA_VPT=4), dict(NUNA_VPT=8), dict(NUNA_TILE_V=32), dict(NUNA_TILE_V=64, NUNA_LPR_MIN_RANKS=2),
             dict(NUNA_LPR_MIN_RANKS=1, NUNA_LPR_MAX_VECTORS=1 << 20)]
+MOE_VARIANTS = [{}, dict(NUNA_COMBINE_LISTS=1), dict(NUNA_MAX_GRID=7), dict(NUNA_WG_THREADS=64, NUNA_COMBINE_VPT=1),
+                dict(NUNA_COMBINE_CHUNKS=3, NUNA_COMBINE_VPT=4)]
 
 
 @pytest.fixture(scope="module")
@@ -104,8 +106,14 @@ def test_fuzz_moe(nuna, seed):
     dtype = np.uint16 if g.random() < 0.6 else np.float32
     place = str(g.choice(["linear", "xcd"]))
     weighted = bool(g.random() < 0.4)
-    what = f"seed={seed} P={P} E={E} k={k} T={T} H={H} {dtype.__name__} {place} weighted={weighted}"
+    variant = MOE_VARIANTS[int(g.integers(len(MOE_VARIANTS)))]
+    what = f"seed={seed} P={P} E={E} k={k} T={T} H={H} {dtype.__name__} {place} weighted={weighted} {variant}"
     print(what, flush=True)
+    with nuna.tunables(**variant):
+        _moe_case(nuna, g, what, P, E, k, T, H, dtype, place, weighted, seed)
+
+
+def _moe_case(nuna, g, what, P, E, k, T, H, dtype, place, weighted, seed):
     topk = wl.moe_routing(P, T, k, E, 20000 + seed)
     lay = nuna.A2ALayout(topk, E).upload()
     rows = lay.recv_rows()

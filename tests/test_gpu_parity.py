@@ -572,6 +572,30 @@ def test_combine_persistent_loop(nuna, cap):
         nuna.set_max_workgroups(0)
 
 
+@pytest.mark.parametrize("P,T,k,E,H,dtype,weighted,cfg", [
+    (8, 520, 2, 16, 4608, np.uint16, False, {}),  # 4160 tokens: 1 chunk by size, 576 vectors, raised to 2
+    (8, 16, 8, 256, 7168, np.uint16, True, {}),
+    (4, 8, 3, 16, 65536, np.uint16, False, {}),  # 8192-vector rows, 32 chunks by size
+    (8, 24, 8, 64, 4096, np.float32, True, {"NUNA_COMBINE_CHUNKS": 1}),  # forced 1 chunk of 1024 vectors, raised
+    (8, 40, 8, 256, 1000, np.float32, False, {"NUNA_WG_THREADS": 64, "NUNA_COMBINE_VPT": 1}),  # raised 2 -> 4
+    (2, 7, 2, 4, 2056, np.uint16, True, {"NUNA_COMBINE_VPT": 4, "NUNA_COMBINE_CHUNKS": 5}),
+    (1, 9, 1, 4, 256, np.float32, False, {}),
+])
+def test_combine_records_match_lists(nuna, P, T, k, E, H, dtype, weighted, cfg):
+    """Per-token records (up to 8 ranks) and the offset lists both give the oracle's bits, also where the
+    record kernel raises the chunk count so that a column chunk fits one pass of the workgroup."""
+    topk = wl.moe_routing(P, T, k, E, 71 * P + T)
+    y = wl.result_rows(oracle.a2a_counts(topk, E), H, dtype, 73 * P + T)
+    w = _gate_weights(topk, E, 79 * P + T) if weighted else None
+    ref = oracle.combine(y, topk, E, w)
+    for lists in (0, 1):
+        with nuna.tunables(NUNA_COMBINE_LISTS=lists, **cfg):
+            for place in PLACES:
+                got = _run_combine(nuna, y, topk, E, place, weights=w)
+                for s in range(P):
+                    assert_bitwise(got[s], ref[s], f"combine lists={lists} {cfg} {place} P={P} T={T} H={H} rank {s}")
+
+
 # ---------------------------------------------------------------- graph capture and replay
 
 def test_graph_replay_matches_eager(nuna):
