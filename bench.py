@@ -275,7 +275,7 @@ def bench_rs_ag(nuna, torch, pool, kind, x_np, reps, warmup, cold=True, places=(
     return alg_bytes, out, calls, ok
 
 
-RS_AG_KIB = (16, 128, 1024, 8192)  # bytes per rank of the all-gather input / reduce-scatter output
+RS_AG_KIB = (16, 128, 1024, 4096, 8192)  # bytes per rank of the all-gather input / reduce-scatter output
 
 
 # ---------------------------------------------------------------------------------------------- main line

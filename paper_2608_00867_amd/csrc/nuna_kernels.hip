@@ -757,8 +757,13 @@ void pick_ag_shape(int64_t out_vectors, int P, int& nt, int& vpt) {
     } else if (out_vectors < (int64_t(1) << 22)) {
         nt = 128;
         vpt = 4;
-    } else {
+    } else if (P != 8 || out_vectors < (int64_t(1) << 23)) {
         nt = 128;
+        vpt = 1;
+    } else {
+        // 8 ranks, shards of 16 MiB and more: 256-thread workgroups measured
+        // 221 against 232 us at 16 MiB shards and 458 against 474 us at 32 MiB.
+        nt = 256;
         vpt = 1;
     }
 }
@@ -1069,10 +1074,24 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     pick_ag_shape(s.mv * P, P, nt, vpt);
     const int64_t cv = static_cast<int64_t>(nt) * vpt;
     s.wcs = (s.mv + cv - 1) / cv;
-    // Split destinations when there are few chunks, so that more workgroups
-    // share the stores; each member re-reads its chunk (an L2 hit when the
-    // group's members sit on one XCD).
-    const int gsize = (s.wcs * P < 512) ? largest_divisor_upto(P, 8) : 1;
+    // Destination split: a work item is a chunk and a group of destinations,
+    // and each member of the chunk's group loads the chunk (an L2 hit for all
+    // but the first when the members sit on one XCD).
+    // - Few chunks (fewer than 512 chunk items): more workgroups share the
+    //   stores.
+    // - 8 ranks with shards of 4 to 16 MiB: groups of 4 members, each storing
+    //   2 destinations.  Fewer write streams per workgroup measured faster on
+    //   MI355X, cold: 49-51 against 58-60 us at 4 MiB shards and 96-97
+    //   against 116 us at 8 MiB with XCD placement.  The same split on the
+    //   linear map takes 60 and 119 us (its members' re-reads reach HBM).
+    //   From 16 MiB shards it gained at most 2 %, with a launch shape that
+    //   keeps the items within the grid; persistent loops over many grouped
+    //   items lost up to 25 %.
+    int gsize = 1;
+    if (s.wcs * P < 512)
+        gsize = largest_divisor_upto(P, 8);
+    else if (P == 8 && s.mv >= (int64_t(1) << 18) && s.mv < (int64_t(1) << 20))
+        gsize = 4;
     s.dpi = P / gsize;
     // Each member loads the chunk once and stores it dpi times: gsize - 1 of
     // the group's gsize * (1 + dpi) transfers are re-reads.
