@@ -1079,18 +1079,18 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     // but the first when the members sit on one XCD).
     // - Few chunks (fewer than 512 chunk items): more workgroups share the
     //   stores.
-    // - 8 ranks with shards of 4 to 16 MiB: groups of 4 members, each storing
+    // - 8 ranks with shards of 4 to 8 MiB: groups of 4 members, each storing
     //   2 destinations.  Fewer write streams per workgroup measured faster on
-    //   MI355X, cold: 49-51 against 58-60 us at 4 MiB shards and 96-97
-    //   against 116 us at 8 MiB with XCD placement.  The same split on the
-    //   linear map takes 60 and 119 us (its members' re-reads reach HBM).
-    //   From 16 MiB shards it gained at most 2 %, with a launch shape that
-    //   keeps the items within the grid; persistent loops over many grouped
-    //   items lost up to 25 %.
+    //   MI355X, cold, with XCD placement: 49-51 against 58-60 us at 4 MiB
+    //   shards, 75 against 89 us at 6 MiB, 96-97 against 116 us at 8 MiB.
+    //   The same split on the linear map takes 60, 88 and 119 us (its
+    //   members' re-reads reach HBM).  From 10 MiB shards the split at these
+    //   launch shapes lost 20-25 % (171 against 143 us at 10 MiB), and with
+    //   256 x 4 shapes it gained at most 2 %.
     int gsize = 1;
     if (s.wcs * P < 512)
         gsize = largest_divisor_upto(P, 8);
-    else if (P == 8 && s.mv >= (int64_t(1) << 18) && s.mv < (int64_t(1) << 20))
+    else if (P == 8 && s.mv >= (int64_t(1) << 18) && s.mv <= (int64_t(1) << 19))
         gsize = 4;
     s.dpi = P / gsize;
     // Each member loads the chunk once and stores it dpi times: gsize - 1 of
