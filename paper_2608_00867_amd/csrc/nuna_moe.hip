@@ -4,7 +4,8 @@
 //
 // Row copies and row sums of 16-byte vectors; the dispatch is driven by a
 // per-item descriptor list in placement order, the combine by per-token
-// (rank, row) lists.  No MFMA: rows are moved and added, never contracted.
+// (rank, row) lists: fixed-size records with up to 8 ranks, offset lists
+// beyond.  No MFMA: rows are moved and added, never contracted.
 #include "device_common.h"
 
 namespace nuna {
