@@ -1079,18 +1079,19 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     // but the first when the members sit on one XCD).
     // - Few chunks (fewer than 512 chunk items): more workgroups share the
     //   stores.
-    // - 8 ranks with shards of 4 to 8 MiB: groups of 4 members, each storing
-    //   2 destinations.  Fewer write streams per workgroup measured faster on
-    //   MI355X, cold, with XCD placement: 49-51 against 58-60 us at 4 MiB
-    //   shards, 75 against 89 us at 6 MiB, 96-97 against 116 us at 8 MiB.
-    //   The same split on the linear map takes 60, 88 and 119 us (its
-    //   members' re-reads reach HBM).  From 10 MiB shards the split at these
-    //   launch shapes lost 20-25 % (171 against 143 us at 10 MiB), and with
-    //   256 x 4 shapes it gained at most 2 %.
+    // - 8 ranks with shards above 2 MiB and up to 8 MiB: groups of 4 members,
+    //   each storing 2 destinations.  Fewer write streams per workgroup
+    //   measured faster on MI355X, cold, with XCD placement: 38.6 against
+    //   44.5 us at 3 MiB shards, 49-51 against 58-60 at 4 MiB, 75 against 89
+    //   at 6 MiB, 96-97 against 116 at 8 MiB.  The same split on the linear
+    //   map takes 47, 60, 88 and 119 us (its members' re-reads reach HBM).
+    //   At 2 MiB shards it gained 2.5 %, at 1 MiB nothing.  From 10 MiB shards
+    //   the split at these launch shapes lost 20-25 % (171 against 143 us at
+    //   10 MiB), and with 256 x 4 shapes it gained at most 2 %.
     int gsize = 1;
     if (s.wcs * P < 512)
         gsize = largest_divisor_upto(P, 8);
-    else if (P == 8 && s.mv >= (int64_t(1) << 18) && s.mv <= (int64_t(1) << 19))
+    else if (P == 8 && s.mv > (int64_t(1) << 17) && s.mv <= (int64_t(1) << 19))
         gsize = 4;
     s.dpi = P / gsize;
     // Each member loads the chunk once and stores it dpi times: gsize - 1 of

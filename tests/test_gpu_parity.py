@@ -266,8 +266,9 @@ def test_reduce_scatter(nuna, P, m, dtype, place):
 @pytest.mark.parametrize("P,m,dtype", [(8, 65536, "bf16"), (8, 1000, "bf16"), (8, 3, "f32"), (3, 4096, "f32"),
                                        (64, 512, "bf16"), (1, 64, "bf16"), (8, 4096 * 64, "bf16"),
                                        (8, 2 ** 17 + 1024 + 8, "bf16"),
-                                       # shards of 4 to 8 MiB (destination groups of 4), ragged and not,
-                                       # and just past 8 MiB (no groups)
+                                       # shards above 2 MiB up to 8 MiB (destination groups of 4), ragged
+                                       # and not, and just outside that range (no groups)
+                                       (8, 2 ** 20, "bf16"), (8, 2 ** 20 + 8, "bf16"), (8, 3 * 2 ** 19 + 8, "bf16"),
                                        (8, 2 ** 21 + 8, "bf16"), (8, 2 ** 22 - 8, "bf16"), (8, 2 ** 20 + 4, "f32"),
                                        (8, 2 ** 22, "bf16"), (8, 2 ** 22 + 8, "bf16"),
                                        # 16 MiB + 48 B shards (256-thread shape, no groups)
