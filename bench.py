@@ -157,7 +157,8 @@ def stats(v):
 
 # ---------------------------------------------------------------------------------------------- workloads
 
-COLD_SPAN = 512 << 20  # bytes a graph replay must sweep to leave L2 and the Infinity Cache cold
+COLD_SPAN = 512 << 20  # bytes a graph's buffer rotation must sweep to leave L2 and the Infinity Cache cold
+GRAPH_BYTES = 8 << 30  # bytes one timed graph moves (calls_for)
 
 
 def dev_copy_of(torch, a):
@@ -201,16 +202,22 @@ def oracle_check_ar(nuna, torch, x_np, algo, place):
     return True
 
 
-def calls_for(fp, cold, max_calls=4096):
-    return int(min(max_calls, max(4, math.ceil(COLD_SPAN / fp)))) if cold else int(min(max_calls, max(
-        4, math.ceil((64 << 20) / fp))))
+def calls_for(fp, max_calls=4096):
+    """Calls per captured graph, each call moving `fp` bytes: enough that one graph moves GRAPH_BYTES
+    (at least 4 calls, at most max_calls).  The timer stops when the graph's last kernel ends, while
+    up to 256 MB of its writes can still sit in the Infinity Cache and drain in the gap before the
+    next replay; over several GiB per graph that gap and the replay's own launch stay a few percent.
+    Graphs of 4 calls at 64-576 MiB each moved the figures both ways on MI355X: most large calls
+    ran 2-8 % slower per call than back to back, and one write-heavy all-gather variant ran 1.5x
+    faster."""
+    return int(min(max_calls, max(4, math.ceil(GRAPH_BYTES / fp))))
 
 
 def bench_allreduce(nuna, torch, pool, x_np, algo, reps, warmup, cold=True, places=("linear", "xcd")):
     P, n = len(x_np), x_np[0].size
     es = 2 if x_np[0].dtype == np.uint16 else 4
     fp = ar_footprint(P, n, es)
-    calls = calls_for(fp, cold)
+    calls = calls_for(fp)
     nsets = max(1, min(calls, pool.nbytes // fp)) if cold else 1
     pool.off = 0
     sets = ar_sets(torch, pool, x_np, nsets)
@@ -240,7 +247,7 @@ def bench_rs_ag(nuna, torch, pool, kind, x_np, reps, warmup, cold=True, places=(
     per_in = (n_in * es + ALIGN - 1) // ALIGN * ALIGN
     per_out = (n_out * es + ALIGN - 1) // ALIGN * ALIGN
     fp = P * (per_in + per_out)
-    calls = calls_for(fp, cold)
+    calls = calls_for(fp)
     nsets = max(1, min(calls, pool.nbytes // fp)) if cold else 1
     pool.off = 0
     src = [dev_copy_of(torch, a) for a in x_np]
@@ -280,23 +287,33 @@ RS_AG_KIB = (16, 128, 1024, 4096, 8192)  # bytes per rank of the all-gather inpu
 
 # ---------------------------------------------------------------------------------------------- main line
 
-DECODE_STEPS_PER_GRAPH = 64
+def steps_per_graph(ksteps, step_bytes):
+    """Steps captured per graph: the largest divisor of the timed step count that keeps one graph
+    within GRAPH_BYTES, so that whole replays time exactly `ksteps` steps.  When that divisor is a
+    small fraction of the target (a step count with few divisors), the graph holds the target and
+    the last replay may run past `ksteps`."""
+    target = max(1, math.ceil(GRAPH_BYTES / step_bytes))
+    best = max(d for d in range(1, min(ksteps, target) + 1) if ksteps % d == 0)
+    return best if best * 4 >= min(ksteps, target) else min(ksteps, target)
 
 
 def decode_steps_timed(nuna, torch, pool, args):
     """The timed region: K steps per placement mode, a step being one all-reduce at each decode size.
-    Steps are replayed from a graph holding 64 steps, each on its own pool region (cold)."""
+    Steps are replayed from graphs of `steps_per_graph` steps (several GiB each); step i uses buffer
+    region i mod R of the pool, R as many regions as the pool holds, so each call meets cold caches."""
     from paper_2608_00867_amd import workloads as wl
     xs = [wl.ar_bf16_decode(T) for T in wl.DECODE_TOKENS]
     step_fp = sum(ar_footprint(8, x[0].size, 2) for x in xs)
-    nsteps = DECODE_STEPS_PER_GRAPH
-    assert step_fp * nsteps <= pool.nbytes
+    step_bytes = sum(2 * 8 * x[0].size * 2 for x in xs)
+    nsteps = steps_per_graph(args.steps, step_bytes)
+    nreg = max(1, min(nsteps, pool.nbytes // step_fp))
+    assert step_fp * nreg <= pool.nbytes
     pool.off = 0
     srcs = [[dev_copy_of(torch, a) for a in x] for x in xs]
-    sets = [[ar_sets(torch, pool, x, 1, src)[0] for x, src in zip(xs, srcs)] for _ in range(nsteps)]
+    sets = [[ar_sets(torch, pool, x, 1, src)[0] for x, src in zip(xs, srcs)] for _ in range(nreg)]
 
     def step(i, place):
-        for ins, outs in sets[i]:
+        for ins, outs in sets[i % nreg]:
             nuna.allreduce(ins, outs, algo="auto", placement=place)
 
     graphs = {p: capture(torch, lambda i, p=p: step(i, p), nsteps) for p in ("linear", "xcd")}
@@ -318,7 +335,6 @@ def decode_steps_timed(nuna, torch, pool, args):
             b.synchronize()
             ev[p].append(a.elapsed_time(b))
     torch.cuda.synchronize()
-    step_bytes = sum(2 * 8 * x[0].size * 2 for x in xs)
     out = {}
     for p in graphs:
         ms = sum(ev[p]) / (reps * nsteps)
@@ -546,7 +562,7 @@ def a2a_case(nuna, torch, pool, args, emit, T_tokens=None):
             for a, b in zip(send, src):
                 a.view(-1).copy_(b)
             sets.append((send, recv))
-        calls = max(nsets, calls_for(set_bytes, cold))
+        calls = max(nsets, calls_for(set_bytes))
         ref = oracle.all_to_all(send_np, topk, E)
         ok = True
         for p in ("linear", "xcd"):
@@ -660,7 +676,7 @@ def combine_case(nuna, torch, pool, args, emit, T_tokens=None):
                 for d in range(P):
                     y[d][:int(rows[d])].view(-1).copy_(src[d])
                 sets.append((y, out))
-            calls = max(nsets, calls_for(set_bytes, cold))
+            calls = max(nsets, calls_for(set_bytes))
             ok = True
             for p in ("linear", "xcd"):
                 nuna.all_to_all_combine(sets[0][0], sets[0][1], lay, placement=p, weights=wt)
@@ -710,7 +726,7 @@ def copy_case(nuna, torch, pool, args, emit):
         nsets = max(1, min(pool.nbytes // (2 * nb), math.ceil(COLD_SPAN / (2 * nb))))
         pool.off = 0
         pairs = [(pool.take(nb), pool.take(nb)) for _ in range(nsets)]
-        calls = max(4, nsets)
+        calls = max(nsets, calls_for(2 * nb))
         s = torch.cuda.current_stream()
 
         def fn(i):
@@ -1235,8 +1251,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": "allreduce_bf16_p8_decode", "ranks": 8, "tokens": list(wl_tokens()),
                    "hidden": 8192, "data_dtype": "bf16", "accumulate": "fp32", "placement": "xcd",
-                   "algo": "auto", "cache": "cold (each call on fresh memory of a 1.5 GiB pool)",
-                   "timing": f"HIP graph of {DECODE_STEPS_PER_GRAPH} steps replayed; HIP events"},
+                   "algo": "auto", "cache": "cold (steps rotate over the regions of a 1.5 GiB pool)",
+                   "timing": f"HIP graphs of {steps_per_graph(args.steps, step_bytes)} steps replayed; HIP events"},
         "step_alg_bytes": step_bytes,
         "linear": {"value": round(main_res["linear"]["gbps"], 2),
                    "ms_per_step": round(main_res["linear"]["ms_per_step"], 6)},

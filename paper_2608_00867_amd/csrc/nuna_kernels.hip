@@ -742,8 +742,10 @@ void pick_rs_shape(int64_t in_vectors, int P, int dtype, int& nt, int& vpt) {
 // All-gather launch shape by the vectors each output rank receives, for up
 // to 16 ranks (measured on MI355X with bf16, 8 ranks, cold): one-wave
 // workgroups with 1 vector per thread below 2 MiB per output, 64 threads with
-// 4 vectors below 16 MiB, 128 with 4 below 64 MiB, and 128 with 1 beyond:
-// 5-20 % faster than the all-reduce's shapes.  Forced tunables win.
+// 4 vectors below 16 MiB, 5-20 % faster than the all-reduce's shapes.  From
+// 16 MiB per output, 8 ranks have a rule of their own (below); other rank
+// counts take 128 threads with 4 vectors below 64 MiB and 128 with 1 beyond.
+// Forced tunables win.
 void pick_ag_shape(int64_t out_vectors, int P, int& nt, int& vpt) {
     nt = pick_threads(out_vectors, P);
     vpt = pick_vpt(out_vectors, P);
@@ -754,16 +756,24 @@ void pick_ag_shape(int64_t out_vectors, int P, int& nt, int& vpt) {
     } else if (out_vectors < (int64_t(1) << 20)) {
         nt = 64;
         vpt = 4;
+    } else if (P == 8) {
+        // 8 ranks from 2 MiB shards, measured on MI355X with back-to-back cold
+        // calls: 256 x 1 at 2-4 MiB shards (3-11 % faster than 128 x 4: 37.9
+        // against 42.8 us at 3 MiB), 128 x 1 above 4 and below 16 MiB (5-6 %
+        // faster at 5-7 MiB), 256 x 1 from 16 MiB (220 against 231 us at
+        // 16 MiB shards).
+        if (out_vectors <= (int64_t(1) << 21) || out_vectors >= (int64_t(1) << 23)) {
+            nt = 256;
+            vpt = 1;
+        } else {
+            nt = 128;
+            vpt = 1;
+        }
     } else if (out_vectors < (int64_t(1) << 22)) {
         nt = 128;
         vpt = 4;
-    } else if (P != 8 || out_vectors < (int64_t(1) << 23)) {
-        nt = 128;
-        vpt = 1;
     } else {
-        // 8 ranks, shards of 16 MiB and more: 256-thread workgroups measured
-        // 221 against 232 us at 16 MiB shards and 458 against 474 us at 32 MiB.
-        nt = 256;
+        nt = 128;
         vpt = 1;
     }
 }
@@ -1074,25 +1084,10 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     pick_ag_shape(s.mv * P, P, nt, vpt);
     const int64_t cv = static_cast<int64_t>(nt) * vpt;
     s.wcs = (s.mv + cv - 1) / cv;
-    // Destination split: a work item is a chunk and a group of destinations,
-    // and each member of the chunk's group loads the chunk (an L2 hit for all
-    // but the first when the members sit on one XCD).
-    // - Few chunks (fewer than 512 chunk items): more workgroups share the
-    //   stores.
-    // - 8 ranks with shards above 2 MiB and up to 8 MiB: groups of 4 members,
-    //   each storing 2 destinations.  Fewer write streams per workgroup
-    //   measured faster on MI355X, cold, with XCD placement: 38.6 against
-    //   44.5 us at 3 MiB shards, 49-51 against 58-60 at 4 MiB, 75 against 89
-    //   at 6 MiB, 96-97 against 116 at 8 MiB.  The same split on the linear
-    //   map takes 47, 60, 88 and 119 us (its members' re-reads reach HBM).
-    //   At 2 MiB shards it gained 2.5 %, at 1 MiB nothing.  From 10 MiB shards
-    //   the split at these launch shapes lost 20-25 % (171 against 143 us at
-    //   10 MiB), and with 256 x 4 shapes it gained at most 2 %.
-    int gsize = 1;
-    if (s.wcs * P < 512)
-        gsize = largest_divisor_upto(P, 8);
-    else if (P == 8 && s.mv > (int64_t(1) << 17) && s.mv <= (int64_t(1) << 19))
-        gsize = 4;
+    // Split destinations when there are few chunks, so that more workgroups
+    // share the stores; each member re-reads its chunk (an L2 hit when the
+    // group's members sit on one XCD).
+    const int gsize = (s.wcs * P < 512) ? largest_divisor_upto(P, 8) : 1;
     s.dpi = P / gsize;
     // Each member loads the chunk once and stores it dpi times: gsize - 1 of
     // the group's gsize * (1 + dpi) transfers are re-reads.
