@@ -266,13 +266,11 @@ def test_reduce_scatter(nuna, P, m, dtype, place):
 @pytest.mark.parametrize("P,m,dtype", [(8, 65536, "bf16"), (8, 1000, "bf16"), (8, 3, "f32"), (3, 4096, "f32"),
                                        (64, 512, "bf16"), (1, 64, "bf16"), (8, 4096 * 64, "bf16"),
                                        (8, 2 ** 17 + 1024 + 8, "bf16"),
-                                       # shards above 2 MiB up to 8 MiB (destination groups of 4), ragged
-                                       # and not, and just outside that range (no groups)
+                                       # 8-rank shards on both sides of the launch-shape boundaries at 2, 4
+                                       # and 16 MiB, ragged and not
                                        (8, 2 ** 20, "bf16"), (8, 2 ** 20 + 8, "bf16"), (8, 3 * 2 ** 19 + 8, "bf16"),
                                        (8, 2 ** 21 + 8, "bf16"), (8, 2 ** 22 - 8, "bf16"), (8, 2 ** 20 + 4, "f32"),
-                                       (8, 2 ** 22, "bf16"), (8, 2 ** 22 + 8, "bf16"),
-                                       # 16 MiB + 48 B shards (256-thread shape, no groups)
-                                       (8, 2 ** 23 + 24, "bf16")])
+                                       (8, 2 ** 22, "bf16"), (8, 2 ** 22 + 8, "bf16"), (8, 2 ** 23 + 24, "bf16")])
 def test_all_gather(nuna, P, m, dtype, place):
     x = wl.random_bits(P, m, np.uint16 if dtype == "bf16" else np.float32, 5 * m + P)
     ref = oracle.all_gather(x)
