@@ -234,6 +234,29 @@ __device__ __forceinline__ void load_vecs(uint4 (&dst)[VPT], const uint4* src, i
     }
 }
 
+// Stores of one work item's chunk with the system-scope cache policy (sc0
+// sc1): the lines are written through towards memory instead of staying as
+// dirty lines in L2 and the Infinity Cache.  The accesses go through a buffer
+// resource based at the chunk (`chunk`, uniform), so the lane offsets are
+// chunk-relative bytes and the resource stays in scalar registers; the
+// resource's size is the chunk's bytes, so the hardware drops any store past
+// it.  Lane j of pass q stores vector lane + q*nt of the chunk when that is
+// below `limit` (chunk-relative).
+constexpr int kCpolSystem = 17;  // sc0 | sc1 in the buffer-store cache-policy operand
+
+template <bool FULL, int VPT>
+__device__ __forceinline__ void store_vecs_wt(uint4* chunk, const uint4 (&y)[VPT], int lane, int nt, int64_t limit) {
+    const int bytes = VPT * nt * 16;
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(chunk, 0, bytes, 0x00020000);
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+        if (FULL || lane + j * nt < limit) {
+            const u32x4_t t = {y[j].x, y[j].y, y[j].z, y[j].w};
+            __builtin_amdgcn_raw_buffer_store_b128(t, r, (lane + j * nt) * 16, 0, kCpolSystem);
+        }
+    }
+}
+
 template <bool FULL, int VPT, bool NT = true>
 __device__ __forceinline__ void store_vecs(uint4* dst, const uint4 (&y)[VPT], int64_t v0, int nt, int64_t limit) {
 #pragma unroll

@@ -27,6 +27,7 @@ struct Tuning {
     int combine_chunks = 0;            // combine column chunks per token (0 = by size)
     int tile_v = 0;                    // rank-major tile all-reduce width (16/32/64; 0 = by size)
     int combine_lists = 0;             // 1: combine reads the offset lists even where records exist
+    int write_through = 0;             // 8-rank one-shot stores: 0 by size, 1 streaming, 2 write-through
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).

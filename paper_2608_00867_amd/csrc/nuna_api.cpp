@@ -182,6 +182,7 @@ const TunableDef kTunables[] = {
     {"NUNA_COMBINE_CHUNKS", nullptr, &nuna::Tuning::combine_chunks, 0, INT32_MAX, 0, {}},
     {"NUNA_TILE_V", nullptr, &nuna::Tuning::tile_v, 0, 0, 4, {0, 16, 32, 64}},
     {"NUNA_COMBINE_LISTS", nullptr, &nuna::Tuning::combine_lists, 0, 1, 0, {}},
+    {"NUNA_WRITE_THROUGH", nullptr, &nuna::Tuning::write_through, 0, 2, 0, {}},
 };
 
 const TunableDef* find_tunable(const char* name) {

@@ -26,9 +26,11 @@ struct ArShape {
     int32_t pad;
 };
 
-template <int PT, int DT, int VPT, bool FULL, bool NT, int MAXP>
+// WT: the item's stores use the system-scope cache policy (store_vecs_wt);
+// `cbase` is the chunk's first vector (v0 less the lane).
+template <int PT, int DT, int VPT, bool FULL, bool NT, bool WT, int MAXP>
 __device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const RankTable& tab, const ArShape& s, int P,
-                                                int64_t v0, int nt, int g, bool all_dests) {
+                                                int64_t v0, int nt, int g, bool all_dests, int64_t cbase) {
     using A = Arith<DT>;
     float acc[VPT][A::kLanes];
     reduce_ranks<PT, DT, VPT, FULL, NT>(p, tab, P, 0, v0, nt, s.nvec, acc);
@@ -37,14 +39,20 @@ __device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const RankT
     for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
     if (PT > 0 && all_dests) {
 #pragma unroll
-        for (int d = 0; d < (PT > 0 ? PT : 1); ++d) store_vecs<FULL, VPT>(out_ptr<PT>(p, tab, d), y, v0, nt, s.nvec);
+        for (int d = 0; d < (PT > 0 ? PT : 1); ++d) {
+            if constexpr (WT)
+                store_vecs_wt<FULL, VPT>(out_ptr<PT>(p, tab, d) + cbase, y, static_cast<int>(threadIdx.x), nt,
+                                         s.nvec - cbase);
+            else
+                store_vecs<FULL, VPT>(out_ptr<PT>(p, tab, d), y, v0, nt, s.nvec);
+        }
     } else {
         const int d0 = g * s.dpi;
         for (int d = d0; d < d0 + s.dpi; ++d) store_vecs<FULL, VPT>(out_ptr<PT>(p, tab, d), y, v0, nt, s.nvec);
     }
 }
 
-template <int PT, int MAXP, int DT, int VPT>
+template <int PT, int MAXP, int DT, int VPT, bool WT>
 __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Place pl) {
     using A = Arith<DT>;
     const int nt = blockDim.x;
@@ -74,14 +82,14 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
         // read through L2 so the group's re-reads hit.
         if (all_dests) {
             if ((c + 1) * cv <= s.nvec)
-                allreduce_chunk<PT, DT, VPT, true, true>(p, tab, s, P, v0, nt, g, all_dests);
+                allreduce_chunk<PT, DT, VPT, true, true, WT>(p, tab, s, P, v0, nt, g, all_dests, c * cv);
             else
-                allreduce_chunk<PT, DT, VPT, false, true>(p, tab, s, P, v0, nt, g, all_dests);
+                allreduce_chunk<PT, DT, VPT, false, true, WT>(p, tab, s, P, v0, nt, g, all_dests, c * cv);
         } else {
             if ((c + 1) * cv <= s.nvec)
-                allreduce_chunk<PT, DT, VPT, true, false>(p, tab, s, P, v0, nt, g, all_dests);
+                allreduce_chunk<PT, DT, VPT, true, false, false>(p, tab, s, P, v0, nt, g, all_dests, c * cv);
             else
-                allreduce_chunk<PT, DT, VPT, false, false>(p, tab, s, P, v0, nt, g, all_dests);
+                allreduce_chunk<PT, DT, VPT, false, false, false>(p, tab, s, P, v0, nt, g, all_dests, c * cv);
         }
     }
     if (s.tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < s.tail) {
@@ -100,7 +108,7 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
 // follow at once.  The general kernel above first reads its placement state
 // and then the pointers, a chain of dependent argument loads that measured
 // about 1 us per launch at 1 MiB per rank on MI355X (5.3 against 4.2 us).
-template <int PT, int DT, int VPT>
+template <int PT, int DT, int VPT, bool WT>
 __global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nvec, int32_t tail) {
     using A = Arith<DT>;
     const int nt = blockDim.x;
@@ -113,9 +121,9 @@ __global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nv
     s.P = PT;
     const RankTable tab{0u, 0u, 0u, 0u};  // compile-time rank count: pointers come from the arguments
     if ((c + 1) * cv <= nvec)
-        allreduce_chunk<PT, DT, VPT, true, true>(p, tab, s, PT, v0, nt, 0, true);
+        allreduce_chunk<PT, DT, VPT, true, true, WT>(p, tab, s, PT, v0, nt, 0, true, c * cv);
     else
-        allreduce_chunk<PT, DT, VPT, false, true>(p, tab, s, PT, v0, nt, 0, true);
+        allreduce_chunk<PT, DT, VPT, false, true, WT>(p, tab, s, PT, v0, nt, 0, true, c * cv);
     if (tail > 0 && blockIdx.x == 0 && static_cast<int>(threadIdx.x) < tail) {
         const int64_t i = nvec * (16 / A::kEsize) + threadIdx.x;
         float a = A::load1(p.in[0], i);
@@ -574,22 +582,31 @@ __global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uin
 
 // ---------------------------------------------------------------- launch helpers
 
-template <int PT, int MAXP, int DT, int VPT>
+template <int PT, int MAXP, int DT, int VPT, bool WT = false>
 void launch_ar_t(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G, int nt,
                  hipStream_t st) {
     Ptrs<MAXP> p = make_ptrs<MAXP>(in, out, P, P);
-    hipLaunchKernelGGL((k_allreduce<PT, MAXP, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p, s, pl);
+    hipLaunchKernelGGL((k_allreduce<PT, MAXP, DT, VPT, WT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p, s,
+                       pl);
+}
+
+// 8 ranks with or without write-through stores.
+template <int DT, int VPT>
+void launch_ar_8(const void* const* in, void* const* out, const ArShape& s, const Place& pl, int64_t G, int nt,
+                 bool wt, hipStream_t st) {
+    if (wt) launch_ar_t<8, 8, DT, VPT, true>(in, out, 8, s, pl, G, nt, st);
+    else launch_ar_t<8, 8, DT, VPT, false>(in, out, 8, s, pl, G, nt, st);
 }
 
 template <int DT, int VPT>
 void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& s, const Place& pl, int64_t G, int nt,
-                 hipStream_t st) {
+                 bool wt, hipStream_t st) {
     if constexpr (VPT == 8) {
         // Eight vectors per thread exist for 2, 4 and 8 ranks only (pick_ar_shape).
         switch (P) {
             case 2: launch_ar_t<2, 2, DT, 8>(in, out, P, s, pl, G, nt, st); break;
             case 4: launch_ar_t<4, 4, DT, 8>(in, out, P, s, pl, G, nt, st); break;
-            case 8: launch_ar_t<8, 8, DT, 8>(in, out, P, s, pl, G, nt, st); break;
+            case 8: launch_ar_8<DT, 8>(in, out, s, pl, G, nt, wt, st); break;
             default: break;  // refused by launch_allreduce
         }
         return;
@@ -597,7 +614,7 @@ void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& 
     switch (P) {
         case 2: launch_ar_t<2, 2, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         case 4: launch_ar_t<4, 4, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
-        case 8: launch_ar_t<8, 8, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
+        case 8: launch_ar_8<DT, VPT>(in, out, s, pl, G, nt, wt, st); break;
         case 16: launch_ar_t<16, 16, DT, VPT>(in, out, P, s, pl, G, nt, st); break;
         default:
             if constexpr (VPT == 1) {
@@ -611,21 +628,25 @@ void launch_ar_p(const void* const* in, void* const* out, int P, const ArShape& 
     }
 }
 
-template <int PT, int DT, int VPT>
+template <int PT, int DT, int VPT, bool WT = false>
 void launch_ar_direct_t(const void* const* in, void* const* out, const ArShape& s, int64_t G, int nt, hipStream_t st) {
     const Ptrs<PT> p = make_ptrs<PT>(in, out, PT, PT);
-    hipLaunchKernelGGL((k_allreduce_direct<PT, DT, VPT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p, s.nvec,
-                       s.tail);
+    hipLaunchKernelGGL((k_allreduce_direct<PT, DT, VPT, WT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p,
+                       s.nvec, s.tail);
 }
 
-// Direct kernel for 2, 4, 8 or 16 ranks (8 vectors per thread: 2, 4 or 8 ranks).
+// Direct kernel for 2, 4, 8 or 16 ranks (8 vectors per thread: 2, 4 or 8 ranks);
+// write-through stores with 8 ranks when `wt`.
 template <int DT, int VPT>
-void launch_ar_direct_p(const void* const* in, void* const* out, int P, const ArShape& s, int64_t G, int nt,
+void launch_ar_direct_p(const void* const* in, void* const* out, int P, const ArShape& s, int64_t G, int nt, bool wt,
                         hipStream_t st) {
     switch (P) {
         case 2: launch_ar_direct_t<2, DT, VPT>(in, out, s, G, nt, st); break;
         case 4: launch_ar_direct_t<4, DT, VPT>(in, out, s, G, nt, st); break;
-        case 8: launch_ar_direct_t<8, DT, VPT>(in, out, s, G, nt, st); break;
+        case 8:
+            if (wt) launch_ar_direct_t<8, DT, VPT, true>(in, out, s, G, nt, st);
+            else launch_ar_direct_t<8, DT, VPT, false>(in, out, s, G, nt, st);
+            break;
         default:
             if constexpr (VPT != 8) launch_ar_direct_t<16, DT, VPT>(in, out, s, G, nt, st);
             break;
@@ -936,32 +957,40 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
                                 : mode;
     const Place pl = make_place_uniform(gmode, groups > 0 ? groups : 1, gsize);
     const int64_t G = cap_grid(place_grid(pl));
+    // Write-through stores (store_vecs_wt): 8 ranks, 8 vectors per thread,
+    // from 16 MiB per rank.  Against streaming stores on MI355X, back-to-back
+    // calls: 1.3 % faster cold and 8 % warm at 16 MiB per rank, 3.4 % and
+    // 13 % at 32 MiB; 1-14 % slower cold below 16 MiB (though 6-24 % faster
+    // warm) and 16 % slower at 64 MiB (the one-vector general kernel).
+    const int wtf = tuning().write_through;
+    const bool wt = P == 8 && gsize == 1 &&
+                    (wtf == 2 || (wtf == 0 && vpt == 8 && bytes >= (size_t(16) << 20)));
     // One item per workgroup on the linear map: the direct kernel.
     if (gsize == 1 && G == groups && G <= kDirectMaxGrid && direct_ranks(P, vpt)) {
         if (dtype == kDtF32) {
-            if (vpt == 8) launch_ar_direct_p<kDtF32, 8>(in, out, P, s, G, nt, stream);
-            else if (vpt == 4) launch_ar_direct_p<kDtF32, 4>(in, out, P, s, G, nt, stream);
-            else if (vpt == 2) launch_ar_direct_p<kDtF32, 2>(in, out, P, s, G, nt, stream);
-            else launch_ar_direct_p<kDtF32, 1>(in, out, P, s, G, nt, stream);
+            if (vpt == 8) launch_ar_direct_p<kDtF32, 8>(in, out, P, s, G, nt, wt, stream);
+            else if (vpt == 4) launch_ar_direct_p<kDtF32, 4>(in, out, P, s, G, nt, wt, stream);
+            else if (vpt == 2) launch_ar_direct_p<kDtF32, 2>(in, out, P, s, G, nt, wt, stream);
+            else launch_ar_direct_p<kDtF32, 1>(in, out, P, s, G, nt, wt, stream);
         } else {
-            if (vpt == 8) launch_ar_direct_p<kDtBf16, 8>(in, out, P, s, G, nt, stream);
-            else if (vpt == 4) launch_ar_direct_p<kDtBf16, 4>(in, out, P, s, G, nt, stream);
-            else if (vpt == 2) launch_ar_direct_p<kDtBf16, 2>(in, out, P, s, G, nt, stream);
-            else launch_ar_direct_p<kDtBf16, 1>(in, out, P, s, G, nt, stream);
+            if (vpt == 8) launch_ar_direct_p<kDtBf16, 8>(in, out, P, s, G, nt, wt, stream);
+            else if (vpt == 4) launch_ar_direct_p<kDtBf16, 4>(in, out, P, s, G, nt, wt, stream);
+            else if (vpt == 2) launch_ar_direct_p<kDtBf16, 2>(in, out, P, s, G, nt, wt, stream);
+            else launch_ar_direct_p<kDtBf16, 1>(in, out, P, s, G, nt, wt, stream);
         }
         return hipGetLastError();
     }
     // The kernel's vectors per thread must be the VPT the chunks were sized with.
     if (dtype == kDtF32) {
-        if (vpt == 8) launch_ar_p<kDtF32, 8>(in, out, P, s, pl, G, nt, stream);
-        else if (vpt == 4) launch_ar_p<kDtF32, 4>(in, out, P, s, pl, G, nt, stream);
-        else if (vpt == 2) launch_ar_p<kDtF32, 2>(in, out, P, s, pl, G, nt, stream);
-        else launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, nt, stream);
+        if (vpt == 8) launch_ar_p<kDtF32, 8>(in, out, P, s, pl, G, nt, wt, stream);
+        else if (vpt == 4) launch_ar_p<kDtF32, 4>(in, out, P, s, pl, G, nt, wt, stream);
+        else if (vpt == 2) launch_ar_p<kDtF32, 2>(in, out, P, s, pl, G, nt, wt, stream);
+        else launch_ar_p<kDtF32, 1>(in, out, P, s, pl, G, nt, wt, stream);
     } else {
-        if (vpt == 8) launch_ar_p<kDtBf16, 8>(in, out, P, s, pl, G, nt, stream);
-        else if (vpt == 4) launch_ar_p<kDtBf16, 4>(in, out, P, s, pl, G, nt, stream);
-        else if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, stream);
-        else launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, stream);
+        if (vpt == 8) launch_ar_p<kDtBf16, 8>(in, out, P, s, pl, G, nt, wt, stream);
+        else if (vpt == 4) launch_ar_p<kDtBf16, 4>(in, out, P, s, pl, G, nt, wt, stream);
+        else if (vpt == 2) launch_ar_p<kDtBf16, 2>(in, out, P, s, pl, G, nt, wt, stream);
+        else launch_ar_p<kDtBf16, 1>(in, out, P, s, pl, G, nt, wt, stream);
     }
     return hipGetLastError();
 }

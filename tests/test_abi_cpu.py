@@ -283,11 +283,13 @@ def test_a2a_layout_rejects_more_than_int32_tokens():
 
 def test_tunables_set_get_restore_and_reject():
     names = ["NUNA_MAX_GRID", "NUNA_WG_THREADS", "NUNA_VPT", "NUNA_LPR_MIN_RANKS", "NUNA_LPR_MAX_VECTORS",
-             "NUNA_COMBINE_VPT", "NUNA_COMBINE_CHUNKS", "NUNA_TILE_V", "NUNA_COMBINE_LISTS"]
+             "NUNA_COMBINE_VPT", "NUNA_COMBINE_CHUNKS", "NUNA_TILE_V", "NUNA_COMBINE_LISTS",
+             "NUNA_WRITE_THROUGH"]
     before = {n: nuna.get_tunable(n) for n in names}
     with nuna.tunables(NUNA_TILE_V=32, NUNA_WG_THREADS=128, NUNA_LPR_MAX_VECTORS=1 << 33, NUNA_COMBINE_CHUNKS=3,
-                       NUNA_VPT=8, NUNA_COMBINE_LISTS=1):
+                       NUNA_VPT=8, NUNA_COMBINE_LISTS=1, NUNA_WRITE_THROUGH=2):
         assert nuna.get_tunable("NUNA_COMBINE_LISTS") == 1
+        assert nuna.get_tunable("NUNA_WRITE_THROUGH") == 2
         assert nuna.get_tunable("NUNA_VPT") == 8
         assert nuna.get_tunable("NUNA_TILE_V") == 32
         assert nuna.get_tunable("NUNA_WG_THREADS") == 128
@@ -296,6 +298,7 @@ def test_tunables_set_get_restore_and_reject():
     assert {n: nuna.get_tunable(n) for n in names} == before
     for name, bad in [("NUNA_TILE_V", 8), ("NUNA_VPT", 3), ("NUNA_WG_THREADS", 32), ("NUNA_LPR_MIN_RANKS", 0),
                       ("NUNA_MAX_GRID", -1), ("NUNA_COMBINE_VPT", 8), ("NUNA_COMBINE_LISTS", 2),
+                      ("NUNA_WRITE_THROUGH", 3),
                       ("NUNA_NOT_A_KNOB", 1)]:
         with pytest.raises(nuna.NunaError):
             nuna.set_tunable(name, bad)

@@ -394,6 +394,35 @@ def test_launch_shape_variants(nuna, cfg):
             _ar_vs_oracle(nuna, wl.normal_bf16(P, n, 31 * P + n), f"{cfg} P={P} n={n}")
 
 
+@pytest.mark.parametrize("cfg", [dict(NUNA_WRITE_THROUGH=w, NUNA_VPT=v, NUNA_WG_THREADS=t)
+                                 for w in (1, 2) for v, t in ((0, 0), (1, 64), (2, 128), (4, 256), (8, 256))],
+                         ids=lambda c: ",".join(f"{k[5:]}={v}" for k, v in c.items()))
+def test_write_through_stores(nuna, cfg):
+    """The 8-rank one-shot with write-through stores forced on (and off), at every launch shape: ragged
+    chunks, one chunk, many chunks, the general kernel (split groups, grid caps) and in place."""
+    with nuna.tunables(**cfg):
+        for n, dt in ((1, np.uint16), (9, np.float32), (4097, np.uint16), (70001, np.float32),
+                      (2 ** 20 + 24, np.uint16), (2 ** 21 + 4, np.float32)):
+            x = wl.normal_bf16(8, n, 13 * n + 5) if dt == np.uint16 else wl.normal_f32(8, n, 13 * n + 5)
+            _ar_vs_oracle(nuna, x, f"{cfg} n={n}")
+        x = wl.normal_bf16(8, 2 ** 19 + 40, 7)
+        ref = oracle.allreduce(x)
+        for cap in (7, 64):
+            nuna.set_max_workgroups(cap)
+            try:
+                for place in PLACES:
+                    got = run_allreduce(nuna, x, "one_shot", place)
+                    for d in range(8):
+                        assert_bitwise(got[d], ref[d], f"{cfg} cap={cap} {place} rank {d}")
+            finally:
+                nuna.set_max_workgroups(0)
+        bufs = [to_dev(a) for a in x]
+        nuna.allreduce(bufs, bufs, algo="one_shot", placement="xcd")
+        torch.cuda.synchronize()
+        for d in range(8):
+            assert_bitwise(to_host(bufs[d]), ref[d], f"{cfg} in place rank {d}")
+
+
 def test_vpt8_every_collective(nuna):
     """Eight vectors per thread exist for the all-reduce with 2, 4 or 8 ranks only; forced for every
     collective, the others fall back to 4 and every result keeps the oracle's bits."""
