@@ -136,9 +136,11 @@ nuna_status_t nuna_set_max_workgroups(int max_workgroups);
  *                         (workgroup threads x combine vectors per thread) vectors
  *   NUNA_COMBINE_LISTS    0: the combine reads per-token records with up to 8 ranks;
  *                         1: always the offset lists
- *   NUNA_WRITE_THROUGH    stores of the 8-rank one-shot all-reduce: 0 (system-scope
- *                         write-through with 8 vectors per thread from 16 MiB per rank,
- *                         streaming elsewhere), 1 (always streaming), 2 (always write-through)
+ *   NUNA_WRITE_THROUGH    stores of the 8-rank one-shot all-reduce and of the 8-rank two-shot's
+ *                         all-gather phase: 0 (system-scope write-through where measured
+ *                         faster: one-shot with 8 vectors per thread from 16 MiB per rank,
+ *                         all-gather phase at 1-2 MiB shards; streaming elsewhere),
+ *                         1 (always streaming), 2 (always write-through)
  *   NUNA_TILE_V           rank-major tile all-reduce width: 0 (16 up to 256 KiB per
  *                         rank, else off), 16, 32, 64
  * Unknown names and values outside these sets: NUNA_ERR_INVALID_ARG. */

@@ -398,8 +398,9 @@ def test_launch_shape_variants(nuna, cfg):
                                  for w in (1, 2) for v, t in ((0, 0), (1, 64), (2, 128), (4, 256), (8, 256))],
                          ids=lambda c: ",".join(f"{k[5:]}={v}" for k, v in c.items()))
 def test_write_through_stores(nuna, cfg):
-    """The 8-rank one-shot with write-through stores forced on (and off), at every launch shape: ragged
-    chunks, one chunk, many chunks, the general kernel (split groups, grid caps) and in place."""
+    """The 8-rank one-shot and the two-shot's all-gather phase with write-through stores forced on (and
+    off), at every launch shape: ragged chunks, one chunk, many chunks, the general kernel (grid caps),
+    in place, and shards with and without whole vectors."""
     with nuna.tunables(**cfg):
         for n, dt in ((1, np.uint16), (9, np.float32), (4097, np.uint16), (70001, np.float32),
                       (2 ** 20 + 24, np.uint16), (2 ** 21 + 4, np.float32)):
@@ -421,6 +422,14 @@ def test_write_through_stores(nuna, cfg):
         torch.cuda.synchronize()
         for d in range(8):
             assert_bitwise(to_host(bufs[d]), ref[d], f"{cfg} in place rank {d}")
+        # the two-shot's all-gather phase (its shards read through the caches)
+        for n in (8 * 1024, 8 * 70001, 8 * 2 ** 18, 8 * (2 ** 19 + 8)):
+            x = wl.normal_bf16(8, n, 11 * n + 3)
+            ref = oracle.allreduce(x)
+            for place in PLACES:
+                got = run_allreduce(nuna, x, "two_shot", place)
+                for d in range(8):
+                    assert_bitwise(got[d], ref[d], f"{cfg} two-shot {place} n={n} rank {d}")
 
 
 def test_vpt8_every_collective(nuna):
