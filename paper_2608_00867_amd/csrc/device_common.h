@@ -240,13 +240,14 @@ __device__ __forceinline__ void load_vecs(uint4 (&dst)[VPT], const uint4* src, i
 // resource based at the chunk (`chunk`, uniform), so the lane offsets are
 // chunk-relative bytes and the resource stays in scalar registers; the
 // resource's size is the chunk's bytes, so the hardware drops any store past
-// it.  Lane j of pass q stores vector lane + q*nt of the chunk when that is
-// below `limit` (chunk-relative).
+// it.  In pass j the thread `lane` stores vector lane + j*nt of the chunk
+// when that is below `limit` (chunk-relative).
 constexpr int kCpolSystem = 17;  // sc0 | sc1 in the buffer-store cache-policy operand
 
 template <bool FULL, int VPT>
 __device__ __forceinline__ void store_vecs_wt(uint4* chunk, const uint4 (&y)[VPT], int lane, int nt, int64_t limit) {
     const int bytes = VPT * nt * 16;
+    // Resource word 3: data format 32 (bits 15-18 = 4), no swizzle.
     const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(chunk, 0, bytes, 0x00020000);
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
