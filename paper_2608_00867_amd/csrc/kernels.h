@@ -18,7 +18,7 @@ inline size_t dtype_size(int dt) { return dt == kDtF32 ? 4u : 2u; }
 // Tunables (read once from the environment by the host API; they change the
 // launch shape only, never the arithmetic).
 struct Tuning {
-    int max_grid = 16384;  // cap on workgroups per launch (persistent loop beyond)
+    int max_grid = 0;      // cap on workgroups per launch (persistent loop beyond); 0: 16384
     int wg_threads = 0;    // workgroup size for the streaming kernels (0 = by size)
     int vpt = 0;           // vectors per thread per work item (0 = by size; 8: one-shot all-reduce only)
     int lpr_min_ranks = 16;           // many-rank all-reduce kernels (tile, lane per rank) from this many ranks
@@ -32,6 +32,10 @@ struct Tuning {
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
 int max_workgroups();
+// Largest grid for a kernel that runs one work item per workgroup and is
+// better off without a persistent loop: the caller's cap when one is set
+// (nuna_set_max_workgroups or NUNA_MAX_GRID), otherwise `dflt`.
+int64_t grid_limit(int64_t dflt);
 
 // One-shot all-reduce.  `dest_groups` > 1 selects the split variant: a work
 // item is (chunk, destination group) and writes P/dest_groups outputs.

@@ -215,6 +215,12 @@ int max_workgroups() {
     if (v > 0) return v;
     return tuning().max_grid > 0 ? tuning().max_grid : 16384;
 }
+
+int64_t grid_limit(int64_t dflt) {
+    const int v = g_max_workgroups.load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    return tuning().max_grid > 0 ? tuning().max_grid : dflt;
+}
 }  // namespace nuna
 
 // ============================================================== C ABI

@@ -674,6 +674,7 @@ bool direct_ranks(int P, int vpt) { return P == 2 || P == 4 || P == 8 || (P == 1
 // against 209 us), while up to 8192 workgroups the direct kernels were as fast
 // or faster at every size measured (1-64 MiB per rank, 1-4 vectors per thread).
 constexpr int64_t kDirectMaxGrid = 8192;
+constexpr int64_t kAgDirectMaxGrid8 = int64_t(1) << 20;  // 8-rank all-gather (launch_all_gather)
 
 template <int PT, int MAXP, int DT, int VPT, bool KEEP>
 void launch_rs_t(const void* const* in, void* const* out, int P, const RsShape& s, const Place& pl, int64_t G, int nt,
@@ -791,18 +792,12 @@ void pick_ag_shape(int64_t out_vectors, int P, int& nt, int& vpt) {
         nt = 64;
         vpt = 4;
     } else if (P == 8) {
-        // 8 ranks from 2 MiB shards, measured on MI355X with back-to-back cold
-        // calls: 256 x 1 at 2-4 MiB shards (3-11 % faster than 128 x 4: 37.9
-        // against 42.8 us at 3 MiB), 128 x 1 above 4 and below 16 MiB (5-6 %
-        // faster at 5-7 MiB), 256 x 1 from 16 MiB (220 against 231 us at
-        // 16 MiB shards).
-        if (out_vectors <= (int64_t(1) << 21) || out_vectors >= (int64_t(1) << 23)) {
-            nt = 256;
-            vpt = 1;
-        } else {
-            nt = 128;
-            vpt = 1;
-        }
+        // 8 ranks from 2 MiB shards: 256 x 1, with the direct kernel at any
+        // grid (launch_all_gather).  Measured on MI355X with back-to-back cold
+        // calls: 3-11 % faster than 128 x 4 at 2-4 MiB shards (37.9 against
+        // 42.8 us at 3 MiB), best or within 1 % of the best shape at 4-32 MiB.
+        nt = 256;
+        vpt = 1;
     } else if (out_vectors < (int64_t(1) << 22)) {
         nt = 128;
         vpt = 4;
@@ -1153,7 +1148,14 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     const int64_t shard = static_cast<int64_t>(m * es);
     const bool wt = P == 8 && src_cached && gsize == 1 &&
                     (wtf == 2 || (wtf == 0 && shard >= (int64_t(1) << 20) && shard <= (int64_t(2) << 20)));
-    if (gsize == 1 && G == s.wcs * P && G <= kDirectMaxGrid && (P == 2 || P == 4 || P == 8)) {
+    // The direct kernel when every chunk item has its own workgroup.  With 8
+    // ranks it takes grids beyond kDirectMaxGrid too: against the general
+    // kernel's persistent loop it measured 6-10 % faster at 6-32 MiB shards on
+    // MI355X (103 against 114 us at 8 MiB, 418 against 457 us at 32 MiB).
+    const int64_t items = s.wcs * P;
+    const bool direct = gsize == 1 && (P == 8 ? items <= grid_limit(kAgDirectMaxGrid8)
+                                              : (P == 2 || P == 4) && G == items && G <= kDirectMaxGrid);
+    if (direct) {
         const dim3 g(static_cast<unsigned>(s.wcs), static_cast<unsigned>(P)), b(nt);
         switch (P) {
             case 2: launch_ag_direct_p<2>(in, out, s, vpt, src_cached, false, g, b, stream); break;
