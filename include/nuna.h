@@ -112,9 +112,12 @@ int nuna_version(void);
 
 /* Cap on workgroups per kernel launch for all later calls of the process
  * (0 restores the default, 16384).  Work beyond the cap is looped over by
- * each workgroup (persistent loop), in the same placement.  Changes the
- * launch shape only, never results; lets a caller leave compute units free
- * for concurrent kernels.  Returns NUNA_ERR_INVALID_ARG for values < 0. */
+ * each workgroup (persistent loop), in the same placement.  Without a cap set
+ * here or through NUNA_MAX_GRID, the 8-rank all-gather and the MoE dispatch
+ * run one workgroup per work item up to 2^20 workgroups; a cap that is set
+ * bounds them too.  Changes the launch shape only, never results; lets a
+ * caller leave compute units free for concurrent kernels.  Returns
+ * NUNA_ERR_INVALID_ARG for values < 0. */
 nuna_status_t nuna_set_max_workgroups(int max_workgroups);
 
 /* Launch-shape tunables, by the name of the environment variable that also
@@ -122,7 +125,8 @@ nuna_status_t nuna_set_max_workgroups(int max_workgroups);
  * kernel variants and grid caps; they never change results.  A setting
  * applies to later calls of the process; it must not race with other calls
  * into the library.
- *   NUNA_MAX_GRID         default workgroup cap, 0..INT32_MAX (0: 16384)
+ *   NUNA_MAX_GRID         default workgroup cap, 0..INT32_MAX (0: 16384, and see
+ *                         nuna_set_max_workgroups)
  *   NUNA_WG_THREADS       0 (by size), 64, 128, 256
  *   NUNA_VPT              vectors per thread of the all-reduce, reduce-scatter and
  *                         all-gather: 0 (by size), 1, 2, 4, 8 (8: one-shot all-reduce
