@@ -67,6 +67,8 @@ def parse():
                     help="profiling run: N cold launches each of the dominant kernel (decode all-reduce T=64, "
                          "XCD), the 64 MiB reference copy, the split all-reduce (T=64), the MoE dispatch and "
                          "combine, eager, then exit")
+    ap.add_argument("--summarize-counters", metavar="CSV", default=None,
+                    help="print per-kernel medians of every counter in one rocprofv3 --pmc CSV")
     ap.add_argument("--summarize-l2", nargs=2, metavar=("LINEAR_CSV", "XCD_CSV"), default=None,
                     help="markdown table of TCC_HIT_sum / TCC_MISS_sum from two --profile runs (LINEAR, XCD)")
     ap.add_argument("--xcc-counter-defs", metavar="YAML", default=None,
@@ -1095,6 +1097,25 @@ def summarize_traffic(fetch_csv, write_csv):
             print(f"| `{k[0]}` | {k[1]} | {fk:.1f} | {wk:.1f} | {fb:.0f} | {wb:.0f} | {(fb + wb) / a:.4f} |")
 
 
+def summarize_counters(path):
+    """Per-kernel medians over dispatches of every counter in one rocprofv3 --pmc CSV (the library's
+    kernels only)."""
+    import csv
+    import collections
+    by = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in csv.DictReader(open(path)):
+        by[(_short(r["Kernel_Name"]), int(r["Grid_Size"]))][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    names = sorted({c for v in by.values() for c in v})
+    print("| kernel | grid (threads) | dispatches | " + " | ".join(names) + " |")
+    print("|---|---|---|" + "---|" * len(names))
+    for k, v in by.items():
+        if not k[0].startswith(("k_", "nuna")):
+            continue
+        n = max(len(x) for x in v.values())
+        cells = [f"{statistics.median(v[c]):.0f}" if c in v else "" for c in names]
+        print(f"| `{k[0]}` | {k[1]} | {n} | " + " | ".join(cells) + " |")
+
+
 def summarize_l2(linear_csv, xcd_csv):
     """TCC_HIT_sum / TCC_MISS_sum (L2 requests per dispatch, summed over the 8 XCDs' L2s) of two
     --profile runs, one per placement: the kernels whose map the placement changes."""
@@ -1199,6 +1220,9 @@ def main():
         return
     if args.summarize_l2_xcc:
         summarize_l2_xcc(args.summarize_l2_xcc)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters)
         return
     if args.summarize_l2:
         summarize_l2(*args.summarize_l2)

@@ -437,3 +437,22 @@ def test_last_error_is_per_thread():
     assert len(results["bad_in"]) == 1
     st, msg = next(iter(results["bad_in"]))
     assert st == nuna.ERR_OVERLAP and "overlap" in msg
+
+
+def test_counter_summary_medians(tmp_path):
+    """`bench.py --summarize-counters` reports per-kernel medians and keeps only the library's kernels."""
+    import subprocess
+    import sys
+    rows = ["Kernel_Name,Grid_Size,Counter_Name,Counter_Value"]
+    for v in (3, 1, 2):
+        rows.append(f'"void k_copy<1>(uint4*, int)",4096,SQ_WAVES,{v}')
+    rows.append('"void k_copy<1>(uint4*, int)",4096,GRBM_GUI_ACTIVE,10')
+    rows.append('"at::native::elementwise_kernel",256,SQ_WAVES,7')
+    csv_path = tmp_path / "c.csv"
+    csv_path.write_text("\n".join(rows) + "\n")
+    out = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--summarize-counters", str(csv_path)],
+                         capture_output=True, text=True, check=True).stdout
+    lines = [ln for ln in out.splitlines() if ln.startswith("| `")]
+    assert len(lines) == 1
+    cells = [c.strip() for c in lines[0].strip("|").split("|")]
+    assert cells[1:] == ["4096", "3", "10", "2"]
