@@ -216,6 +216,8 @@ __global__ __launch_bounds__(kWG) void k_combine_rec(Ptrs<kCombRecRanks> p, cons
                 if constexpr (WT) wq[q] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w_lane), r));
             }
         }
+        // Every token has at least one destination (the layout requires top-k >= 1 and experts in
+        // range) and its records are packed from word 0, so record 0 always starts the sum.
         float acc[VPT][A::kLanes];
 #pragma unroll
         for (int q = 0; q < kCombRecRanks; ++q)
