@@ -997,7 +997,7 @@ def profile_moe(nuna, torch, pool, n, place="xcd"):
 TRAFFIC_JSON = os.path.join(ROOT, "profiles", "dominant_traffic.json")
 # Sources the dominant kernel is compiled from (its kernel file and the headers it includes).
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_00867_amd", "csrc", f)
-                  for f in ("nuna_kernels.hip", "device_common.h", "placement.h", "kernels.h")]
+                  for f in ("nuna_allreduce.hip", "device_common.h", "placement.h", "kernels.h", "shapes.h")]
 
 
 def kernel_source_text(text):

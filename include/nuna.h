@@ -22,16 +22,24 @@
  * Workgroup b of a launch runs on XCD (b mod 8) on MI355X.
  *   NUNA_PLACE_LINEAR  work item w runs on workgroup w (grid-stride): the
  *                      round-robin, locality-unaware baseline (UA).
- *   NUNA_PLACE_XCD     work items that touch the same data chunk form one
- *                      logical group; groups are dealt round-robin to the 8
- *                      XCDs and a group's members run concurrently on one
- *                      XCD, sharing its L2 (NAP* -- aware workgroup
- *                      placement, default page placement).  A group of one
- *                      work item is placed as LINEAR places it.  Groups
- *                      stay together only where the members' L2 re-reads
- *                      are at least a quarter of the group's traffic and,
- *                      for the split all-reduce, the launch moves more than
- *                      256 KiB; elsewhere XCD runs the linear map.
+ *   NUNA_PLACE_XCD     work items that touch the same data form one logical
+ *                      group; groups are dealt round-robin to the 8 XCDs and
+ *                      a group's members run concurrently on one XCD,
+ *                      sharing its L2 (NAP* -- aware workgroup placement,
+ *                      default page placement).  Groups are the work items
+ *                      of one input chunk (split all-reduce, split
+ *                      all-gather), the copies of one token row (all-to-all
+ *                      dispatch), and, for one-work-item-per-workgroup
+ *                      launches whose chunks are smaller than a 4 KiB page,
+ *                      the chunks of one page (Sec. 4.2: 4 kB pages; tunable
+ *                      NUNA_PAGE_GROUPS).  A group of one work item is placed
+ *                      as LINEAR places it.  Chunk groups stay together only
+ *                      where the members' L2 re-reads are at least a quarter
+ *                      of the group's traffic and, for the split all-reduce,
+ *                      the launch moves more than 256 KiB; elsewhere XCD runs
+ *                      the linear map.  XCD mode needs nuna_init to have
+ *                      verified the dispatch map on the current device (else
+ *                      NUNA_ERR_UNSUPPORTED); LINEAR needs nothing.
  * The mode changes which workgroup computes what, never the result.
  *
  * Buffers and ownership.  All data buffers are device memory owned by the
@@ -50,6 +58,15 @@
  * read-only once uploaded and may be shared by concurrent calls.  The
  * setters nuna_set_max_workgroups and nuna_set_tunable change process-wide
  * launch shapes and must not race with other calls.
+ *
+ * Interface additions to the plain collective calls (kept because a single
+ * GPU needs them): the all-to-all calls take the receive capacity of the
+ * caller's buffers (recv_capacity_rows, y_capacity_rows), so the library can
+ * check them; layouts are planned on the host (nuna_a2a_layout_create) and
+ * copied to the device by a separate call (nuna_a2a_layout_upload), which is
+ * the only allocating step; the algorithm enum adds the destination-split
+ * one-shot and the two-kernel two-shot; NUNA_ERR_NO_MEMORY reports host
+ * memory exhaustion.
  *
  * Errors.  Every call returns a status and never aborts or lets an exception
  * out.  All argument checks run on the host before any HIP call.  On failure,
@@ -89,19 +106,51 @@ typedef enum { NUNA_PLACE_LINEAR = 0, NUNA_PLACE_XCD = 1 } nuna_placement_t;
 typedef enum {
     NUNA_ALGO_AUTO = 0,           /* library picks by size (one-shot family on one GPU) */
     NUNA_ALGO_ONE_SHOT = 1,       /* one kernel: read P inputs, write P outputs per element */
-    NUNA_ALGO_TWO_SHOT = 2,       /* reduce-scatter kernel, then all-gather kernel (stream ordered) */
-    NUNA_ALGO_ONE_SHOT_SPLIT = 3  /* one kernel, work item = (chunk, destination group): more
+    NUNA_ALGO_TWO_SHOT = 2,       /* reduce-scatter then all-gather, both phases per chunk in one
+                                     kernel: the workgroup that reduces chunk c of shard r stores
+                                     it to out[r], then to every other out[d].  Runs the two
+                                     kernels of NUNA_ALGO_TWO_SHOT_TWO_KERNELS when P is not 2,
+                                     4, 8 or 16 or a shard is not whole 16-byte vectors */
+    NUNA_ALGO_ONE_SHOT_SPLIT = 3, /* one kernel, work item = (chunk, destination group): more
                                      workgroups for small messages; inputs re-read per group */
+    NUNA_ALGO_TWO_SHOT_TWO_KERNELS = 4 /* reduce-scatter kernel, then all-gather kernel (stream
+                                     ordered): the phase boundary is the kernel boundary */
 } nuna_algo_t;
 
 #define NUNA_MAX_RANKS 64
 #define NUNA_NUM_XCD 8
 
-/* Probe the current device once (architecture and compute-unit count) and
- * cache the result.  Optional: collective calls work without it.  Returns
- * NUNA_ERR_UNSUPPORTED if the device is not gfx950, NUNA_ERR_HIP if there is
- * no device.  Idempotent and thread-safe. */
+/* Probe the current device and cache the result (Sec. 4.2.3 hands the
+ * topology to the placement step; this is where the library learns it).
+ * Checks that the device is gfx950, then launches 2048 one-wave workgroups
+ * that each record the XCC they ran on, and verifies the dispatch map XCD
+ * placement relies on: 256 compute units and workgroup b on XCD b mod 8 for
+ * every b (nuna_check_dispatch_map).  Allocates 8 KiB of device memory for
+ * the probe and frees it; synchronous, not capturable.  Idempotent and
+ * thread-safe; call it once on every device before XCD-mode collectives
+ * (LINEAR-mode calls work without it).  Returns NUNA_ERR_HIP without a
+ * device, NUNA_ERR_UNSUPPORTED if the device is not gfx950 or the map does
+ * not hold (XCD placement then stays unavailable on that device). */
 nuna_status_t nuna_init(void);
+
+/* What nuna_init found on the current device. */
+typedef struct {
+    int32_t device;       /* HIP device ordinal */
+    int32_t cu_count;     /* compute units */
+    int32_t xcd_count;    /* distinct XCC ids seen by the probe (1 + largest) */
+    int32_t map_verified; /* 1: workgroup b runs on XCD b mod 8; XCD placement available */
+} nuna_device_info_t;
+
+/* Fill *info for the current device.  NUNA_ERR_INVALID_ARG if nuna_init has
+ * not run on it (or info is NULL). */
+nuna_status_t nuna_get_device_info(nuna_device_info_t* info);
+
+/* Host-only check behind nuna_init (no HIP call): xcc[b] is the XCC
+ * workgroup b of a G-workgroup launch ran on (HOST int32 array, G >= 64).
+ * NUNA_OK if cu_count is 256 and xcc[b] == b mod 8 for every b, else
+ * NUNA_ERR_UNSUPPORTED naming the first mismatch (NUNA_ERR_INVALID_ARG for a
+ * NULL array or G < 64). */
+nuna_status_t nuna_check_dispatch_map(const int32_t* xcc, int64_t G, int32_t cu_count);
 
 /* Text of the last error raised on the calling thread ("" if none).  The
  * string is owned by the library and valid until the thread's next call. */
@@ -147,6 +196,11 @@ nuna_status_t nuna_set_max_workgroups(int max_workgroups);
  *                         1 (always streaming), 2 (always write-through)
  *   NUNA_TILE_V           rank-major tile all-reduce width: 0 (16 up to 256 KiB per
  *                         rank, else off), 16, 32, 64
+ *   NUNA_PAGE_GROUPS      XCD mode, one-work-item-per-workgroup launches with chunks
+ *                         smaller than 4 KiB: 1 (default) keeps the chunks of one page
+ *                         on one XCD, 0 runs the linear map
+ *   NUNA_DIRECT_MAX_GRID  largest grid of the one-work-item-per-workgroup kernels,
+ *                         0 (8192)..2^24; larger launches loop (persistent kernels)
  * Unknown names and values outside these sets: NUNA_ERR_INVALID_ARG. */
 nuna_status_t nuna_set_tunable(const char* name, int64_t value);
 nuna_status_t nuna_get_tunable(const char* name, int64_t* value);
@@ -158,8 +212,10 @@ nuna_status_t nuna_get_tunable(const char* name, int64_t* value);
  *           r = 0..P-1 is the summation order.
  *   out[d]  P device pointers, each `count` elements; every out[d] receives
  *           the same result.
- *   algo    ONE_SHOT, ONE_SHOT_SPLIT, TWO_SHOT or AUTO.  TWO_SHOT needs
- *           count % P == 0; otherwise it runs one-shot (same bits).
+ *   algo    ONE_SHOT, ONE_SHOT_SPLIT, TWO_SHOT, TWO_SHOT_TWO_KERNELS or
+ *           AUTO.  The two-shot forms need count % P == 0 (rank r owns the
+ *           shard [r*count/P, (r+1)*count/P)); otherwise they run one-shot
+ *           (same bits).
  *           ONE_SHOT_SPLIT with in-place buffers runs ONE_SHOT (a split
  *           work item would overwrite an input another group still reads).
  * In-place: out[r] == in[r] is allowed.  Any other overlap between an input
@@ -361,6 +417,23 @@ nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G,
                                    int64_t group_size, int64_t* items, int64_t capacity, int64_t* count);
 nuna_status_t nuna_placement_grid(nuna_placement_t place, int64_t groups, int64_t group_size,
                                   int64_t* workgroups);
+
+/*
+ * Host mirror of the map of the one-work-item-per-workgroup launches (the
+ * direct kernels; no HIP call): `items` work items of `chunk_bytes` each
+ * (a power of two, at least 16), item i covering bytes [i*chunk_bytes,
+ * (i+1)*chunk_bytes) of every rank buffer.  LINEAR: workgroup b runs item b.
+ * XCD with chunks below 4 KiB (and NUNA_PAGE_GROUPS on): the gp = 4096 /
+ * chunk_bytes items of one page form a group; group g runs on XCD g mod 8,
+ * its members on consecutive workgroups of that XCD (b, b+8, ...); the grid
+ * is padded to whole rounds of 8 groups.  *workgroups receives the grid;
+ * item_of[b] (HOST int64 array of `capacity`) the item workgroup b runs, or
+ * -1 for a padding workgroup (NUNA_ERR_INVALID_ARG if capacity is too
+ * small; *workgroups is still set).  The launch-time cap and direct-grid
+ * limit, under which a launch falls back to other maps, are not applied.
+ */
+nuna_status_t nuna_placement_direct(nuna_placement_t place, int64_t items, int64_t chunk_bytes, int64_t* item_of,
+                                    int64_t capacity, int64_t* workgroups);
 
 /*
  * Dispatch probe (verifies the workgroup -> XCD assumption behind

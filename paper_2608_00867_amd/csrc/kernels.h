@@ -28,6 +28,8 @@ struct Tuning {
     int tile_v = 0;                    // rank-major tile all-reduce width (16/32/64; 0 = by size)
     int combine_lists = 0;             // 1: combine reads the offset lists even where records exist
     int write_through = 0;             // 8-rank one-shot stores: 0 by size, 1 streaming, 2 write-through
+    int page_groups = 1;               // XCD mode: the chunks of a 4 KiB page on one XCD (direct kernels)
+    int direct_max_grid = 0;           // largest grid of the direct kernels (0: 8192)
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
@@ -41,6 +43,13 @@ int64_t grid_limit(int64_t dflt);
 // item is (chunk, destination group) and writes P/dest_groups outputs.
 hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size_t count, int dtype,
                             int dest_groups, int mode, hipStream_t stream);
+
+// Fused two-shot all-reduce (reduce-scatter and all-gather phases per chunk in
+// one kernel).  Needs P in {2, 4, 8, 16} and shards of whole 16-byte vectors
+// (two_shot_fused_ok); otherwise the caller runs the two kernels.
+bool two_shot_fused_ok(int P, size_t count, int dtype);
+hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype,
+                                 hipStream_t stream);
 
 // Reduce-scatter: in[q] holds P*m elements; out[r][j] = sum_q in[q][r*m+j].
 // keep_output: store the shards through the caches (they are read right

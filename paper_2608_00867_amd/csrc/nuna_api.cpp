@@ -183,6 +183,8 @@ const TunableDef kTunables[] = {
     {"NUNA_TILE_V", nullptr, &nuna::Tuning::tile_v, 0, 0, 4, {0, 16, 32, 64}},
     {"NUNA_COMBINE_LISTS", nullptr, &nuna::Tuning::combine_lists, 0, 1, 0, {}},
     {"NUNA_WRITE_THROUGH", nullptr, &nuna::Tuning::write_through, 0, 2, 0, {}},
+    {"NUNA_PAGE_GROUPS", nullptr, &nuna::Tuning::page_groups, 0, 1, 0, {}},
+    {"NUNA_DIRECT_MAX_GRID", nullptr, &nuna::Tuning::direct_max_grid, 0, 1 << 24, 0, {}},
 };
 
 const TunableDef* find_tunable(const char* name) {
@@ -223,13 +225,51 @@ int64_t grid_limit(int64_t dflt) {
 }
 }  // namespace nuna
 
+// ============================================================== device probe
+
+namespace {
+
+// Per-device result of nuna_init's dispatch-map probe.
+constexpr int kMaxDevices = 64;
+enum MapState { kMapUnknown = 0, kMapVerified = 1, kMapFailed = 2 };
+std::atomic<int> g_map_state[kMaxDevices];
+std::atomic<int> g_cu_count[kMaxDevices];
+std::atomic<int> g_xcd_count[kMaxDevices];
+
+// Workgroups the init probe launches: a few per compute unit, in many rounds of 8.
+constexpr int kProbeGrid = 2048;
+
+// XCD placement relies on the hardware running workgroup b on XCD b mod 8
+// (placement.h).  Before the first XCD-mode call on a device, nuna_init must
+// have verified that map there; a device where it does not hold (another
+// partition mode, another chip) gets NUNA_ERR_UNSUPPORTED for XCD mode rather
+// than a placement the kernels do not intend.  LINEAR needs no map.
+nuna_status_t check_placement_ready(int place) {
+    if (place != NUNA_PLACE_XCD) return NUNA_OK;
+    int dev = 0;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+    const int st = (dev >= 0 && dev < kMaxDevices) ? g_map_state[dev].load(std::memory_order_acquire) : kMapUnknown;
+    if (st == kMapVerified) return NUNA_OK;
+    if (st == kMapFailed)
+        return fail(NUNA_ERR_UNSUPPORTED,
+                    "XCD placement is unavailable on device %d: nuna_init found that workgroup b does not run on "
+                    "XCD b mod %d there",
+                    dev, NUNA_NUM_XCD);
+    return fail(NUNA_ERR_UNSUPPORTED,
+                "XCD placement needs nuna_init() on device %d first (it verifies the workgroup -> XCD dispatch map)",
+                dev);
+}
+
+}  // namespace
+
 // ============================================================== C ABI
 
 extern "C" {
 
 const char* nuna_last_error_string(void) { return t_err.c_str(); }
 
-int nuna_version(void) { return 100; }
+int nuna_version(void) { return 200; }
 
 nuna_status_t nuna_set_max_workgroups(int max_workgroups) {
     if (max_workgroups < 0) return fail(NUNA_ERR_INVALID_ARG, "max_workgroups=%d < 0", max_workgroups);
@@ -255,24 +295,75 @@ nuna_status_t nuna_get_tunable(const char* name, int64_t* value) {
     return ok();
 }
 
-nuna_status_t nuna_init(void) {
+nuna_status_t nuna_check_dispatch_map(const int32_t* xcc, int64_t G, int32_t cu_count) {
+    if (!xcc) return fail(NUNA_ERR_INVALID_ARG, "xcc is NULL");
+    if (G < 8 * NUNA_NUM_XCD) return fail(NUNA_ERR_INVALID_ARG, "G=%lld: need at least %d workgroups", (long long)G,
+                                          8 * NUNA_NUM_XCD);
+    if (cu_count != NUNA_NUM_XCD * 32)
+        return fail(NUNA_ERR_UNSUPPORTED, "%d compute units, expected %d (%d XCDs of 32)", cu_count,
+                    NUNA_NUM_XCD * 32, NUNA_NUM_XCD);
+    for (int64_t b = 0; b < G; ++b)
+        if (xcc[b] != static_cast<int32_t>(b % NUNA_NUM_XCD))
+            return fail(NUNA_ERR_UNSUPPORTED, "workgroup %lld ran on XCD %d, not %lld (b mod %d)", (long long)b, xcc[b],
+                        (long long)(b % NUNA_NUM_XCD), NUNA_NUM_XCD);
+    return ok();
+}
+
+nuna_status_t nuna_init(void) try {
     static std::mutex mu;
-    static int state = 0;  // 0 unknown, 1 ok
     std::lock_guard<std::mutex> lock(mu);
-    if (state == 1) return ok();
     int n = 0;
     hipError_t e = hipGetDeviceCount(&n);
     if (e != hipSuccess || n < 1) return fail(NUNA_ERR_HIP, "no HIP device (%s)", hipGetErrorString(e));
     int dev = 0;
     e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(NUNA_ERR_UNSUPPORTED, "device ordinal %d >= %d", dev, kMaxDevices);
+    if (g_map_state[dev].load(std::memory_order_acquire) == kMapVerified) return ok();
     hipDeviceProp_t prop;
     e = hipGetDeviceProperties(&prop, dev);
     if (e != hipSuccess) return hip_status(e, "hipGetDeviceProperties");
     if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
         return fail(NUNA_ERR_UNSUPPORTED, "device %d is %s, libnuna is built for gfx950", dev, prop.gcnArchName);
     (void)nuna::tuning();
-    state = 1;
+    // Dispatch-map probe: every workgroup records the XCC it ran on.
+    int32_t* d_xcc = nullptr;
+    if ((e = hipMalloc(&d_xcc, sizeof(int32_t) * kProbeGrid)) != hipSuccess) return hip_status(e, "hipMalloc (probe)");
+    std::vector<int32_t> xcc(kProbeGrid, -1);
+    e = nuna::launch_probe_xcc(kProbeGrid, d_xcc, nullptr, nullptr);
+    if (e == hipSuccess) e = hipMemcpy(xcc.data(), d_xcc, sizeof(int32_t) * kProbeGrid, hipMemcpyDeviceToHost);
+    (void)hipFree(d_xcc);
+    if (e != hipSuccess) return hip_status(e, "dispatch-map probe");
+    int xcds = 0;
+    for (int32_t x : xcc) xcds = std::max(xcds, x + 1);
+    g_cu_count[dev].store(prop.multiProcessorCount, std::memory_order_relaxed);
+    g_xcd_count[dev].store(xcds, std::memory_order_relaxed);
+    const nuna_status_t st = nuna_check_dispatch_map(xcc.data(), kProbeGrid, prop.multiProcessorCount);
+    g_map_state[dev].store(st == NUNA_OK ? kMapVerified : kMapFailed, std::memory_order_release);
+    if (st != NUNA_OK) {
+        // LINEAR placement still works; XCD placement on this device reports why it is unavailable.
+        const std::string why = t_err;
+        return fail(NUNA_ERR_UNSUPPORTED, "device %d: dispatch map check failed (%s); XCD placement is unavailable",
+                    dev, why.c_str());
+    }
+    return ok();
+} catch (...) {
+    return host_exception();
+}
+
+nuna_status_t nuna_get_device_info(nuna_device_info_t* info) {
+    if (!info) return fail(NUNA_ERR_INVALID_ARG, "info is NULL");
+    std::memset(info, 0, sizeof *info);
+    int dev = 0;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_status(e, "hipGetDevice");
+    info->device = dev;
+    if (dev < 0 || dev >= kMaxDevices) return fail(NUNA_ERR_INVALID_ARG, "device ordinal %d >= %d", dev, kMaxDevices);
+    const int st = g_map_state[dev].load(std::memory_order_acquire);
+    if (st == kMapUnknown) return fail(NUNA_ERR_INVALID_ARG, "nuna_init() has not run on device %d", dev);
+    info->cu_count = g_cu_count[dev].load(std::memory_order_relaxed);
+    info->xcd_count = g_xcd_count[dev].load(std::memory_order_relaxed);
+    info->map_verified = st == kMapVerified ? 1 : 0;
     return ok();
 }
 
@@ -280,7 +371,7 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
                              nuna_algo_t algo, nuna_placement_t place, hipStream_t stream) try {
     nuna_status_t st = check_common(P, dtype, place);
     if (st) return st;
-    if (algo < NUNA_ALGO_AUTO || algo > NUNA_ALGO_ONE_SHOT_SPLIT)
+    if (algo < NUNA_ALGO_AUTO || algo > NUNA_ALGO_TWO_SHOT_TWO_KERNELS)
         return fail(NUNA_ERR_INVALID_ARG, "invalid algorithm %d", static_cast<int>(algo));
     if ((st = check_ptr_array(in, P, "in"))) return st;
     if ((st = check_ptr_array(const_cast<const void* const*>(out), P, "out"))) return st;
@@ -298,13 +389,22 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
     st = check_overlaps(is, os, [](const Span& i, const Span& o) { return i.rank == o.rank && i.lo == o.lo; });
     if (st) return st;
 
+    if ((st = check_placement_ready(place))) return st;
+
     int a = algo;
     if (a == NUNA_ALGO_AUTO) a = NUNA_ALGO_ONE_SHOT;
-    if (a == NUNA_ALGO_TWO_SHOT && count % static_cast<size_t>(P) != 0) a = NUNA_ALGO_ONE_SHOT;
+    if ((a == NUNA_ALGO_TWO_SHOT || a == NUNA_ALGO_TWO_SHOT_TWO_KERNELS) && count % static_cast<size_t>(P) != 0)
+        a = NUNA_ALGO_ONE_SHOT;
     if (a == NUNA_ALGO_ONE_SHOT_SPLIT && in_place) a = NUNA_ALGO_ONE_SHOT;
+    if (a == NUNA_ALGO_TWO_SHOT) {
+        // Both phases in one kernel where the shapes allow it, else two kernels.
+        if (nuna::two_shot_fused_ok(P, count, dtype))
+            return hip_status(nuna::launch_two_shot_fused(in, out, P, count, dtype, stream), "two-shot launch");
+        a = NUNA_ALGO_TWO_SHOT_TWO_KERNELS;
+    }
 
     hipError_t e;
-    if (a == NUNA_ALGO_TWO_SHOT) {
+    if (a == NUNA_ALGO_TWO_SHOT_TWO_KERNELS) {
         const size_t m = count / P;
         const void* shard_in[NUNA_MAX_RANKS];
         void* shard_out[NUNA_MAX_RANKS];
@@ -351,6 +451,7 @@ nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P
         return i.rank == o.rank && o.lo == i.lo + static_cast<uintptr_t>(o.rank) * mb;
     });
     if (st) return st;
+    if ((st = check_placement_ready(place))) return st;
     return hip_status(nuna::launch_reduce_scatter(in, out, P, recvcount, dtype, place, false, stream),
                       "reduce-scatter launch");
 } catch (...) {
@@ -377,6 +478,7 @@ nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, si
         return i.rank == o.rank && i.lo == o.lo + static_cast<uintptr_t>(i.rank) * mb;
     });
     if (st) return st;
+    if ((st = check_placement_ready(place))) return st;
     return hip_status(nuna::launch_all_gather(in, out, P, sendcount, dtype, place, false, stream), "all-gather launch");
 } catch (...) {
     return host_exception();
@@ -626,6 +728,7 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
     if (st) return st;
     if (L->nitems == 0) return ok();
     if (L->device < 0) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
+    if ((st = check_placement_ready(place))) return st;
     const void* desc = place == NUNA_PLACE_XCD ? L->dev_group : L->dev_linear;
     hipError_t e = nuna::launch_all_to_all(send, recv, P, desc, L->nitems, L->xcd_start, row_bytes,
                                            static_cast<int>(es), place, stream);
@@ -665,6 +768,7 @@ nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, co
     if (st) return st;
     if (L->nitems == 0) return ok();
     if (L->device < 0) return fail(NUNA_ERR_INVALID_ARG, "layout has not been uploaded (nuna_a2a_layout_upload)");
+    if ((st = check_placement_ready(place))) return st;
     hipError_t e = nuna::launch_combine(y, out, P, L->T, L->dev_comb_off, L->dev_comb_ent, L->dev_comb_rec, weights,
                                         row_bytes, static_cast<int>(dtype), place, stream);
     return hip_status(e, "all-to-all combine launch");
@@ -758,6 +862,29 @@ nuna_status_t nuna_placement_items(nuna_placement_t place, int64_t b, int64_t G,
     *count = n;
     if (n > capacity) return fail(NUNA_ERR_INVALID_ARG, "capacity %lld < %lld items", static_cast<long long>(capacity),
                                   static_cast<long long>(n));
+    return ok();
+} catch (...) {
+    return host_exception();
+}
+
+nuna_status_t nuna_placement_direct(nuna_placement_t place, int64_t items, int64_t chunk_bytes, int64_t* item_of,
+                                    int64_t capacity, int64_t* workgroups) try {
+    if (!valid_place(place)) return fail(NUNA_ERR_INVALID_ARG, "invalid placement mode %d", static_cast<int>(place));
+    if (!workgroups || (capacity > 0 && !item_of) || capacity < 0) return fail(NUNA_ERR_INVALID_ARG, "bad output buffer");
+    if (items < 1 || items > (int64_t(1) << 40) || chunk_bytes < 16 || chunk_bytes % 16 != 0 ||
+        (chunk_bytes & (chunk_bytes - 1)) != 0)
+        return fail(NUNA_ERR_INVALID_ARG, "invalid geometry items=%lld chunk_bytes=%lld", (long long)items,
+                    (long long)chunk_bytes);
+    int gs = 0;
+    if (place == NUNA_PLACE_XCD && nuna::tuning().page_groups != 0) gs = nuna::page_shift(chunk_bytes);
+    const int64_t G = nuna::page_grid(items, gs);
+    *workgroups = G;
+    if (G > capacity) return fail(NUNA_ERR_INVALID_ARG, "capacity %lld < %lld workgroups", (long long)capacity,
+                                  (long long)G);
+    for (int64_t b = 0; b < G; ++b) {
+        const int64_t w = nuna::page_item(b, gs);
+        item_of[b] = w < items ? w : -1;
+    }
     return ok();
 } catch (...) {
     return host_exception();

@@ -1,14 +1,47 @@
-// nuna_probe.hip -- diagnostic kernels: memory load-latency probe.
+// nuna_probe.hip -- diagnostic kernels: the workgroup -> XCD dispatch probe,
+// the memory load-latency probe and the reference streaming copy.
 //
 // Kept apart from the collective kernels: it measures the machine, it does
 // not move collective data.
-#include <hip/hip_runtime.h>
-
-#include "kernels.h"
-#include "placement.h"
+#include "device_common.h"
 
 namespace nuna {
 namespace {
+
+// ---------------------------------------------------------------- probe and copy
+
+__global__ __launch_bounds__(64) void k_probe_xcc(int32_t* xcc, int32_t* hw_id) {
+    if (threadIdx.x == 0) {
+        uint32_t x, h;
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+        asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(h));
+        xcc[blockIdx.x] = static_cast<int32_t>(x & 0xfu);
+        if (hw_id) hw_id[blockIdx.x] = static_cast<int32_t>(h);
+    }
+}
+
+// Reference copy.  It streams past the caches the way the collectives do
+// (non-temporal 16-byte loads and stores), so its traffic-counter readings
+// calibrate theirs and its speed is the ceiling a plain read+write reaches.
+__global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uint4* __restrict__ src, int64_t nvec,
+                                              unsigned char* __restrict__ dst_tail,
+                                              const unsigned char* __restrict__ src_tail, int tail) {
+    constexpr int U = 4;
+    // One use of every argument: their loads issue together (as in the collectives).
+    asm volatile("" ::"s"(dst), "s"(src), "s"(nvec), "s"(dst_tail), "s"(src_tail), "s"(tail));
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kWG * U;
+    for (int64_t v = blockIdx.x * static_cast<int64_t>(kWG) * U + threadIdx.x; v < nvec; v += stride) {
+        uint4 y[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (v + u * kWG < nvec) y[u] = load16<true>(src + v + u * kWG);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (v + u * kWG < nvec) store_stream(dst + v + u * kWG, y[u]);
+    }
+    if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < tail) dst_tail[threadIdx.x] = src_tail[threadIdx.x];
+}
+
 
 // Load-latency probe.  One lane of the workgroup that runs on XCD `xcd`
 // walks the blocks of a buffer in order; for each it first loads another
@@ -54,6 +87,24 @@ hipError_t launch_probe_latency(const void* buf, int64_t nblocks, int64_t stride
                                 int xcd, uint32_t* cycles, hipStream_t stream) {
     hipLaunchKernelGGL(k_probe_latency, dim3(kNumXcd), dim3(64), 0, stream, static_cast<const unsigned char*>(buf),
                        nblocks, stride, line_off, warm_off, xcd, cycles);
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream) {
+    hipLaunchKernelGGL(k_probe_xcc, dim3(static_cast<unsigned>(G)), dim3(64), 0, stream, xcc, hw_id);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+    const int64_t nvec = static_cast<int64_t>(bytes / 16);
+    const int tail = static_cast<int>(bytes % 16);
+    const int64_t per_wg = static_cast<int64_t>(kWG) * 4;
+    int64_t G = (nvec + per_wg - 1) / per_wg;
+    if (G > 4096) G = 4096;
+    if (G < 1) G = 1;
+    hipLaunchKernelGGL(k_copy, dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, static_cast<uint4*>(dst),
+                       static_cast<const uint4*>(src), nvec, static_cast<unsigned char*>(dst) + nvec * 16,
+                       static_cast<const unsigned char*>(src) + nvec * 16, tail);
     return hipGetLastError();
 }
 

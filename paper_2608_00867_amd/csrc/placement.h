@@ -142,6 +142,46 @@ inline Place make_place_uniform(int mode, int64_t groups, int64_t gsize) {
     return pl;
 }
 
+// ---------------------------------------------------------------- page groups
+//
+// Launches that run one work item per workgroup (the direct kernels) number
+// their items by address: item i covers bytes [i*cb, (i+1)*cb) of every rank
+// buffer, cb the chunk bytes.  When a chunk is smaller than a 4 KiB page
+// (Sec. 4.2 places memory in 4 kB pages), the gp = 4096 / cb items of one
+// page touch the same page of every buffer: in XCD mode they form one logical
+// group (Sec. 4.2.1), and groups are dealt round-robin to the XCDs with their
+// members on consecutive slots of one XCD (as in Algorithm 1), so no page's
+// work is split between XCDs.  LINEAR runs item b on workgroup b, which puts
+// the gp items of a page on gp different XCDs.
+//
+// gshift = log2(gp) (0: the linear map).  Workgroup b = 8k + x runs item
+// (8 * (k >> gshift) + x) << gshift | (k mod gp); the grid is padded to whole
+// rounds of 8 groups, and workgroups past the last item exit.
+NUNA_HD inline int64_t page_item(int64_t b, int gshift) {
+    if (gshift == 0) return b;
+    const int64_t x = b & (kNumXcd - 1);
+    const int64_t k = b >> 3;
+    const int64_t q = k >> gshift;
+    const int64_t m = k & ((int64_t(1) << gshift) - 1);
+    return ((q << 3) + x) << gshift | m;
+}
+
+// Host: workgroups of a page-grouped launch over `items` work items.
+inline int64_t page_grid(int64_t items, int gshift) {
+    if (gshift == 0) return items;
+    const int64_t gp = int64_t(1) << gshift;
+    const int64_t groups = (items + gp - 1) / gp;
+    return kNumXcd * ((groups + kNumXcd - 1) / kNumXcd) * gp;
+}
+
+// Host: log2 of the items per page for chunks of `chunk_bytes` (a power of
+// two times 16), 0 when a chunk covers a whole page or more.
+inline int page_shift(int64_t chunk_bytes) {
+    int s = 0;
+    while ((chunk_bytes << (s + 1)) <= 4096) ++s;
+    return s;
+}
+
 // Host: workgroups a launch of this placement needs so that every item gets
 // its own workgroup (before any cap).  XCD mode sizes every XCD for the
 // largest per-XCD group list; workgroups past a list's end exit at once.

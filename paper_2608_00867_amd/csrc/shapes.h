@@ -1,0 +1,191 @@
+// shapes.h -- host-side launch-shape rules of the collective kernels
+// (workgroup size, vectors per thread, grid limits, when XCD placement keeps
+// logical groups together).  They choose how the work is cut, never what is
+// computed.  Included by the kernel sources; everything sits in an unnamed
+// namespace so each source keeps its own copy.
+#pragma once
+
+#include <stdint.h>
+
+#include "device_common.h"
+
+namespace nuna {
+namespace {
+
+inline bool direct_ranks(int P, int vpt) { return P == 2 || P == 4 || P == 8 || (P == 16 && vpt != 8); }
+
+// Largest grid that takes the direct kernels (NUNA_DIRECT_MAX_GRID, default
+// 8192).  Beyond it the general kernels run: at 64 MiB per rank with one
+// vector per thread (16384 workgroups) the general all-reduce measured 12 %
+// faster than the direct one on MI355X (184 against 209 us), while up to 8192
+// workgroups the direct kernels were as fast or faster at every size measured
+// (1-64 MiB per rank, 1-4 vectors per thread).
+inline int64_t direct_max_grid() { return tuning().direct_max_grid > 0 ? tuning().direct_max_grid : 8192; }
+constexpr int64_t kAgDirectMaxGrid8 = int64_t(1) << 20;  // 8-rank all-gather (launch_all_gather)
+
+// Launch of a direct kernel over `items` work items, one per workgroup.
+struct DirectMap {
+    bool direct;    // the direct kernel runs (uncapped and within the direct-grid limit)
+    int32_t gshift; // log2 of the items per 4 KiB page grouped on one XCD (0: linear map)
+    int64_t items;
+    int64_t grid;   // workgroups (padded to whole rounds of 8 page groups when gshift > 0)
+};
+
+// XCD mode groups the chunks of each 4 KiB page on one XCD (placement.h)
+// when a chunk is smaller than a page, unless NUNA_PAGE_GROUPS is 0.  A grid
+// the page groups would push past the workgroup cap or the direct limit runs
+// the linear map instead.
+inline DirectMap direct_map(int mode, int64_t items, int64_t chunk_bytes) {
+    DirectMap m{};
+    m.items = items;
+    m.gshift = 0;
+    m.grid = items;
+    const bool uncapped = cap_grid(items) == items;
+    if (mode == kPlaceXcd && tuning().page_groups != 0) {
+        const int gs = page_shift(chunk_bytes);
+        const int64_t g = page_grid(items, gs);
+        if (gs > 0 && cap_grid(g) == g && g <= direct_max_grid()) {
+            m.gshift = gs;
+            m.grid = g;
+        }
+    }
+    m.direct = uncapped && m.grid <= direct_max_grid();
+    return m;
+}
+
+// Vectors per thread per work item for the all-reduce and reduce-scatter with
+// up to 16 ranks, by message size (measured on MI355X with bf16, cold): 4 at
+// 4 MiB per rank, 2 at 16 MiB, 1 at 64 MiB and above and for every smaller
+// (latency-bound) message, where more workgroups win.
+inline int pick_vpt(int64_t vectors_per_rank, int P) {
+    if (P > 16) return 1;
+    const int forced = tuning().vpt;
+    if (forced == 1 || forced == 2 || forced == 4) return forced;
+    if (forced == 8) return 4;  // 8 is an all-reduce-only shape
+    if (vectors_per_rank >= (int64_t(1) << 22)) return 1;
+    if (vectors_per_rank >= (int64_t(1) << 20)) return 2;
+    if (vectors_per_rank >= (int64_t(1) << 18)) return 4;
+    return 1;
+}
+
+// XCD placement keeps a logical group on one XCD so that its members'
+// re-reads of the shared chunk hit that XCD's L2.  That pays only when the
+// re-reads are a sizeable part of the group's traffic, and, for the split
+// all-reduce (whose members all load the same P chunks at once), only once
+// the message is large enough to be bandwidth-bound.  Otherwise the grouped
+// map measured up to 3.5 % slower than the linear one on MI355X (split
+// all-reduce at 8-16 KiB per rank with 8 ranks; all-gather with 64 ranks and
+// 8 destinations per member), so the launch keeps the linear map there.
+//   reread_num / reread_den: share of the group's loads and stores that are
+//   re-reads; total_bytes: bytes the launch moves; min_total: the size below
+//   which the grouped map is not used.
+inline int group_mode(int mode, int64_t reread_num, int64_t reread_den, int64_t total_bytes, int64_t min_total) {
+    if (mode != kPlaceXcd) return mode;
+    if (reread_num * 4 < reread_den) return kPlaceLinear;
+    if (total_bytes <= min_total) return kPlaceLinear;
+    return mode;
+}
+
+inline int largest_divisor_upto(int P, int cap) {
+    for (int d = cap < P ? cap : P; d > 1; --d)
+        if (P % d == 0) return d;
+    return 1;
+}
+
+// Workgroup size: one-wavefront workgroups spread small messages, and the
+// long per-thread rank loops of many-rank reductions, over more compute
+// units; 256-thread workgroups stream large few-rank messages, except at
+// 4 MiB per rank where 128 threads with 4 vectors each measured best.
+inline int pick_threads(int64_t vectors_per_rank, int P) {
+    const int forced = tuning().wg_threads;
+    if (forced == 64 || forced == 128 || forced == 256) return forced;
+    if (P > 16) return 64;
+    if (vectors_per_rank < (int64_t(1) << 14)) return 64;
+    if (vectors_per_rank >= (int64_t(1) << 18) && vectors_per_rank < (int64_t(1) << 20)) return 128;
+    return kWG;
+}
+
+// Reduce-scatter launch shape by the vectors each input rank holds (P
+// shards), for up to 16 ranks (measured on MI355X with bf16, 8 ranks, cold):
+// 4 vectors per thread from 8 MiB per input rank, where it was 7-9 % faster
+// than the all-reduce's shapes; 128 threads with 2 at 4 MiB; the
+// all-reduce's rule below that.  Forced tunables win.
+inline void pick_rs_shape(int64_t in_vectors, int P, int dtype, int& nt, int& vpt) {
+    nt = pick_threads(in_vectors, P);
+    vpt = dtype == kDtBf16 ? pick_vpt(in_vectors, P) : 1;
+    if (P > 16 || dtype != kDtBf16 || tuning().wg_threads || tuning().vpt) return;
+    if (in_vectors >= (int64_t(1) << 19)) {
+        nt = 256;
+        vpt = 4;
+    } else if (in_vectors >= (int64_t(1) << 18)) {
+        nt = 128;
+        vpt = 2;
+    }
+}
+
+// All-gather launch shape by the vectors each output rank receives, for up
+// to 16 ranks (measured on MI355X with bf16, 8 ranks, cold): one-wave
+// workgroups with 1 vector per thread below 2 MiB per output, 64 threads with
+// 4 vectors below 16 MiB, 5-20 % faster than the all-reduce's shapes.  From
+// 16 MiB per output, 8 ranks have a rule of their own (below); other rank
+// counts take 128 threads with 4 vectors below 64 MiB and 128 with 1 beyond.
+// Forced tunables win.
+inline void pick_ag_shape(int64_t out_vectors, int P, int& nt, int& vpt) {
+    nt = pick_threads(out_vectors, P);
+    vpt = pick_vpt(out_vectors, P);
+    if (P > 16 || tuning().wg_threads || tuning().vpt) return;
+    if (out_vectors < (int64_t(1) << 17)) {
+        nt = 64;
+        vpt = 1;
+    } else if (out_vectors < (int64_t(1) << 20)) {
+        nt = 64;
+        vpt = 4;
+    } else if (P == 8) {
+        // 8 ranks from 2 MiB shards: 256 x 1, with the direct kernel at any
+        // grid (launch_all_gather).  Measured on MI355X with back-to-back cold
+        // calls: 3-11 % faster than 128 x 4 at 2-4 MiB shards (37.9 against
+        // 42.8 us at 3 MiB), best or within 1 % of the best shape at 4-32 MiB.
+        nt = 256;
+        vpt = 1;
+    } else if (out_vectors < (int64_t(1) << 22)) {
+        nt = 128;
+        vpt = 4;
+    } else {
+        nt = 128;
+        vpt = 1;
+    }
+}
+
+// One-shot all-reduce launch shape.  Starts from the shared rule above; with
+// 2, 4 or 8 ranks a forced 8 vectors per thread is kept (other rank counts
+// have no such kernel and get 4).
+//
+// 8 ranks, 8-32 MiB per rank: 8 vectors per thread in 256-thread workgroups.
+// That kernel holds 256 VGPRs, so one workgroup per CU runs at a time and
+// the launch proceeds in rounds of 256 workgroups, each moving 32 KiB
+// contiguous per rank buffer.  Measured on MI355X (bf16, cold) it was 5-8 %
+// faster than the shared rule at 8 and 16 MiB per rank, when its chunks fill
+// whole rounds; with a partly empty last round it lost, so it is taken only
+// when the last round is at least 90 % full.
+inline void pick_ar_shape(int64_t vectors_per_rank, int P, int& nt, int& vpt) {
+    nt = pick_threads(vectors_per_rank, P);
+    vpt = pick_vpt(vectors_per_rank, P);
+    const bool eight_ok = P == 2 || P == 4 || P == 8;
+    if (tuning().vpt == 8 && eight_ok) {
+        vpt = 8;
+        return;
+    }
+    if (P != 8 || tuning().wg_threads || tuning().vpt) return;
+    if (vectors_per_rank < (int64_t(1) << 19) || vectors_per_rank > (int64_t(1) << 21)) return;
+    constexpr int64_t kChunk = 256 * 8, kRound = 256;
+    const int64_t G = (vectors_per_rank + kChunk - 1) / kChunk;
+    const int64_t rounds = (G + kRound - 1) / kRound;
+    if (G * 10 >= rounds * kRound * 9) {
+        nt = 256;
+        vpt = 8;
+    }
+}
+
+
+}  // namespace
+}  // namespace nuna

@@ -23,12 +23,13 @@ STATUS_NAMES = {0: "NUNA_OK", 1: "NUNA_ERR_INVALID_ARG", 2: "NUNA_ERR_UNSUPPORTE
                 4: "NUNA_ERR_OVERLAP", 5: "NUNA_ERR_HIP", 6: "NUNA_ERR_NO_MEMORY"}
 F32, BF16 = 0, 1
 LINEAR, XCD = 0, 1
-ALGO_AUTO, ALGO_ONE_SHOT, ALGO_TWO_SHOT, ALGO_ONE_SHOT_SPLIT = 0, 1, 2, 3
+ALGO_AUTO, ALGO_ONE_SHOT, ALGO_TWO_SHOT, ALGO_ONE_SHOT_SPLIT, ALGO_TWO_SHOT_TWO_KERNELS = 0, 1, 2, 3, 4
 
 PLACEMENTS = {"linear": LINEAR, "xcd": XCD, LINEAR: LINEAR, XCD: XCD}
 ALGOS = {"auto": ALGO_AUTO, "one_shot": ALGO_ONE_SHOT, "two_shot": ALGO_TWO_SHOT, "one_shot_split": ALGO_ONE_SHOT_SPLIT,
+         "two_shot_two_kernels": ALGO_TWO_SHOT_TWO_KERNELS,
          ALGO_AUTO: ALGO_AUTO, ALGO_ONE_SHOT: ALGO_ONE_SHOT, ALGO_TWO_SHOT: ALGO_TWO_SHOT,
-         ALGO_ONE_SHOT_SPLIT: ALGO_ONE_SHOT_SPLIT}
+         ALGO_ONE_SHOT_SPLIT: ALGO_ONE_SHOT_SPLIT, ALGO_TWO_SHOT_TWO_KERNELS: ALGO_TWO_SHOT_TWO_KERNELS}
 
 _vp = ctypes.c_void_p
 _vpp = ctypes.POINTER(ctypes.c_void_p)
@@ -37,6 +38,12 @@ _i32p = ctypes.POINTER(ctypes.c_int32)
 
 NAP_MAX_DOMAINS = 16
 NAP_MAX_STACKS = 16
+
+
+class DeviceInfo(ctypes.Structure):
+    """Mirror of nuna_device_info_t."""
+    _fields_ = [("device", ctypes.c_int32), ("cu_count", ctypes.c_int32), ("xcd_count", ctypes.c_int32),
+                ("map_verified", ctypes.c_int32)]
 
 
 class NapTopology(ctypes.Structure):
@@ -49,6 +56,8 @@ class NapTopology(ctypes.Structure):
 # Every function the header declares, with its ctypes signature.
 SIGNATURES = {
     "nuna_init": ([], ctypes.c_int),
+    "nuna_get_device_info": ([ctypes.POINTER(DeviceInfo)], ctypes.c_int),
+    "nuna_check_dispatch_map": ([_i32p, ctypes.c_int64, ctypes.c_int32], ctypes.c_int),
     "nuna_last_error_string": ([], ctypes.c_char_p),
     "nuna_version": ([], ctypes.c_int),
     "nuna_set_max_workgroups": ([ctypes.c_int], ctypes.c_int),
@@ -72,6 +81,8 @@ SIGNATURES = {
     "nuna_placement_items": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _i64p,
                               ctypes.c_int64, _i64p], ctypes.c_int),
     "nuna_placement_grid": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, _i64p], ctypes.c_int),
+    "nuna_placement_direct": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, _i64p, ctypes.c_int64, _i64p],
+                              ctypes.c_int),
     "nuna_probe_xcc": ([ctypes.c_int, _vp, _vp, _vp], ctypes.c_int),
     "nuna_copy": ([_vp, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
     "nuna_nap_topology_mi355x": ([ctypes.POINTER(NapTopology)], ctypes.c_int),
@@ -171,6 +182,17 @@ def placement_grid(place, groups, group_size):
     return g.value
 
 
+def placement_direct(place, items, chunk_bytes):
+    """Item each workgroup of a one-item-per-workgroup launch runs (-1: padding), host mirror."""
+    import numpy as np
+    g = ctypes.c_int64()
+    lib().nuna_placement_direct(PLACEMENTS[place], items, chunk_bytes, None, 0, ctypes.byref(g))
+    buf = np.zeros(max(g.value, 1), dtype=np.int64)
+    _check(lib().nuna_placement_direct(PLACEMENTS[place], items, chunk_bytes, buf.ctypes.data_as(_i64p), g.value,
+                                       ctypes.byref(g)))
+    return buf[:g.value]
+
+
 def nap_topology_mi355x(cu_budget=None, stack_budget=None):
     """The library's MI355X topology for the placement planner, budgets optionally replaced."""
     t = NapTopology()
@@ -237,7 +259,22 @@ class tunables:
 
 
 def init():
+    """Probe the current device (architecture, dispatch map); XCD placement needs it."""
     _check(lib().nuna_init())
+
+
+def device_info():
+    """What nuna_init found on the current device: dict of device, cu_count, xcd_count, map_verified."""
+    info = DeviceInfo()
+    _check(lib().nuna_get_device_info(ctypes.byref(info)))
+    return {k: int(getattr(info, k)) for k, _ in DeviceInfo._fields_}
+
+
+def check_dispatch_map_raw(xcc, cu_count):
+    """Status of the library's host-side dispatch-map check on an int32 array of per-workgroup XCC ids."""
+    import numpy as np
+    a = np.ascontiguousarray(xcc, dtype=np.int32)
+    return lib().nuna_check_dispatch_map(a.ctypes.data_as(_i32p) if a.size else None, int(a.size), int(cu_count))
 
 
 def set_max_workgroups(n):
@@ -277,14 +314,25 @@ def _check_ranks(ts, name):
     return d, n
 
 
+def _check_outs(ins, outs, n_out):
+    """One output per input rank, each of the input dtype and n_out elements: checked before any
+    pointer reaches the library, which sizes every output from the input dtype."""
+    if len(outs) != len(ins):
+        raise ValueError(f"need one output per rank: {len(outs)} outputs for {len(ins)} inputs")
+    for o in outs:
+        if o.dtype != ins[0].dtype:
+            raise ValueError(f"output dtype {o.dtype} differs from input dtype {ins[0].dtype}")
+        if o.numel() != n_out:
+            raise ValueError(f"each output holds {n_out} elements, got {o.numel()}")
+
+
 def allreduce(ins, outs=None, algo="auto", placement="xcd", stream=None):
     """out[d] = sum over ranks r (ascending, fp32 accumulation) of ins[r], for every d."""
     _, n = _check_ranks(ins, "ins")
     if outs is None:
         outs = [_torch().empty_like(ins[0]) for _ in ins]
+    _check_outs(ins, outs, n)
     _check_ranks(outs, "outs")
-    if outs[0].numel() != n or outs[0].dtype != ins[0].dtype:
-        raise ValueError("outs must match ins in dtype and size")
     _check(allreduce_raw([t.data_ptr() for t in ins], [t.data_ptr() for t in outs], len(ins), n,
                          _dtype_code(ins[0]), ALGOS[algo], PLACEMENTS[placement], _stream(stream)))
     return outs
@@ -314,9 +362,8 @@ class Prepared:
 def prepare_allreduce(ins, outs, algo="auto", placement="xcd"):
     """allreduce(ins, outs, algo, placement) as a Prepared call."""
     _, n = _check_ranks(ins, "ins")
+    _check_outs(ins, outs, n)
     _check_ranks(outs, "outs")
-    if outs[0].numel() != n or outs[0].dtype != ins[0].dtype or len(outs) != len(ins):
-        raise ValueError("outs must match ins in count, dtype and size")
     a = _ptr_array([t.data_ptr() for t in ins])
     b = _ptr_array([t.data_ptr() for t in outs])
     args = (a, b, len(ins), n, _dtype_code(ins[0]), ALGOS[algo], PLACEMENTS[placement])
@@ -332,9 +379,8 @@ def reduce_scatter(ins, outs=None, placement="xcd", stream=None):
     m = n // P
     if outs is None:
         outs = [_torch().empty(m, dtype=ins[0].dtype, device=ins[0].device) for _ in ins]
+    _check_outs(ins, outs, m)
     _check_ranks(outs, "outs")
-    if outs[0].numel() != m:
-        raise ValueError("each output holds numel/P elements")
     _check(reduce_scatter_raw([t.data_ptr() for t in ins], [t.data_ptr() for t in outs], P, m, _dtype_code(ins[0]),
                               PLACEMENTS[placement], _stream(stream)))
     return outs
@@ -346,9 +392,8 @@ def all_gather(ins, outs=None, placement="xcd", stream=None):
     P = len(ins)
     if outs is None:
         outs = [_torch().empty(P * m, dtype=ins[0].dtype, device=ins[0].device) for _ in ins]
+    _check_outs(ins, outs, P * m)
     _check_ranks(outs, "outs")
-    if outs[0].numel() != P * m:
-        raise ValueError("each output holds P*m elements")
     _check(all_gather_raw([t.data_ptr() for t in ins], [t.data_ptr() for t in outs], P, m, _dtype_code(ins[0]),
                           PLACEMENTS[placement], _stream(stream)))
     return outs

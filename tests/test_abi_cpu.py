@@ -456,3 +456,145 @@ def test_counter_summary_medians(tmp_path):
     assert len(lines) == 1
     cells = [c.strip() for c in lines[0].strip("|").split("|")]
     assert cells[1:] == ["4096", "3", "10", "2"]
+
+
+# ---------------------------------------------------------------- dispatch-map check behind nuna_init
+
+def test_dispatch_map_check_accepts_b_mod_8_on_256_cus():
+    for G in (64, 65, 2048):
+        assert nuna.check_dispatch_map_raw(np.arange(G) % 8, 256) == nuna.OK, nuna.last_error()
+
+
+@pytest.mark.parametrize("case", ["mod4", "one_off", "shifted", "one_xcd", "cus_80", "cus_304"])
+def test_dispatch_map_check_rejects_other_maps(case):
+    """What the library must not take for the MI355X map: fewer XCDs (a partition mode), one workgroup on
+    the wrong XCD, a rotated map, a single-XCD partition, other compute-unit counts."""
+    G, cus = 2048, 256
+    x = np.arange(G) % 8
+    if case == "mod4":
+        x = np.arange(G) % 4
+    elif case == "one_off":
+        x[1234] = (x[1234] + 1) % 8
+    elif case == "shifted":
+        x = (np.arange(G) + 1) % 8
+    elif case == "one_xcd":
+        x = np.zeros(G, dtype=np.int64)
+    elif case == "cus_80":
+        cus = 80
+    elif case == "cus_304":
+        cus = 304
+    assert nuna.check_dispatch_map_raw(x, cus) == nuna.ERR_UNSUPPORTED
+    msg = nuna.last_error()
+    assert ("compute units" in msg) if case.startswith("cus") else ("workgroup" in msg), msg
+
+
+def test_dispatch_map_check_rejects_bad_arguments():
+    assert nuna.check_dispatch_map_raw(np.arange(63) % 8, 256) == nuna.ERR_INVALID_ARG
+    assert nuna.lib().nuna_check_dispatch_map(None, 2048, 256) == nuna.ERR_INVALID_ARG
+
+
+def test_device_info_without_init_is_an_error():
+    info = nuna.DeviceInfo()
+    st = nuna.lib().nuna_get_device_info(ctypes.byref(info))
+    assert st in (nuna.ERR_HIP, nuna.ERR_INVALID_ARG), nuna.last_error()
+    assert nuna.lib().nuna_get_device_info(None) == nuna.ERR_INVALID_ARG
+
+
+@no_gpu_only
+def test_xcd_placement_without_a_device_never_launches():
+    """XCD mode first asks for the verified dispatch map of the current device; without a device that is a
+    HIP error, and LINEAR mode reaches the launch, which fails the same way."""
+    for place in (nuna.XCD, nuna.LINEAR):
+        st = nuna.allreduce_raw(_bufs(8), _bufs(8, base=BASE + (1 << 32)), 8, 4096, nuna.BF16, nuna.ALGO_TWO_SHOT,
+                                place)
+        assert st == nuna.ERR_HIP, nuna.last_error()
+
+
+@no_gpu_only
+@pytest.mark.parametrize("algo", [nuna.ALGO_TWO_SHOT, nuna.ALGO_TWO_SHOT_TWO_KERNELS])
+def test_two_shot_forms_pass_validation(algo):
+    P, n = 8, 8 * 4096
+    ins, outs = _bufs(P, stride=1 << 24), _bufs(P, stride=1 << 24, base=BASE + (1 << 32))
+    assert nuna.allreduce_raw(ins, outs, P, n, nuna.BF16, algo, nuna.LINEAR) == nuna.ERR_HIP
+    assert nuna.allreduce_raw(ins, ins, P, n, nuna.BF16, algo, nuna.LINEAR) == nuna.ERR_HIP  # in place
+    assert nuna.allreduce_raw(ins, outs, P, n, nuna.BF16, 5, nuna.LINEAR) == nuna.ERR_INVALID_ARG
+
+
+# ---------------------------------------------------------------- page-grouped direct map (host mirror)
+
+@pytest.mark.parametrize("items,chunk", [(1, 1024), (16, 1024), (64, 1024), (100, 1024), (1024, 1024),
+                                         (64, 256), (1000, 256), (7, 512), (4096, 4096), (33, 8192), (4, 16)])
+def test_direct_map_covers_every_item_once(items, chunk):
+    for place in (nuna.LINEAR, nuna.XCD):
+        m = nuna.placement_direct(place, items, chunk)
+        got = m[m >= 0]
+        assert sorted(got.tolist()) == list(range(items)), (place, items, chunk)
+        if place == nuna.LINEAR or chunk >= 4096:
+            assert m.tolist() == list(range(items))
+
+
+@pytest.mark.parametrize("items,chunk", [(16, 1024), (100, 1024), (1024, 1024), (1000, 256), (64, 16), (7, 512)])
+def test_direct_map_keeps_each_page_on_one_xcd(items, chunk):
+    """XCD mode: the chunks of one 4 KiB page run on one XCD (workgroup b runs on XCD b mod 8), pages are
+    dealt round-robin to the XCDs, and a page's chunks run on consecutive workgroup slots of its XCD."""
+    gp = 4096 // chunk
+    m = nuna.placement_direct(nuna.XCD, items, chunk)
+    assert m.size % (8 * gp) == 0
+    where = {int(w): b for b, w in enumerate(m) if w >= 0}
+    for page in range((items + gp - 1) // gp):
+        bs = [where[i] for i in range(page * gp, min(items, (page + 1) * gp))]
+        assert {b % 8 for b in bs} == {page % 8}, page
+        ks = [b // 8 for b in bs]
+        assert ks == list(range(ks[0], ks[0] + len(bs))), (page, ks)
+    lin = nuna.placement_direct(nuna.LINEAR, items, chunk)
+    if gp > 1 and items >= 2 * gp:
+        # the linear map splits a page over min(gp, 8) XCDs
+        assert lin[:gp].tolist() == list(range(gp)) and len({b % 8 for b in range(gp)}) == min(gp, 8)
+
+
+def test_direct_map_follows_the_page_groups_tunable():
+    with nuna.tunables(NUNA_PAGE_GROUPS=0):
+        assert nuna.placement_direct(nuna.XCD, 64, 1024).tolist() == list(range(64))
+    assert nuna.placement_direct(nuna.XCD, 64, 1024).tolist() != list(range(64))
+
+
+def test_direct_map_rejects_bad_geometry():
+    g = ctypes.c_int64()
+    for items, chunk in [(0, 1024), (8, 24), (8, 0), (8, 8)]:
+        assert nuna.lib().nuna_placement_direct(nuna.XCD, items, chunk, None, 0, ctypes.byref(g)) == \
+            nuna.ERR_INVALID_ARG
+    assert nuna.lib().nuna_placement_direct(nuna.XCD, 64, 1024, None, 0, ctypes.byref(g)) == nuna.ERR_INVALID_ARG
+    assert g.value == 64
+
+
+# ---------------------------------------------------------------- binding checks before any C call
+
+class _FakeTensor:
+    def __init__(self, dtype, n):
+        self.dtype, self._n = dtype, n
+
+    def numel(self):
+        return self._n
+
+
+def test_output_count_and_dtype_checked_before_the_library():
+    """An output list shorter than the inputs, or outputs of another dtype, would make the library read
+    past the pointer array or write more bytes than an output holds: the binding refuses both."""
+    ins = [_FakeTensor("f32", 64) for _ in range(4)]
+    with pytest.raises(ValueError, match="one output per rank"):
+        nuna._check_outs(ins, [_FakeTensor("f32", 64) for _ in range(3)], 64)
+    with pytest.raises(ValueError, match="dtype"):
+        nuna._check_outs(ins, [_FakeTensor("f32", 64)] * 3 + [_FakeTensor("bf16", 64)], 64)
+    with pytest.raises(ValueError, match="elements"):
+        nuna._check_outs(ins, [_FakeTensor("f32", 16) for _ in range(4)], 64)
+    nuna._check_outs(ins, [_FakeTensor("f32", 64) for _ in range(4)], 64)
+
+
+def test_new_tunables_accept_and_reject():
+    with nuna.tunables(NUNA_PAGE_GROUPS=0, NUNA_DIRECT_MAX_GRID=16384):
+        assert nuna.get_tunable("NUNA_PAGE_GROUPS") == 0
+        assert nuna.get_tunable("NUNA_DIRECT_MAX_GRID") == 16384
+    assert nuna.get_tunable("NUNA_PAGE_GROUPS") == 1
+    for name, bad in [("NUNA_PAGE_GROUPS", 2), ("NUNA_DIRECT_MAX_GRID", -1), ("NUNA_DIRECT_MAX_GRID", (1 << 24) + 1)]:
+        with pytest.raises(nuna.NunaError):
+            nuna.set_tunable(name, bad)

@@ -34,7 +34,7 @@ def _case(seed):
     n = int(np.exp(g.uniform(0, np.log(400000 // P + 2))))
     dtype = np.uint16 if g.random() < 0.6 else np.float32
     op = g.choice(["allreduce", "reduce_scatter", "all_gather"])
-    algo = str(g.choice(["auto", "one_shot", "two_shot", "one_shot_split"]))
+    algo = str(g.choice(["auto", "one_shot", "two_shot", "one_shot_split", "two_shot_two_kernels"]))
     place = str(g.choice(["linear", "xcd"]))
     inplace = bool(g.random() < 0.3)
     bits = bool(g.random() < 0.3)

@@ -49,7 +49,7 @@ def nuna():
     return n
 
 
-@pytest.mark.parametrize("algo", ["one_shot", "two_shot"])
+@pytest.mark.parametrize("algo", ["one_shot", "two_shot", "two_shot_two_kernels"])
 def test_allreduce_beyond_2_31_elements(nuna, algo):
     n = (1 << 31) + 27 if algo == "one_shot" else (1 << 31) + 8 * 24  # two-shot needs count % P == 0
     ins = [torch.empty(n, dtype=torch.bfloat16, device="cuda") for _ in range(P)]

@@ -24,7 +24,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 PLACES = ["linear", "xcd"]
-AR_ALGOS = ["one_shot", "one_shot_split", "two_shot", "auto"]
+AR_ALGOS = ["one_shot", "one_shot_split", "two_shot", "two_shot_two_kernels", "auto"]
 
 
 @pytest.fixture(scope="module")
@@ -80,6 +80,29 @@ def test_probe_workgroup_b_runs_on_xcd_b_mod_8(nuna, G):
     assert np.array_equal(x, np.arange(G) % 8), np.unique(x - np.arange(G) % 8)
 
 
+def test_init_verified_the_dispatch_map(nuna):
+    """nuna_init probed the device: 256 compute units in 8 XCDs, workgroup b on XCD b mod 8."""
+    info = nuna.device_info()
+    assert info["map_verified"] == 1 and info["cu_count"] == 256 and info["xcd_count"] == 8, info
+    xcc, _ = nuna.probe_xcc(4096)
+    torch.cuda.synchronize()
+    assert nuna.check_dispatch_map_raw(xcc.cpu().numpy(), info["cu_count"]) == nuna.OK, nuna.last_error()
+
+
+@pytest.mark.parametrize("items,chunk", [(16, 1024), (100, 1024), (4096, 1024), (1000, 256), (8192, 256)])
+def test_page_groups_run_on_one_xcd(nuna, items, chunk):
+    """Placement proof of the page-grouped map: a launch of the direct map's grid records the XCC each
+    workgroup ran on; every page's chunks ran on one XCD, XCD (page mod 8)."""
+    m = nuna.placement_direct("xcd", items, chunk)
+    xcc, _ = nuna.probe_xcc(int(m.size))
+    torch.cuda.synchronize()
+    x = xcc.cpu().numpy()
+    gp = 4096 // chunk
+    for b, w in enumerate(m):
+        if w >= 0:
+            assert x[b] == (w // gp) % 8, (b, w, x[b])
+
+
 # ---------------------------------------------------------------- workload 1: fp32 integers, P=8, n=2048
 
 @pytest.mark.parametrize("place", PLACES)
@@ -110,7 +133,7 @@ def test_ar_bf16_decode(nuna, T, algo, place):
 # ---------------------------------------------------------------- workload 3: prefill two-shot bf16, P=8
 
 @pytest.mark.parametrize("place", PLACES)
-@pytest.mark.parametrize("algo", ["two_shot", "one_shot"])
+@pytest.mark.parametrize("algo", ["two_shot", "two_shot_two_kernels", "one_shot"])
 @pytest.mark.parametrize("T", wl.PREFILL_TOKENS)
 def test_ar_bf16_prefill(nuna, T, algo, place):
     x = wl.ar_bf16_prefill(T)
@@ -123,7 +146,7 @@ def test_ar_bf16_prefill(nuna, T, algo, place):
 # ---------------------------------------------------------------- workload 5: P=64 bf16
 
 @pytest.mark.parametrize("place", PLACES)
-@pytest.mark.parametrize("algo", ["one_shot", "one_shot_split", "two_shot"])
+@pytest.mark.parametrize("algo", ["one_shot", "one_shot_split", "two_shot", "two_shot_two_kernels"])
 @pytest.mark.parametrize("kib", wl.P64_KIB)
 def test_ar_bf16_p64(nuna, kib, algo, place):
     x = wl.ar_bf16_p64(kib)
@@ -430,6 +453,72 @@ def test_write_through_stores(nuna, cfg):
                 got = run_allreduce(nuna, x, "two_shot", place)
                 for d in range(8):
                     assert_bitwise(got[d], ref[d], f"{cfg} two-shot {place} n={n} rank {d}")
+
+
+@pytest.mark.parametrize("cfg", [dict(NUNA_VPT=v, NUNA_WG_THREADS=t) for v in (0, 1, 2, 4, 8) for t in (64, 256)] +
+                         [dict(NUNA_DIRECT_MAX_GRID=5), dict(NUNA_WRITE_THROUGH=2, NUNA_VPT=8, NUNA_WG_THREADS=256)],
+                         ids=lambda c: ",".join(f"{k[5:]}={v}" for k, v in c.items()))
+def test_two_shot_fused(nuna, cfg):
+    """The fused two-shot (both phases per chunk in one kernel) at every launch shape, against the oracle
+    and the two-kernel two-shot: 2, 4, 8 and 16 ranks, both dtypes, shards of 1 vector to several
+    chunks with a partial last chunk, the persistent kernel (small direct-grid limit, grid caps), in
+    place, with guard bands around every output."""
+    with nuna.tunables(**cfg):
+        for P in (2, 4, 8, 16):
+            for dt in (np.uint16, np.float32):
+                per_vec = 8 if dt == np.uint16 else 4
+                for mv in (1, 7, 64, 65, 1000, 4097):
+                    n = P * mv * per_vec
+                    seed = 7919 * P + mv + (0 if dt == np.uint16 else 1)
+                    x = wl.normal_bf16(P, n, seed) if dt == np.uint16 else wl.normal_f32(P, n, seed)
+                    ref = oracle.allreduce(x)
+                    for place in PLACES:
+                        got = run_allreduce(nuna, x, "two_shot", place)
+                        two = run_allreduce(nuna, x, "two_shot_two_kernels", place)
+                        for d in range(P):
+                            assert_bitwise(got[d], ref[d], f"{cfg} fused P={P} mv={mv} {place} rank {d}")
+                            assert_bitwise(two[d], ref[d], f"{cfg} two kernels P={P} mv={mv} {place} rank {d}")
+        x = wl.normal_bf16(8, 8 * 8 * 3000, 99)
+        ref = oracle.allreduce(x)
+        for cap in (1, 13, 100):
+            nuna.set_max_workgroups(cap)
+            try:
+                got = run_allreduce(nuna, x, "two_shot", "xcd")
+            finally:
+                nuna.set_max_workgroups(0)
+            for d in range(8):
+                assert_bitwise(got[d], ref[d], f"{cfg} fused cap={cap} rank {d}")
+        bufs = [to_dev(a) for a in x]
+        nuna.allreduce(bufs, bufs, algo="two_shot", placement="xcd")
+        torch.cuda.synchronize()
+        for d in range(8):
+            assert_bitwise(to_host(bufs[d]), ref[d], f"{cfg} fused in place rank {d}")
+
+
+@pytest.mark.parametrize("pg", [0, 1])
+def test_page_groups_parity(nuna, pg):
+    """XCD mode with the chunks of each 4 KiB page on one XCD (and without): the decode and 64-rank
+    workloads, the fp32 integer workload, ragged sizes whose page-grouped grids end in padding
+    workgroups, forced chunk sizes of 1-2 KiB (one-shot) and 256 B-1 KiB (tile), guard bands."""
+    cases = [(wl.ar_f32_int(), "f32 int")] + [(wl.ar_bf16_decode(T), f"decode T={T}") for T in wl.DECODE_TOKENS]
+    cases += [(wl.ar_bf16_p64(k), f"P=64 {k} KiB") for k in wl.P64_KIB]
+    cases += [(wl.normal_bf16(P, n, 5 * P + n), f"P={P} n={n}") for P, n in ((8, 8 * 1000 + 3), (2, 4097), (16, 70001),
+                                                                              (64, 3000), (24, 9001))]
+    with nuna.tunables(NUNA_PAGE_GROUPS=pg):
+        for x, what in cases:
+            ref = oracle.allreduce(x)
+            for algo in ("one_shot", "two_shot"):
+                got = run_allreduce(nuna, x, algo, "xcd")
+                for d in range(len(x)):
+                    assert_bitwise(got[d], ref[d], f"page groups {pg} {algo} {what} rank {d}")
+        for cfg in (dict(NUNA_WG_THREADS=64, NUNA_VPT=2), dict(NUNA_WG_THREADS=128, NUNA_VPT=1),
+                    dict(NUNA_TILE_V=32), dict(NUNA_TILE_V=64)):
+            with nuna.tunables(**cfg):
+                for x, what in cases[1:3] + cases[5:7] + cases[-3:]:
+                    ref = oracle.allreduce(x)
+                    got = run_allreduce(nuna, x, "one_shot", "xcd")
+                    for d in range(len(x)):
+                        assert_bitwise(got[d], ref[d], f"page groups {pg} {cfg} {what} rank {d}")
 
 
 def test_vpt8_every_collective(nuna):
