@@ -1,21 +1,26 @@
 #!/usr/bin/env python3
 """Benchmark of the collective copy/reduce path on one MI355X.
 
-Default workload (one JSON line on stdout): one-shot all-reduce, bf16 data
-with fp32 accumulation, P=8 simulated ranks, decode-shaped messages [T, 8192]
-for T in {1, 4, 16, 64} (16 KiB - 1 MiB per rank).  One step = one
-all-reduce at each of the four sizes.  Calls are captured in a HIP graph and
-replayed; each call works on buffers carved from a rotating 1.5 GiB pool, so
-its inputs are not resident in L2 or the 256 MB Infinity Cache when it runs
-(cold).  NUNA-aware (XCD) and locality-unaware (LINEAR) placement are timed
-interleaved A/B; ``value`` is the XCD-placement throughput.
+Default workload (one JSON line on stdout): the two-shot all-reduce, bf16 data
+with fp32 accumulation, P=8 simulated ranks, prefill-shaped messages [T, 8192]
+for T in {256, 1024, 4096} (4, 16 and 64 MiB per rank).  One step = one
+two-shot all-reduce at each of the three sizes.  Calls are captured in HIP
+graphs and replayed; the buffers sit in a 3 GiB pool and every call meets
+inputs that are not resident in L2 or the 256 MB Infinity Cache (cold).
+NUNA-aware (XCD) and locality-unaware (LINEAR) placement are timed
+interleaved A/B; ``value`` is the XCD-placement throughput.  The same line
+carries per-size figures of the fused and the two-kernel two-shot and of the
+one-shot, the decode all-reduce sweep, the MoE dispatch, the dominant
+kernel's roofline and the oracle timed on the host.
 
 Throughput = algorithmic bytes / time.  Algorithmic bytes of an all-reduce
 call are (P reads + P writes) * n * element size.
 
 ``--full`` instead sweeps every workload (fp32 integer all-reduce, decode and
-prefill all-reduce, MoE all-to-all dispatch, P=64 all-reduce) in both modes,
-cold and warm, and writes JSONL to ``--out``.
+prefill all-reduce, MoE all-to-all dispatch and combine, P=64 all-reduce,
+standalone reduce-scatter and all-gather) in both modes, cold and warm, and
+writes JSONL to ``--out``.  ``--set NAME=VALUE`` applies a launch-shape
+tunable to any run (shape sweeps).
 """
 import argparse
 import json
@@ -33,7 +38,7 @@ import numpy as np  # noqa: E402
 
 METRIC = ("collective latency (µs) + effective HBM GB/s vs msg size, NUNA-aware vs unaware, 1 GPU")
 HBM_PEAK_GBPS = 8000.0
-POOL_BYTES_MAIN = 3 << 29  # 1.5 GiB
+POOL_BYTES_MAIN = 3 << 30  # 3 GiB
 ALIGN = 4096
 
 
@@ -64,9 +69,10 @@ def parse():
                          "buffers (decode T=64 and prefill T=1024 layouts of the pool) and print how well the "
                          "buffers agree offset by offset")
     ap.add_argument("--profile", type=int, default=0, metavar="N",
-                    help="profiling run: N cold launches each of the dominant kernel (decode all-reduce T=64, "
-                         "XCD), the 64 MiB reference copy, the split all-reduce (T=64), the MoE dispatch and "
-                         "combine, eager, then exit")
+                    help="profiling run: N cold launches each of the dominant kernel (fused two-shot all-reduce, "
+                         "P=8, [4096, 8192] bf16, XCD), the 64 MiB reference copy, the two-kernel two-shot at "
+                         "[256, 8192], the split all-reduce (decode T=64), the MoE dispatch and combine, eager, "
+                         "then exit")
     ap.add_argument("--summarize-counters", metavar="CSV", default=None,
                     help="print per-kernel medians of every counter in one rocprofv3 --pmc CSV")
     ap.add_argument("--summarize-l2", nargs=2, metavar=("LINEAR_CSV", "XCD_CSV"), default=None,
@@ -79,6 +85,13 @@ def parse():
                          "counters, e.g. linear=a.csv linear=b.csv xcd=c.csv ...")
     ap.add_argument("--profile-place", choices=("linear", "xcd"), default="xcd",
                     help="placement of the split all-reduce and MoE kernels in --profile")
+    ap.add_argument("--set", action="append", default=[], metavar="NAME=VALUE",
+                    help="launch-shape tunable for this run (repeatable), e.g. NUNA_VPT=2")
+    ap.add_argument("--kernel-json", metavar="JSON", default=None,
+                    help="with --summarize-trace: also write the dominant kernel's traced average duration to JSON")
+    ap.add_argument("--summarize-phases", metavar="KERNEL_TRACE_CSV", default=None,
+                    help="per-phase durations and the gap between the phases of the two-kernel two-shot, from a "
+                         "rocprofv3 --kernel-trace CSV of the default bench")
     return ap.parse_args()
 
 
@@ -154,7 +167,7 @@ def capture(torch, fn, ncalls):
 def stats(v):
     v = sorted(v)
     q = lambda p: v[min(len(v) - 1, max(0, int(round(p * (len(v) - 1)))))]  # noqa: E731
-    return {"median": statistics.median(v), "p10": q(0.1), "p90": q(0.9)}
+    return {"median": statistics.median(v), "p10": q(0.1), "p90": q(0.9), "mean": statistics.mean(v)}
 
 
 # ---------------------------------------------------------------------------------------------- workloads
@@ -188,10 +201,10 @@ def ar_sets(torch, pool, x_np, nsets, src=None):
     return sets
 
 
-def oracle_check_ar(nuna, torch, x_np, algo, place):
-    """One call on fresh buffers compared bit for bit with the oracle."""
+def oracle_check_ar(nuna, torch, x_np, algo, place, ref=None):
+    """One call on fresh buffers compared bit for bit with the oracle (`ref`: its result, if known)."""
     import oracle
-    ref = oracle.allreduce(x_np)
+    ref = oracle.allreduce(x_np) if ref is None else ref
     dt = torch.bfloat16 if x_np[0].dtype == np.uint16 else torch.float32
     ins = [dev_copy_of(torch, a) for a in x_np]
     outs = nuna.allreduce(ins, algo=algo, placement=place)
@@ -215,11 +228,12 @@ def calls_for(fp, max_calls=4096):
     return int(min(max_calls, max(4, math.ceil(GRAPH_BYTES / fp))))
 
 
-def bench_allreduce(nuna, torch, pool, x_np, algo, reps, warmup, cold=True, places=("linear", "xcd")):
+def bench_allreduce(nuna, torch, pool, x_np, algo, reps, warmup, cold=True, places=("linear", "xcd"),
+                    max_calls=4096):
     P, n = len(x_np), x_np[0].size
     es = 2 if x_np[0].dtype == np.uint16 else 4
     fp = ar_footprint(P, n, es)
-    calls = calls_for(fp)
+    calls = calls_for(fp, max_calls)
     nsets = max(1, min(calls, pool.nbytes // fp)) if cold else 1
     pool.off = 0
     sets = ar_sets(torch, pool, x_np, nsets)
@@ -265,8 +279,10 @@ def bench_rs_ag(nuna, torch, pool, kind, x_np, reps, warmup, cold=True, places=(
     op = nuna.reduce_scatter if kind == "rs" else nuna.all_gather
     ref = oracle.reduce_scatter(x_np) if kind == "rs" else oracle.all_gather(x_np)
     ok = True
+    launches = {}
     for place in places:
         op(sets[0][0], sets[0][1], placement=place)
+        launches[place] = nuna.last_launch()
         torch.cuda.synchronize()
         for d in range(P):
             g = sets[0][1][d].cpu()
@@ -279,7 +295,7 @@ def bench_rs_ag(nuna, torch, pool, kind, x_np, reps, warmup, cold=True, places=(
     out = {}
     for place in places:
         st = stats(t[place])
-        out[place] = {"us": st, "gbps": alg_bytes / (st["median"] * 1e-6) / 1e9}
+        out[place] = {"us": st, "gbps": alg_bytes / (st["median"] * 1e-6) / 1e9, "launch": launches[place]}
     del graphs, sets
     return alg_bytes, out, calls, ok
 
@@ -299,24 +315,25 @@ def steps_per_graph(ksteps, step_bytes):
     return best if best * 4 >= min(ksteps, target) else min(ksteps, target)
 
 
-def decode_steps_timed(nuna, torch, pool, args):
-    """The timed region: K steps per placement mode, a step being one all-reduce at each decode size.
-    Steps are replayed from graphs of `steps_per_graph` steps (several GiB each); step i uses buffer
-    region i mod R of the pool, R as many regions as the pool holds, so each call meets cold caches."""
-    from paper_2608_00867_amd import workloads as wl
-    xs = [wl.ar_bf16_decode(T) for T in wl.DECODE_TOKENS]
-    step_fp = sum(ar_footprint(8, x[0].size, 2) for x in xs)
-    step_bytes = sum(2 * 8 * x[0].size * 2 for x in xs)
+def steps_timed(nuna, torch, pool, args, xs, algo):
+    """The timed region: K steps per placement mode, a step being one all-reduce (`algo`) of each input
+    set in `xs`.  Steps are replayed from graphs of `steps_per_graph` steps (several GiB each); step i
+    uses buffer region i mod R of the pool, R as many step regions as the pool holds.  With one region,
+    each call is still cold: between two uses of a buffer set, the other sets of the step (and the
+    set's own larger part) stream more bytes than the 256 MB Infinity Cache holds."""
+    step_fp = sum(ar_footprint(len(x), x[0].size, 2) for x in xs)
+    step_bytes = sum(2 * len(x) * x[0].size * 2 for x in xs)
     nsteps = steps_per_graph(args.steps, step_bytes)
     nreg = max(1, min(nsteps, pool.nbytes // step_fp))
     assert step_fp * nreg <= pool.nbytes
     pool.off = 0
     srcs = [[dev_copy_of(torch, a) for a in x] for x in xs]
     sets = [[ar_sets(torch, pool, x, 1, src)[0] for x, src in zip(xs, srcs)] for _ in range(nreg)]
+    del srcs
 
     def step(i, place):
         for ins, outs in sets[i % nreg]:
-            nuna.allreduce(ins, outs, algo="auto", placement=place)
+            nuna.allreduce(ins, outs, algo=algo, placement=place)
 
     graphs = {p: capture(torch, lambda i, p=p: step(i, p), nsteps) for p in ("linear", "xcd")}
     reps = max(1, math.ceil(args.steps / nsteps))
@@ -343,36 +360,118 @@ def decode_steps_timed(nuna, torch, pool, args):
         out[p] = {"ms_per_step": ms, "gbps": step_bytes / (ms * 1e-3) / 1e9,
                   "replay_ms": stats(ev[p])}
     del graphs, sets
-    return step_bytes, reps * nsteps, out
+    torch.cuda.empty_cache()
+    return step_bytes, reps * nsteps, nsteps, out
+
+
+def launch_of(nuna, torch, x, algo, place):
+    """Kernels and map of one call (nuna_last_launch) on scratch buffers."""
+    ins = [dev_copy_of(torch, a) for a in x]
+    outs = [torch.empty_like(t) for t in ins]
+    nuna.allreduce(ins, outs, algo=algo, placement=place)
+    info = nuna.last_launch()
+    torch.cuda.synchronize()
+    del ins, outs
+    return info
+
+
+def same_map(li_linear, li_xcd):
+    """True when both placements ran identical launches: same kernels, same grid, the linear map."""
+    return (li_linear["kernels"] == li_xcd["kernels"] and li_linear["grid"] == li_xcd["grid"]
+            and li_linear["map"] == li_xcd["map"] == "linear")
+
+
+def ar_sweep(nuna, torch, pool, args, cases, algos, max_calls=4096):
+    """Per size and algorithm: µs per call (median, p10, p90, mean) and GB/s in both placements, from
+    graph replays on cold buffers; bit-for-bit parity of both placements with the oracle; the launches
+    each placement ran and whether they are the same map."""
+    import oracle
+    rows = []
+    for label, x in cases:
+        P, n = len(x), x[0].size
+        es = 2 if x[0].dtype == np.uint16 else 4
+        ref = oracle.allreduce(x)
+        for algo in algos:
+            ok = all(oracle_check_ar(nuna, torch, x, algo, p, ref) for p in ("linear", "xcd"))
+            li = {p: launch_of(nuna, torch, x, algo, p) for p in ("linear", "xcd")}
+            nbytes, res, calls = bench_allreduce(nuna, torch, pool, x, algo, args.reps, args.warmup,
+                                                 max_calls=max_calls)
+            rows.append({**label, "algo": algo, "bytes_per_rank": n * es, "alg_bytes": nbytes, "parity": ok,
+                         "calls_per_graph": calls,
+                         "xcd_us": {k: round(v, 3) for k, v in res["xcd"]["us"].items()},
+                         "linear_us": {k: round(v, 3) for k, v in res["linear"]["us"].items()},
+                         "xcd_gbps": round(res["xcd"]["gbps"], 1), "linear_gbps": round(res["linear"]["gbps"], 1),
+                         "xcd_frac_hbm": round(res["xcd"]["gbps"] / HBM_PEAK_GBPS, 4),
+                         "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4),
+                         "same_map": same_map(li["linear"], li["xcd"]),
+                         "xcd_launch": {k: li["xcd"][k] for k in ("kernels", "map", "group_size", "grid", "threads",
+                                                                   "vectors_per_thread")},
+                         "linear_launch": {k: li["linear"][k] for k in ("kernels", "map", "grid")}})
+            annotate_targets(rows[-1])
+        del ref
+    return rows
+
+
+def prefill_sweep(nuna, torch, pool, args, xs):
+    from paper_2608_00867_amd import workloads as wl
+    cases = [({"tokens": T}, x) for T, x in zip(wl.PREFILL_TOKENS, xs)]
+    return ar_sweep(nuna, torch, pool, args, cases, ["two_shot", "two_shot_two_kernels", "one_shot"])
 
 
 def decode_sweep(nuna, torch, pool, args):
     from paper_2608_00867_amd import workloads as wl
-    sweep = []
-    for T in wl.DECODE_TOKENS:
-        x = wl.ar_bf16_decode(T)
-        ok = oracle_check_ar(nuna, torch, x, "auto", "xcd") and oracle_check_ar(nuna, torch, x, "auto", "linear")
-        nbytes, res, calls = bench_allreduce(nuna, torch, pool, x, "auto", args.reps, args.warmup)
-        sweep.append({"tokens": T, "bytes_per_rank": T * 8192 * 2, "alg_bytes": nbytes, "parity": ok,
-                      "calls_per_graph": calls,
-                      "xcd_us": {k: round(v, 3) for k, v in res["xcd"]["us"].items()},
-                      "linear_us": {k: round(v, 3) for k, v in res["linear"]["us"].items()},
-                      "xcd_gbps": round(res["xcd"]["gbps"], 1), "linear_gbps": round(res["linear"]["gbps"], 1),
-                      "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
-    return sweep
+    cases = [({"tokens": T}, wl.ar_bf16_decode(T)) for T in wl.DECODE_TOKENS]
+    return ar_sweep(nuna, torch, pool, args, cases, ["auto"], max_calls=1024)
+
+
+DOMINANT_JSON = os.path.join(ROOT, "profiles", "dominant_kernel.json")
+
+
+def profiled_dominant():
+    """The dominant kernel's traced average duration from the committed kernel-trace summary, or None
+    when the kernel sources have changed since the trace was taken."""
+    try:
+        rec = json.load(open(DOMINANT_JSON))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_sha():
+        return None
+    return rec
 
 
 def roofline_dominant(sweep):
-    """Dominant kernel of the step: the all-reduce at T=64 (1 MiB per rank), XCD placement.  Its
-    average launch duration comes from HIP events around back-to-back cold launches replayed from a
-    graph on the launching stream."""
-    row = sweep[-1]
-    us = row["xcd_us"]["median"]
+    """Dominant kernel of the step: the fused two-shot all-reduce at T=4096 (64 MiB per rank), one
+    kernel per call, XCD placement.  Its average duration per launch comes from HIP events around
+    graph replays of back-to-back cold launches on the launching stream (the mean over the replays of
+    replay time / launches).  The committed rocprofv3 kernel-trace average of the same kernel, from a
+    run of this bench command on the same sources, is carried beside it."""
+    row = [r for r in sweep if r["tokens"] == 4096 and r["algo"] == "two_shot"][0]
+    us = row["xcd_us"]["mean"]
     achieved = row["alg_bytes"] / (us * 1e-6) / 1e9
-    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(),
-            "kernel": "k_allreduce_direct<P=8,bf16,VPT=1> one-shot, [64,8192] bf16 per rank, XCD placement",
-            "alg_bytes_per_launch": row["alg_bytes"], "avg_launch_us": us}
+            "kernel": row["xcd_launch"]["kernels"], "grid_workgroups": row["xcd_launch"]["grid"],
+            "threads": row["xcd_launch"]["threads"], "vectors_per_thread": row["xcd_launch"]["vectors_per_thread"],
+            "workload": "two-shot all-reduce, P=8, [4096, 8192] bf16 per rank (64 MiB), XCD placement, cold",
+            "alg_bytes_per_launch": row["alg_bytes"],
+            "alg_bytes_rule": "2 * P * n * 2 B: each element read from P inputs and written to P outputs",
+            "kernel_us_events_mean": us}
+    prof = profiled_dominant()
+    if prof is not None:
+        pa = row["alg_bytes"] / (prof["avg_us"] * 1e-6) / 1e9
+        roof["profile"] = {"kernel": prof["kernel"], "avg_us": prof["avg_us"], "dispatches": prof["dispatches"],
+                           "frac": round(pa / HBM_PEAK_GBPS, 4), "source": prof["source"],
+                           "events_over_profile": round(us / prof["avg_us"], 4)}
+    return roof
+
+
+def moe_dispatch_summary(nuna, torch, pool, args):
+    """The MoE dispatch (8 ranks, 512 tokens x 7168 bf16 per rank, top-8 of 256 experts), cold."""
+    recs = []
+    a2a_case(nuna, torch, pool, args, recs.append, None, colds=(True,))
+    r = recs[0]
+    annotate_targets(r)
+    return r
 
 
 def cpu_model():
@@ -385,15 +484,14 @@ def cpu_model():
     return "unknown"
 
 
-def cpu_baseline(seconds):
-    """The oracle (single-threaded C) on the same decode step, repeated for about `seconds`; then the
-    same oracle on all host cores, each thread running it on a contiguous element range of every
-    rank buffer (each element still adds its ranks in ascending order, so the bits are the same;
-    checked).  The oracle call releases the interpreter lock while it runs."""
+def cpu_baseline(seconds, xs):
+    """The oracle (single-threaded C) on the same step (one all-reduce of each input set in `xs`),
+    repeated for about `seconds`; then the same oracle on all host cores, each thread running it on a
+    contiguous element range of every rank buffer (each element still adds its ranks in ascending
+    order, so the bits are the same; checked).  The oracle call releases the interpreter lock while it
+    runs.  Inputs are already in host memory; their generation is not timed."""
     import concurrent.futures
     import oracle
-    from paper_2608_00867_amd import workloads as wl
-    xs = [wl.ar_bf16_decode(T) for T in wl.DECODE_TOKENS]
     step_bytes = sum(2 * len(x) * x[0].size * 2 for x in xs)
     outs = [[np.empty_like(a) for a in x] for x in xs]
     oracle.get()
@@ -413,9 +511,10 @@ def cpu_baseline(seconds):
             oracle.allreduce(x, o)
 
     steps, el = timed(single, seconds)
+    shape = "all-reduce bf16 P=8 at [T, 8192], T=" + ",".join(str(x[0].size // 8192) for x in xs)
     res = {"value": round(step_bytes * steps / el / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
-           "sample": f"{steps} decode steps (all-reduce bf16 P=8 at T=1,4,16,64) in {el:.1f} s, "
-                     f"single thread, inputs resident in host memory; host reports {os.cpu_count()} CPUs",
+           "sample": f"{steps} steps ({shape}) in {el:.1f} s, single thread, inputs resident in host memory; "
+                     f"host reports {os.cpu_count()} CPUs",
            "cpu_model": cpu_model(), "ms_per_step": round(el / steps * 1e3, 3)}
     nthreads = max(1, min(os.cpu_count() or 1, 16))
     outs_mt = [[np.empty_like(a) for a in x] for x in xs]
@@ -432,7 +531,7 @@ def cpu_baseline(seconds):
         steps, el = timed(multi, seconds / 2)
     res["all_cores"] = {"value": round(step_bytes * steps / el / 1e9, 3), "unit": "GB/s", "threads": nthreads,
                         "same_bits_as_single": bool(same),
-                        "sample": f"{steps} decode steps in {el:.1f} s, element ranges split over {nthreads} threads"}
+                        "sample": f"{steps} steps in {el:.1f} s, element ranges split over {nthreads} threads"}
     return res
 
 
@@ -490,21 +589,25 @@ def full_sweep(nuna, torch, pool, args):
         es = 2 if x[0].dtype == np.uint16 else 4
         for algo in algos:
             ok = all(oracle_check_ar(nuna, torch, x, algo, p) for p in ("linear", "xcd"))
+            li = {p: launch_of(nuna, torch, x, algo, p) for p in ("linear", "xcd")}
             for cold in (True, False):
                 nb, res, calls = bench_allreduce(nuna, torch, pool, x, algo, args.reps, args.warmup, cold=cold)
                 emit({"workload": name, "P": P, "bytes_per_rank": n * es, "algo": algo,
                       "cache": "cold" if cold else "warm", "alg_bytes": nb, "calls_per_graph": calls,
-                      "parity": ok,
+                      "parity": ok, "same_map": same_map(li["linear"], li["xcd"]),
+                      "xcd_kernels": li["xcd"]["kernels"], "xcd_map": li["xcd"]["map"],
                       **{f"{p}_us": {k: round(v, 3) for k, v in res[p]["us"].items()} for p in res},
                       **{f"{p}_gbps": round(res[p]["gbps"], 1) for p in res},
                       **{f"{p}_frac_hbm": round(res[p]["gbps"] / HBM_PEAK_GBPS, 4) for p in res},
                       "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
 
-    ar_case("ar_f32_int_p8", wl.ar_f32_int, ["one_shot", "one_shot_split", "two_shot"])
+    ar_case("ar_f32_int_p8", wl.ar_f32_int, ["one_shot", "one_shot_split", "two_shot", "two_shot_two_kernels"])
     for T in wl.DECODE_TOKENS:
-        ar_case(f"ar_bf16_decode_T{T}", lambda T=T: wl.ar_bf16_decode(T), ["one_shot", "one_shot_split", "two_shot"])
+        ar_case(f"ar_bf16_decode_T{T}", lambda T=T: wl.ar_bf16_decode(T), ["one_shot", "one_shot_split", "two_shot",
+                                                                           "two_shot_two_kernels"])
     for T in wl.PREFILL_TOKENS:
-        ar_case(f"ar_bf16_prefill_T{T}", lambda T=T: wl.ar_bf16_prefill(T), ["two_shot", "one_shot"])
+        ar_case(f"ar_bf16_prefill_T{T}", lambda T=T: wl.ar_bf16_prefill(T), ["two_shot", "two_shot_two_kernels",
+                                                                             "one_shot"])
     for kib in wl.P64_KIB:
         ar_case(f"ar_bf16_p64_{kib}KiB", lambda kib=kib: wl.ar_bf16_p64(kib), ["one_shot", "one_shot_split",
                                                                              "two_shot"])
@@ -521,6 +624,8 @@ def full_sweep(nuna, torch, pool, args):
                 nb, res, calls, ok = bench_rs_ag(nuna, torch, pool, kind, x, args.reps, args.warmup, cold=cold)
                 emit({"workload": name, "P": 8, "shard_bytes": kib * 1024, "algo": "standalone",
                       "cache": "cold" if cold else "warm", "alg_bytes": nb, "calls_per_graph": calls, "parity": ok,
+                      "same_map": same_map(res["linear"]["launch"], res["xcd"]["launch"]),
+                      "xcd_kernels": res["xcd"]["launch"]["kernels"], "xcd_map": res["xcd"]["launch"]["map"],
                       **{f"{p}_us": {k: round(v, 3) for k, v in res[p]["us"].items()} for p in res},
                       **{f"{p}_gbps": round(res[p]["gbps"], 1) for p in res},
                       **{f"{p}_frac_hbm": round(res[p]["gbps"] / HBM_PEAK_GBPS, 4) for p in res},
@@ -538,7 +643,7 @@ def full_sweep(nuna, torch, pool, args):
     f.close()
 
 
-def a2a_case(nuna, torch, pool, args, emit, T_tokens=None):
+def a2a_case(nuna, torch, pool, args, emit, T_tokens=None, colds=(True, False)):
     """MoE dispatch at T_tokens per rank (default: the 512-token shape); decode-shaped token counts
     measure the latency regime."""
     import oracle
@@ -553,7 +658,7 @@ def a2a_case(nuna, torch, pool, args, emit, T_tokens=None):
     alg_bytes = int(P * T * rb + rows.sum() * rb)
     set_bytes = P * T * rb + P * cap * rb
     src = [dev_copy_of(torch, a.reshape(-1)) for a in send_np]
-    for cold in (True, False):
+    for cold in colds:
         nsets = max(1, min(pool.nbytes // (set_bytes + 16 * ALIGN), math.ceil(COLD_SPAN / set_bytes) + 1)) \
             if cold else 1
         pool.off = 0
@@ -578,7 +683,13 @@ def a2a_case(nuna, torch, pool, args, emit, T_tokens=None):
                   for p in ("linear", "xcd")}
         t = time_graphs(torch, graphs, calls, args.reps, args.warmup)
         res = {p: stats(t[p]) for p in t}
+        li = {}
+        for p in ("linear", "xcd"):
+            nuna.all_to_all(sets[0][0], sets[0][1], lay, placement=p)
+            li[p] = nuna.last_launch()
+        torch.cuda.synchronize()
         emit({"workload": "a2a_moe_dispatch_bf16_p8" + ("" if T_tokens is None else f"_T{T}"), "P": P,
+              "same_map": same_map(li["linear"], li["xcd"]), "xcd_map": li["xcd"]["map"],
               "tokens_per_rank": T, "hidden": H,
               "rows_received": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
               "calls_per_graph": calls, "parity": bool(ok),
@@ -680,8 +791,10 @@ def combine_case(nuna, torch, pool, args, emit, T_tokens=None):
                 sets.append((y, out))
             calls = max(nsets, calls_for(set_bytes))
             ok = True
+            li = {}
             for p in ("linear", "xcd"):
                 nuna.all_to_all_combine(sets[0][0], sets[0][1], lay, placement=p, weights=wt)
+                li[p] = nuna.last_launch()
                 torch.cuda.synchronize()
                 for d in range(P):
                     g = sets[0][1][d].cpu().view(torch.int16).numpy().view(np.uint16)
@@ -693,7 +806,8 @@ def combine_case(nuna, torch, pool, args, emit, T_tokens=None):
             res = {p: stats(t[p]) for p in t}
             emit({"workload": name, "P": P, "tokens_per_rank": T, "hidden": H,
                   "result_rows": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
-                  "calls_per_graph": calls, "parity": bool(ok),
+                  "calls_per_graph": calls, "parity": bool(ok), "same_map": same_map(li["linear"], li["xcd"]),
+                  "xcd_kernels": li["xcd"]["kernels"], "xcd_map": li["xcd"]["map"],
                   **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
                   **{f"{p}_gbps": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9, 1) for p in res},
                   **{f"{p}_frac_hbm": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
@@ -914,38 +1028,42 @@ def affinity(nuna, torch, pool):
 PROFILE_COPY_BYTES = 64 << 20
 
 
+PROFILE_PHASE_TOKENS = 256  # the two-kernel two-shot traced per phase (4 MiB per rank)
+
+
 def profile_run(nuna, torch, pool, n, place="xcd"):
-    """Short eager run for rocprofv3 counter passes: the dominant kernel on cold buffers, the
-    reference copy of PROFILE_COPY_BYTES (the calibration kernel for the traffic counters), then the
-    kernels whose map the placement changes (split all-reduce, MoE dispatch; the combine too) in
-    placement `place`."""
+    """Short eager run for rocprofv3 counter passes, in dispatch order: the dominant kernel (fused
+    two-shot, [4096, 8192] bf16 per rank, XCD) on cold buffers; the reference copy of
+    PROFILE_COPY_BYTES (the calibration kernel for the traffic counters); the two-kernel two-shot at
+    [256, 8192] (its reduce-scatter and all-gather phases); then the kernels whose map the placement
+    changes (split all-reduce at decode T=64, MoE dispatch; the combine too) in placement `place`."""
     from paper_2608_00867_amd import workloads as wl
-    x = wl.ar_bf16_decode(64)
-    pool.off = 0
-    sets = ar_sets(torch, pool, x, min(n, pool.nbytes // ar_footprint(8, x[0].size, 2)))
-    torch.cuda.synchronize()
-    for i in range(n):
-        ins, outs = sets[i % len(sets)]
-        nuna.allreduce(ins, outs, algo="auto", placement="xcd")
-    torch.cuda.synchronize()
+
+    def run(x, algo, plc):
+        pool.off = 0
+        sets = ar_sets(torch, pool, x, max(1, min(n, pool.nbytes // ar_footprint(8, x[0].size, 2))))
+        torch.cuda.synchronize()
+        for i in range(n):
+            ins, outs = sets[i % len(sets)]
+            nuna.allreduce(ins, outs, algo=algo, placement=plc)
+        torch.cuda.synchronize()
+        del sets
+
+    xd = wl.ar_bf16_prefill(4096)
+    run(xd, "two_shot", "xcd")
+    del xd
     pool.off = 0
     a = pool.take(PROFILE_COPY_BYTES)
     b = pool.take(PROFILE_COPY_BYTES)
     for _ in range(n):
         nuna.copy(b, a)
     torch.cuda.synchronize()
+    run(wl.ar_bf16_prefill(PROFILE_PHASE_TOKENS), "two_shot_two_kernels", "xcd")
     # The split all-reduce: 8 destination groups per chunk, the placement under study.
-    pool.off = 0
-    sets = ar_sets(torch, pool, x, min(n, pool.nbytes // ar_footprint(8, x[0].size, 2)))
-    torch.cuda.synchronize()
-    for i in range(n):
-        ins, outs = sets[i % len(sets)]
-        nuna.allreduce(ins, outs, algo="one_shot_split", placement=place)
-    torch.cuda.synchronize()
+    run(wl.ar_bf16_decode(64), "one_shot_split", place)
     moe = profile_moe(nuna, torch, pool, n, place)
-    print(json.dumps({"profile": {"place": place, "dominant_launches": n,
-                                  "dominant_alg_bytes": 2 * 8 * x[0].size * 2, "copy_launches": n,
-                                  "copy_bytes": PROFILE_COPY_BYTES, **moe}}), flush=True)
+    print(json.dumps({"profile": {"place": place, "dominant_launches": n, "dominant_alg_bytes": DOMINANT_ALG_BYTES,
+                                  "copy_launches": n, "copy_bytes": PROFILE_COPY_BYTES, **moe}}), flush=True)
 
 
 def moe_alg_bytes():
@@ -1028,24 +1146,96 @@ def _short(name):
     return name.split("(")[0] if "(" in name else name
 
 
-def summarize_trace(path):
+def _trace_rows(path):
     import csv
+    rows = []
+    for r in csv.DictReader(open(path)):
+        rows.append({"name": _short(r["Kernel_Name"]), "start": int(r["Start_Timestamp"]),
+                     "end": int(r["End_Timestamp"]), "grid": int(r["Grid_Size_X"]),
+                     "grid_y": int(r.get("Grid_Size_Y") or 1), "wg": int(r["Workgroup_Size_X"]),
+                     "queue": r.get("Queue_Id", "")})
+    rows.sort(key=lambda r: r["start"])
+    return rows
+
+
+def summarize_trace(path, kernel_json=None):
+    """Per (kernel, grid) durations of a rocprofv3 --kernel-trace CSV, as markdown.  With kernel_json,
+    also write the dominant kernel's average (the fused two-shot kernel with the most total time: the
+    64 MiB-per-rank launch of the default bench) for the bench line's cross-check."""
     import collections
     by = collections.defaultdict(list)
-    for r in csv.DictReader(open(path)):
-        dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-        by[(_short(r["Kernel_Name"]), int(r["Grid_Size_X"]), int(r["Workgroup_Size_X"]))].append(dur)
+    for r in _trace_rows(path):
+        by[(r["name"], r["grid"] * r["grid_y"], r["wg"])].append((r["end"] - r["start"]) / 1e3)
     print("| kernel | grid (threads) | workgroup | dispatches | avg µs | median µs | p10 µs | p90 µs |")
     print("|---|---|---|---|---|---|---|---|")
     for (k, g, w), v in sorted(by.items(), key=lambda kv: -sum(kv[1])):
         v = sorted(v)
         print(f"| `{k}` | {g} | {w} | {len(v)} | {statistics.mean(v):.3f} | {statistics.median(v):.3f} | "
               f"{v[len(v) // 10]:.3f} | {v[(9 * len(v)) // 10]:.3f} |")
+    if kernel_json:
+        cands = [(sum(v), k, v) for k, v in by.items() if k[0].startswith("k_two_shot")]
+        _, (k, g, w), v = max(cands)
+        rec = {"kernel": k, "grid_threads": g, "workgroup": w, "dispatches": len(v),
+               "avg_us": round(statistics.mean(v), 3), "median_us": round(statistics.median(v), 3),
+               "source": os.path.relpath(kernel_json, ROOT).replace(".json", ".md"),
+               "kernel_source_sha256": kernel_source_sha()}
+        json.dump(rec, open(kernel_json, "w"), indent=1)
+        print(f"\nDominant kernel: `{k}`, grid {g} threads, {len(v)} dispatches, average "
+              f"{rec['avg_us']:.3f} µs (written to {os.path.basename(kernel_json)}).")
+
+
+def _template_args(name):
+    inner = name[name.index("<") + 1:name.rindex(">")]
+    return [a.strip() for a in inner.split(",")]
+
+
+def summarize_phases(path):
+    """The two-kernel two-shot all-reduce from a kernel trace: each reduce-scatter launch that keeps
+    its shards in cache (`k_reduce_scatter_direct<P, dtype, VPT, true>`) followed on its queue by an
+    all-gather reading them (`k_all_gather_direct<P, VPT, true, WT>`).  Per message size: the two
+    kernels' durations, the gap from the end of the first to the start of the second, and each
+    phase's rate against its own bytes (reduce-scatter (P + 1) * n * s, all-gather P * n * s with the
+    in-place shard skipped) and the call's against the collective's 2 * P * n * s."""
+    import collections
+    rows = _trace_rows(path)
+    by_q = collections.defaultdict(list)
+    for r in rows:
+        by_q[r["queue"]].append(r)
+    pairs = collections.defaultdict(list)
+    for q in by_q.values():
+        for a, b in zip(q, q[1:]):
+            if not (a["name"].startswith("k_reduce_scatter_direct") and a["name"].endswith("true>")):
+                continue
+            if not b["name"].startswith("k_all_gather_direct") or _template_args(b["name"])[2] != "true":
+                continue
+            ta = _template_args(a["name"])
+            P, es, vpt = int(ta[0]), (2 if ta[1] == "1" else 4), int(ta[2])
+            shard = a["grid"] * vpt * 16  # bytes per shard (whole chunks at these sizes)
+            pairs[(P, es, shard)].append(((a["end"] - a["start"]) / 1e3, (b["start"] - a["end"]) / 1e3,
+                                          (b["end"] - b["start"]) / 1e3, a["name"], b["name"]))
+    print("| P | bytes per rank | pairs | reduce-scatter µs | % of peak | gap µs | all-gather µs | % of peak | "
+          "call µs (first start to last end) | % of peak (2·P·n·s) |")
+    print("|---|---|---|---|---|---|---|---|---|---|")
+    for (P, es, shard), v in sorted(pairs.items()):
+        nb = P * shard
+        rs = statistics.mean(x[0] for x in v)
+        gap = statistics.mean(x[1] for x in v)
+        ag = statistics.mean(x[2] for x in v)
+        call = rs + gap + ag
+        pct = lambda b, us: 100 * b / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS  # noqa: E731
+        print(f"| {P} | {nb >> 20} MiB | {len(v)} | {rs:.3f} | {pct((P + 1) * nb, rs):.1f} | {gap:.3f} | "
+              f"{ag:.3f} | {pct(P * nb, ag):.1f} | {call:.3f} | {pct(2 * P * nb, call):.1f} |")
+    kinds = sorted({(x[3], x[4]) for v in pairs.values() for x in v})
+    print("\nKernels: " + "; ".join(f"`{a}` then `{b}`" for a, b in kinds))
+
+
+DOMINANT_ALG_BYTES = 2 * 8 * 4096 * 8192 * 2  # fused two-shot, P=8, [4096, 8192] bf16 per rank
 
 
 def summarize_traffic(fetch_csv, write_csv):
     """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the --profile run.  The reference copy moves
-    PROFILE_COPY_BYTES each way; its readings give the scale factor of each counter."""
+    PROFILE_COPY_BYTES each way; its readings give the scale factor of each counter.  The dominant
+    kernel is the first one dispatched."""
     import csv
     import collections
 
@@ -1056,15 +1246,15 @@ def summarize_traffic(fetch_csv, write_csv):
         return by
 
     f, w = read(fetch_csv), read(write_csv)
-    dom = [k for k in f if k[0].startswith("k_allreduce")][:1]  # dispatched first: the dominant kernel
+    dom = list(f)[:1]
     cpy = [k for k in f if k[0].startswith("k_copy")]
-    assert len(dom) == 1 and len(cpy) == 1, (dom, cpy)
+    assert len(dom) == 1 and dom[0][0].startswith("k_two_shot") and len(cpy) == 1, (dom, cpy)
     kib = PROFILE_COPY_BYTES / 1024
     ff = kib / statistics.median(f[cpy[0]])
     wf = kib / statistics.median(w[cpy[0]])
     fetch = statistics.median(f[dom[0]]) * ff * 1024
     write = statistics.median(w[dom[0]]) * wf * 1024
-    alg = 2 * 8 * 64 * 8192 * 2
+    alg = DOMINANT_ALG_BYTES
     rec = {"kernel": dom[0][0], "grid": dom[0][1], "fetch_bytes": round(fetch), "write_bytes": round(write),
            "traffic_bytes": round(fetch + write), "alg_bytes": alg, "fetch_scale": round(ff, 4),
            "write_scale": round(wf, 4), "kernel_source_sha256": kernel_source_sha(),
@@ -1080,21 +1270,33 @@ def summarize_traffic(fetch_csv, write_csv):
     print(f"| WRITE_SIZE | {statistics.median(w[cpy[0]]):.1f} | {wf:.4f} | {statistics.median(w[dom[0]]):.1f} | "
           f"{write:.0f} |")
     print(f"\nTraffic per launch {fetch + write:.0f} B vs algorithmic {alg} B: ratio {(fetch + write) / alg:.4f}.")
-    others = [k for k in f if k not in dom and (k[0].startswith("k_allreduce") or k[0].startswith("k_all_to_all")
-                                                 or k[0].startswith("k_combine"))]
+    others = [k for k in f if k not in dom and not k[0].startswith("k_copy")]
     if others:
         malg = moe_alg_bytes()
-        print("\nOther kernels of the same runs: the split all-reduce (same message, 8 destination groups per "
-              "chunk) and the MoE kernels (8 ranks, 512 tokens x 7168 bf16 per rank, top-8 of 256 experts; "
-              f"algorithmic bytes per launch {malg}):\n")
+        nb = PROFILE_PHASE_TOKENS * 8192 * 2  # bytes per rank of the traced two-kernel two-shot
+        dec = 2 * 8 * 64 * 8192 * 2           # split all-reduce, decode T=64
+
+        def alg_of(name):
+            if name.startswith("k_reduce_scatter"):
+                return 9 * nb, "(P + 1) n s"
+            if name.startswith("k_all_gather"):
+                return 8 * nb, "P n s (in-place shard skipped: (P - 1) n s written, n s read)"
+            if name.startswith("k_allreduce"):
+                return dec, "2 P n s"
+            return malg, "rows read + rows written"
+        print("\nOther kernels of the same runs: the two-kernel two-shot at [256, 8192] bf16 per rank (its "
+              "reduce-scatter and all-gather phases), the split all-reduce (decode T=64, 8 destination groups "
+              "per chunk) and the MoE kernels (8 ranks, 512 tokens x 7168 bf16 per rank, top-8 of 256 "
+              f"experts):\n")
         print("| kernel | grid (threads) | FETCH_SIZE (KiB) | WRITE_SIZE (KiB) | scaled fetch B | scaled write B | "
-              "traffic / algorithmic |")
-        print("|---|---|---|---|---|---|---|")
+              "algorithmic B | traffic / algorithmic |")
+        print("|---|---|---|---|---|---|---|---|")
         for k in others:
-            a = alg if k[0].startswith("k_allreduce") else malg
+            a, rule = alg_of(k[0])
             fk, wk = statistics.median(f[k]), statistics.median(w.get(k, [0.0]))
             fb, wb = fk * ff * 1024, wk * wf * 1024
-            print(f"| `{k[0]}` | {k[1]} | {fk:.1f} | {wk:.1f} | {fb:.0f} | {wb:.0f} | {(fb + wb) / a:.4f} |")
+            print(f"| `{k[0]}` | {k[1]} | {fk:.1f} | {wk:.1f} | {fb:.0f} | {wb:.0f} | {a} ({rule}) | "
+                  f"{(fb + wb) / a:.4f} |")
 
 
 def summarize_counters(path):
@@ -1210,7 +1412,10 @@ def measured_traffic():
 def main():
     args = parse()
     if args.summarize_trace:
-        summarize_trace(args.summarize_trace)
+        summarize_trace(args.summarize_trace, args.kernel_json)
+        return
+    if args.summarize_phases:
+        summarize_phases(args.summarize_phases)
         return
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic)
@@ -1238,6 +1443,9 @@ def main():
     from paper_2608_00867_amd import nuna
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     nuna.init()
+    for kv in args.set:
+        name, _, val = kv.partition("=")
+        nuna.set_tunable(name, int(val))
     pool = Pool(torch, POOL_BYTES_MAIN)
 
     if args.full:
@@ -1253,13 +1461,16 @@ def main():
         interference(nuna, torch, args)
         return
 
+    from paper_2608_00867_amd import workloads as wl
+    xs = [wl.ar_bf16_prefill(T) for T in wl.PREFILL_TOKENS]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    step_bytes, ksteps, main_res = decode_steps_timed(nuna, torch, pool, args)
+    step_bytes, ksteps, per_graph, main_res = steps_timed(nuna, torch, pool, args, xs, "two_shot")
     t_timed = time.perf_counter() - t0
-    sweep = decode_sweep(nuna, torch, pool, args)
+    sweep = prefill_sweep(nuna, torch, pool, args, xs)
     roof = roofline_dominant(sweep)
     x = main_res["xcd"]
+    step_launch = [r for r in sweep if r["algo"] == "two_shot"]
     line = {
         "metric": METRIC,
         "value": round(x["gbps"], 2),
@@ -1271,29 +1482,31 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "allreduce_bf16_p8_decode", "ranks": 8, "tokens": list(wl_tokens()),
-                   "hidden": 8192, "data_dtype": "bf16", "accumulate": "fp32", "placement": "xcd",
-                   "algo": "auto", "cache": "cold (steps rotate over the regions of a 1.5 GiB pool)",
-                   "timing": f"HIP graphs of {steps_per_graph(args.steps, step_bytes)} steps replayed; HIP events"},
+        "config": {"workload": "allreduce_two_shot_bf16_p8_prefill", "ranks": 8, "tokens": list(wl.PREFILL_TOKENS),
+                   "hidden": 8192, "bytes_per_rank": [T * 8192 * 2 for T in wl.PREFILL_TOKENS], "data_dtype": "bf16",
+                   "accumulate": "fp32", "placement": "xcd", "algo": "two_shot",
+                   "cache": "cold (each call's inputs evicted from L2 and the Infinity Cache by the other calls)",
+                   "timing": f"HIP graphs of {per_graph} steps replayed, LINEAR and XCD interleaved; HIP events"},
         "step_alg_bytes": step_bytes,
+        "step_alg_bytes_rule": "sum over T of 2 * P * T * 8192 * 2 B (P reads and P writes per element)",
         "linear": {"value": round(main_res["linear"]["gbps"], 2),
                    "ms_per_step": round(main_res["linear"]["ms_per_step"], 6)},
         "linear_over_xcd_time": round(main_res["linear"]["ms_per_step"] / x["ms_per_step"], 4),
+        "step_same_map": all(r["same_map"] for r in step_launch),
         "sweep": sweep,
         "roofline": roof,
-        "parity": all(s["parity"] for s in sweep),
+        "parity": all(r["parity"] for r in sweep),
         "timed_region_s": round(t_timed, 3),
     }
+    dec = decode_sweep(nuna, torch, pool, args)
+    line["decode_sweep"] = dec
+    line["moe_dispatch"] = moe_dispatch_summary(nuna, torch, pool, args)
+    line["parity"] = line["parity"] and all(r["parity"] for r in dec) and bool(line["moe_dispatch"]["parity"])
     if not args.no_cpu:
-        line["cpu_baseline"] = cpu_baseline(args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(args.cpu_seconds, xs)
     print(json.dumps(line), flush=True)
-
-
-def wl_tokens():
-    from paper_2608_00867_amd import workloads as wl
-    return wl.DECODE_TOKENS
 
 
 if __name__ == "__main__":

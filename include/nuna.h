@@ -145,6 +145,28 @@ typedef struct {
  * not run on it (or info is NULL). */
 nuna_status_t nuna_get_device_info(nuna_device_info_t* info);
 
+/* Launches of the calling thread's last collective call (nuna_allreduce,
+ * nuna_reduce_scatter, nuna_all_gather, nuna_all_to_all,
+ * nuna_all_to_all_combine): which kernels ran and under which map.  A call
+ * that launched nothing (count 0, an argument error) leaves launches == 0.
+ * Lets a caller or a benchmark see whether the two placement modes ran the
+ * same launches. */
+#define NUNA_MAP_LINEAR 0     /* workgroup b runs work item b (grid-stride) */
+#define NUNA_MAP_XCD_GROUPS 1 /* logical groups of work items sharing a chunk, one XCD each */
+#define NUNA_MAP_XCD_PAGES 2  /* the chunks of each 4 KiB page on one XCD */
+#define NUNA_MAP_XCD_LISTS 3  /* per-XCD work lists from the placement planner (all-to-all) */
+typedef struct {
+    char kernels[96];           /* kernel names, '+'-separated, in launch order */
+    int32_t launches;           /* kernels launched */
+    int32_t map;                /* NUNA_MAP_*: a non-linear map if any launch ran one */
+    int64_t group_size;         /* work items per logical group of that map (0: variable) */
+    int64_t grid;               /* workgroups of the last launch */
+    int32_t threads;            /* workgroup size of the last launch */
+    int32_t vectors_per_thread; /* 16-byte vectors per thread per work item of the last launch */
+} nuna_launch_info_t;
+
+nuna_status_t nuna_last_launch(nuna_launch_info_t* info);
+
 /* Host-only check behind nuna_init (no HIP call): xcc[b] is the XCC
  * workgroup b of a G-workgroup launch ran on (HOST int32 array, G >= 64).
  * NUNA_OK if cu_count is 256 and xcc[b] == b mod 8 for every b, else

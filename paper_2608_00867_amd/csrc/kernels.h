@@ -39,6 +39,14 @@ int max_workgroups();
 // (nuna_set_max_workgroups or NUNA_MAX_GRID), otherwise `dflt`.
 int64_t grid_limit(int64_t dflt);
 
+// Record of the kernel launches of the calling thread's current collective
+// call (read back through nuna_last_launch): the API starts a record before
+// its launches, every launcher appends to it.  map: the workgroup -> work
+// item map the launch ran (placement.h); group_size: work items per logical
+// group of that map.
+enum MapKind { kMapLinear = 0, kMapXcdGroups = 1, kMapXcdPages = 2, kMapXcdLists = 3 };
+void note_launch(const char* kernel, int map, int64_t group_size, int64_t grid, int threads, int vpt);
+
 // One-shot all-reduce.  `dest_groups` > 1 selects the split variant: a work
 // item is (chunk, destination group) and writes P/dest_groups outputs.
 hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size_t count, int dtype,

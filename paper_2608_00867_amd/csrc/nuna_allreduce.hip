@@ -583,6 +583,7 @@ hipError_t launch_allreduce_lpr(const void* const* in, void* const* out, int P, 
     const int64_t groups = (s.nvec + s.V - 1) / s.V;
     const Place pl = make_place_uniform(mode, groups > 0 ? groups : 1, 1);
     const int64_t G = cap_grid(place_grid(pl));
+    note_launch("k_allreduce_lpr", kMapLinear, 1, G, kWG, 1);
     if (dtype == kDtF32)
         launch_lpr_p<kDtF32>(in, out, P, s, pl, G, stream);
     else
@@ -628,6 +629,11 @@ hipError_t launch_allreduce_tile(const void* const* in, void* const* out, int P,
     const int64_t G = cap_grid(place_grid(pl));
     // One item per workgroup, no placement state: the direct kernel, page-grouped in XCD mode.
     const DirectMap m = direct_map(mode, groups > 0 ? groups : 1, int64_t(V) * 16);
+    if (m.direct)
+        note_launch("k_allreduce_tile_direct", m.gshift > 0 ? kMapXcdPages : kMapLinear, int64_t(1) << m.gshift, m.grid,
+                    kWG, V);
+    else
+        note_launch("k_allreduce_tile", kMapLinear, 1, G, kWG, V);
     if (dtype == kDtF32) {
         if (V == 16) launch_tile_p<kDtF32, 16>(in, out, P, s, pl, G, m, stream);
         else if (V == 32) launch_tile_p<kDtF32, 32>(in, out, P, s, pl, G, m, stream);
@@ -686,6 +692,8 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
     // One item per workgroup: the direct kernel (page-grouped in XCD mode).
     const DirectMap m = direct_map(mode, groups > 0 ? groups : 1, cv * 16);
     if (gsize == 1 && m.direct && direct_ranks(P, vpt)) {
+        note_launch("k_allreduce_direct", m.gshift > 0 ? kMapXcdPages : kMapLinear, int64_t(1) << m.gshift, m.grid, nt,
+                    vpt);
         if (dtype == kDtF32) {
             if (vpt == 8) launch_ar_direct_p<kDtF32, 8>(in, out, P, s, m, nt, wt, stream);
             else if (vpt == 4) launch_ar_direct_p<kDtF32, 4>(in, out, P, s, m, nt, wt, stream);
@@ -700,6 +708,8 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
         return hipGetLastError();
     }
     // The kernel's vectors per thread must be the VPT the chunks were sized with.
+    note_launch("k_allreduce", pl.mode == kPlaceXcd && !linear_map(pl, G) ? kMapXcdGroups : kMapLinear, pl.gsize, G,
+                nt, vpt);
     if (dtype == kDtF32) {
         if (vpt == 8) launch_ar_p<kDtF32, 8>(in, out, P, s, pl, G, nt, wt, stream);
         else if (vpt == 4) launch_ar_p<kDtF32, 4>(in, out, P, s, pl, G, nt, wt, stream);
@@ -740,6 +750,7 @@ hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P,
     const bool direct = G == items && items <= direct_max_grid();
     const int wtf = tuning().write_through;
     const bool wt = P == 8 && (wtf == 2 || (wtf == 0 && vpt == 8 && bytes >= (size_t(16) << 20)));
+    note_launch(direct ? "k_two_shot_direct" : "k_two_shot", kMapLinear, 1, direct ? items : G, nt, vpt);
     if (dtype == kDtF32) {
         if (vpt == 8) launch_two_shot_p<kDtF32, 8>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
         else if (vpt == 4) launch_two_shot_p<kDtF32, 4>(in, out, P, mv, wcs, G, direct, nt, wt, stream);

@@ -140,6 +140,12 @@ nuna_status_t check_common(int P, int dtype, int place) {
 nuna::Tuning g_tuning;
 std::once_flag g_tuning_once;
 
+// Launches of the calling thread's last collective call (nuna_last_launch).
+thread_local nuna_launch_info_t t_launch;
+
+// Start the record of a call's launches (after its argument checks).
+void begin_launches() { std::memset(&t_launch, 0, sizeof t_launch); }
+
 
 }  // namespace
 
@@ -197,6 +203,22 @@ const TunableDef* find_tunable(const char* name) {
 }  // namespace
 
 namespace nuna {
+void note_launch(const char* kernel, int map, int64_t group_size, int64_t grid, int threads, int vpt) {
+    nuna_launch_info_t& r = t_launch;
+    const size_t used = std::strlen(r.kernels);
+    std::snprintf(r.kernels + used, sizeof r.kernels - used, "%s%s", used ? "+" : "", kernel);
+    ++r.launches;
+    if (map != kMapLinear) {
+        r.map = map;
+        r.group_size = group_size;
+    } else if (r.launches == 1) {
+        r.group_size = group_size;
+    }
+    r.grid = grid;
+    r.threads = threads;
+    r.vectors_per_thread = vpt;
+}
+
 const Tuning& tuning() {
     std::call_once(g_tuning_once, [] {
         for (const TunableDef& d : kTunables) {
@@ -351,6 +373,12 @@ nuna_status_t nuna_init(void) try {
     return host_exception();
 }
 
+nuna_status_t nuna_last_launch(nuna_launch_info_t* info) {
+    if (!info) return fail(NUNA_ERR_INVALID_ARG, "info is NULL");
+    *info = t_launch;
+    return ok();
+}
+
 nuna_status_t nuna_get_device_info(nuna_device_info_t* info) {
     if (!info) return fail(NUNA_ERR_INVALID_ARG, "info is NULL");
     std::memset(info, 0, sizeof *info);
@@ -369,6 +397,7 @@ nuna_status_t nuna_get_device_info(nuna_device_info_t* info) {
 
 nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, size_t count, nuna_dtype_t dtype,
                              nuna_algo_t algo, nuna_placement_t place, hipStream_t stream) try {
+    begin_launches();
     nuna_status_t st = check_common(P, dtype, place);
     if (st) return st;
     if (algo < NUNA_ALGO_AUTO || algo > NUNA_ALGO_TWO_SHOT_TWO_KERNELS)
@@ -433,6 +462,7 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
 
 nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P, size_t recvcount,
                                   nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream) try {
+    begin_launches();
     nuna_status_t st = check_common(P, dtype, place);
     if (st) return st;
     if ((st = check_ptr_array(in, P, "in"))) return st;
@@ -460,6 +490,7 @@ nuna_status_t nuna_reduce_scatter(const void* const* in, void* const* out, int P
 
 nuna_status_t nuna_all_gather(const void* const* in, void* const* out, int P, size_t sendcount, nuna_dtype_t dtype,
                               nuna_placement_t place, hipStream_t stream) try {
+    begin_launches();
     nuna_status_t st = check_common(P, dtype, place);
     if (st) return st;
     if ((st = check_ptr_array(in, P, "in"))) return st;
@@ -703,6 +734,7 @@ void nuna_a2a_layout_destroy(nuna_a2a_layout_t* L) {
 nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const nuna_a2a_layout_t* L,
                               size_t row_elems, size_t recv_capacity_rows, nuna_dtype_t dtype,
                               nuna_placement_t place, hipStream_t stream) try {
+    begin_launches();
     if (!L) return fail(NUNA_ERR_INVALID_ARG, "layout is NULL");
     const int P = L->P;
     nuna_status_t st = check_common(P, dtype, place);
@@ -740,6 +772,7 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
 nuna_status_t nuna_all_to_all_combine(const void* const* y, void* const* out, const nuna_a2a_layout_t* L,
                                       const float* weights, size_t row_elems, size_t y_capacity_rows,
                                       nuna_dtype_t dtype, nuna_placement_t place, hipStream_t stream) try {
+    begin_launches();
     if (!L) return fail(NUNA_ERR_INVALID_ARG, "layout is NULL");
     const int P = L->P;
     nuna_status_t st = check_common(P, dtype, place);

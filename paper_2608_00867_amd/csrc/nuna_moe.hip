@@ -329,6 +329,9 @@ hipError_t launch_all_to_all(const void* const* send, void* const* recv, int P, 
     // workgroups (55.2 against 56.2 us, back-to-back cold calls).
     const int64_t G = want < grid_limit(int64_t(1) << 20) ? (want > 0 ? want : 1) : grid_limit(int64_t(1) << 20);
     const int4* d = static_cast<const int4*>(desc);
+    // XCD mode runs the per-XCD lists of the planner (each token row's copies on one XCD).
+    note_launch(vec ? "k_all_to_all" : "k_all_to_all_elem", mode == kPlaceXcd ? kMapXcdLists : kMapLinear, 0, G, kWG,
+                vec ? 4 : 0);
     if (vec) {
         if (P <= 8) {
             Ptrs<8> p = make_ptrs<8>(send, recv, P, P);
@@ -388,6 +391,7 @@ hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, 
         // the items in the linear order.
         const int64_t items = ntok * s.chunks;
         const int64_t G = cap_grid(items);
+        note_launch(rc && P <= kCombRecRanks ? "k_combine_rec" : "k_combine", kMapLinear, 1, G, nt, vpt);
         if (P <= kCombRecRanks) {
             if (dtype == kDtF32)
                 launch_combine_w<kCombRecRanks, kDtF32>(y, out, P, o, e, rc, weights, s, items, G, nt, vpt, stream);
@@ -402,6 +406,7 @@ hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, 
     } else {
         const Place pl = make_place_uniform(mode, ntok, 1);
         const int64_t G = cap_grid(ntok);
+        note_launch("k_combine_elem", kMapLinear, 1, G, kWG, 0);
         Ptrs<64> p = make_ptrs<64>(y, out, P, P);
         const int64_t esz = static_cast<int64_t>(dtype_size(dtype));
         const int64_t rowelems = static_cast<int64_t>(row_bytes) / esz;

@@ -284,6 +284,7 @@ hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P,
         Ptrs<64> p = make_ptrs<64>(in, out, P, P);
         const int64_t total = static_cast<int64_t>(m) * P;
         const int64_t G = cap_grid((total + kWG - 1) / kWG);
+        note_launch("k_reduce_scatter_elem", kMapLinear, 1, G, kWG, 0);
         if (dtype == kDtF32)
             hipLaunchKernelGGL((k_reduce_scatter_elem<kDtF32>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream,
                                p, P, static_cast<int64_t>(m));
@@ -302,8 +303,12 @@ hipError_t launch_reduce_scatter(const void* const* in, void* const* out, int P,
     s.wcs = (s.mv + cv - 1) / cv;
     const Place pl = make_place_uniform(mode, s.wcs * P, 1);
     const int64_t G = cap_grid(place_grid(pl));
-    if (G == s.wcs * P && G <= direct_max_grid() && (P == 2 || P == 4 || P == 8 || P == 16))
+    // Every work item is its own group: both placements run the linear map.
+    if (G == s.wcs * P && G <= direct_max_grid() && (P == 2 || P == 4 || P == 8 || P == 16)) {
+        note_launch("k_reduce_scatter_direct", kMapLinear, 1, G, nt, vpt);
         return launch_rs_direct(in, out, P, s, dtype, vpt, nt, keep_output, stream);
+    }
+    note_launch("k_reduce_scatter", kMapLinear, 1, G, nt, vpt);
     if (dtype == kDtF32) {
         if (keep_output) launch_rs_p<kDtF32, 1, true>(in, out, P, s, pl, G, nt, stream);
         else launch_rs_p<kDtF32, 1, false>(in, out, P, s, pl, G, nt, stream);
@@ -347,6 +352,7 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
         Ptrs<64> p = make_ptrs<64>(in, out, P, P);
         const int64_t total = static_cast<int64_t>(m) * P;
         const int64_t G = cap_grid((total + kWG - 1) / kWG);
+        note_launch("k_all_gather_elem", kMapLinear, 1, G, kWG, 0);
         if (es == 4)
             hipLaunchKernelGGL((k_all_gather_elem<4>), dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P,
                                static_cast<int64_t>(m));
@@ -393,6 +399,7 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     const bool direct = gsize == 1 && (P == 8 ? items <= grid_limit(kAgDirectMaxGrid8)
                                               : (P == 2 || P == 4) && G == items && G <= direct_max_grid());
     if (direct) {
+        note_launch("k_all_gather_direct", kMapLinear, 1, items, nt, vpt);
         const dim3 g(static_cast<unsigned>(s.wcs), static_cast<unsigned>(P)), b(nt);
         switch (P) {
             case 2: launch_ag_direct_p<2>(in, out, s, vpt, src_cached, false, g, b, stream); break;
@@ -401,6 +408,8 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
         }
         return hipGetLastError();
     }
+    note_launch("k_all_gather", pl.mode == kPlaceXcd && !linear_map(pl, G) ? kMapXcdGroups : kMapLinear, pl.gsize, G,
+                nt, vpt);
     if (P <= 8) {
         Ptrs<8> p = make_ptrs<8>(in, out, P, P);
         const dim3 g(static_cast<unsigned>(G)), b(nt);

@@ -46,6 +46,16 @@ class DeviceInfo(ctypes.Structure):
                 ("map_verified", ctypes.c_int32)]
 
 
+class LaunchInfo(ctypes.Structure):
+    """Mirror of nuna_launch_info_t."""
+    _fields_ = [("kernels", ctypes.c_char * 96), ("launches", ctypes.c_int32), ("map", ctypes.c_int32),
+                ("group_size", ctypes.c_int64), ("grid", ctypes.c_int64), ("threads", ctypes.c_int32),
+                ("vectors_per_thread", ctypes.c_int32)]
+
+
+MAP_NAMES = {0: "linear", 1: "xcd_groups", 2: "xcd_pages", 3: "xcd_lists"}
+
+
 class NapTopology(ctypes.Structure):
     """Mirror of nuna_nap_topology_t."""
     _fields_ = [("num_domains", ctypes.c_int32), ("cus_per_domain", ctypes.c_int32),
@@ -57,6 +67,7 @@ class NapTopology(ctypes.Structure):
 SIGNATURES = {
     "nuna_init": ([], ctypes.c_int),
     "nuna_get_device_info": ([ctypes.POINTER(DeviceInfo)], ctypes.c_int),
+    "nuna_last_launch": ([ctypes.POINTER(LaunchInfo)], ctypes.c_int),
     "nuna_check_dispatch_map": ([_i32p, ctypes.c_int64, ctypes.c_int32], ctypes.c_int),
     "nuna_last_error_string": ([], ctypes.c_char_p),
     "nuna_version": ([], ctypes.c_int),
@@ -268,6 +279,16 @@ def device_info():
     info = DeviceInfo()
     _check(lib().nuna_get_device_info(ctypes.byref(info)))
     return {k: int(getattr(info, k)) for k, _ in DeviceInfo._fields_}
+
+
+def last_launch():
+    """Kernels and map of the calling thread's last collective call (dict)."""
+    info = LaunchInfo()
+    _check(lib().nuna_last_launch(ctypes.byref(info)))
+    d = {k: getattr(info, k) for k, _ in LaunchInfo._fields_}
+    d["kernels"] = info.kernels.decode()
+    d["map"] = MAP_NAMES.get(int(info.map), int(info.map))
+    return d
 
 
 def check_dispatch_map_raw(xcc, cu_count):
