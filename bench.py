@@ -1235,7 +1235,7 @@ DOMINANT_ALG_BYTES = 2 * 8 * 4096 * 8192 * 2  # fused two-shot, P=8, [4096, 8192
 def summarize_traffic(fetch_csv, write_csv):
     """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the --profile run.  The reference copy moves
     PROFILE_COPY_BYTES each way; its readings give the scale factor of each counter.  The dominant
-    kernel is the first one dispatched."""
+    kernel is the first collective kernel dispatched (after the dispatch probe of nuna_init)."""
     import csv
     import collections
 
@@ -1246,7 +1246,7 @@ def summarize_traffic(fetch_csv, write_csv):
         return by
 
     f, w = read(fetch_csv), read(write_csv)
-    dom = list(f)[:1]
+    dom = [k for k in f if k[0].startswith("k_two_shot")][:1]  # dispatched first of the collectives
     cpy = [k for k in f if k[0].startswith("k_copy")]
     assert len(dom) == 1 and dom[0][0].startswith("k_two_shot") and len(cpy) == 1, (dom, cpy)
     kib = PROFILE_COPY_BYTES / 1024
@@ -1270,7 +1270,7 @@ def summarize_traffic(fetch_csv, write_csv):
     print(f"| WRITE_SIZE | {statistics.median(w[cpy[0]]):.1f} | {wf:.4f} | {statistics.median(w[dom[0]]):.1f} | "
           f"{write:.0f} |")
     print(f"\nTraffic per launch {fetch + write:.0f} B vs algorithmic {alg} B: ratio {(fetch + write) / alg:.4f}.")
-    others = [k for k in f if k not in dom and not k[0].startswith("k_copy")]
+    others = [k for k in f if k not in dom and k[0].startswith("k_") and not k[0].startswith(("k_copy", "k_probe"))]
     if others:
         malg = moe_alg_bytes()
         nb = PROFILE_PHASE_TOKENS * 8192 * 2  # bytes per rank of the traced two-kernel two-shot

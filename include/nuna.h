@@ -31,8 +31,8 @@
  *                      all-gather), the copies of one token row (all-to-all
  *                      dispatch), and, for one-work-item-per-workgroup
  *                      launches whose chunks are smaller than a 4 KiB page,
- *                      the chunks of one page (Sec. 4.2: 4 kB pages; tunable
- *                      NUNA_PAGE_GROUPS).  A group of one work item is placed
+ *                      the chunks of one page when NUNA_PAGE_GROUPS asks for
+ *                      it (Sec. 4.2: 4 kB pages).  A group of one work item is placed
  *                      as LINEAR places it.  Chunk groups stay together only
  *                      where the members' L2 re-reads are at least a quarter
  *                      of the group's traffic and, for the split all-reduce,
@@ -110,7 +110,8 @@ typedef enum {
                                      kernel: the workgroup that reduces chunk c of shard r stores
                                      it to out[r], then to every other out[d].  Runs the two
                                      kernels of NUNA_ALGO_TWO_SHOT_TWO_KERNELS when P is not 2,
-                                     4, 8 or 16 or a shard is not whole 16-byte vectors */
+                                     4, 8 or 16, a shard is not whole 16-byte vectors, or at the
+                                     sizes where they measured faster (NUNA_TWO_SHOT_FORM) */
     NUNA_ALGO_ONE_SHOT_SPLIT = 3, /* one kernel, work item = (chunk, destination group): more
                                      workgroups for small messages; inputs re-read per group */
     NUNA_ALGO_TWO_SHOT_TWO_KERNELS = 4 /* reduce-scatter kernel, then all-gather kernel (stream
@@ -219,10 +220,13 @@ nuna_status_t nuna_set_max_workgroups(int max_workgroups);
  *   NUNA_TILE_V           rank-major tile all-reduce width: 0 (16 up to 256 KiB per
  *                         rank, else off), 16, 32, 64
  *   NUNA_PAGE_GROUPS      XCD mode, one-work-item-per-workgroup launches with chunks
- *                         smaller than 4 KiB: 1 (default) keeps the chunks of one page
- *                         on one XCD, 0 runs the linear map
+ *                         smaller than 4 KiB: 0 (default) runs the linear map, 1 keeps
+ *                         the chunks of one page on one XCD
  *   NUNA_DIRECT_MAX_GRID  largest grid of the one-work-item-per-workgroup kernels,
  *                         0 (8192)..2^24; larger launches loop (persistent kernels)
+ *   NUNA_TWO_SHOT_FORM    NUNA_ALGO_TWO_SHOT: 0 (by size: fused, except 8 ranks of bf16
+ *                         at 16-40 MiB per rank, which run the two kernels), 1 (fused
+ *                         wherever it applies), 2 (always the two kernels)
  * Unknown names and values outside these sets: NUNA_ERR_INVALID_ARG. */
 nuna_status_t nuna_set_tunable(const char* name, int64_t value);
 nuna_status_t nuna_get_tunable(const char* name, int64_t* value);
@@ -445,7 +449,7 @@ nuna_status_t nuna_placement_grid(nuna_placement_t place, int64_t groups, int64_
  * direct kernels; no HIP call): `items` work items of `chunk_bytes` each
  * (a power of two, at least 16), item i covering bytes [i*chunk_bytes,
  * (i+1)*chunk_bytes) of every rank buffer.  LINEAR: workgroup b runs item b.
- * XCD with chunks below 4 KiB (and NUNA_PAGE_GROUPS on): the gp = 4096 /
+ * XCD with chunks below 4 KiB and NUNA_PAGE_GROUPS set to 1: the gp = 4096 /
  * chunk_bytes items of one page form a group; group g runs on XCD g mod 8,
  * its members on consecutive workgroups of that XCD (b, b+8, ...); the grid
  * is padded to whole rounds of 8 groups.  *workgroups receives the grid;

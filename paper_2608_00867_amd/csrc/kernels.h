@@ -28,8 +28,9 @@ struct Tuning {
     int tile_v = 0;                    // rank-major tile all-reduce width (16/32/64; 0 = by size)
     int combine_lists = 0;             // 1: combine reads the offset lists even where records exist
     int write_through = 0;             // 8-rank one-shot stores: 0 by size, 1 streaming, 2 write-through
-    int page_groups = 1;               // XCD mode: the chunks of a 4 KiB page on one XCD (direct kernels)
+    int page_groups = 0;               // XCD mode: 1 puts the chunks of a 4 KiB page on one XCD (direct kernels)
     int direct_max_grid = 0;           // largest grid of the direct kernels (0: 8192)
+    int two_shot_form = 0;             // two-shot: 0 by size, 1 fused where it applies, 2 two kernels
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
@@ -56,6 +57,8 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
 // one kernel).  Needs P in {2, 4, 8, 16} and shards of whole 16-byte vectors
 // (two_shot_fused_ok); otherwise the caller runs the two kernels.
 bool two_shot_fused_ok(int P, size_t count, int dtype);
+// The fused form applies and is the one to run (size rule, NUNA_TWO_SHOT_FORM).
+bool two_shot_runs_fused(int P, size_t count, int dtype);
 hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype,
                                  hipStream_t stream);
 

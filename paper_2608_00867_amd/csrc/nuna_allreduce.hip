@@ -730,6 +730,22 @@ bool two_shot_fused_ok(int P, size_t count, int dtype) {
     return ((count / P) * dtype_size(dtype)) % 16 == 0;  // shards of whole 16-byte vectors
 }
 
+// Which form of the two-shot runs (NUNA_TWO_SHOT_FORM: 0 by size, 1 fused
+// wherever it applies, 2 two kernels).  By size: the fused kernel, except
+// with 8 ranks of bf16 at 16-40 MiB per rank, where the two kernels measured
+// 1-7 % faster on MI355X (cold, back to back: 46.8 against 48.4 us at 16 MiB,
+// 58.1 against 62.4 at 20 MiB, 113.8 against 118.7 at 40 MiB), while the
+// fused kernel was faster at 4-10 MiB (11.8 against 14.3 us at 4 MiB) and at
+// 48-64 MiB (179.8 against 189.2 us at 64 MiB).
+bool two_shot_runs_fused(int P, size_t count, int dtype) {
+    if (!two_shot_fused_ok(P, count, dtype)) return false;
+    const int form = tuning().two_shot_form;
+    if (form == 1) return true;
+    if (form == 2) return false;
+    const size_t bytes = count * dtype_size(dtype);
+    return !(P == 8 && dtype == kDtBf16 && bytes >= (size_t(16) << 20) && bytes <= (size_t(40) << 20));
+}
+
 // Fused two-shot all-reduce (k_two_shot_direct / k_two_shot): launch shape by
 // the bytes per rank, as for the one-shot (the two move the same bytes);
 // chunks are cut per shard.

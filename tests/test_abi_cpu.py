@@ -526,7 +526,8 @@ def test_two_shot_forms_pass_validation(algo):
                                          (64, 256), (1000, 256), (7, 512), (4096, 4096), (33, 8192), (4, 16)])
 def test_direct_map_covers_every_item_once(items, chunk):
     for place in (nuna.LINEAR, nuna.XCD):
-        m = nuna.placement_direct(place, items, chunk)
+        with nuna.tunables(NUNA_PAGE_GROUPS=1):
+            m = nuna.placement_direct(place, items, chunk)
         got = m[m >= 0]
         assert sorted(got.tolist()) == list(range(items)), (place, items, chunk)
         if place == nuna.LINEAR or chunk >= 4096:
@@ -538,7 +539,8 @@ def test_direct_map_keeps_each_page_on_one_xcd(items, chunk):
     """XCD mode: the chunks of one 4 KiB page run on one XCD (workgroup b runs on XCD b mod 8), pages are
     dealt round-robin to the XCDs, and a page's chunks run on consecutive workgroup slots of its XCD."""
     gp = 4096 // chunk
-    m = nuna.placement_direct(nuna.XCD, items, chunk)
+    with nuna.tunables(NUNA_PAGE_GROUPS=1):
+        m = nuna.placement_direct(nuna.XCD, items, chunk)
     assert m.size % (8 * gp) == 0
     where = {int(w): b for b, w in enumerate(m) if w >= 0}
     for page in range((items + gp - 1) // gp):
@@ -553,9 +555,10 @@ def test_direct_map_keeps_each_page_on_one_xcd(items, chunk):
 
 
 def test_direct_map_follows_the_page_groups_tunable():
-    with nuna.tunables(NUNA_PAGE_GROUPS=0):
-        assert nuna.placement_direct(nuna.XCD, 64, 1024).tolist() == list(range(64))
-    assert nuna.placement_direct(nuna.XCD, 64, 1024).tolist() != list(range(64))
+    """Page groups are off by default (XCD mode runs the linear map for single-item launches)."""
+    assert nuna.placement_direct(nuna.XCD, 64, 1024).tolist() == list(range(64))
+    with nuna.tunables(NUNA_PAGE_GROUPS=1):
+        assert nuna.placement_direct(nuna.XCD, 64, 1024).tolist() != list(range(64))
 
 
 def test_direct_map_rejects_bad_geometry():
@@ -591,10 +594,21 @@ def test_output_count_and_dtype_checked_before_the_library():
 
 
 def test_new_tunables_accept_and_reject():
-    with nuna.tunables(NUNA_PAGE_GROUPS=0, NUNA_DIRECT_MAX_GRID=16384):
-        assert nuna.get_tunable("NUNA_PAGE_GROUPS") == 0
+    with nuna.tunables(NUNA_PAGE_GROUPS=1, NUNA_DIRECT_MAX_GRID=16384, NUNA_TWO_SHOT_FORM=2):
+        assert nuna.get_tunable("NUNA_PAGE_GROUPS") == 1
         assert nuna.get_tunable("NUNA_DIRECT_MAX_GRID") == 16384
-    assert nuna.get_tunable("NUNA_PAGE_GROUPS") == 1
-    for name, bad in [("NUNA_PAGE_GROUPS", 2), ("NUNA_DIRECT_MAX_GRID", -1), ("NUNA_DIRECT_MAX_GRID", (1 << 24) + 1)]:
+        assert nuna.get_tunable("NUNA_TWO_SHOT_FORM") == 2
+    assert nuna.get_tunable("NUNA_PAGE_GROUPS") == 0
+    assert nuna.get_tunable("NUNA_TWO_SHOT_FORM") == 0
+    for name, bad in [("NUNA_PAGE_GROUPS", 2), ("NUNA_DIRECT_MAX_GRID", -1), ("NUNA_DIRECT_MAX_GRID", (1 << 24) + 1),
+                      ("NUNA_TWO_SHOT_FORM", 3)]:
         with pytest.raises(nuna.NunaError):
             nuna.set_tunable(name, bad)
+
+
+def test_last_launch_of_a_call_that_launched_nothing():
+    """A call rejected by its argument checks, or with nothing to do, leaves an empty launch record."""
+    assert nuna.allreduce_raw(None, None, 8, 16, nuna.BF16) == nuna.ERR_INVALID_ARG
+    rec = nuna.last_launch()
+    assert rec["launches"] == 0 and rec["kernels"] == "" and rec["map"] == "linear"
+    assert nuna.lib().nuna_last_launch(None) == nuna.ERR_INVALID_ARG

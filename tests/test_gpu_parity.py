@@ -93,7 +93,8 @@ def test_init_verified_the_dispatch_map(nuna):
 def test_page_groups_run_on_one_xcd(nuna, items, chunk):
     """Placement proof of the page-grouped map: a launch of the direct map's grid records the XCC each
     workgroup ran on; every page's chunks ran on one XCD, XCD (page mod 8)."""
-    m = nuna.placement_direct("xcd", items, chunk)
+    with nuna.tunables(NUNA_PAGE_GROUPS=1):
+        m = nuna.placement_direct("xcd", items, chunk)
     xcc, _ = nuna.probe_xcc(int(m.size))
     torch.cuda.synchronize()
     x = xcc.cpu().numpy()
@@ -463,7 +464,7 @@ def test_two_shot_fused(nuna, cfg):
     and the two-kernel two-shot: 2, 4, 8 and 16 ranks, both dtypes, shards of 1 vector to several
     chunks with a partial last chunk, the persistent kernel (small direct-grid limit, grid caps), in
     place, with guard bands around every output."""
-    with nuna.tunables(**cfg):
+    with nuna.tunables(NUNA_TWO_SHOT_FORM=1, **cfg):
         for P in (2, 4, 8, 16):
             for dt in (np.uint16, np.float32):
                 per_vec = 8 if dt == np.uint16 else 4
@@ -493,6 +494,37 @@ def test_two_shot_fused(nuna, cfg):
         torch.cuda.synchronize()
         for d in range(8):
             assert_bitwise(to_host(bufs[d]), ref[d], f"{cfg} fused in place rank {d}")
+
+
+def _kernels(nuna, x, algo, place):
+    ins = [to_dev(a) for a in x]
+    outs = [torch.empty_like(t) for t in ins]
+    nuna.allreduce(ins, outs, algo=algo, placement=place)
+    rec = nuna.last_launch()
+    torch.cuda.synchronize()
+    return rec
+
+
+def test_launch_record_names_what_ran(nuna):
+    """nuna_last_launch: the two-shot's form by size and its tunable, the page-grouped map in XCD mode,
+    the destination-split groups, the per-XCD lists of the dispatch."""
+    x16 = wl.normal_bf16(8, 1024 * 8192, 3)  # 16 MiB per rank
+    assert _kernels(nuna, x16, "two_shot", "xcd")["kernels"] == "k_reduce_scatter_direct+k_all_gather_direct"
+    with nuna.tunables(NUNA_TWO_SHOT_FORM=1):
+        assert _kernels(nuna, x16, "two_shot", "xcd")["kernels"] == "k_two_shot_direct"
+    x4 = wl.ar_bf16_prefill(256)
+    r = _kernels(nuna, x4, "two_shot", "xcd")
+    assert r["kernels"] == "k_two_shot_direct" and r["launches"] == 1 and r["map"] == "linear"
+    with nuna.tunables(NUNA_TWO_SHOT_FORM=2):
+        assert _kernels(nuna, x4, "two_shot", "xcd")["launches"] == 2
+    d1 = wl.ar_bf16_decode(1)
+    with nuna.tunables(NUNA_PAGE_GROUPS=1):
+        r = _kernels(nuna, d1, "one_shot", "xcd")
+        assert r["map"] == "xcd_pages" and r["group_size"] == 4 and r["grid"] % 32 == 0, r
+        assert _kernels(nuna, d1, "one_shot", "linear")["map"] == "linear"
+    assert _kernels(nuna, d1, "one_shot", "xcd")["map"] == "linear"
+    r = _kernels(nuna, wl.ar_bf16_decode(64), "one_shot_split", "xcd")
+    assert r["map"] == "xcd_groups" and r["group_size"] == 8, r
 
 
 @pytest.mark.parametrize("pg", [0, 1])
