@@ -330,6 +330,37 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
                               nuna_placement_t place, hipStream_t stream);
 
 /*
+ * All-to-all dispatch that allocates nothing, for callers that cannot call
+ * hipMalloc: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation.  Same result as nuna_all_to_all on a layout built from
+ * the same top-k table, but the routing is read from DEVICE memory and the
+ * receive rows are computed on the device, in the library's static scratch
+ * array (8 MiB per GPU, held by each GPU the library runs on until the
+ * process ends) instead of layout tables the library allocates.
+ *   send[s]        P device pointers, each [tokens_per_rank][row_elems].
+ *   recv[d]        P device pointers, each with room for recv_capacity_rows rows;
+ *                  rows past the capacity are not written.
+ *   topk_idx       DEVICE int32 [P][tokens_per_rank][topk], 4-byte aligned;
+ *                  entries outside [0, num_experts) route nowhere.
+ *   rows_per_rank  DEVICE int64 [P + 1], 8-byte aligned, written by the call:
+ *                  [d] = rows rank d receives (compare with the capacity),
+ *                  [P] = top-k entries outside [0, num_experts).
+ * The routing tables need 4*P*P + 4*P + 4*P*tokens_per_rank*min(topk, P)
+ * bytes of the scratch: larger calls return NUNA_ERR_INVALID_ARG, as do
+ * P*tokens_per_rank >= 2^26.  Rows must be whole 16-byte vectors
+ * (NUNA_ERR_UNSUPPORTED otherwise).  Needs nuna_init on the current device
+ * (it looks up the scratch array's address there; NUNA_ERR_UNSUPPORTED
+ * without it).  Every call on a GPU uses that GPU's one array: calls on one
+ * stream run in order, calls that overlap on one GPU (other streams, other
+ * threads) race and must not be made.  Both placement modes run the same map
+ * (one workgroup per token row holds all of its copies).  Capture-safe.
+ */
+nuna_status_t nuna_all_to_all_routed(const void* const* send, void* const* recv, const int32_t* topk_idx, int P,
+                                     int tokens_per_rank, int topk, int num_experts, size_t row_elems,
+                                     size_t recv_capacity_rows, nuna_dtype_t dtype, nuna_placement_t place,
+                                     int64_t* rows_per_rank, hipStream_t stream);
+
+/*
  * All-to-all combine: the result-collection step of MoE expert parallelism
  * (Sec. 2.1: the all-to-all that sends tokens to their experts also brings
  * the expert outputs back).  It reverses a dispatch made with the same

@@ -14,8 +14,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libnuna.so")
 OBJDIR = os.path.join(ROOT, "_build", "libnuna")
 
-SOURCES = [os.path.join(CSRC, f) for f in ("nuna_allreduce.hip", "nuna_rs_ag.hip", "nuna_moe.hip", "nuna_probe.hip",
-                                           "nap_planner.cpp", "nuna_api.cpp")]
+SOURCES = [os.path.join(CSRC, f) for f in ("nuna_allreduce.hip", "nuna_rs_ag.hip", "nuna_moe.hip", "nuna_routed.hip",
+                                           "nuna_probe.hip", "nap_planner.cpp", "nuna_api.cpp")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

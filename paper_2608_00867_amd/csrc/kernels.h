@@ -91,6 +91,20 @@ hipError_t launch_combine(const void* const* y, void* const* out, int P, int T, 
                           const void* rec, const float* weights, size_t row_bytes, int dtype, int mode,
                           hipStream_t stream);
 
+// Routed all-to-all dispatch (routing on the device, tables in the library's
+// static scratch array, nothing allocated per call).  The scratch holds
+// cnt int32[P][P], bad int32[P] and R = min(k, P) uint32 record words per token.
+constexpr size_t kRoutedScratchBytes = size_t(8) << 20;
+inline size_t routed_scratch_need(int P, int T, int k) {
+    const size_t R = static_cast<size_t>(k < P ? k : P);
+    return 4 * static_cast<size_t>(P) * P + 4 * static_cast<size_t>(P) + 4 * static_cast<size_t>(P) * T * R;
+}
+// Device address of the scratch array on the current device (hipGetSymbolAddress).
+hipError_t routed_scratch_address(void** ptr);
+hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, const int32_t* topk, int P, int T,
+                                  int k, int E, int64_t rowvec, int64_t cap, void* scratch_ptr, int64_t* rows_out,
+                                  hipStream_t stream);
+
 hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
 
 hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);

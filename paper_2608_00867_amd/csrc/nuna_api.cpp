@@ -258,6 +258,9 @@ enum MapState { kMapUnknown = 0, kMapVerified = 1, kMapFailed = 2 };
 std::atomic<int> g_map_state[kMaxDevices];
 std::atomic<int> g_cu_count[kMaxDevices];
 std::atomic<int> g_xcd_count[kMaxDevices];
+// Device address of the routed dispatch's static scratch array, per device
+// (set by nuna_init with that device current).
+std::atomic<void*> g_scratch[kMaxDevices];
 
 // Workgroups the init probe launches: a few per compute unit, in many rounds of 8.
 constexpr int kProbeGrid = 2048;
@@ -361,6 +364,11 @@ nuna_status_t nuna_init(void) try {
     for (int32_t x : xcc) xcds = std::max(xcds, x + 1);
     g_cu_count[dev].store(prop.multiProcessorCount, std::memory_order_relaxed);
     g_xcd_count[dev].store(xcds, std::memory_order_relaxed);
+    // The routed dispatch's scratch array: each device holds its own copy at its own address.
+    void* scr = nullptr;
+    if ((e = nuna::routed_scratch_address(&scr)) != hipSuccess || !scr)
+        return hip_status(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress (scratch)");
+    g_scratch[dev].store(scr, std::memory_order_release);
     const nuna_status_t st = nuna_check_dispatch_map(xcc.data(), kProbeGrid, prop.multiProcessorCount);
     g_map_state[dev].store(st == NUNA_OK ? kMapVerified : kMapFailed, std::memory_order_release);
     if (st != NUNA_OK) {
@@ -767,6 +775,66 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
     hipError_t e = nuna::launch_all_to_all(send, recv, P, desc, L->nitems, L->xcd_start, row_bytes,
                                            static_cast<int>(es), place, stream);
     return hip_status(e, "all-to-all launch");
+} catch (...) {
+    return host_exception();
+}
+
+nuna_status_t nuna_all_to_all_routed(const void* const* send, void* const* recv, const int32_t* topk_idx, int P,
+                                     int tokens_per_rank, int topk, int num_experts, size_t row_elems,
+                                     size_t recv_capacity_rows, nuna_dtype_t dtype, nuna_placement_t place,
+                                     int64_t* rows_per_rank, hipStream_t stream) try {
+    begin_launches();
+    nuna_status_t st = check_common(P, dtype, place);
+    if (st) return st;
+    const int T = tokens_per_rank;
+    if (T < 0) return fail(NUNA_ERR_INVALID_ARG, "tokens_per_rank=%d < 0", T);
+    if (num_experts < P || num_experts % P != 0)
+        return fail(NUNA_ERR_INVALID_ARG, "num_experts=%d is not a positive multiple of P=%d", num_experts, P);
+    if (topk < 1 || topk > num_experts)
+        return fail(NUNA_ERR_INVALID_ARG, "topk=%d outside [1, num_experts=%d]", topk, num_experts);
+    if ((st = check_ptr_array(send, P, "send"))) return st;
+    if ((st = check_ptr_array(const_cast<const void* const*>(recv), P, "recv"))) return st;
+    if (T > 0 && !topk_idx) return fail(NUNA_ERR_INVALID_ARG, "topk_idx is NULL");
+    if (!rows_per_rank) return fail(NUNA_ERR_INVALID_ARG, "rows_per_rank is NULL");
+    if ((reinterpret_cast<uintptr_t>(topk_idx) & 3u) || (reinterpret_cast<uintptr_t>(rows_per_rank) & 7u))
+        return fail(NUNA_ERR_MISALIGNED, "topk_idx must be 4-byte and rows_per_rank 8-byte aligned");
+    const size_t es = nuna::dtype_size(dtype);
+    if (row_elems == 0) return fail(NUNA_ERR_INVALID_ARG, "row_elems is 0");
+    if (row_elems > kMaxBytes / es) return fail(NUNA_ERR_INVALID_ARG, "row_elems %zu too large", row_elems);
+    const size_t row_bytes = row_elems * es;
+    if (row_bytes % 16 != 0)
+        return fail(NUNA_ERR_UNSUPPORTED, "routed dispatch rows must be whole 16-byte vectors (%zu bytes)", row_bytes);
+    const int64_t ntok = static_cast<int64_t>(P) * T;
+    if (ntok >= (int64_t(1) << 26))
+        return fail(NUNA_ERR_INVALID_ARG, "P*tokens_per_rank=%lld: the routed dispatch takes fewer than 2^26 tokens",
+                    static_cast<long long>(ntok));
+    const size_t need = nuna::routed_scratch_need(P, T, topk);
+    if (need > nuna::kRoutedScratchBytes)
+        return fail(NUNA_ERR_INVALID_ARG,
+                    "routing tables need %zu bytes (4*P*P + 4*P + 4*P*T*min(topk, P)), more than the %zu-byte scratch",
+                    need, nuna::kRoutedScratchBytes);
+    if (static_cast<size_t>(T) > kMaxBytes / row_bytes || recv_capacity_rows > kMaxBytes / row_bytes)
+        return fail(NUNA_ERR_INVALID_ARG, "buffer sizes too large");
+    SpanSet ins, outs;
+    for (int r = 0; r < P; ++r) {
+        ins.add(send[r], row_bytes * T, r);
+        outs.add(recv[r], row_bytes * recv_capacity_rows, r);
+    }
+    if (T > 0) ins.add(topk_idx, sizeof(int32_t) * static_cast<size_t>(ntok) * topk, -1);
+    outs.add(rows_per_rank, sizeof(int64_t) * (static_cast<size_t>(P) + 1), -1);
+    st = check_overlaps(ins, outs, [](const Span&, const Span&) { return false; });
+    if (st) return st;
+    if ((st = check_placement_ready(place))) return st;
+    int dev = 0;
+    const hipError_t ge = hipGetDevice(&dev);
+    if (ge != hipSuccess) return hip_status(ge, "hipGetDevice");
+    void* scr = dev >= 0 && dev < kMaxDevices ? g_scratch[dev].load(std::memory_order_acquire) : nullptr;
+    if (!scr) return fail(NUNA_ERR_UNSUPPORTED, "the routed dispatch needs nuna_init() on device %d first", dev);
+    return hip_status(nuna::launch_routed_dispatch(send, recv, topk_idx, P, T, topk, num_experts,
+                                                   static_cast<int64_t>(row_bytes / 16),
+                                                   static_cast<int64_t>(recv_capacity_rows), scr, rows_per_rank,
+                                                   stream),
+                      "routed dispatch launch");
 } catch (...) {
     return host_exception();
 }

@@ -87,6 +87,8 @@ SIGNATURES = {
     "nuna_a2a_layout_destroy": ([_vp], None),
     "nuna_all_to_all": ([_vpp, _vpp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp],
                         ctypes.c_int),
+    "nuna_all_to_all_routed": ([_vpp, _vpp, _vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, ctypes.c_int, _vp, _vp], ctypes.c_int),
     "nuna_all_to_all_combine": ([_vpp, _vpp, _vp, _vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int,
                                  ctypes.c_int, _vp], ctypes.c_int),
     "nuna_placement_items": ([ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, _i64p,
@@ -482,6 +484,43 @@ def all_to_all(send, recv, layout, placement="xcd", stream=None):
         cap = min(cap, t.shape[0])
     _check(all_to_all_raw([t.data_ptr() for t in send], [t.data_ptr() for t in recv], layout.handle, row, cap,
                           _dtype_code(send[0]), PLACEMENTS[placement], _stream(stream)))
+    return recv
+
+
+def all_to_all_routed_raw(send_ptrs, recv_ptrs, topk_ptr, P, T, k, E, row_elems, recv_capacity_rows, dtype,
+                          rows_ptr, place=XCD, stream=0):
+    a = _ptr_array(send_ptrs) if send_ptrs is not None else None
+    b = _ptr_array(recv_ptrs) if recv_ptrs is not None else None
+    return lib().nuna_all_to_all_routed(a, b, topk_ptr, P, T, k, E, row_elems, recv_capacity_rows, dtype, place,
+                                        rows_ptr, stream)
+
+
+def all_to_all_routed(send, recv, topk_idx, num_experts, rows_per_rank, placement="xcd", stream=None):
+    """Dispatch with the routing on the device and no allocation: topk_idx an int32 CUDA tensor
+    [P, T, k]; rows_per_rank an int64 CUDA tensor of P + 1 that receives the rows each rank gets
+    (and, last, the count of out-of-range experts)."""
+    torch = _torch()
+    P = len(send)
+    if len(recv) != P or topk_idx.dim() != 3 or topk_idx.shape[0] != P or topk_idx.dtype != torch.int32:
+        raise ValueError("one send and one recv buffer per rank; topk_idx int32 [P, T, k]")
+    if not topk_idx.is_cuda or not topk_idx.is_contiguous():
+        raise ValueError("topk_idx must be a contiguous CUDA tensor")
+    if (not rows_per_rank.is_cuda or rows_per_rank.dtype != torch.int64 or rows_per_rank.numel() != P + 1
+            or not rows_per_rank.is_contiguous()):
+        raise ValueError("rows_per_rank must be a contiguous int64 CUDA tensor of P + 1")
+    T, k = int(topk_idx.shape[1]), int(topk_idx.shape[2])
+    for t in send:
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 2 or t.shape != (T, send[0].shape[1]):
+            raise ValueError("send buffers must be contiguous CUDA tensors [T, row]")
+    row = send[0].shape[1]
+    cap = recv[0].shape[0]
+    for t in recv:
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 2 or t.shape[1] != row or t.dtype != send[0].dtype:
+            raise ValueError("recv buffers must be contiguous CUDA tensors [capacity, row] of the send dtype")
+        cap = min(cap, t.shape[0])
+    _check(all_to_all_routed_raw([t.data_ptr() for t in send], [t.data_ptr() for t in recv], topk_idx.data_ptr(),
+                                 P, T, k, int(num_experts), row, cap, _dtype_code(send[0]), rows_per_rank.data_ptr(),
+                                 PLACEMENTS[placement], _stream(stream)))
     return recv
 
 

@@ -171,6 +171,26 @@ hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t) {
     return hipSuccess;
 }
 
+hipError_t routed_scratch_address(void** ptr) {
+    static unsigned char* scr = static_cast<unsigned char*>(std::malloc(kRoutedScratchBytes));
+    *ptr = scr;
+    return scr ? hipSuccess : hipErrorOutOfMemory;
+}
+
+hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, const int32_t* topk, int P, int T, int k,
+                                  int E, int64_t rowvec, int64_t cap, void* scratch_ptr, int64_t*, hipStream_t) {
+    check(send && recv && P >= 1 && P <= 64 && T >= 0 && k >= 1 && E % P == 0 && rowvec > 0 && cap >= 0,
+          "routed dispatch arguments");
+    check(scratch_ptr != nullptr && routed_scratch_need(P, T, k) <= kRoutedScratchBytes, "routed dispatch scratch");
+    // The routing tables cover the whole scratch need: touch its last byte.
+    if (T > 0) {
+        check(topk != nullptr, "routed dispatch top-k");
+        static_cast<unsigned char*>(scratch_ptr)[routed_scratch_need(P, T, k) - 1] = 0;
+    }
+    note_launch("stub_routed", kMapLinear, 1, static_cast<int64_t>(P) * T, 256, 4);
+    return hipSuccess;
+}
+
 hipError_t launch_copy(void*, const void*, size_t, hipStream_t) { return hipSuccess; }
 
 hipError_t launch_probe_latency(const void*, int64_t nblocks, int64_t stride, int64_t line_off, int64_t, int xcd,

@@ -167,6 +167,13 @@ void layout_fuzz(int iters) {
         st = nuna_all_to_all_combine(ys.data(), outs.data(), L, w, row, static_cast<size_t>(cap), dt, place, nullptr);
         expect(st == NUNA_OK, "combine", st);
         nuna_a2a_layout_destroy(L);
+        // The allocation-free dispatch on the same routing (topk_idx is host memory here; the stand-in
+        // launcher does not read it).
+        std::vector<int64_t> rows_dev(P + 1);
+        const size_t rrow = static_cast<size_t>(rnd_in(1, 512)) * 8;
+        st = nuna_all_to_all_routed(send.data(), recv.data(), topk.empty() ? nullptr : topk.data(), P, T, k, E, rrow,
+                                    static_cast<size_t>(cap), NUNA_BF16, place, rows_dev.data(), nullptr);
+        expect(st == NUNA_OK || st == NUNA_ERR_INVALID_ARG, "routed dispatch", st);
     }
     nuna_a2a_layout_destroy(nullptr);
 }

@@ -612,3 +612,25 @@ def test_last_launch_of_a_call_that_launched_nothing():
     rec = nuna.last_launch()
     assert rec["launches"] == 0 and rec["kernels"] == "" and rec["map"] == "linear"
     assert nuna.lib().nuna_last_launch(None) == nuna.ERR_INVALID_ARG
+
+
+@no_gpu_only
+def test_routed_dispatch_validation():
+    """The allocation-free dispatch rejects, before any HIP call, routing tables larger than its scratch,
+    rows that are not whole 16-byte vectors, and the usual bad arguments."""
+    P, H = 8, 64
+    send, recv = _bufs(P, stride=1 << 24), _bufs(P, stride=1 << 24, base=BASE + (1 << 32))
+    topk, rows = BASE + (1 << 34), BASE + (1 << 35)
+    call = lambda **kw: nuna.all_to_all_routed_raw(  # noqa: E731
+        kw.get("send", send), kw.get("recv", recv), kw.get("topk", topk), kw.get("P", P), kw.get("T", 16),
+        kw.get("k", 8), kw.get("E", 64), kw.get("row", H), kw.get("cap", 64), kw.get("dtype", nuna.BF16),
+        kw.get("rows", rows))
+    assert call(T=40000) == nuna.ERR_INVALID_ARG and "scratch" in nuna.last_error()
+    assert call(row=7) == nuna.ERR_UNSUPPORTED
+    assert call(E=60) == nuna.ERR_INVALID_ARG
+    assert call(k=0) == nuna.ERR_INVALID_ARG
+    assert call(topk=None) == nuna.ERR_INVALID_ARG
+    assert call(rows=None) == nuna.ERR_INVALID_ARG
+    assert call(topk=topk + 2) == nuna.ERR_MISALIGNED
+    assert call(rows=recv[0]) == nuna.ERR_OVERLAP
+    assert call() == nuna.ERR_HIP  # valid: reaches the device lookup, and there is no device here
