@@ -68,6 +68,9 @@ def parse():
                     help="probe which die (XCDs 0-3 or 4-7) is near each 8 KiB block of an all-reduce's 16 rank "
                          "buffers (decode T=64 and prefill T=1024 layouts of the pool) and print how well the "
                          "buffers agree offset by offset")
+    ap.add_argument("--cu-affinity", action="store_true",
+                    help="per-compute-unit cold-load latency from every CU of every XCD to every 8 KiB block of a "
+                         "64 MiB buffer; prints a JSON summary and a markdown table")
     ap.add_argument("--profile", type=int, default=0, metavar="N",
                     help="profiling run: N cold launches each of the dominant kernel (fused two-shot all-reduce, "
                          "P=8, [4096, 8192] bf16, XCD), the 64 MiB reference copy, the two-kernel two-shot at "
@@ -1023,6 +1026,58 @@ def affinity(nuna, torch, pool):
               flush=True)
 
 
+CU_PROBE_BYTES = 64 << 20
+
+
+def cu_affinity(nuna, torch):
+    """The paper's latency profiling over every compute unit and target address (Sec. 3.2), on one GPU:
+    every CU of every XCD times one cold load per 8 KiB block of a 64 MiB buffer.  Each block is labelled
+    by the XCD group (0-3 or 4-7) whose CUs load it faster on average; the summary gives, per XCD, the
+    CUs reached, the spread of the per-CU median latencies to near and to far blocks, how often a single
+    CU's own near/far call agrees with the block's label, and the spread over addresses."""
+    buf = torch.zeros(CU_PROBE_BYTES // 4, dtype=torch.int32, device="cuda")
+    res = nuna.cu_latency_map(buf, stride=8192)
+    lat = {x: res[x][0].numpy() for x in res}
+    group_a = np.concatenate([lat[x] for x in range(4)]).mean(axis=0)
+    group_b = np.concatenate([lat[x] for x in range(4, 8)]).mean(axis=0)
+    near_a = group_a < group_b  # block is near XCDs 0-3
+    rows = []
+    for x in sorted(lat):
+        L = lat[x]
+        near = near_a if x < 4 else ~near_a
+        med_near = np.median(L[:, near], axis=1)
+        med_far = np.median(L[:, ~near], axis=1)
+        thr = (med_near + med_far)[:, None] / 2
+        own = L < thr  # each CU's own near call per block
+        agree = np.mean(own == near[None, :], axis=1)
+        q = np.percentile(L, [10, 50, 90], axis=1)
+        rows.append({"xcd": x, "cus_seen": int(res[x][2]), "cus_probed": int(L.shape[0]),
+                     "distinct_cu_keys": int(np.unique(res[x][1].numpy()).size),
+                     "near_median_cycles": [round(float(med_near.min()), 1), round(float(np.median(med_near)), 1),
+                                            round(float(med_near.max()), 1)],
+                     "far_median_cycles": [round(float(med_far.min()), 1), round(float(np.median(med_far)), 1),
+                                           round(float(med_far.max()), 1)],
+                     "cu_spread_near": round(float(med_near.max() / med_near.min()), 3),
+                     "far_over_near": round(float(np.median(med_far) / np.median(med_near)), 3),
+                     "own_call_agreement": [round(float(agree.min()), 3), round(float(np.median(agree)), 3)],
+                     "address_p10_p50_p90": [round(float(np.median(q[0])), 1), round(float(np.median(q[1])), 1),
+                                             round(float(np.median(q[2])), 1)],
+                     "address_max_over_min": round(float(np.median(L.max(axis=1) / np.maximum(L.min(axis=1), 1))), 3)})
+    summary = {"buffer_bytes": CU_PROBE_BYTES, "block_bytes": 8192, "blocks": int(near_a.size),
+               "near_group_0_3_fraction": round(float(near_a.mean()), 3), "per_xcd": rows}
+    print(json.dumps({"cu_affinity": summary}), flush=True)
+    print("\n| XCD | CUs probed (distinct) | near: per-CU median cycles min / median / max | far: min / median / max | "
+          "CU spread (near, max/min) | far / near | CU's own near call agrees with the block label (min, median) | "
+          "one CU over addresses: p10 / p50 / p90 | max / min over addresses |")
+    print("|---|---|---|---|---|---|---|---|---|")
+    for r in rows:
+        print(f"| {r['xcd']} | {r['cus_probed']} ({r['distinct_cu_keys']}) | "
+              f"{' / '.join(str(v) for v in r['near_median_cycles'])} | "
+              f"{' / '.join(str(v) for v in r['far_median_cycles'])} | {r['cu_spread_near']} | {r['far_over_near']} | "
+              f"{r['own_call_agreement'][0]}, {r['own_call_agreement'][1]} | "
+              f"{' / '.join(str(v) for v in r['address_p10_p50_p90'])} | {r['address_max_over_min']} |")
+
+
 # ---------------------------------------------------------------------------------------------- --profile
 
 PROFILE_COPY_BYTES = 64 << 20
@@ -1456,6 +1511,9 @@ def main():
         return
     if args.affinity:
         affinity(nuna, torch, pool)
+        return
+    if args.cu_affinity:
+        cu_affinity(nuna, torch)
         return
     if args.interference:
         interference(nuna, torch, args)

@@ -518,6 +518,30 @@ nuna_status_t nuna_probe_load_latency(const void* buf, size_t nbytes, size_t str
                                       uint32_t* cycles, hipStream_t stream);
 
 /*
+ * Per-compute-unit load-latency probe (the paper's latency profiling over
+ * every CU and target address, Sec. 3.2, on one GPU).  Launches 512 one-wave
+ * workgroups; each of those that run on XCD `xcd` claims the compute unit it
+ * runs on if no earlier workgroup did, and the claimed compute units (at most
+ * 32, in claim order: slot j) each walk the nbytes / stride blocks of `buf`
+ * with one lane, timing one cold load per block.  Slot j loads lines 2j
+ * (warm-up of the block's address translation) and 2j + 1 (timed) of each
+ * block, so no two compute units of the XCD share a line.
+ *   work    device int32 [257], zeroed by the caller before each call (claim
+ *           words, then the slot counter; work[256] ends as the number of
+ *           compute units found, counting any past 32).
+ *   cycles  device uint32 [32][nbytes / stride]: slot j's latency of block i
+ *           in shader clock cycles at [j * nblocks + i].
+ *   cu_of   device int32 [32]: bits 8-15 of the HW_ID register (CU, array and
+ *           shader-engine fields) of the compute unit in slot j; untouched
+ *           for unused slots.
+ * The loads should be cold: the caller evicts the caches beforehand, and
+ * between two XCDs' calls on the same buffer.  stride: a multiple of 128 of
+ * at least 8 KiB; buffers 4-byte aligned.  About half a microsecond per block.
+ */
+nuna_status_t nuna_probe_load_latency_cus(const void* buf, size_t nbytes, size_t stride, int xcd, int32_t* work,
+                                          uint32_t* cycles, int32_t* cu_of, hipStream_t stream);
+
+/*
  * Plain device copy of `bytes` bytes (16-byte aligned pointers, no overlap):
  * the reference streaming kernel used to calibrate memory-traffic counters
  * and the copy-bandwidth ceiling.

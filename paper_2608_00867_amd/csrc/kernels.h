@@ -109,6 +109,12 @@ hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t str
 
 hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
 
+// Per-compute-unit load-latency probe on XCD `xcd` (lines 2j and 2j + 1 of each
+// block for probe slot j; claimed: 257 zeroed int32 words).
+constexpr int kProbeCuSlotsMax = 32;
+hipError_t launch_probe_latency_cus(const void* buf, int64_t nblocks, int64_t stride, int xcd, int32_t* claimed,
+                                    uint32_t* cycles, int32_t* cu_of, hipStream_t stream);
+
 // Serial load-latency probe from XCD `xcd` (warm_off < 0: no translation warm-up).
 hipError_t launch_probe_latency(const void* buf, int64_t nblocks, int64_t stride, int64_t line_off, int64_t warm_off,
                                 int xcd, uint32_t* cycles, hipStream_t stream);

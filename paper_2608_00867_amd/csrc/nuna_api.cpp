@@ -1029,6 +1029,25 @@ nuna_status_t nuna_probe_load_latency(const void* buf, size_t nbytes, size_t str
                       "latency probe launch");
 }
 
+nuna_status_t nuna_probe_load_latency_cus(const void* buf, size_t nbytes, size_t stride, int xcd, int32_t* work,
+                                          uint32_t* cycles, int32_t* cu_of, hipStream_t stream) {
+    if (!buf || !work || !cycles || !cu_of) return fail(NUNA_ERR_INVALID_ARG, "NULL pointer");
+    if ((reinterpret_cast<uintptr_t>(buf) & 3u) || (reinterpret_cast<uintptr_t>(work) & 3u) ||
+        (reinterpret_cast<uintptr_t>(cycles) & 3u) || (reinterpret_cast<uintptr_t>(cu_of) & 3u))
+        return fail(NUNA_ERR_MISALIGNED, "probe buffers must be 4-byte aligned");
+    const size_t lines = 2 * static_cast<size_t>(nuna::kProbeCuSlotsMax) * 128;
+    if (stride < lines || stride % 128 != 0)
+        return fail(NUNA_ERR_INVALID_ARG, "stride %zu: need a multiple of 128 of at least %zu bytes (two lines per slot)",
+                    stride, lines);
+    if (xcd < 0 || xcd >= NUNA_NUM_XCD) return fail(NUNA_ERR_INVALID_ARG, "xcd %d outside [0, %d)", xcd, NUNA_NUM_XCD);
+    if (nbytes > kMaxBytes) return fail(NUNA_ERR_INVALID_ARG, "nbytes too large");
+    const int64_t nblocks = static_cast<int64_t>(nbytes / stride);
+    if (nblocks < 1) return fail(NUNA_ERR_INVALID_ARG, "buffer holds no whole block");
+    return hip_status(nuna::launch_probe_latency_cus(buf, nblocks, static_cast<int64_t>(stride), xcd, work, cycles,
+                                                     cu_of, stream),
+                      "per-CU latency probe launch");
+}
+
 nuna_status_t nuna_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
     if (!dst || !src) return fail(NUNA_ERR_INVALID_ARG, "NULL pointer");
     if (!aligned16(dst) || !aligned16(src)) return fail(NUNA_ERR_MISALIGNED, "copy pointers must be 16-byte aligned");

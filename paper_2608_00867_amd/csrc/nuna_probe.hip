@@ -81,7 +81,67 @@ __global__ __launch_bounds__(64) void k_probe_latency(const unsigned char* buf, 
     }
 }
 
+// Per-compute-unit load-latency probe on XCD `xcd`.  Many one-wave workgroups
+// are launched; those that land on `xcd` read the compute unit they run on
+// (shader engine, array and CU fields of HW_ID), and the first workgroup on
+// each compute unit claims it (claimed[hw cu], zeroed by the caller) and takes
+// the next probe slot j (slot counter after the 256 claim words).  Slot j
+// walks every block of the buffer with one lane, as k_probe_latency does, but
+// on lines 2j (warm-up) and 2j + 1 (timed) of each block, so the compute units
+// of one XCD never touch each other's lines and each timed load misses its
+// XCD's L2.  cycles[j * nblocks + i] is slot j's latency for block i and
+// cu_of[j] the HW_ID CU key (bits 8-15) of the compute unit in slot j.  Up to
+// kProbeCuSlots slots; workgroups past them exit.
+constexpr int kProbeCuSlots = 32;
+
+__global__ __launch_bounds__(64) void k_probe_latency_cus(const unsigned char* buf, int64_t nblocks, int64_t stride,
+                                                          int xcd, int32_t* claimed, uint32_t* cycles,
+                                                          int32_t* cu_of) {
+    uint32_t me, hw;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(me));
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID)" : "=s"(hw));
+    if ((me & 0xfu) != static_cast<uint32_t>(xcd) || threadIdx.x != 0) return;
+    const int key = static_cast<int>((hw >> 8) & 0xffu);
+    if (atomicCAS(&claimed[key], 0, 1) != 0) return;
+    const int j = atomicAdd(&claimed[256], 1);
+    if (j >= kProbeCuSlots) return;
+    cu_of[j] = key;
+    const int64_t line = static_cast<int64_t>(2 * j + 1) * 128;
+    const int64_t warm = static_cast<int64_t>(2 * j) * 128;
+    uint32_t sink = 0;
+    for (int64_t i = 0; i < nblocks; ++i) {
+        const unsigned char* blk = buf + i * stride;
+        uint32_t v;
+        const uint32_t* w = reinterpret_cast<const uint32_t*>(blk + warm);
+        asm volatile("global_load_dword %0, %1, off nt\n s_waitcnt vmcnt(0)" : "=v"(v) : "v"(w) : "memory");
+        sink += v;
+        const uint32_t* q = reinterpret_cast<const uint32_t*>(blk + line);
+        uint64_t t0, t1;
+        asm volatile(
+            "s_waitcnt vmcnt(0) lgkmcnt(0)\n"
+            "s_memtime %0\n"
+            "s_waitcnt lgkmcnt(0)\n"
+            "global_load_dword %2, %3, off nt\n"
+            "s_waitcnt vmcnt(0)\n"
+            "s_memtime %1\n"
+            "s_waitcnt lgkmcnt(0)\n"
+            : "=s"(t0), "=s"(t1), "=v"(v)
+            : "v"(q)
+            : "memory");
+        sink += v;
+        cycles[j * nblocks + i] = static_cast<uint32_t>(t1 - t0) | (sink & 0u);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_probe_latency_cus(const void* buf, int64_t nblocks, int64_t stride, int xcd, int32_t* claimed,
+                                    uint32_t* cycles, int32_t* cu_of, hipStream_t stream) {
+    // 64 workgroups per XCD: the first to reach each of its compute units claims it.
+    hipLaunchKernelGGL(k_probe_latency_cus, dim3(kNumXcd * 64), dim3(64), 0, stream,
+                       static_cast<const unsigned char*>(buf), nblocks, stride, xcd, claimed, cycles, cu_of);
+    return hipGetLastError();
+}
 
 hipError_t launch_probe_latency(const void* buf, int64_t nblocks, int64_t stride, int64_t line_off, int64_t warm_off,
                                 int xcd, uint32_t* cycles, hipStream_t stream) {

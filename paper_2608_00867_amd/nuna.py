@@ -101,6 +101,8 @@ SIGNATURES = {
     "nuna_nap_topology_mi355x": ([ctypes.POINTER(NapTopology)], ctypes.c_int),
     "nuna_nap_plan": ([ctypes.POINTER(NapTopology), ctypes.c_int, ctypes.c_int64, _i64p, _i64p, _i64p, _i64p,
                        _i64p, _i32p, _i32p, _i32p, _i64p], ctypes.c_int),
+    "nuna_probe_load_latency_cus": ([_vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, _vp, _vp, _vp, _vp],
+                                    ctypes.c_int),
     "nuna_probe_load_latency": ([_vp, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_size_t, ctypes.c_int, _vp, _vp],
                                 ctypes.c_int),
 }
@@ -594,3 +596,35 @@ def memory_affinity(buf, stride=8192, line_offset=256, xcds=(0, 4), evict_bytes=
     lat = torch.stack(lats)
     return lat, lat.argmin(dim=0)
 
+
+def probe_load_latency_cus(buf, xcd, stride=8192, stream=None):
+    """Cold-load latency (shader cycles) of every stride-sized block of `buf` from each compute unit of
+    XCD `xcd` it reaches.  Returns (latencies int64 [cus, nblocks] on the CPU, HW_ID CU keys [cus],
+    compute units seen).  The caller evicts the caches first."""
+    torch = _torch()
+    nbytes = buf.numel() * buf.element_size()
+    nb = nbytes // stride
+    work = torch.zeros(257, dtype=torch.int32, device=buf.device)
+    cyc = torch.zeros((32, nb), dtype=torch.int32, device=buf.device)
+    cu = torch.full((32,), -1, dtype=torch.int32, device=buf.device)
+    _check(lib().nuna_probe_load_latency_cus(buf.data_ptr(), nbytes, stride, xcd, work.data_ptr(), cyc.data_ptr(),
+                                             cu.data_ptr(), _stream(stream)))
+    torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+    seen = int(work[256].item())
+    n = min(seen, 32)
+    return cyc[:n].cpu().to(torch.int64), cu[:n].cpu().to(torch.int64), seen
+
+
+def cu_latency_map(buf, stride=8192, xcds=range(8), evict_bytes=1 << 30):
+    """Per-XCD, per-compute-unit cold-load latencies over every block of `buf`: dict xcd ->
+    (latencies [cus, nblocks], CU keys, compute units seen).  Caches are evicted before each XCD's
+    pass by streaming `evict_bytes` through a scratch tensor (plumbing on the host side)."""
+    torch = _torch()
+    ev = torch.empty(evict_bytes // 4, dtype=torch.int32, device=buf.device)
+    out = {}
+    for j, x in enumerate(xcds):
+        ev.fill_(j)
+        torch.cuda.synchronize()
+        out[x] = probe_load_latency_cus(buf, x, stride)
+    del ev
+    return out

@@ -193,6 +193,13 @@ hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, co
 
 hipError_t launch_copy(void*, const void*, size_t, hipStream_t) { return hipSuccess; }
 
+hipError_t launch_probe_latency_cus(const void*, int64_t nblocks, int64_t stride, int xcd, int32_t* claimed,
+                                    uint32_t*, int32_t*, hipStream_t) {
+    check(nblocks > 0 && stride >= 2 * kProbeCuSlotsMax * 128 && xcd >= 0 && xcd < 8 && claimed,
+          "per-CU probe arguments");
+    return hipSuccess;
+}
+
 hipError_t launch_probe_latency(const void*, int64_t nblocks, int64_t stride, int64_t line_off, int64_t, int xcd,
                                 uint32_t*, hipStream_t) {
     check(nblocks > 0 && line_off + 4 <= stride && xcd >= 0 && xcd < 8, "latency probe arguments");
