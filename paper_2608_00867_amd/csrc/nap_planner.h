@@ -1,6 +1,8 @@
 // nap_planner.h -- host planner for NUNA-aware placement (Algorithm 1,
 // Sec. 4.2.2 of the paper): threadblocks and the chunks they touch in,
 // threadblock -> (logical group, NAR domain, CU) and chunk -> HBM stack out.
+// The implementation runs four passes (form groups, rank them, place
+// threadblocks under budgets, home chunks); the rules they apply:
 //
 // Logical allocation: threadblocks are taken in the given order; one whose
 // chunks belong to no group starts a group, otherwise it joins the group it
@@ -41,6 +43,7 @@ struct NapPlan {
     std::vector<int64_t> tb_group;   // group index in creation order
     std::vector<int32_t> tb_domain;  // NAR domain
     std::vector<int32_t> tb_cu;      // physical domain * cus_per_domain + CU within it
+    std::vector<int32_t> tb_stack;     // stack charged for each threadblock
     std::vector<int32_t> entry_stack;  // stack of each (threadblock, chunk) entry's chunk
     std::vector<int64_t> group_order;  // group indices in placement order (decreasing size)
     std::vector<std::vector<int64_t>> groups;  // members of each group, in joining order

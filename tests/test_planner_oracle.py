@@ -31,12 +31,17 @@ def test_pin(nap, pin):
     pin(nap)
 
 
+# Planted mistakes, plus one reading: "domain_counter_first_advanced" is not a mistake against the
+# printed listing of Algorithm 1, which increments the domain counter before its first use (so the first
+# group would land in domain 1).  The oracle takes the reading that the first group lands in domain 0, as
+# the algorithm's figure deals threadblock groups round-robin starting from NAR domain 0; the pins fix
+# that reading, and the variant checks that they do.
 MUTANTS = {
     "join_fewest_shared": ("if best is None or shared[g_i] > shared[best]:",
                            "if best is None or shared[g_i] < shared[best]:"),
     "tie_to_latest_group": ("for g_i in sorted(shared):", "for g_i in sorted(shared, reverse=True):"),
     "sort_increasing": ("key=lambda g: (-len(groups[g]), g)", "key=lambda g: (len(groups[g]), g)"),
-    "domain_counter_first_advanced": ("nar = i % nar_max", "nar = (i + 1) % nar_max"),
+    "domain_counter_first_advanced": ("nar = i % nar_max", "nar = (i + 1) % nar_max"),  # the other reading
     "last_fitting_cu": ("                if R_cu[c] >= cs:\n                    cu = c\n                    break",
                         "                if R_cu[c] >= cs:\n                    cu = c"),
     "stack_ignores_budget": ("if R_st[s] >= cs:", "if True:"),
