@@ -156,6 +156,7 @@ nuna_status_t nuna_get_device_info(nuna_device_info_t* info);
 #define NUNA_MAP_XCD_GROUPS 1 /* logical groups of work items sharing a chunk, one XCD each */
 #define NUNA_MAP_XCD_PAGES 2  /* the chunks of each 4 KiB page on one XCD */
 #define NUNA_MAP_XCD_LISTS 3  /* per-XCD work lists from the placement planner (all-to-all) */
+#define NUNA_MAP_XCD_SHARDS 4 /* fused two-shot: every chunk of shard r on XCD r mod 8 */
 typedef struct {
     char kernels[96];           /* kernel names, '+'-separated, in launch order */
     int32_t launches;           /* kernels launched */
@@ -224,6 +225,9 @@ nuna_status_t nuna_set_max_workgroups(int max_workgroups);
  *                         the chunks of one page on one XCD
  *   NUNA_DIRECT_MAX_GRID  largest grid of the one-work-item-per-workgroup kernels,
  *                         0 (8192)..2^24; larger launches loop (persistent kernels)
+ *   NUNA_SHARD_XCD        fused two-shot, every chunk of shard r on XCD r mod 8: 0 (in XCD
+ *                         mode with 16 ranks, where it measured faster), 1 (never), 2 (in
+ *                         both modes with 8 or 16 ranks)
  *   NUNA_TWO_SHOT_FORM    NUNA_ALGO_TWO_SHOT: 0 (by size: fused, except 8 ranks of bf16
  *                         at 16-40 MiB per rank, which run the two kernels), 1 (fused
  *                         wherever it applies), 2 (always the two kernels)

@@ -31,6 +31,7 @@ struct Tuning {
     int page_groups = 0;               // XCD mode: 1 puts the chunks of a 4 KiB page on one XCD (direct kernels)
     int direct_max_grid = 0;           // largest grid of the direct kernels (0: 8192)
     int two_shot_form = 0;             // two-shot: 0 by size, 1 fused where it applies, 2 two kernels
+    int shard_xcd = 0;                 // fused two-shot shard-per-XCD order: 0 in XCD mode, 1 never, 2 always
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).
@@ -45,7 +46,7 @@ int64_t grid_limit(int64_t dflt);
 // its launches, every launcher appends to it.  map: the workgroup -> work
 // item map the launch ran (placement.h); group_size: work items per logical
 // group of that map.
-enum MapKind { kMapLinear = 0, kMapXcdGroups = 1, kMapXcdPages = 2, kMapXcdLists = 3 };
+enum MapKind { kMapLinear = 0, kMapXcdGroups = 1, kMapXcdPages = 2, kMapXcdLists = 3, kMapXcdShards = 4 };
 void note_launch(const char* kernel, int map, int64_t group_size, int64_t grid, int threads, int vpt);
 
 // One-shot all-reduce.  `dest_groups` > 1 selects the split variant: a work
@@ -59,7 +60,7 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
 bool two_shot_fused_ok(int P, size_t count, int dtype);
 // The fused form applies and is the one to run (size rule, NUNA_TWO_SHOT_FORM).
 bool two_shot_runs_fused(int P, size_t count, int dtype);
-hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype,
+hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype, int mode,
                                  hipStream_t stream);
 
 // Reduce-scatter: in[q] holds P*m elements; out[r][j] = sum_q in[q][r*m+j].

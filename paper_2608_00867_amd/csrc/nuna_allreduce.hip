@@ -181,13 +181,30 @@ __device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, in
     }
 }
 
-// Direct form: grid (chunks per shard, P), workgroup (c, r) runs chunk c of shard r.
-template <int PT, int DT, int VPT, bool WT>
+// Item order.  Chunk-major (the linear map): item w is chunk (w mod wcs) of
+// shard (w div wcs), so consecutive workgroups, which the hardware deals to
+// consecutive XCDs, take consecutive chunks of one shard.  Shard-interleaved
+// (XCD mode with a rank count that is a multiple of 8): item w is chunk
+// (w div P) of shard (w mod P), so workgroup b runs shard b mod P and, with
+// workgroup b on XCD b mod 8, every chunk of shard r runs on XCD r mod 8: the
+// reduce-scatter and all-gather work of simulated rank r stays on one XCD, as
+// a rank's own kernel would stay on its own device.
+
+// Direct form, one item per workgroup.  Chunk-major: grid (chunks per shard,
+// P), workgroup (c, r).  Shard-interleaved: grid P * wcs, workgroup b.
+template <int PT, int DT, int VPT, bool WT, bool ILV>
 __global__ __launch_bounds__(kWG) void k_two_shot_direct(Ptrs<PT> p, int64_t mv) {
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
-    const int64_t c = blockIdx.x;
-    const int r = static_cast<int>(blockIdx.y);
+    int64_t c;
+    int r;
+    if constexpr (ILV) {
+        c = blockIdx.x / PT;
+        r = static_cast<int>(blockIdx.x % PT);
+    } else {
+        c = blockIdx.x;
+        r = static_cast<int>(blockIdx.y);
+    }
     if ((c + 1) * cv <= mv)
         two_shot_chunk<PT, DT, VPT, true, WT>(p, mv, r, c, nt);
     else
@@ -195,18 +212,25 @@ __global__ __launch_bounds__(kWG) void k_two_shot_direct(Ptrs<PT> p, int64_t mv)
 }
 
 // Persistent form for grids beyond the direct limit or under a workgroup cap:
-// workgroup b runs items b, b + G, ... of the P * wcs items, item w being
-// chunk (w mod wcs) of shard (w div wcs).  Every item is its own logical
-// group, so both placement modes run this linear map.
-template <int PT, int DT, int VPT, bool WT>
+// workgroup b runs items b, b + G, ... of the P * wcs items, in chunk-major
+// or (ILV) shard-interleaved order.  With ILV and G a multiple of P, each
+// workgroup keeps to shard b mod P.
+template <int PT, int DT, int VPT, bool WT, bool ILV>
 __global__ __launch_bounds__(kWG) void k_two_shot(Ptrs<PT> p, int64_t mv, int64_t wcs) {
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     asm volatile("" ::"s"(mv), "s"(wcs), "s"(blockDim.x));
     const int64_t items = wcs * PT;
     for (int64_t w = blockIdx.x; w < items; w += gridDim.x) {
-        const int r = static_cast<int>(w / wcs);
-        const int64_t c = w - static_cast<int64_t>(r) * wcs;
+        int r;
+        int64_t c;
+        if constexpr (ILV) {
+            r = static_cast<int>(w % PT);
+            c = w / PT;
+        } else {
+            r = static_cast<int>(w / wcs);
+            c = w - static_cast<int64_t>(r) * wcs;
+        }
         if ((c + 1) * cv <= mv)
             two_shot_chunk<PT, DT, VPT, true, WT>(p, mv, r, c, nt);
         else
@@ -517,31 +541,43 @@ void launch_ar_direct_p(const void* const* in, void* const* out, int P, const Ar
     }
 }
 
-// Fused two-shot: the direct kernel (grid (wcs, P)) or the persistent one.
+// Fused two-shot: the direct kernel or the persistent one, in chunk-major or
+// (ilv, 8 and 16 ranks) shard-interleaved order.
 template <int PT, int DT, int VPT, bool WT>
 void launch_two_shot_t(const void* const* in, void* const* out, int64_t mv, int64_t wcs, int64_t G, bool direct,
-                       int nt, hipStream_t st) {
+                       bool ilv, int nt, hipStream_t st) {
     const Ptrs<PT> p = make_ptrs<PT>(in, out, PT, PT);
+    if constexpr (PT % 8 == 0) {
+        if (ilv) {
+            if (direct)
+                hipLaunchKernelGGL((k_two_shot_direct<PT, DT, VPT, WT, true>), dim3(static_cast<unsigned>(wcs * PT)),
+                                   dim3(nt), 0, st, p, mv);
+            else
+                hipLaunchKernelGGL((k_two_shot<PT, DT, VPT, WT, true>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st,
+                                   p, mv, wcs);
+            return;
+        }
+    }
     if (direct)
-        hipLaunchKernelGGL((k_two_shot_direct<PT, DT, VPT, WT>), dim3(static_cast<unsigned>(wcs), PT), dim3(nt), 0,
-                           st, p, mv);
+        hipLaunchKernelGGL((k_two_shot_direct<PT, DT, VPT, WT, false>), dim3(static_cast<unsigned>(wcs), PT), dim3(nt),
+                           0, st, p, mv);
     else
-        hipLaunchKernelGGL((k_two_shot<PT, DT, VPT, WT>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p, mv,
-                           wcs);
+        hipLaunchKernelGGL((k_two_shot<PT, DT, VPT, WT, false>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p,
+                           mv, wcs);
 }
 
 template <int DT, int VPT>
 void launch_two_shot_p(const void* const* in, void* const* out, int P, int64_t mv, int64_t wcs, int64_t G,
-                       bool direct, int nt, bool wt, hipStream_t st) {
+                       bool direct, bool ilv, int nt, bool wt, hipStream_t st) {
     switch (P) {
-        case 2: launch_two_shot_t<2, DT, VPT, false>(in, out, mv, wcs, G, direct, nt, st); break;
-        case 4: launch_two_shot_t<4, DT, VPT, false>(in, out, mv, wcs, G, direct, nt, st); break;
+        case 2: launch_two_shot_t<2, DT, VPT, false>(in, out, mv, wcs, G, direct, ilv, nt, st); break;
+        case 4: launch_two_shot_t<4, DT, VPT, false>(in, out, mv, wcs, G, direct, ilv, nt, st); break;
         case 8:
-            if (wt) launch_two_shot_t<8, DT, VPT, true>(in, out, mv, wcs, G, direct, nt, st);
-            else launch_two_shot_t<8, DT, VPT, false>(in, out, mv, wcs, G, direct, nt, st);
+            if (wt) launch_two_shot_t<8, DT, VPT, true>(in, out, mv, wcs, G, direct, ilv, nt, st);
+            else launch_two_shot_t<8, DT, VPT, false>(in, out, mv, wcs, G, direct, ilv, nt, st);
             break;
         default:
-            if constexpr (VPT != 8) launch_two_shot_t<16, DT, VPT, false>(in, out, mv, wcs, G, direct, nt, st);
+            if constexpr (VPT != 8) launch_two_shot_t<16, DT, VPT, false>(in, out, mv, wcs, G, direct, ilv, nt, st);
             break;
     }
 }
@@ -749,7 +785,7 @@ bool two_shot_runs_fused(int P, size_t count, int dtype) {
 // Fused two-shot all-reduce (k_two_shot_direct / k_two_shot): launch shape by
 // the bytes per rank, as for the one-shot (the two move the same bytes);
 // chunks are cut per shard.
-hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype,
+hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype, int mode,
                                  hipStream_t stream) {
     if (!two_shot_fused_ok(P, count, dtype)) return hipErrorInvalidValue;
     const size_t es = dtype_size(dtype);
@@ -766,17 +802,27 @@ hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P,
     const bool direct = G == items && items <= direct_max_grid();
     const int wtf = tuning().write_through;
     const bool wt = P == 8 && (wtf == 2 || (wtf == 0 && vpt == 8 && bytes >= (size_t(16) << 20)));
-    note_launch(direct ? "k_two_shot_direct" : "k_two_shot", kMapLinear, 1, direct ? items : G, nt, vpt);
+    // Shard-interleaved order (each shard's work on one XCD): in XCD mode with
+    // 16 ranks, where it measured faster on MI355X than the chunk-major order
+    // (cold: 3.45 against 3.71 us at 64 KiB per rank, 11.71 against 11.89 at
+    // 1 MiB, 51.3 against 52.0 at 4 MiB).  With 8 ranks it measured slower
+    // (4.29 against 4.02 us at 1 MiB per rank, 11.87 against 11.78 at 4 MiB,
+    // 184.1 against 178.6 at 64 MiB), so XCD mode keeps the chunk-major order
+    // there.  NUNA_SHARD_XCD: 0 by this rule, 1 never, 2 always (8 or 16 ranks).
+    const int sx = tuning().shard_xcd;
+    const bool ilv = P % 8 == 0 && (sx == 2 || (sx == 0 && mode == kPlaceXcd && P == 16));
+    note_launch(direct ? "k_two_shot_direct" : "k_two_shot", ilv ? kMapXcdShards : kMapLinear, ilv ? wcs : 1,
+                direct ? items : G, nt, vpt);
     if (dtype == kDtF32) {
-        if (vpt == 8) launch_two_shot_p<kDtF32, 8>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
-        else if (vpt == 4) launch_two_shot_p<kDtF32, 4>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
-        else if (vpt == 2) launch_two_shot_p<kDtF32, 2>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
-        else launch_two_shot_p<kDtF32, 1>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
+        if (vpt == 8) launch_two_shot_p<kDtF32, 8>(in, out, P, mv, wcs, G, direct, ilv, nt, wt, stream);
+        else if (vpt == 4) launch_two_shot_p<kDtF32, 4>(in, out, P, mv, wcs, G, direct, ilv, nt, wt, stream);
+        else if (vpt == 2) launch_two_shot_p<kDtF32, 2>(in, out, P, mv, wcs, G, direct, ilv, nt, wt, stream);
+        else launch_two_shot_p<kDtF32, 1>(in, out, P, mv, wcs, G, direct, ilv, nt, wt, stream);
     } else {
-        if (vpt == 8) launch_two_shot_p<kDtBf16, 8>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
-        else if (vpt == 4) launch_two_shot_p<kDtBf16, 4>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
-        else if (vpt == 2) launch_two_shot_p<kDtBf16, 2>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
-        else launch_two_shot_p<kDtBf16, 1>(in, out, P, mv, wcs, G, direct, nt, wt, stream);
+        if (vpt == 8) launch_two_shot_p<kDtBf16, 8>(in, out, P, mv, wcs, G, direct, ilv, nt, wt, stream);
+        else if (vpt == 4) launch_two_shot_p<kDtBf16, 4>(in, out, P, mv, wcs, G, direct, ilv, nt, wt, stream);
+        else if (vpt == 2) launch_two_shot_p<kDtBf16, 2>(in, out, P, mv, wcs, G, direct, ilv, nt, wt, stream);
+        else launch_two_shot_p<kDtBf16, 1>(in, out, P, mv, wcs, G, direct, ilv, nt, wt, stream);
     }
     return hipGetLastError();
 }

@@ -192,6 +192,7 @@ const TunableDef kTunables[] = {
     {"NUNA_PAGE_GROUPS", nullptr, &nuna::Tuning::page_groups, 0, 1, 0, {}},
     {"NUNA_DIRECT_MAX_GRID", nullptr, &nuna::Tuning::direct_max_grid, 0, 1 << 24, 0, {}},
     {"NUNA_TWO_SHOT_FORM", nullptr, &nuna::Tuning::two_shot_form, 0, 2, 0, {}},
+    {"NUNA_SHARD_XCD", nullptr, &nuna::Tuning::shard_xcd, 0, 2, 0, {}},
 };
 
 const TunableDef* find_tunable(const char* name) {
@@ -438,7 +439,8 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
         // Both phases in one kernel, or two kernels where the shapes need it or
         // they measured faster (two_shot_runs_fused).
         if (nuna::two_shot_runs_fused(P, count, dtype))
-            return hip_status(nuna::launch_two_shot_fused(in, out, P, count, dtype, stream), "two-shot launch");
+            return hip_status(nuna::launch_two_shot_fused(in, out, P, count, dtype, place, stream),
+                              "two-shot launch");
         a = NUNA_ALGO_TWO_SHOT_TWO_KERNELS;
     }
 

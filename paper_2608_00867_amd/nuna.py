@@ -53,7 +53,7 @@ class LaunchInfo(ctypes.Structure):
                 ("vectors_per_thread", ctypes.c_int32)]
 
 
-MAP_NAMES = {0: "linear", 1: "xcd_groups", 2: "xcd_pages", 3: "xcd_lists"}
+MAP_NAMES = {0: "linear", 1: "xcd_groups", 2: "xcd_pages", 3: "xcd_lists", 4: "xcd_shards"}
 
 
 class NapTopology(ctypes.Structure):

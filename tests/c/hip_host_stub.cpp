@@ -99,7 +99,7 @@ bool two_shot_fused_ok(int P, size_t count, int dtype) {
 
 bool two_shot_runs_fused(int P, size_t count, int dtype) { return two_shot_fused_ok(P, count, dtype); }
 
-hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype,
+hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype, int,
                                  hipStream_t) {
     check(two_shot_fused_ok(P, count, dtype), "fused two-shot launched where it does not apply");
     for (int r = 0; r < P; ++r) check(in[r] && out[r], "two-shot rank pointer");

@@ -457,7 +457,9 @@ def test_write_through_stores(nuna, cfg):
 
 
 @pytest.mark.parametrize("cfg", [dict(NUNA_VPT=v, NUNA_WG_THREADS=t) for v in (0, 1, 2, 4, 8) for t in (64, 256)] +
-                         [dict(NUNA_DIRECT_MAX_GRID=5), dict(NUNA_WRITE_THROUGH=2, NUNA_VPT=8, NUNA_WG_THREADS=256)],
+                         [dict(NUNA_DIRECT_MAX_GRID=5), dict(NUNA_WRITE_THROUGH=2, NUNA_VPT=8, NUNA_WG_THREADS=256),
+                          dict(NUNA_SHARD_XCD=2), dict(NUNA_SHARD_XCD=2, NUNA_DIRECT_MAX_GRID=5),
+                          dict(NUNA_SHARD_XCD=2, NUNA_MAX_GRID=13), dict(NUNA_SHARD_XCD=1)],
                          ids=lambda c: ",".join(f"{k[5:]}={v}" for k, v in c.items()))
 def test_two_shot_fused(nuna, cfg):
     """The fused two-shot (both phases per chunk in one kernel) at every launch shape, against the oracle
@@ -525,6 +527,12 @@ def test_launch_record_names_what_ran(nuna):
     assert _kernels(nuna, d1, "one_shot", "xcd")["map"] == "linear"
     r = _kernels(nuna, wl.ar_bf16_decode(64), "one_shot_split", "xcd")
     assert r["map"] == "xcd_groups" and r["group_size"] == 8, r
+    x16 = wl.normal_bf16(16, 1 << 16, 9)
+    assert _kernels(nuna, x16, "two_shot", "xcd")["map"] == "xcd_shards"
+    assert _kernels(nuna, x16, "two_shot", "linear")["map"] == "linear"
+    assert _kernels(nuna, x4, "two_shot", "xcd")["map"] == "linear"
+    with nuna.tunables(NUNA_SHARD_XCD=2):
+        assert _kernels(nuna, x4, "two_shot", "linear")["map"] == "xcd_shards"
 
 
 @pytest.mark.parametrize("pg", [0, 1])
