@@ -231,6 +231,10 @@ nuna_status_t nuna_set_max_workgroups(int max_workgroups);
  *   NUNA_TWO_SHOT_FORM    NUNA_ALGO_TWO_SHOT: 0 (by size: fused, except 8 ranks of bf16
  *                         at 16-40 MiB per rank, which run the two kernels), 1 (fused
  *                         wherever it applies), 2 (always the two kernels)
+ *   NUNA_STORE_GAP        pause between the stores of consecutive destinations when one
+ *                         result is stored to several outputs (one-shot and fused two-shot
+ *                         all-reduce, all-gather), in units of 8 wait states of the wave:
+ *                         -1 (by size: 1 from 32 MiB per rank, else 0), 0..32
  * Unknown names and values outside these sets: NUNA_ERR_INVALID_ARG. */
 nuna_status_t nuna_set_tunable(const char* name, int64_t value);
 nuna_status_t nuna_get_tunable(const char* name, int64_t* value);

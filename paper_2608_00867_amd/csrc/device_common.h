@@ -258,6 +258,21 @@ __device__ __forceinline__ void store_vecs_wt(uint4* chunk, const uint4 (&y)[VPT
     }
 }
 
+// Pause between the stores of consecutive destinations in a fan-out (one
+// result stored to several outputs): `gap` (uniform) times s_nop 7, i.e. at
+// least 8 * gap wait states of this wave.  Once its loads have landed, a
+// wave would otherwise issue its P output stores back to back, and across
+// the chip these store bursts cost HBM throughput on MI355X.  A plain
+// 8-in/8-out kernel at 64 MiB per rank took 200 us with back-to-back stores
+// and 179-182 us with any pause of 1-8 s_nop 7 or 1-3 s_sleep 1.  The
+// library's one-shot went from 184-196 us to 181-182 us with one pause.
+// Pauses cost latency on short launches (decode, 1 MiB per rank: 3.94 us
+// with none, 4.09 with two, 4.45 with four), so the launchers pause only
+// from 32 MiB per rank (store_gap_for).
+__device__ __forceinline__ void store_gap(int gap) {
+    for (int n = 0; n < gap; ++n) asm volatile("s_nop 7");
+}
+
 template <bool FULL, int VPT, bool NT = true>
 __device__ __forceinline__ void store_vecs(uint4* dst, const uint4 (&y)[VPT], int64_t v0, int nt, int64_t limit) {
 #pragma unroll

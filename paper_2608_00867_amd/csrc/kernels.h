@@ -32,6 +32,7 @@ struct Tuning {
     int direct_max_grid = 0;           // largest grid of the direct kernels (0: 8192)
     int two_shot_form = 0;             // two-shot: 0 by size, 1 fused where it applies, 2 two kernels
     int shard_xcd = 0;                 // fused two-shot shard-per-XCD order: 0 in XCD mode, 1 never, 2 always
+    int store_gap = -1;                // s_nop 7 pauses between a fan-out's per-destination stores: -1 by size
 };
 const Tuning& tuning();
 // Current workgroup cap (nuna_set_max_workgroups, else the tuning default).

@@ -24,7 +24,7 @@ struct ArShape {
     int32_t dpi;   // destinations per work item (P / group size)
     int32_t P;
     int32_t tail;  // elements after the last full vector
-    int32_t pad;
+    int32_t gap;   // store_gap between destinations
 };
 
 // WT: the item's stores use the system-scope cache policy (store_vecs_wt);
@@ -41,6 +41,7 @@ __device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const RankT
     if (PT > 0 && all_dests) {
 #pragma unroll
         for (int d = 0; d < (PT > 0 ? PT : 1); ++d) {
+            if (d > 0) store_gap(s.gap);
             if constexpr (WT)
                 store_vecs_wt<FULL, VPT>(out_ptr<PT>(p, tab, d) + cbase, y, static_cast<int>(threadIdx.x), nt,
                                          s.nvec - cbase);
@@ -49,7 +50,10 @@ __device__ __forceinline__ void allreduce_chunk(const Ptrs<MAXP>& p, const RankT
         }
     } else {
         const int d0 = g * s.dpi;
-        for (int d = d0; d < d0 + s.dpi; ++d) store_vecs<FULL, VPT>(out_ptr<PT>(p, tab, d), y, v0, nt, s.nvec);
+        for (int d = d0; d < d0 + s.dpi; ++d) {
+            if (d > d0) store_gap(s.gap);
+            store_vecs<FULL, VPT>(out_ptr<PT>(p, tab, d), y, v0, nt, s.nvec);
+        }
     }
 }
 
@@ -67,10 +71,11 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
         asm volatile("" ::"s"(p.in[0]), "s"(p.in[1]), "s"(p.in[2]), "s"(p.in[3]), "s"(p.in[4]), "s"(p.in[5]),
                      "s"(p.in[6]), "s"(p.in[7]), "s"(p.out[0]), "s"(p.out[1]), "s"(p.out[2]), "s"(p.out[3]),
                      "s"(p.out[4]), "s"(p.out[5]), "s"(p.out[6]), "s"(p.out[7]), "s"(s.nvec), "s"(s.dpi),
-                     "s"(s.tail), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize), "s"(pl.gshift), "s"(blockDim.x));
+                     "s"(s.tail), "s"(s.gap), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize), "s"(pl.gshift),
+                     "s"(blockDim.x));
     } else {
-        asm volatile("" ::"s"(s.nvec), "s"(s.dpi), "s"(s.tail), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize),
-                     "s"(pl.gshift), "s"(blockDim.x));
+        asm volatile("" ::"s"(s.nvec), "s"(s.dpi), "s"(s.tail), "s"(s.gap), "s"(pl.groups), "s"(pl.mode),
+                     "s"(pl.gsize), "s"(pl.gshift), "s"(blockDim.x));
     }
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
     for (int64_t i = it.first; i < it.end; i += it.stride) {
@@ -113,7 +118,7 @@ __global__ __launch_bounds__(kWG) void k_allreduce(Ptrs<MAXP> p, ArShape s, Plac
 // per launch at 1 MiB per rank on MI355X (5.3 against 4.2 us).
 template <int PT, int DT, int VPT, bool WT>
 __global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nvec, int32_t tail, int32_t gshift,
-                                                          int64_t nitems) {
+                                                          int64_t nitems, int32_t gap) {
     using A = Arith<DT>;
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
@@ -124,6 +129,7 @@ __global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nv
     s.nvec = nvec;
     s.dpi = PT;
     s.P = PT;
+    s.gap = gap;
     const RankTable tab{0u, 0u, 0u, 0u};  // compile-time rank count: pointers come from the arguments
     if ((c + 1) * cv <= nvec)
         allreduce_chunk<PT, DT, VPT, true, true, WT>(p, tab, s, PT, v0, nt, 0, true, c * cv);
@@ -155,7 +161,7 @@ __global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nv
 
 // Chunk c of shard r (vector offsets relative to the shard; mv vectors per shard).
 template <int PT, int DT, int VPT, bool FULL, bool WT>
-__device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, int r, int64_t c, int nt) {
+__device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, int r, int64_t c, int nt, int gap) {
     using A = Arith<DT>;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int64_t base = static_cast<int64_t>(r) * mv;
@@ -172,12 +178,18 @@ __device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, in
         store_vecs_wt<FULL, VPT>(p.out[r] + base + c * cv, y, lane, nt, mv - c * cv);
 #pragma unroll
         for (int d = 0; d < PT; ++d)
-            if (d != r) store_vecs_wt<FULL, VPT>(p.out[d] + base + c * cv, y, lane, nt, mv - c * cv);
+            if (d != r) {
+                store_gap(gap);
+                store_vecs_wt<FULL, VPT>(p.out[d] + base + c * cv, y, lane, nt, mv - c * cv);
+            }
     } else {
         store_vecs<FULL, VPT>(p.out[r] + base, y, v0, nt, mv);
 #pragma unroll
         for (int d = 0; d < PT; ++d)
-            if (d != r) store_vecs<FULL, VPT>(p.out[d] + base, y, v0, nt, mv);
+            if (d != r) {
+                store_gap(gap);
+                store_vecs<FULL, VPT>(p.out[d] + base, y, v0, nt, mv);
+            }
     }
 }
 
@@ -193,7 +205,7 @@ __device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, in
 // Direct form, one item per workgroup.  Chunk-major: grid (chunks per shard,
 // P), workgroup (c, r).  Shard-interleaved: grid P * wcs, workgroup b.
 template <int PT, int DT, int VPT, bool WT, bool ILV>
-__global__ __launch_bounds__(kWG) void k_two_shot_direct(Ptrs<PT> p, int64_t mv) {
+__global__ __launch_bounds__(kWG) void k_two_shot_direct(Ptrs<PT> p, int64_t mv, int32_t gap) {
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     int64_t c;
@@ -206,9 +218,9 @@ __global__ __launch_bounds__(kWG) void k_two_shot_direct(Ptrs<PT> p, int64_t mv)
         r = static_cast<int>(blockIdx.y);
     }
     if ((c + 1) * cv <= mv)
-        two_shot_chunk<PT, DT, VPT, true, WT>(p, mv, r, c, nt);
+        two_shot_chunk<PT, DT, VPT, true, WT>(p, mv, r, c, nt, gap);
     else
-        two_shot_chunk<PT, DT, VPT, false, WT>(p, mv, r, c, nt);
+        two_shot_chunk<PT, DT, VPT, false, WT>(p, mv, r, c, nt, gap);
 }
 
 // Persistent form for grids beyond the direct limit or under a workgroup cap:
@@ -216,10 +228,10 @@ __global__ __launch_bounds__(kWG) void k_two_shot_direct(Ptrs<PT> p, int64_t mv)
 // or (ILV) shard-interleaved order.  With ILV and G a multiple of P, each
 // workgroup keeps to shard b mod P.
 template <int PT, int DT, int VPT, bool WT, bool ILV>
-__global__ __launch_bounds__(kWG) void k_two_shot(Ptrs<PT> p, int64_t mv, int64_t wcs) {
+__global__ __launch_bounds__(kWG) void k_two_shot(Ptrs<PT> p, int64_t mv, int64_t wcs, int32_t gap) {
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
-    asm volatile("" ::"s"(mv), "s"(wcs), "s"(blockDim.x));
+    asm volatile("" ::"s"(mv), "s"(wcs), "s"(gap), "s"(blockDim.x));
     const int64_t items = wcs * PT;
     for (int64_t w = blockIdx.x; w < items; w += gridDim.x) {
         int r;
@@ -232,9 +244,9 @@ __global__ __launch_bounds__(kWG) void k_two_shot(Ptrs<PT> p, int64_t mv, int64_
             c = w - static_cast<int64_t>(r) * wcs;
         }
         if ((c + 1) * cv <= mv)
-            two_shot_chunk<PT, DT, VPT, true, WT>(p, mv, r, c, nt);
+            two_shot_chunk<PT, DT, VPT, true, WT>(p, mv, r, c, nt, gap);
         else
-            two_shot_chunk<PT, DT, VPT, false, WT>(p, mv, r, c, nt);
+            two_shot_chunk<PT, DT, VPT, false, WT>(p, mv, r, c, nt, gap);
     }
 }
 
@@ -520,7 +532,7 @@ void launch_ar_direct_t(const void* const* in, void* const* out, const ArShape& 
                         hipStream_t st) {
     const Ptrs<PT> p = make_ptrs<PT>(in, out, PT, PT);
     hipLaunchKernelGGL((k_allreduce_direct<PT, DT, VPT, WT>), dim3(static_cast<unsigned>(m.grid)), dim3(nt), 0, st, p,
-                       s.nvec, s.tail, m.gshift, m.items);
+                       s.nvec, s.tail, m.gshift, m.items, s.gap);
 }
 
 // Direct kernel for 2, 4, 8 or 16 ranks (8 vectors per thread: 2, 4 or 8 ranks);
@@ -547,23 +559,24 @@ template <int PT, int DT, int VPT, bool WT>
 void launch_two_shot_t(const void* const* in, void* const* out, int64_t mv, int64_t wcs, int64_t G, bool direct,
                        bool ilv, int nt, hipStream_t st) {
     const Ptrs<PT> p = make_ptrs<PT>(in, out, PT, PT);
+    const int32_t gap = store_gap_for(static_cast<size_t>(mv) * 16 * PT);
     if constexpr (PT % 8 == 0) {
         if (ilv) {
             if (direct)
                 hipLaunchKernelGGL((k_two_shot_direct<PT, DT, VPT, WT, true>), dim3(static_cast<unsigned>(wcs * PT)),
-                                   dim3(nt), 0, st, p, mv);
+                                   dim3(nt), 0, st, p, mv, gap);
             else
                 hipLaunchKernelGGL((k_two_shot<PT, DT, VPT, WT, true>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st,
-                                   p, mv, wcs);
+                                   p, mv, wcs, gap);
             return;
         }
     }
     if (direct)
         hipLaunchKernelGGL((k_two_shot_direct<PT, DT, VPT, WT, false>), dim3(static_cast<unsigned>(wcs), PT), dim3(nt),
-                           0, st, p, mv);
+                           0, st, p, mv, gap);
     else
         hipLaunchKernelGGL((k_two_shot<PT, DT, VPT, WT, false>), dim3(static_cast<unsigned>(G)), dim3(nt), 0, st, p,
-                           mv, wcs);
+                           mv, wcs, gap);
 }
 
 template <int DT, int VPT>
@@ -702,6 +715,7 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
     s.nvec = static_cast<int64_t>(bytes / 16);
     s.tail = static_cast<int32_t>((bytes % 16) / es);
     s.P = P;
+    s.gap = store_gap_for(bytes);
     const int gsize = dest_groups > 1 ? dest_groups : 1;
     s.dpi = P / gsize;
     int nt, vpt;

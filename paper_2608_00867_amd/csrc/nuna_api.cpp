@@ -193,6 +193,7 @@ const TunableDef kTunables[] = {
     {"NUNA_DIRECT_MAX_GRID", nullptr, &nuna::Tuning::direct_max_grid, 0, 1 << 24, 0, {}},
     {"NUNA_TWO_SHOT_FORM", nullptr, &nuna::Tuning::two_shot_form, 0, 2, 0, {}},
     {"NUNA_SHARD_XCD", nullptr, &nuna::Tuning::shard_xcd, 0, 2, 0, {}},
+    {"NUNA_STORE_GAP", nullptr, &nuna::Tuning::store_gap, -1, 32, 0, {}},
 };
 
 const TunableDef* find_tunable(const char* name) {

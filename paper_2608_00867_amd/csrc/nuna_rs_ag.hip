@@ -101,6 +101,8 @@ struct AgShape {
     int64_t wcs;  // chunks per shard
     int32_t P;
     int32_t dpi;  // destinations per item
+    int32_t gap;  // store_gap between destinations
+    int32_t pad;
 };
 
 // WT: write-through stores (store_vecs_wt); `cbase` is the chunk's first
@@ -115,6 +117,7 @@ __device__ __forceinline__ void all_gather_chunk(const RankTable& tab, const AgS
     for (int d = d0; d < d0 + s.dpi; ++d) {
         uint4* dst = rank_out(tab, d) + r * s.mv;
         if (dst == src) continue;  // in-place shard
+        if (d > d0) store_gap(s.gap);
         if constexpr (WT)
             store_vecs_wt<FULL, VPT>(dst + cbase, y, static_cast<int>(threadIdx.x), nt, s.mv - cbase);
         else
@@ -130,7 +133,7 @@ __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Pla
     __builtin_assume(pl.gsize > 0);  // the collectives always place uniform groups
     const RankTable tab = load_rank_table(p, s.P);
     // One use of every scalar argument the item loop needs: their loads issue together.
-    asm volatile("" ::"s"(s.mv), "s"(s.wcs), "s"(s.dpi), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize),
+    asm volatile("" ::"s"(s.mv), "s"(s.wcs), "s"(s.dpi), "s"(s.gap), "s"(pl.groups), "s"(pl.mode), "s"(pl.gsize),
                  "s"(pl.gshift), "s"(blockDim.x));
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
@@ -162,7 +165,7 @@ __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Pla
 // The source pointer is an argument indexed by the workgroup's y index; the
 // destinations are compile-time offsets (see k_allreduce_direct).
 template <int PT, int VPT, bool CACHED, bool WT>
-__global__ __launch_bounds__(kWG) void k_all_gather_direct(Ptrs<PT> p, int64_t mv) {
+__global__ __launch_bounds__(kWG) void k_all_gather_direct(Ptrs<PT> p, int64_t mv, int32_t gap) {
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int64_t c = blockIdx.x;
@@ -179,6 +182,7 @@ __global__ __launch_bounds__(kWG) void k_all_gather_direct(Ptrs<PT> p, int64_t m
     for (int d = 0; d < PT; ++d) {
         uint4* dst = p.out[d] + r * mv;
         if (dst == src) continue;  // in-place shard
+        if (d > 0) store_gap(gap);
         if constexpr (WT) {
             if (full)
                 store_vecs_wt<true, VPT>(dst + c * cv, y, static_cast<int>(threadIdx.x), nt, mv - c * cv);
@@ -331,17 +335,17 @@ void launch_ag_direct_p(const void* const* in, void* const* out, const AgShape& 
                         dim3 g, dim3 b, hipStream_t st) {
     const Ptrs<PT> p = make_ptrs<PT>(in, out, PT, PT);
     if (cached && wt && PT == 8) {
-        if (vpt == 4) hipLaunchKernelGGL((k_all_gather_direct<PT, 4, true, true>), g, b, 0, st, p, s.mv);
-        else if (vpt == 2) hipLaunchKernelGGL((k_all_gather_direct<PT, 2, true, true>), g, b, 0, st, p, s.mv);
-        else hipLaunchKernelGGL((k_all_gather_direct<PT, 1, true, true>), g, b, 0, st, p, s.mv);
+        if (vpt == 4) hipLaunchKernelGGL((k_all_gather_direct<PT, 4, true, true>), g, b, 0, st, p, s.mv, s.gap);
+        else if (vpt == 2) hipLaunchKernelGGL((k_all_gather_direct<PT, 2, true, true>), g, b, 0, st, p, s.mv, s.gap);
+        else hipLaunchKernelGGL((k_all_gather_direct<PT, 1, true, true>), g, b, 0, st, p, s.mv, s.gap);
     } else if (cached) {
-        if (vpt == 4) hipLaunchKernelGGL((k_all_gather_direct<PT, 4, true, false>), g, b, 0, st, p, s.mv);
-        else if (vpt == 2) hipLaunchKernelGGL((k_all_gather_direct<PT, 2, true, false>), g, b, 0, st, p, s.mv);
-        else hipLaunchKernelGGL((k_all_gather_direct<PT, 1, true, false>), g, b, 0, st, p, s.mv);
+        if (vpt == 4) hipLaunchKernelGGL((k_all_gather_direct<PT, 4, true, false>), g, b, 0, st, p, s.mv, s.gap);
+        else if (vpt == 2) hipLaunchKernelGGL((k_all_gather_direct<PT, 2, true, false>), g, b, 0, st, p, s.mv, s.gap);
+        else hipLaunchKernelGGL((k_all_gather_direct<PT, 1, true, false>), g, b, 0, st, p, s.mv, s.gap);
     } else {
-        if (vpt == 4) hipLaunchKernelGGL((k_all_gather_direct<PT, 4, false, false>), g, b, 0, st, p, s.mv);
-        else if (vpt == 2) hipLaunchKernelGGL((k_all_gather_direct<PT, 2, false, false>), g, b, 0, st, p, s.mv);
-        else hipLaunchKernelGGL((k_all_gather_direct<PT, 1, false, false>), g, b, 0, st, p, s.mv);
+        if (vpt == 4) hipLaunchKernelGGL((k_all_gather_direct<PT, 4, false, false>), g, b, 0, st, p, s.mv, s.gap);
+        else if (vpt == 2) hipLaunchKernelGGL((k_all_gather_direct<PT, 2, false, false>), g, b, 0, st, p, s.mv, s.gap);
+        else hipLaunchKernelGGL((k_all_gather_direct<PT, 1, false, false>), g, b, 0, st, p, s.mv, s.gap);
     }
 }
 
@@ -364,6 +368,7 @@ hipError_t launch_all_gather(const void* const* in, void* const* out, int P, siz
     AgShape s{};
     s.mv = static_cast<int64_t>(m * es / 16);
     s.P = P;
+    s.gap = store_gap_for(m * es * P);
     // Shape by the vectors each output rank receives (P shards of mv vectors).
     int nt, vpt;
     pick_ag_shape(s.mv * P, P, nt, vpt);

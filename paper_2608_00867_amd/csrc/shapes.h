@@ -20,6 +20,15 @@ inline bool direct_ranks(int P, int vpt) { return P == 2 || P == 4 || P == 8 || 
 // faster than the direct one on MI355X (184 against 209 us), while up to 8192
 // workgroups the direct kernels were as fast or faster at every size measured
 // (1-64 MiB per rank, 1-4 vectors per thread).
+// store_gap pauses of a fan-out kernel by the bytes each output rank
+// receives: one from 32 MiB per rank (long, throughput-bound launches), none
+// below (latency-bound ones), unless the tunable fixes the count.
+inline int store_gap_for(size_t bytes_per_rank) {
+    const int g = tuning().store_gap;
+    if (g >= 0) return g;
+    return bytes_per_rank >= (size_t(32) << 20) ? 1 : 0;
+}
+
 inline int64_t direct_max_grid() { return tuning().direct_max_grid > 0 ? tuning().direct_max_grid : 8192; }
 constexpr int64_t kAgDirectMaxGrid8 = int64_t(1) << 20;  // 8-rank all-gather (launch_all_gather)
 

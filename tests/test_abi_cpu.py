@@ -606,6 +606,19 @@ def test_new_tunables_accept_and_reject():
             nuna.set_tunable(name, bad)
 
 
+def test_store_gap_tunable():
+    """NUNA_STORE_GAP: -1 (by size, the default) or a fixed pause count 0..32."""
+    assert nuna.get_tunable("NUNA_STORE_GAP") == -1
+    with nuna.tunables(NUNA_STORE_GAP=0):
+        assert nuna.get_tunable("NUNA_STORE_GAP") == 0
+    with nuna.tunables(NUNA_STORE_GAP=32):
+        assert nuna.get_tunable("NUNA_STORE_GAP") == 32
+    assert nuna.get_tunable("NUNA_STORE_GAP") == -1
+    for bad in (-2, 33):
+        with pytest.raises(nuna.NunaError):
+            nuna.set_tunable("NUNA_STORE_GAP", bad)
+
+
 def test_last_launch_of_a_call_that_launched_nothing():
     """A call rejected by its argument checks, or with nothing to do, leaves an empty launch record."""
     assert nuna.allreduce_raw(None, None, 8, 16, nuna.BF16) == nuna.ERR_INVALID_ARG

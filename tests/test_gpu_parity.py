@@ -418,6 +418,50 @@ def test_launch_shape_variants(nuna, cfg):
             _ar_vs_oracle(nuna, wl.normal_bf16(P, n, 31 * P + n), f"{cfg} P={P} n={n}")
 
 
+@pytest.mark.parametrize("gap", [0, 1, 5])
+def test_store_gap_parity(nuna, gap):
+    """Pauses between the per-destination stores change timing only: the one-shot (with and without
+    destination split), the fused and two-kernel two-shot and the all-gather give the oracle's bits with
+    the pause count forced, at 2-16 ranks, ragged and multi-chunk sizes, in place and under a grid cap."""
+    with nuna.tunables(NUNA_STORE_GAP=gap):
+        for P, n in ((2, 70001), (4, 4097), (8, 1), (8, 4097), (8, 262144 + 24), (16, 70001)):
+            x = wl.normal_bf16(P, n, 37 * P + n + gap)
+            ref = oracle.allreduce(x)
+            for algo in ("one_shot", "one_shot_split", "two_shot", "two_shot_two_kernels"):
+                for place in PLACES:
+                    got = run_allreduce(nuna, x, algo, place)
+                    for d in range(P):
+                        assert_bitwise(got[d], ref[d], f"gap={gap} {algo} {place} P={P} n={n} rank {d}")
+        x = wl.normal_bf16(8, 8 * 70001, 41 + gap)
+        ref = oracle.allreduce(x)
+        with nuna.tunables(NUNA_TWO_SHOT_FORM=1):
+            got = run_allreduce(nuna, x, "two_shot", "xcd")
+        for d in range(8):
+            assert_bitwise(got[d], ref[d], f"gap={gap} fused two-shot rank {d}")
+        nuna.set_max_workgroups(13)
+        try:
+            got = run_allreduce(nuna, x, "one_shot", "linear")
+        finally:
+            nuna.set_max_workgroups(0)
+        for d in range(8):
+            assert_bitwise(got[d], ref[d], f"gap={gap} capped one-shot rank {d}")
+        bufs = [to_dev(a) for a in x]
+        nuna.allreduce(bufs, bufs, algo="one_shot", placement="xcd")
+        torch.cuda.synchronize()
+        for d in range(8):
+            assert_bitwise(to_host(bufs[d]), ref[d], f"gap={gap} in-place rank {d}")
+        for P, m in ((8, 4096), (8, 70001 * 8), (16, 1024)):
+            xs = wl.random_bits(P, m, np.uint16, 3 * m + P + gap)
+            ref = oracle.all_gather(xs)
+            ins = [to_dev(a) for a in xs]
+            for place in PLACES:
+                outs = [torch.empty(P * m, dtype=ins[0].dtype, device="cuda") for _ in range(P)]
+                nuna.all_gather(ins, outs, placement=place)
+                torch.cuda.synchronize()
+                for d in range(P):
+                    assert_bitwise(to_host(outs[d]), ref[d], f"gap={gap} AG {place} P={P} m={m} rank {d}")
+
+
 @pytest.mark.parametrize("cfg", [dict(NUNA_WRITE_THROUGH=w, NUNA_VPT=v, NUNA_WG_THREADS=t)
                                  for w in (1, 2) for v, t in ((0, 0), (1, 64), (2, 128), (4, 256), (8, 256))],
                          ids=lambda c: ",".join(f"{k[5:]}={v}" for k, v in c.items()))
