@@ -641,6 +641,8 @@ def full_sweep(nuna, torch, pool, args):
             combine_case(nuna, torch, pool, args, emit, T_tok)
     if want("copy_reference"):
         copy_case(nuna, torch, pool, args, emit)
+    if want("ref_stream"):
+        ref_stream_case(nuna, torch, pool, args, emit)
     if want("launch_floor"):
         launch_floor_case(nuna, torch, args, emit)
     f.close()
@@ -858,6 +860,50 @@ def copy_case(nuna, torch, pool, args, emit):
               "gbps_read_plus_write": round(2 * nb / (t["median"] * 1e-6) / 1e9, 1)})
         del g, pairs
         del s
+
+
+REF_STREAMS = (("read", 1, 512), ("read", 8, 64), ("write", 1, 512), ("write", 8, 64), ("copy", 1, 512),
+               ("copy", 2, 256), ("copy", 4, 128), ("copy", 8, 64))  # (kind, buffers, MiB per buffer)
+
+
+def ref_stream_case(nuna, torch, pool, args, emit):
+    """The plain access patterns that bound the collectives (nuna_ref_stream), cold, one 4 KiB item of every
+    buffer per workgroup: reads only, writes only, and copies of 1 to 8 buffers at once.  The 8-buffer rows
+    have the 8-rank all-reduce's streams at 64 MiB per rank (8 inputs and 8 outputs at one offset) without
+    the reduction; the 1-buffer rows, the same bytes in one stream."""
+    for kind, n, mib in REF_STREAMS:
+        nb = mib << 20
+        items = (nb + 4095) // 4096
+        per = {"read": n * nb + items * 16, "write": n * nb, "copy": 2 * n * nb}[kind]
+        moved = {"read": n * nb, "write": n * nb, "copy": 2 * n * nb}[kind]
+        nsets = max(1, min(pool.nbytes // per, math.ceil(COLD_SPAN / per)))
+        pool.off = 0
+        sets = []
+        for _ in range(nsets):
+            region = pool.take(per)
+            u8 = region.view(torch.uint8)
+            if kind == "read":
+                srcs = [u8[r * nb:(r + 1) * nb] for r in range(n)]
+                dsts = [u8[n * nb:n * nb + items * 16]]
+            elif kind == "write":
+                srcs, dsts = None, [u8[r * nb:(r + 1) * nb] for r in range(n)]
+            else:
+                srcs = [u8[r * nb:(r + 1) * nb] for r in range(n)]
+                dsts = [u8[(n + r) * nb:(n + r + 1) * nb] for r in range(n)]
+            sets.append((srcs, dsts))
+        calls = max(nsets, calls_for(moved))
+
+        def fn(i):
+            srcs, dsts = sets[i % nsets]
+            nuna.ref_stream(kind, srcs, dsts)
+
+        g = {"ref": capture(torch, fn, calls)}
+        t = stats(time_graphs(torch, g, calls, args.reps, args.warmup)["ref"])
+        gbps = moved / (t["median"] * 1e-6) / 1e9
+        emit({"workload": "ref_stream", "kind": kind, "buffers": n, "bytes_per_buffer": nb, "bytes_moved": moved,
+              "cache": "cold", "calls_per_graph": calls, "us": {k: round(v, 3) for k, v in t.items()},
+              "gbps": round(gbps, 1), "frac_hbm": round(gbps / HBM_PEAK_GBPS, 4)})
+        del g, sets
 
 
 # ---------------------------------------------------------------------------------------------- --interference

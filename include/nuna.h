@@ -550,6 +550,34 @@ nuna_status_t nuna_probe_load_latency_cus(const void* buf, size_t nbytes, size_t
                                           uint32_t* cycles, int32_t* cu_of, hipStream_t stream);
 
 /*
+ * Reference streams: the plain access patterns that bound the collectives'
+ * HBM rooflines (Sec. 6.1 reports collective bandwidth against what the
+ * memory system sustains), for calibration and comparison; not collectives.
+ * n buffers of `bytes` bytes each, n in {1, 2, 4, 8, 16}, bytes a multiple
+ * of 16 up to 2^34 (0: no launch).  Pointers 16-byte aligned; no written
+ * range may overlap another or any source (NUNA_ERR_OVERLAP).  One work item
+ * is 4 KiB of every buffer (one 16-byte vector per thread and buffer), one
+ * item per workgroup, like the collectives' one-vector launches; loads and
+ * stores are non-temporal.
+ *   NUNA_REF_READ   reads src[0..n); writes only dst[0]: one 16-byte checksum
+ *                   per item (the XOR of the item's vectors of all n buffers),
+ *                   so that the loads are kept.  A read item is b = 8/n
+ *                   consecutive 4 KiB blocks of every buffer (b = 1 for n >= 8),
+ *                   so that every thread has 8 or more loads in flight; dst[0]
+ *                   receives ceil(bytes / (b * 4096)) * 16 bytes.
+ *   NUNA_REF_WRITE  writes dst[0..n) (src unused, may be NULL): 16-byte vector
+ *                   v of buffer r holds the 32-bit words {v mod 2^32,
+ *                   v div 2^32, r, 0x52454631}.
+ *   NUNA_REF_COPY   dst[r] = src[r] for every r, each thread's n loads issued
+ *                   before its n stores.
+ * Errors: NUNA_ERR_INVALID_ARG (kind, n, bytes, NULL), NUNA_ERR_MISALIGNED,
+ * NUNA_ERR_OVERLAP, NUNA_ERR_HIP.
+ */
+typedef enum { NUNA_REF_READ = 0, NUNA_REF_WRITE = 1, NUNA_REF_COPY = 2 } nuna_ref_t;
+nuna_status_t nuna_ref_stream(nuna_ref_t kind, const void* const* src, void* const* dst, int n, size_t bytes,
+                              hipStream_t stream);
+
+/*
  * Plain device copy of `bytes` bytes (16-byte aligned pointers, no overlap):
  * the reference streaming kernel used to calibrate memory-traffic counters
  * and the copy-bandwidth ceiling.

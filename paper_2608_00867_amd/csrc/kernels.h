@@ -110,6 +110,11 @@ hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, co
 hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
 
 hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream);
+// Reference streams (nuna_ref_stream): kind 0 read, 1 write, 2 copy; n in {1, 2, 4, 8, 16};
+// bytes a multiple of 16.  Read: dst[0] receives one 16-byte checksum per item of
+// max(1, 8 / n) 4 KiB blocks.
+hipError_t launch_ref_stream(int kind, const void* const* src, void* const* dst, int n, size_t bytes,
+                             hipStream_t stream);
 
 // Per-compute-unit load-latency probe on XCD `xcd` (lines 2j and 2j + 1 of each
 // block for probe slot j; claimed: 257 zeroed int32 words).

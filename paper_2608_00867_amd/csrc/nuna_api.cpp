@@ -65,6 +65,9 @@ nuna_status_t hip_status(hipError_t e, const char* what) {
 // Largest byte count a single rank buffer may have (2^48 B keeps every
 // index computation far from int64 overflow).
 constexpr size_t kMaxBytes = size_t(1) << 48;
+// Reference streams: one 4 KiB item per workgroup, and a grid of at most 2^22
+// workgroups.
+constexpr size_t kRefMaxBytes = size_t(1) << 34;
 
 bool valid_dtype(int dt) { return dt == NUNA_F32 || dt == NUNA_BF16; }
 bool valid_place(int p) { return p == NUNA_PLACE_LINEAR || p == NUNA_PLACE_XCD; }
@@ -1049,6 +1052,35 @@ nuna_status_t nuna_probe_load_latency_cus(const void* buf, size_t nbytes, size_t
     return hip_status(nuna::launch_probe_latency_cus(buf, nblocks, static_cast<int64_t>(stride), xcd, work, cycles,
                                                      cu_of, stream),
                       "per-CU latency probe launch");
+}
+
+nuna_status_t nuna_ref_stream(nuna_ref_t kind, const void* const* src, void* const* dst, int n, size_t bytes,
+                              hipStream_t stream) try {
+    begin_launches();
+    if (kind != NUNA_REF_READ && kind != NUNA_REF_WRITE && kind != NUNA_REF_COPY)
+        return fail(NUNA_ERR_INVALID_ARG, "invalid reference stream kind %d", static_cast<int>(kind));
+    if (n != 1 && n != 2 && n != 4 && n != 8 && n != 16)
+        return fail(NUNA_ERR_INVALID_ARG, "n=%d: reference streams take 1, 2, 4, 8 or 16 buffers", n);
+    if (bytes % 16 != 0) return fail(NUNA_ERR_INVALID_ARG, "bytes %zu is not a multiple of 16", bytes);
+    if (bytes > kRefMaxBytes) return fail(NUNA_ERR_INVALID_ARG, "bytes %zu too large", bytes);
+    nuna_status_t st;
+    if (kind != NUNA_REF_WRITE && (st = check_ptr_array(src, n, "src"))) return st;
+    if ((st = check_ptr_array(const_cast<const void* const*>(dst), kind == NUNA_REF_READ ? 1 : n, "dst"))) return st;
+    if (bytes == 0) return ok();
+    SpanSet is, os;
+    if (kind != NUNA_REF_WRITE)
+        for (int r = 0; r < n; ++r) is.add(src[r], bytes, r);
+    if (kind == NUNA_REF_READ) {
+        const size_t item = static_cast<size_t>(n >= 8 ? 1 : 8 / n) * 4096;  // read item: 8/n blocks of 4 KiB
+        os.add(dst[0], (bytes + item - 1) / item * 16, 0);
+    }
+    else
+        for (int r = 0; r < n; ++r) os.add(dst[r], bytes, r);
+    if ((st = check_overlaps(is, os, [](const Span&, const Span&) { return false; }))) return st;
+    return hip_status(nuna::launch_ref_stream(static_cast<int>(kind), src, dst, n, bytes, stream),
+                      "reference stream launch");
+} catch (...) {
+    return host_exception();
 }
 
 nuna_status_t nuna_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {

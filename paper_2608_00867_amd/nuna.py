@@ -98,6 +98,7 @@ SIGNATURES = {
                               ctypes.c_int),
     "nuna_probe_xcc": ([ctypes.c_int, _vp, _vp, _vp], ctypes.c_int),
     "nuna_copy": ([_vp, _vp, ctypes.c_size_t, _vp], ctypes.c_int),
+    "nuna_ref_stream": ([ctypes.c_int, _vpp, _vpp, ctypes.c_int, ctypes.c_size_t, _vp], ctypes.c_int),
     "nuna_nap_topology_mi355x": ([ctypes.POINTER(NapTopology)], ctypes.c_int),
     "nuna_nap_plan": ([ctypes.POINTER(NapTopology), ctypes.c_int, ctypes.c_int64, _i64p, _i64p, _i64p, _i64p,
                        _i64p, _i32p, _i32p, _i32p, _i64p], ctypes.c_int),
@@ -567,6 +568,42 @@ def copy(dst, src, stream=None):
         raise ValueError("dst too small")
     _check(lib().nuna_copy(dst.data_ptr(), src.data_ptr(), nbytes, _stream(stream)))
     return dst
+
+
+REF_KINDS = {"read": 0, "write": 1, "copy": 2}
+
+
+def ref_read_checksum_bytes(n, nbytes):
+    """Bytes a reference read of n buffers of nbytes writes to dst[0]: one 16-byte checksum per item of
+    max(1, 8 // n) blocks of 4 KiB."""
+    item = (1 if n >= 8 else 8 // n) * 4096
+    return (nbytes + item - 1) // item * 16
+
+
+def ref_stream_raw(kind, src_ptrs, dst_ptrs, n, nbytes, stream=0):
+    """nuna_ref_stream on raw device addresses (lists of ints or None) and a raw stream handle;
+    returns the status code."""
+    src = _ptr_array(src_ptrs) if src_ptrs is not None else None
+    dst = _ptr_array(dst_ptrs) if dst_ptrs is not None else None
+    return lib().nuna_ref_stream(REF_KINDS[kind], src, dst, n, nbytes, stream)
+
+
+def ref_stream(kind, srcs, dsts, stream=None):
+    """Reference stream over CUDA tensors: "read" (srcs; dsts[0] receives ref_read_checksum_bytes of
+    checksums), "write" (dsts), or "copy" (dsts[r] = srcs[r]).  Every buffer holds the same number of
+    bytes."""
+    bufs = dsts if kind == "write" else srcs
+    nbytes = bufs[0].numel() * bufs[0].element_size()
+    if any(b.numel() * b.element_size() != nbytes for b in bufs):
+        raise ValueError("reference stream buffers differ in size")
+    if kind == "read" and dsts[0].numel() * dsts[0].element_size() < ref_read_checksum_bytes(len(srcs), nbytes):
+        raise ValueError("checksum buffer too small")
+    if kind == "copy" and (len(dsts) != len(srcs) or any(d.numel() * d.element_size() < nbytes for d in dsts)):
+        raise ValueError("copy destinations must match the sources")
+    n = len(bufs)
+    _check(ref_stream_raw(kind, None if kind == "write" else [s.data_ptr() for s in srcs],
+                          [d.data_ptr() for d in dsts], n, nbytes, _stream(stream)))
+    return dsts
 
 
 def probe_load_latency(buf, stride, line_offset, xcd, stream=None):

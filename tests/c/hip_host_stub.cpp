@@ -193,6 +193,16 @@ hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, co
 
 hipError_t launch_copy(void*, const void*, size_t, hipStream_t) { return hipSuccess; }
 
+hipError_t launch_ref_stream(int kind, const void* const* src, void* const* dst, int n, size_t bytes, hipStream_t) {
+    check(kind >= 0 && kind <= 2 && (n == 1 || n == 2 || n == 4 || n == 8 || n == 16) && bytes % 16 == 0 && bytes > 0,
+          "reference stream arguments");
+    for (int r = 0; r < n; ++r) {
+        if (kind != 1) check(src[r] != nullptr, "reference stream source");
+        if (kind != 0 || r == 0) check(dst[r] != nullptr, "reference stream destination");
+    }
+    return hipSuccess;
+}
+
 hipError_t launch_probe_latency_cus(const void*, int64_t nblocks, int64_t stride, int xcd, int32_t* claimed,
                                     uint32_t*, int32_t*, hipStream_t) {
     check(nblocks > 0 && stride >= 2 * kProbeCuSlotsMax * 128 && xcd >= 0 && xcd < 8 && claimed,

@@ -265,6 +265,27 @@ int main() {
     int32_t probe[64];
     expect(nuna_probe_xcc(0, probe, nullptr, nullptr) == NUNA_ERR_INVALID_ARG, "probe G=0", 0);
     expect(nuna_copy(nullptr, probe, 16, nullptr) == NUNA_ERR_INVALID_ARG, "copy null", 0);
+    {
+        // Reference streams: every kind at every buffer count through the launch stub, and refusals.
+        static unsigned char pool[32 * 8192 + 16] __attribute__((aligned(16)));
+        const void* src[16];
+        void* dst[16];
+        for (int r = 0; r < 16; ++r) {
+            src[r] = pool + r * 8192;
+            dst[r] = pool + (16 + r) * 8192;
+        }
+        for (int kind = 0; kind < 3; ++kind)
+            for (int n : {1, 2, 4, 8, 16})
+                expect(nuna_ref_stream(static_cast<nuna_ref_t>(kind), src, dst, n, 8192, nullptr) == NUNA_OK,
+                       "reference stream", kind * 100 + n);
+        expect(nuna_ref_stream(NUNA_REF_COPY, src, dst, 3, 8192, nullptr) == NUNA_ERR_INVALID_ARG, "ref n=3", 0);
+        void* src_as_dst[16];
+        for (int r = 0; r < 16; ++r) src_as_dst[r] = pool + r * 8192;
+        expect(nuna_ref_stream(NUNA_REF_COPY, src, src_as_dst, 2, 8192, nullptr) == NUNA_ERR_OVERLAP, "ref overlap",
+               0);
+        expect(nuna_ref_stream(NUNA_REF_WRITE, nullptr, dst, 16, 8192 + 16, nullptr) == NUNA_ERR_OVERLAP,
+               "ref write overlap", 0);
+    }
     const int sf = stub_failures();
     std::printf("sanitize driver: %d failed expectations, %d failed launch checks\n", g_bad, sf);
     return g_bad == 0 && sf == 0 ? 0 : 1;

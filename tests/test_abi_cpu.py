@@ -165,6 +165,43 @@ def test_copy_and_probe_validation():
     assert L.nuna_probe_xcc(8, None, None, None) == nuna.ERR_INVALID_ARG
 
 
+@no_gpu_only
+def test_ref_stream_validation():
+    """nuna_ref_stream refuses bad kinds, buffer counts, sizes, NULL, misaligned and overlapping buffers
+    before any launch; zero bytes is a no-op."""
+    MiB = 1 << 20
+    src = [BASE + r * 4 * MiB for r in range(8)]
+    dst = [BASE + (8 + r) * 4 * MiB for r in range(8)]
+    raw = nuna.ref_stream_raw
+    L = nuna.lib()
+    assert L.nuna_ref_stream(3, nuna._ptr_array(src), nuna._ptr_array(dst), 1, 4096, None) == nuna.ERR_INVALID_ARG
+    assert L.nuna_ref_stream(-1, nuna._ptr_array(src), nuna._ptr_array(dst), 1, 4096, None) == nuna.ERR_INVALID_ARG
+    for n in (0, 3, 5, 32):
+        assert raw("copy", src[:1] * max(n, 1), dst[:1] * max(n, 1), n, 4096) == nuna.ERR_INVALID_ARG
+    assert raw("copy", src, dst, 8, 4095 * 4) == nuna.ERR_INVALID_ARG      # not a multiple of 16
+    assert raw("copy", src, dst, 8, (1 << 34) + 16) == nuna.ERR_INVALID_ARG
+    assert raw("read", None, dst, 8, 4096) == nuna.ERR_INVALID_ARG
+    assert raw("copy", src, None, 8, 4096) == nuna.ERR_INVALID_ARG
+    assert raw("copy", src[:7] + [None], dst, 8, 4096) == nuna.ERR_INVALID_ARG
+    assert raw("write", None, dst[:3] + [None] + dst[4:], 8, 4096) == nuna.ERR_INVALID_ARG
+    assert raw("copy", src[:7] + [src[7] + 8], dst, 8, 4096) == nuna.ERR_MISALIGNED
+    assert raw("read", src, [dst[0] + 4], 8, 4096) == nuna.ERR_MISALIGNED
+    # overlaps: a copy destination on a source, two write destinations, the read checksums on a source
+    assert raw("copy", src, dst[:7] + [src[3] + 4096], 8, 8192) == nuna.ERR_OVERLAP
+    assert raw("write", None, dst[:7] + [dst[6] + 4096], 8, 8192) == nuna.ERR_OVERLAP
+    assert raw("read", src, [src[5] + 4 * MiB - 16], 8, 4 * MiB) == nuna.ERR_OVERLAP
+    # a read's checksum range is ceil(bytes / item) * 16 bytes, item = max(1, 8 / n) * 4 KiB: 4 MiB + 16
+    # bytes of 8 sources need 1025 checksums, so a range starting 1024 vectors below a source reaches
+    # into it; with one source (32 KiB items) 129 checksums reach 16 bytes into it
+    assert raw("read", src, [src[1] - 1024 * 16], 8, 4 * MiB + 16) == nuna.ERR_OVERLAP
+    assert raw("read", src[1:2], [src[1] - 128 * 16], 1, 4 * MiB + 16) == nuna.ERR_OVERLAP
+    assert nuna.ref_read_checksum_bytes(1, 4 * MiB + 16) == 129 * 16
+    assert nuna.ref_read_checksum_bytes(8, 4 * MiB + 16) == 1025 * 16
+    for kind in ("read", "write", "copy"):
+        assert raw(kind, None if kind == "write" else src, dst, 8, 0) == nuna.OK
+    assert nuna.last_launch()["launches"] == 0
+
+
 def test_init_without_device_fails_cleanly():
     if _gpu_visible():
         pytest.skip("GPU visible")

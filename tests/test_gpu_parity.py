@@ -980,6 +980,51 @@ def test_copy_kernel(nuna):
         assert int(dst[nbytes:].abs().sum()) == 0
 
 
+@pytest.mark.parametrize("n", [1, 2, 4, 8, 16])
+def test_ref_streams(nuna, n):
+    """Reference read / write / copy streams over n buffers: the read's per-item XOR checksums, the write
+    pattern and the copies, at one partial item, one item, and many items with a partial last one, with
+    guard bands after every written range."""
+    for nbytes in (16, 4096, 4096 * 5 + 48, (1 << 20) + 4096):
+        words = nbytes // 4
+        nv = nbytes // 16
+        blocks = 1 if n >= 8 else 8 // n                # 4 KiB blocks per read item
+        items = (nbytes + blocks * 4096 - 1) // (blocks * 4096)
+        assert nuna.ref_read_checksum_bytes(n, nbytes) == items * 16
+        srcs = [torch.randint(-2 ** 31, 2 ** 31 - 1, (words,), dtype=torch.int32, device="cuda") for _ in range(n)]
+        host = np.stack([s.cpu().numpy().view(np.uint32).reshape(nv, 4) for s in srcs])
+        # read: one checksum per item, the XOR of the item's vectors of all buffers
+        sink = torch.zeros(items * 4 + 16, dtype=torch.int32, device="cuda")
+        nuna.ref_stream("read", srcs, [sink[:items * 4]])
+        torch.cuda.synchronize()
+        padded = np.zeros((n, items * blocks * 256, 4), dtype=np.uint32)
+        padded[:, :nv] = host
+        per_item = padded.reshape(n, items, blocks * 256, 4)
+        want = np.bitwise_xor.reduce(np.bitwise_xor.reduce(per_item, axis=2), axis=0)
+        got = sink.cpu().numpy().view(np.uint32)
+        assert np.array_equal(got[:items * 4].reshape(items, 4), want), f"read n={n} bytes={nbytes}"
+        assert not got[items * 4:].any(), f"read n={n} bytes={nbytes}: write past the checksums"
+        # write: vector v of buffer r = {v mod 2^32, v div 2^32, r, 0x52454631}
+        outs = [torch.full((words + 16,), -1, dtype=torch.int32, device="cuda") for _ in range(n)]
+        nuna.ref_stream("write", None, [o[:words] for o in outs])
+        torch.cuda.synchronize()
+        v = np.arange(nv, dtype=np.uint64)
+        for r in range(n):
+            g = outs[r].cpu().numpy().view(np.uint32)
+            w = np.stack([(v & 0xFFFFFFFF).astype(np.uint32), (v >> 32).astype(np.uint32),
+                          np.full(nv, r, dtype=np.uint32), np.full(nv, 0x52454631, dtype=np.uint32)], axis=1)
+            assert np.array_equal(g[:words].reshape(nv, 4), w), f"write n={n} bytes={nbytes} buffer {r}"
+            assert np.all(g[words:] == 0xFFFFFFFF), f"write n={n} bytes={nbytes} buffer {r}: past the end"
+        # copy
+        outs = [torch.full((words + 16,), -1, dtype=torch.int32, device="cuda") for _ in range(n)]
+        nuna.ref_stream("copy", srcs, [o[:words] for o in outs])
+        torch.cuda.synchronize()
+        for r in range(n):
+            g = outs[r].cpu().numpy().view(np.uint32)
+            assert np.array_equal(g[:words].reshape(nv, 4), host[r]), f"copy n={n} bytes={nbytes} buffer {r}"
+            assert np.all(g[words:] == 0xFFFFFFFF), f"copy n={n} bytes={nbytes} buffer {r}: past the end"
+
+
 def test_concurrent_host_threads(nuna):
     """Four host threads, each on its own stream, issue all-reduces, reduce-scatters, all-gathers,
     dispatches and combines at the same time (one layout shared by all); every result keeps the
