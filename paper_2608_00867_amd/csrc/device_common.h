@@ -137,6 +137,64 @@ Ptrs<MAXP> make_ptrs(const void* const* in, void* const* out, int nin, int nout)
     return p;
 }
 
+// Direct kernels with 2, 4 or 8 ranks: one use of every rank pointer and of
+// the given scalar arguments in a single statement, so that the kernel's
+// first round of scalar loads brings all of them.  Without it the compiler
+// loads a pointer where it is first used: a chain of argument loads behind
+// the kernel's early tests, and a load and wait before a store to each
+// output, each a round trip a short launch pays (0.12-0.15 us per call of
+// the 8-rank one-shot at 16-256 KiB per rank on MI355X).
+#define NUNA_PIN_PTRS8(p)                                                                                  \
+    "s"(p.in[0]), "s"(p.in[1]), "s"(p.in[2]), "s"(p.in[3]), "s"(p.in[4]), "s"(p.in[5]), "s"(p.in[6]),         \
+        "s"(p.in[7]), "s"(p.out[0]), "s"(p.out[1]), "s"(p.out[2]), "s"(p.out[3]), "s"(p.out[4]), "s"(p.out[5]), \
+        "s"(p.out[6]), "s"(p.out[7])
+#define NUNA_PIN_PTRS4(p) \
+    "s"(p.in[0]), "s"(p.in[1]), "s"(p.in[2]), "s"(p.in[3]), "s"(p.out[0]), "s"(p.out[1]), "s"(p.out[2]), "s"(p.out[3])
+#define NUNA_PIN_PTRS2(p) "s"(p.in[0]), "s"(p.in[1]), "s"(p.out[0]), "s"(p.out[1])
+
+template <int PT, class A, class B, class C>
+__device__ __forceinline__ void pin_args(const Ptrs<PT>& p, A a, B b, C c) {
+    if constexpr (PT == 8)
+        asm volatile("" ::NUNA_PIN_PTRS8(p), "s"(a), "s"(b), "s"(c));
+    else if constexpr (PT == 4)
+        asm volatile("" ::NUNA_PIN_PTRS4(p), "s"(a), "s"(b), "s"(c));
+    else if constexpr (PT == 2)
+        asm volatile("" ::NUNA_PIN_PTRS2(p), "s"(a), "s"(b), "s"(c));
+    else
+        asm volatile("" ::"s"(a), "s"(b), "s"(c));
+}
+
+template <int PT, class A, class B, class C, class D, class E, class F>
+__device__ __forceinline__ void pin_args(const Ptrs<PT>& p, A a, B b, C c, D d, E e, F f) {
+    if constexpr (PT == 8)
+        asm volatile("" ::NUNA_PIN_PTRS8(p), "s"(a), "s"(b), "s"(c), "s"(d), "s"(e), "s"(f));
+    else if constexpr (PT == 4)
+        asm volatile("" ::NUNA_PIN_PTRS4(p), "s"(a), "s"(b), "s"(c), "s"(d), "s"(e), "s"(f));
+    else if constexpr (PT == 2)
+        asm volatile("" ::NUNA_PIN_PTRS2(p), "s"(a), "s"(b), "s"(c), "s"(d), "s"(e), "s"(f));
+    else
+        asm volatile("" ::"s"(a), "s"(b), "s"(c), "s"(d), "s"(e), "s"(f));
+}
+
+// Rank r's pointer for a uniform run-time r, chosen among the pointers
+// already in SGPRs (a chain of scalar selects) instead of a scalar load from
+// the argument segment.
+template <int PT>
+__device__ __forceinline__ const uint4* in_at(const Ptrs<PT>& p, int r) {
+    const uint4* x = p.in[0];
+#pragma unroll
+    for (int q = 1; q < PT; ++q) x = r == q ? p.in[q] : x;
+    return x;
+}
+
+template <int PT>
+__device__ __forceinline__ uint4* out_at(const Ptrs<PT>& p, int r) {
+    uint4* x = p.out[0];
+#pragma unroll
+    for (int q = 1; q < PT; ++q) x = r == q ? p.out[q] : x;
+    return x;
+}
+
 // Rank pointer table.  With a handful of ranks the kernels index the
 // kernel-argument pointer array with compile-time offsets, and the pointers
 // arrive in SGPRs with the first scalar loads.  With many ranks, or a rank

@@ -120,6 +120,7 @@ template <int PT, int DT, int VPT, bool WT>
 __global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nvec, int32_t tail, int32_t gshift,
                                                           int64_t nitems, int32_t gap) {
     using A = Arith<DT>;
+    pin_args(p, nvec, tail, gshift, nitems, gap, blockDim.x);
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int64_t c = page_item(blockIdx.x, gshift);
@@ -160,7 +161,10 @@ __global__ __launch_bounds__(kWG) void k_allreduce_direct(Ptrs<PT> p, int64_t nv
 // the work of the workgroups with y = r here.
 
 // Chunk c of shard r (vector offsets relative to the shard; mv vectors per shard).
-template <int PT, int DT, int VPT, bool FULL, bool WT>
+// SEL: the owner's output pointer is picked among the pinned pointers (direct
+// kernel); otherwise it is loaded from the arguments, which keeps the
+// persistent kernel's loop from holding every pointer in SGPRs.
+template <int PT, int DT, int VPT, bool FULL, bool WT, bool SEL>
 __device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, int r, int64_t c, int nt, int gap) {
     using A = Arith<DT>;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
@@ -175,7 +179,7 @@ __device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, in
     // Reduce-scatter phase: the owner's shard.  All-gather phase: every other rank.
     if constexpr (WT) {
         const int lane = static_cast<int>(threadIdx.x);
-        store_vecs_wt<FULL, VPT>(p.out[r] + base + c * cv, y, lane, nt, mv - c * cv);
+        store_vecs_wt<FULL, VPT>((SEL ? out_at(p, r) : p.out[r]) + base + c * cv, y, lane, nt, mv - c * cv);
 #pragma unroll
         for (int d = 0; d < PT; ++d)
             if (d != r) {
@@ -183,7 +187,7 @@ __device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, in
                 store_vecs_wt<FULL, VPT>(p.out[d] + base + c * cv, y, lane, nt, mv - c * cv);
             }
     } else {
-        store_vecs<FULL, VPT>(p.out[r] + base, y, v0, nt, mv);
+        store_vecs<FULL, VPT>((SEL ? out_at(p, r) : p.out[r]) + base, y, v0, nt, mv);
 #pragma unroll
         for (int d = 0; d < PT; ++d)
             if (d != r) {
@@ -206,6 +210,7 @@ __device__ __forceinline__ void two_shot_chunk(const Ptrs<PT>& p, int64_t mv, in
 // P), workgroup (c, r).  Shard-interleaved: grid P * wcs, workgroup b.
 template <int PT, int DT, int VPT, bool WT, bool ILV>
 __global__ __launch_bounds__(kWG) void k_two_shot_direct(Ptrs<PT> p, int64_t mv, int32_t gap) {
+    pin_args(p, mv, gap, blockDim.x);
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     int64_t c;
@@ -218,9 +223,9 @@ __global__ __launch_bounds__(kWG) void k_two_shot_direct(Ptrs<PT> p, int64_t mv,
         r = static_cast<int>(blockIdx.y);
     }
     if ((c + 1) * cv <= mv)
-        two_shot_chunk<PT, DT, VPT, true, WT>(p, mv, r, c, nt, gap);
+        two_shot_chunk<PT, DT, VPT, true, WT, (PT <= 8)>(p, mv, r, c, nt, gap);
     else
-        two_shot_chunk<PT, DT, VPT, false, WT>(p, mv, r, c, nt, gap);
+        two_shot_chunk<PT, DT, VPT, false, WT, (PT <= 8)>(p, mv, r, c, nt, gap);
 }
 
 // Persistent form for grids beyond the direct limit or under a workgroup cap:
@@ -244,9 +249,9 @@ __global__ __launch_bounds__(kWG) void k_two_shot(Ptrs<PT> p, int64_t mv, int64_
             c = w - static_cast<int64_t>(r) * wcs;
         }
         if ((c + 1) * cv <= mv)
-            two_shot_chunk<PT, DT, VPT, true, WT>(p, mv, r, c, nt, gap);
+            two_shot_chunk<PT, DT, VPT, true, WT, false>(p, mv, r, c, nt, gap);
         else
-            two_shot_chunk<PT, DT, VPT, false, WT>(p, mv, r, c, nt, gap);
+            two_shot_chunk<PT, DT, VPT, false, WT, false>(p, mv, r, c, nt, gap);
     }
 }
 

@@ -17,7 +17,9 @@ struct RsShape {
     int32_t pad;
 };
 
-template <int PT, int DT, int VPT, bool FULL, bool KEEP, int MAXP>
+// SEL: the output pointer of shard r is picked among the pinned pointers
+// (direct kernel, up to 8 ranks) instead of loaded from the arguments.
+template <int PT, int DT, int VPT, bool FULL, bool KEEP, int MAXP, bool SEL = false>
 __device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const RankTable& tab, const RsShape& s,
                                                      int P, int64_t r, int64_t v0, int nt) {
     using A = Arith<DT>;
@@ -26,7 +28,12 @@ __device__ __forceinline__ void reduce_scatter_chunk(const Ptrs<MAXP>& p, const 
     uint4 y[VPT];
 #pragma unroll
     for (int j = 0; j < VPT; ++j) y[j] = A::narrow(acc[j]);
-    store_vecs<FULL, VPT, !KEEP>(use_table<PT>() ? rank_out(tab, static_cast<int>(r)) : p.out[r], y, v0, nt, s.mv);
+    uint4* dst;
+    if constexpr (SEL)
+        dst = out_at(p, static_cast<int>(r));
+    else
+        dst = use_table<PT>() ? rank_out(tab, static_cast<int>(r)) : p.out[r];
+    store_vecs<FULL, VPT, !KEEP>(dst, y, v0, nt, s.mv);
 }
 
 // KEEP: the shard is read again right away (the all-gather phase of a two-shot
@@ -65,6 +72,7 @@ __global__ __launch_bounds__(kWG) void k_reduce_scatter(Ptrs<MAXP> p, RsShape s,
 // offsets (see k_allreduce_direct).
 template <int PT, int DT, int VPT, bool KEEP>
 __global__ __launch_bounds__(kWG) void k_reduce_scatter_direct(Ptrs<PT> p, int64_t mv) {
+    pin_args(p, mv, blockDim.x, blockIdx.y);
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int64_t c = blockIdx.x;
@@ -75,9 +83,9 @@ __global__ __launch_bounds__(kWG) void k_reduce_scatter_direct(Ptrs<PT> p, int64
     s.P = PT;
     const RankTable tab{0u, 0u, 0u, 0u};  // compile-time rank count: pointers come from the arguments
     if ((c + 1) * cv <= mv)
-        reduce_scatter_chunk<PT, DT, VPT, true, KEEP>(p, tab, s, PT, r, v0, nt);
+        reduce_scatter_chunk<PT, DT, VPT, true, KEEP, PT, (PT <= 8)>(p, tab, s, PT, r, v0, nt);
     else
-        reduce_scatter_chunk<PT, DT, VPT, false, KEEP>(p, tab, s, PT, r, v0, nt);
+        reduce_scatter_chunk<PT, DT, VPT, false, KEEP, PT, (PT <= 8)>(p, tab, s, PT, r, v0, nt);
 }
 
 // Element-wise fallback when a shard is not a whole number of 16-byte vectors.
@@ -166,12 +174,13 @@ __global__ __launch_bounds__(kWG) void k_all_gather(Ptrs<MAXP> p, AgShape s, Pla
 // destinations are compile-time offsets (see k_allreduce_direct).
 template <int PT, int VPT, bool CACHED, bool WT>
 __global__ __launch_bounds__(kWG) void k_all_gather_direct(Ptrs<PT> p, int64_t mv, int32_t gap) {
+    pin_args(p, mv, gap, blockDim.x);
     const int nt = blockDim.x;
     const int64_t cv = static_cast<int64_t>(nt) * VPT;
     const int64_t c = blockIdx.x;
     const int r = static_cast<int>(blockIdx.y);
     const int64_t v0 = c * cv + threadIdx.x;
-    const uint4* src = p.in[r];
+    const uint4* src = in_at(p, r);
     uint4 y[VPT];
     const bool full = (c + 1) * cv <= mv;
     if (full)
