@@ -25,18 +25,27 @@ __global__ __launch_bounds__(64) void k_probe_xcc(int32_t* xcc, int32_t* hw_id) 
 // Reference copy.  It streams past the caches the way the collectives do
 // (non-temporal 16-byte loads and stores), so its traffic-counter readings
 // calibrate theirs and its speed is the ceiling a plain read+write reaches.
-// One vector per thread, one 4 KiB item per workgroup (a grid-stride loop
-// only beyond 2^22 workgroups): on MI355X this shape copied 512 MiB, cold,
-// at 6.5 TB/s, against 6.1-6.3 TB/s for persistent grids with 4 vectors per
-// thread and 5.1-6.0 TB/s with 2, 8 or 16 vectors per thread per item.
+// U vectors per thread per pass of a grid-stride loop.  From 32 MiB: U = 1,
+// one 4 KiB item per workgroup (2^22 workgroups at most), which copied
+// 128-512 MiB, cold, on MI355X at 6.3-6.5 TB/s against 6.1-6.2 TB/s for a
+// persistent grid of 4096 workgroups with U = 4.  Below 32 MiB the persistent
+// U = 4 grid was faster (16 MiB: 5.8 against 6.9 us) and runs.
+template <int U>
 __global__ __launch_bounds__(kWG) void k_copy(uint4* __restrict__ dst, const uint4* __restrict__ src, int64_t nvec,
                                               unsigned char* __restrict__ dst_tail,
                                               const unsigned char* __restrict__ src_tail, int tail) {
     // One use of every argument: their loads issue together (as in the collectives).
     asm volatile("" ::"s"(dst), "s"(src), "s"(nvec), "s"(dst_tail), "s"(src_tail), "s"(tail));
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kWG;
-    for (int64_t v = blockIdx.x * static_cast<int64_t>(kWG) + threadIdx.x; v < nvec; v += stride)
-        store_stream(dst + v, load16<true>(src + v));
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kWG * U;
+    for (int64_t v = blockIdx.x * static_cast<int64_t>(kWG) * U + threadIdx.x; v < nvec; v += stride) {
+        uint4 y[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (v + u * kWG < nvec) y[u] = load16<true>(src + v + u * kWG);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (v + u * kWG < nvec) store_stream(dst + v + u * kWG, y[u]);
+    }
     if (blockIdx.x == 0 && static_cast<int>(threadIdx.x) < tail) dst_tail[threadIdx.x] = src_tail[threadIdx.x];
 }
 
@@ -289,12 +298,20 @@ hipError_t launch_ref_stream(int kind, const void* const* src, void* const* dst,
 hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t stream) {
     const int64_t nvec = static_cast<int64_t>(bytes / 16);
     const int tail = static_cast<int>(bytes % 16);
-    int64_t G = (nvec + kWG - 1) / kWG;
-    if (G > (int64_t(1) << 22)) G = int64_t(1) << 22;
-    if (G < 1) G = 1;
-    hipLaunchKernelGGL(k_copy, dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, static_cast<uint4*>(dst),
-                       static_cast<const uint4*>(src), nvec, static_cast<unsigned char*>(dst) + nvec * 16,
-                       static_cast<const unsigned char*>(src) + nvec * 16, tail);
+    uint4* d = static_cast<uint4*>(dst);
+    const uint4* s = static_cast<const uint4*>(src);
+    unsigned char* dt = static_cast<unsigned char*>(dst) + nvec * 16;
+    const unsigned char* st = static_cast<const unsigned char*>(src) + nvec * 16;
+    if (bytes >= (size_t(32) << 20)) {
+        int64_t G = (nvec + kWG - 1) / kWG;
+        if (G > (int64_t(1) << 22)) G = int64_t(1) << 22;
+        hipLaunchKernelGGL(k_copy<1>, dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, d, s, nvec, dt, st, tail);
+    } else {
+        int64_t G = (nvec + kWG * 4 - 1) / (kWG * 4);
+        if (G > 4096) G = 4096;
+        if (G < 1) G = 1;
+        hipLaunchKernelGGL(k_copy<4>, dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, d, s, nvec, dt, st, tail);
+    }
     return hipGetLastError();
 }
 
