@@ -283,7 +283,8 @@ hipError_t launch_ref_stream(int kind, const void* const* src, void* const* dst,
     const Ptrs<16> p = make_ptrs<16>(kind == 1 ? nullptr : src, dst, kind == 1 ? 0 : n, kind == 0 ? 1 : n);
     const int gap = store_gap_for(bytes * static_cast<size_t>(n));
     static const char* const names[3] = {"k_ref_read", "k_ref_write", "k_ref_copy"};
-    note_launch(names[kind], kMapLinear, 1, G, kWG, 1);
+    const int64_t blocks = kind == 0 ? (n >= 8 ? 1 : 8 / n) : 1;  // 4 KiB blocks per item (ref_read_blocks)
+    note_launch(names[kind], kMapLinear, 1, (G + blocks - 1) / blocks, kWG, static_cast<int>(blocks));
     switch (n) {
         case 1: launch_ref_t<1>(kind, p, nvec, G, gap, stream); break;
         case 2: launch_ref_t<2>(kind, p, nvec, G, gap, stream); break;

@@ -996,6 +996,8 @@ def test_ref_streams(nuna, n):
         # read: one checksum per item, the XOR of the item's vectors of all buffers
         sink = torch.zeros(items * 4 + 16, dtype=torch.int32, device="cuda")
         nuna.ref_stream("read", srcs, [sink[:items * 4]])
+        rec = nuna.last_launch()
+        assert rec["kernels"] == "k_ref_read" and rec["grid"] == items and rec["vectors_per_thread"] == blocks
         torch.cuda.synchronize()
         padded = np.zeros((n, items * blocks * 256, 4), dtype=np.uint32)
         padded[:, :nv] = host
