@@ -288,6 +288,7 @@ def test_reduce_scatter(nuna, P, m, dtype, place):
 
 @pytest.mark.parametrize("place", PLACES)
 @pytest.mark.parametrize("P,m,dtype", [(8, 65536, "bf16"), (8, 1000, "bf16"), (8, 3, "f32"), (3, 4096, "f32"),
+                                       (2, 4096, "bf16"), (4, 2 ** 18 + 8, "bf16"), (2, 70001 * 4, "f32"),
                                        (64, 512, "bf16"), (1, 64, "bf16"), (8, 4096 * 64, "bf16"),
                                        (8, 2 ** 17 + 1024 + 8, "bf16"),
                                        # 8-rank shards on both sides of the launch-shape boundaries at 2, 4
