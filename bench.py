@@ -639,6 +639,7 @@ def full_sweep(nuna, torch, pool, args):
     if want("a2a_moe_combine"):
         for T_tok in (None,) + MOE_DECODE_TOKENS:
             combine_case(nuna, torch, pool, args, emit, T_tok)
+    size_sweep(nuna, torch, pool, args, emit, want)  # each size checks want() itself
     if want("copy_reference"):
         copy_case(nuna, torch, pool, args, emit)
     if want("ref_stream"):
@@ -860,6 +861,54 @@ def copy_case(nuna, torch, pool, args, emit):
               "gbps_read_plus_write": round(2 * nb / (t["median"] * 1e-6) / 1e9, 1)})
         del g, pairs
         del s
+
+
+SIZE_SWEEP_AR_KIB = (16, 64, 256, 1024, 4096, 16384, 65536, 131072)  # bytes per rank of the all-reduce
+SIZE_SWEEP_AG_KIB = (2, 8, 32, 128, 512, 2048, 8192, 16384)            # shard bytes of the all-gather (x8 out)
+
+
+def size_sweep(nuna, torch, pool, args, emit, want):
+    """Latency and HBM GB/s against message size, both placements, cold, 8 ranks of bf16: the all-reduce
+    (AUTO, the destination-split one-shot and the two-shot) from 16 KiB to 128 MiB per rank, and the
+    all-gather from 2 KiB to 16 MiB shards (16 KiB to 128 MiB received per rank), in steps of 4x."""
+    import oracle
+    from paper_2608_00867_amd import workloads as wl
+    for kib in SIZE_SWEEP_AR_KIB:
+        name = f"size_ar_bf16_p8_{kib}KiB"
+        if not want(name):
+            continue
+        n = kib * 1024 // 2
+        x = wl.normal_bf16(8, n, wl.seed_for(11, kib))
+        ref = oracle.allreduce(x)
+        for algo in ("auto", "one_shot_split", "two_shot"):
+            ok = all(oracle_check_ar(nuna, torch, x, algo, p, ref) for p in ("linear", "xcd"))
+            li = {p: launch_of(nuna, torch, x, algo, p) for p in ("linear", "xcd")}
+            nb, res, calls = bench_allreduce(nuna, torch, pool, x, algo, args.reps, args.warmup)
+            emit({"workload": name, "P": 8, "bytes_per_rank": kib * 1024, "algo": algo, "cache": "cold",
+                  "alg_bytes": nb, "calls_per_graph": calls, "parity": ok,
+                  "same_map": same_map(li["linear"], li["xcd"]),
+                  "xcd_kernels": li["xcd"]["kernels"], "xcd_map": li["xcd"]["map"],
+                  **{f"{p}_us": {k: round(v, 3) for k, v in res[p]["us"].items()} for p in res},
+                  **{f"{p}_gbps": round(res[p]["gbps"], 1) for p in res},
+                  **{f"{p}_frac_hbm": round(res[p]["gbps"] / HBM_PEAK_GBPS, 4) for p in res},
+                  "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
+        del x, ref
+    for kib in SIZE_SWEEP_AG_KIB:
+        name = f"size_ag_bf16_p8_{kib}KiB"
+        if not want(name):
+            continue
+        m = kib * 1024 // 2
+        x = wl.normal_bf16(8, m, wl.seed_for(12, kib))
+        nb, res, calls, ok = bench_rs_ag(nuna, torch, pool, "ag", x, args.reps, args.warmup)
+        emit({"workload": name, "P": 8, "shard_bytes": kib * 1024, "bytes_per_rank": 8 * kib * 1024,
+              "algo": "standalone", "cache": "cold", "alg_bytes": nb, "calls_per_graph": calls, "parity": ok,
+              "same_map": same_map(res["linear"]["launch"], res["xcd"]["launch"]),
+              "xcd_kernels": res["xcd"]["launch"]["kernels"], "xcd_map": res["xcd"]["launch"]["map"],
+              **{f"{p}_us": {k: round(v, 3) for k, v in res[p]["us"].items()} for p in res},
+              **{f"{p}_gbps": round(res[p]["gbps"], 1) for p in res},
+              **{f"{p}_frac_hbm": round(res[p]["gbps"] / HBM_PEAK_GBPS, 4) for p in res},
+              "linear_over_xcd_time": round(res["linear"]["us"]["median"] / res["xcd"]["us"]["median"], 4)})
+        del x
 
 
 REF_STREAMS = (("read", 1, 512), ("read", 8, 64), ("write", 1, 512), ("write", 8, 64), ("copy", 1, 512),

@@ -104,7 +104,9 @@ typedef enum { NUNA_F32 = 0, NUNA_BF16 = 1 } nuna_dtype_t;
 typedef enum { NUNA_PLACE_LINEAR = 0, NUNA_PLACE_XCD = 1 } nuna_placement_t;
 
 typedef enum {
-    NUNA_ALGO_AUTO = 0,           /* library picks by size (one-shot family on one GPU) */
+    NUNA_ALGO_AUTO = 0,           /* library picks by size: NUNA_ALGO_TWO_SHOT for 8 ranks of bf16
+                                     from 16 MiB per rank when a shard is whole 16-byte vectors,
+                                     NUNA_ALGO_ONE_SHOT otherwise */
     NUNA_ALGO_ONE_SHOT = 1,       /* one kernel: read P inputs, write P outputs per element */
     NUNA_ALGO_TWO_SHOT = 2,       /* reduce-scatter then all-gather, both phases per chunk in one
                                      kernel: the workgroup that reduces chunk c of shard r stores

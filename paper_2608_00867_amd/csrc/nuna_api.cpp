@@ -435,7 +435,7 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
     if ((st = check_placement_ready(place))) return st;
 
     int a = algo;
-    if (a == NUNA_ALGO_AUTO) a = NUNA_ALGO_ONE_SHOT;
+    if (a == NUNA_ALGO_AUTO) a = nuna::auto_two_shot(P, count, dtype) ? NUNA_ALGO_TWO_SHOT : NUNA_ALGO_ONE_SHOT;
     if ((a == NUNA_ALGO_TWO_SHOT || a == NUNA_ALGO_TWO_SHOT_TWO_KERNELS) && count % static_cast<size_t>(P) != 0)
         a = NUNA_ALGO_ONE_SHOT;
     if (a == NUNA_ALGO_ONE_SHOT_SPLIT && in_place) a = NUNA_ALGO_ONE_SHOT;

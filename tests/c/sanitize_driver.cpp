@@ -266,6 +266,31 @@ int main() {
     expect(nuna_probe_xcc(0, probe, nullptr, nullptr) == NUNA_ERR_INVALID_ARG, "probe G=0", 0);
     expect(nuna_copy(nullptr, probe, 16, nullptr) == NUNA_ERR_INVALID_ARG, "copy null", 0);
     {
+        // NUNA_ALGO_AUTO: the two-shot for 8 ranks of bf16 from 16 MiB per rank, the one-shot below and for
+        // other rank counts, dtypes and ragged shards (the launch stubs touch no buffer: made-up addresses).
+        const void* in[8];
+        void* out[8];
+        const uintptr_t base = uintptr_t(1) << 44;
+        for (int r = 0; r < 8; ++r) {
+            in[r] = reinterpret_cast<const void*>(base + (uintptr_t(2 * r) << 28));
+            out[r] = reinterpret_cast<void*>(base + (uintptr_t(2 * r + 1) << 28));
+        }
+        struct Case { int P; size_t count; nuna_dtype_t dt; const char* kernel; };
+        const Case cases[] = {{8, size_t(8) << 20, NUNA_BF16, "stub_two_shot"},
+                              {8, size_t(32) << 20, NUNA_BF16, "stub_two_shot"},
+                              {8, (size_t(8) << 20) - 64, NUNA_BF16, "stub_allreduce"},
+                              {8, (size_t(8) << 20) + 4, NUNA_BF16, "stub_allreduce"},
+                              {8, size_t(4) << 20, NUNA_F32, "stub_allreduce"},
+                              {4, size_t(8) << 20, NUNA_BF16, "stub_allreduce"}};
+        for (const Case& c : cases) {
+            const int st = nuna_allreduce(in, out, c.P, c.count, c.dt, NUNA_ALGO_AUTO, NUNA_PLACE_LINEAR, nullptr);
+            nuna_launch_info_t li;
+            nuna_last_launch(&li);
+            expect(st == NUNA_OK && std::strcmp(li.kernels, c.kernel) == 0, "AUTO algorithm choice",
+                   static_cast<int>(c.count >> 10));
+        }
+    }
+    {
         // Reference streams: every kind at every buffer count through the launch stub, and refusals.
         static unsigned char pool[32 * 8192 + 16] __attribute__((aligned(16)));
         const void* src[16];

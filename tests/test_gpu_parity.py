@@ -559,7 +559,10 @@ def test_launch_record_names_what_ran(nuna):
     assert _kernels(nuna, x16, "two_shot", "xcd")["kernels"] == "k_reduce_scatter_direct+k_all_gather_direct"
     with nuna.tunables(NUNA_TWO_SHOT_FORM=1):
         assert _kernels(nuna, x16, "two_shot", "xcd")["kernels"] == "k_two_shot_direct"
+    # AUTO: the two-shot for 8 ranks of bf16 from 16 MiB per rank, the one-shot below
+    assert _kernels(nuna, x16, "auto", "xcd")["kernels"] == "k_reduce_scatter_direct+k_all_gather_direct"
     x4 = wl.ar_bf16_prefill(256)
+    assert _kernels(nuna, x4, "auto", "xcd")["kernels"] == "k_allreduce_direct"
     r = _kernels(nuna, x4, "two_shot", "xcd")
     assert r["kernels"] == "k_two_shot_direct" and r["launches"] == 1 and r["map"] == "linear"
     with nuna.tunables(NUNA_TWO_SHOT_FORM=2):
