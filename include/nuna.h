@@ -553,8 +553,8 @@ nuna_status_t nuna_probe_load_latency_cus(const void* buf, size_t nbytes, size_t
 
 /*
  * Reference streams: the plain access patterns that bound the collectives'
- * HBM rooflines (Sec. 6.1 reports collective bandwidth against what the
- * memory system sustains), for calibration and comparison; not collectives.
+ * HBM rooflines, for calibration and comparison.  Not an operation of the
+ * paper and not a collective: measurement support, like nuna_copy.
  * n buffers of `bytes` bytes each, n in {1, 2, 4, 8, 16}, bytes a multiple
  * of 16 up to 2^34 (0: no launch).  Pointers 16-byte aligned; no written
  * range may overlap another or any source (NUNA_ERR_OVERLAP).  One work item
