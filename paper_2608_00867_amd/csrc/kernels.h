@@ -61,8 +61,6 @@ hipError_t launch_allreduce(const void* const* in, void* const* out, int P, size
 bool two_shot_fused_ok(int P, size_t count, int dtype);
 // The fused form applies and is the one to run (size rule, NUNA_TWO_SHOT_FORM).
 bool two_shot_runs_fused(int P, size_t count, int dtype);
-// NUNA_ALGO_AUTO takes the two-shot for this call (else the one-shot).
-bool auto_two_shot(int P, size_t count, int dtype);
 hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype, int mode,
                                  hipStream_t stream);
 

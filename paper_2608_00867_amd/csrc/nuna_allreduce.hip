@@ -801,17 +801,6 @@ bool two_shot_runs_fused(int P, size_t count, int dtype) {
     return !(P == 8 && dtype == kDtBf16 && bytes >= (size_t(16) << 20) && bytes <= (size_t(40) << 20));
 }
 
-// NUNA_ALGO_AUTO: the two-shot for 8 ranks of bf16 from 16 MiB per rank
-// (fused or two kernels, two_shot_runs_fused), the one-shot elsewhere.
-// Measured on MI355X, cold, per call: 46.2-46.6 against 47.9-48.2 us at
-// 16 MiB per rank, 177-179 against 179-181 at 64 MiB, 380-390 against
-// 386-421 at 128 MiB; at 4 MiB the one-shot leads (11.4-11.6 against
-// 11.6-11.7 us), as at every smaller size.
-bool auto_two_shot(int P, size_t count, int dtype) {
-    return P == 8 && dtype == kDtBf16 && count * dtype_size(dtype) >= (size_t(16) << 20) &&
-           two_shot_fused_ok(P, count, dtype);
-}
-
 // Fused two-shot all-reduce (k_two_shot_direct / k_two_shot): launch shape by
 // the bytes per rank, as for the one-shot (the two move the same bytes);
 // chunks are cut per shard.

@@ -409,6 +409,21 @@ nuna_status_t nuna_get_device_info(nuna_device_info_t* info) {
     return ok();
 }
 
+namespace {
+
+// NUNA_ALGO_AUTO: the two-shot for 8 ranks of bf16 from 16 MiB per rank
+// (fused or two kernels, two_shot_runs_fused), the one-shot elsewhere.
+// Measured on MI355X, cold, per call: 46.2-46.6 against 47.9-48.2 us at
+// 16 MiB per rank, 177-179 against 179-181 at 64 MiB, 380-390 against
+// 386-421 at 128 MiB; at 4 MiB the one-shot leads (11.4-11.6 against
+// 11.6-11.7 us), as at every smaller size.
+bool auto_two_shot(int P, size_t count, int dtype) {
+    return P == 8 && dtype == nuna::kDtBf16 && count * nuna::dtype_size(dtype) >= (size_t(16) << 20) &&
+           nuna::two_shot_fused_ok(P, count, dtype);
+}
+
+}  // namespace
+
 nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, size_t count, nuna_dtype_t dtype,
                              nuna_algo_t algo, nuna_placement_t place, hipStream_t stream) try {
     begin_launches();
@@ -435,7 +450,7 @@ nuna_status_t nuna_allreduce(const void* const* in, void* const* out, int P, siz
     if ((st = check_placement_ready(place))) return st;
 
     int a = algo;
-    if (a == NUNA_ALGO_AUTO) a = nuna::auto_two_shot(P, count, dtype) ? NUNA_ALGO_TWO_SHOT : NUNA_ALGO_ONE_SHOT;
+    if (a == NUNA_ALGO_AUTO) a = auto_two_shot(P, count, dtype) ? NUNA_ALGO_TWO_SHOT : NUNA_ALGO_ONE_SHOT;
     if ((a == NUNA_ALGO_TWO_SHOT || a == NUNA_ALGO_TWO_SHOT_TWO_KERNELS) && count % static_cast<size_t>(P) != 0)
         a = NUNA_ALGO_ONE_SHOT;
     if (a == NUNA_ALGO_ONE_SHOT_SPLIT && in_place) a = NUNA_ALGO_ONE_SHOT;

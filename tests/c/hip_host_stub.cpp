@@ -99,11 +99,6 @@ bool two_shot_fused_ok(int P, size_t count, int dtype) {
 
 bool two_shot_runs_fused(int P, size_t count, int dtype) { return two_shot_fused_ok(P, count, dtype); }
 
-bool auto_two_shot(int P, size_t count, int dtype) {
-    return P == 8 && dtype == kDtBf16 && count * dtype_size(dtype) >= (size_t(16) << 20) &&
-           two_shot_fused_ok(P, count, dtype);
-}
-
 hipError_t launch_two_shot_fused(const void* const* in, void* const* out, int P, size_t count, int dtype, int,
                                  hipStream_t) {
     check(two_shot_fused_ok(P, count, dtype), "fused two-shot launched where it does not apply");
