@@ -562,7 +562,16 @@ def probe_xcc(G, stream=None):
     return xcc, hw
 
 
+def _check_flat(ts, name):
+    """Each tensor is a contiguous CUDA tensor, so that its data pointer and numel() * element_size() bytes
+    span exactly its own storage (an expanded or strided view would span more or other memory)."""
+    for t in ts:
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name}: buffers must be contiguous CUDA tensors")
+
+
 def copy(dst, src, stream=None):
+    _check_flat((dst, src), "copy")
     nbytes = src.numel() * src.element_size()
     if dst.numel() * dst.element_size() < nbytes:
         raise ValueError("dst too small")
@@ -592,7 +601,12 @@ def ref_stream(kind, srcs, dsts, stream=None):
     """Reference stream over CUDA tensors: "read" (srcs; dsts[0] receives ref_read_checksum_bytes of
     checksums), "write" (dsts), or "copy" (dsts[r] = srcs[r]).  Every buffer holds the same number of
     bytes."""
+    if kind not in REF_KINDS:
+        raise ValueError(f"reference stream kind {kind!r} is not one of {sorted(REF_KINDS)}")
     bufs = dsts if kind == "write" else srcs
+    if not bufs or not dsts:
+        raise ValueError("reference stream needs its buffers and at least one destination")
+    _check_flat(list(bufs) + list(dsts), "ref_stream")
     nbytes = bufs[0].numel() * bufs[0].element_size()
     if any(b.numel() * b.element_size() != nbytes for b in bufs):
         raise ValueError("reference stream buffers differ in size")
@@ -610,6 +624,7 @@ def probe_load_latency(buf, stride, line_offset, xcd, stream=None):
     """Cold-load latency (shader cycles) of each stride-sized block of `buf` (a CUDA tensor) seen from
     XCD `xcd`.  The caller evicts the caches first.  Returns an int64 CPU tensor."""
     torch = _torch()
+    _check_flat((buf,), "probe")
     nbytes = buf.numel() * buf.element_size()
     cyc = torch.zeros(nbytes // stride, dtype=torch.int32, device=buf.device)
     _check(lib().nuna_probe_load_latency(buf.data_ptr(), nbytes, stride, line_offset, xcd, cyc.data_ptr(),
@@ -639,6 +654,7 @@ def probe_load_latency_cus(buf, xcd, stride=8192, stream=None):
     XCD `xcd` it reaches.  Returns (latencies int64 [cus, nblocks] on the CPU, HW_ID CU keys [cus],
     compute units seen).  The caller evicts the caches first."""
     torch = _torch()
+    _check_flat((buf,), "probe")
     nbytes = buf.numel() * buf.element_size()
     nb = nbytes // stride
     work = torch.zeros(257, dtype=torch.int32, device=buf.device)

@@ -165,6 +165,32 @@ def test_copy_and_probe_validation():
     assert L.nuna_probe_xcc(8, None, None, None) == nuna.ERR_INVALID_ARG
 
 
+def test_flat_buffer_wrappers_refuse_views_and_host_tensors():
+    """copy(), ref_stream() and the latency probes take a data pointer and numel() * element_size() bytes,
+    so they accept only contiguous CUDA tensors: a host tensor or an expanded view (whose byte span exceeds
+    its storage) is refused before any library call, as are an unknown kind and empty buffer lists."""
+    import torch
+    a, b = torch.zeros(64), torch.zeros(64)
+    with pytest.raises(ValueError, match="contiguous CUDA"):
+        nuna.copy(b, a)
+    with pytest.raises(ValueError, match="contiguous CUDA"):
+        nuna.copy(b, torch.zeros(1).expand(64))
+    with pytest.raises(ValueError, match="contiguous CUDA"):
+        nuna.ref_stream("copy", [a], [b])
+    with pytest.raises(ValueError, match="contiguous CUDA"):
+        nuna.ref_stream("write", None, [torch.zeros(8, 8).t()])
+    with pytest.raises(ValueError, match="kind"):
+        nuna.ref_stream("move", [a], [b])
+    with pytest.raises(ValueError, match="at least one destination"):
+        nuna.ref_stream("read", [a], [])
+    with pytest.raises(ValueError, match="at least one destination"):
+        nuna.ref_stream("write", None, [])
+    with pytest.raises(ValueError, match="contiguous CUDA"):
+        nuna.probe_load_latency(torch.zeros(1 << 12), 8192, 256, 0)
+    with pytest.raises(ValueError, match="contiguous CUDA"):
+        nuna.probe_load_latency_cus(torch.zeros(1 << 12), 0)
+
+
 @no_gpu_only
 def test_ref_stream_validation():
     """nuna_ref_stream refuses bad kinds, buffer counts, sizes, NULL, misaligned and overlapping buffers
