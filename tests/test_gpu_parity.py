@@ -16,7 +16,8 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import assert_bitwise, assert_bitwise_nan_aware, to_dev, to_host
+from gpu_util import assert_bitwise, assert_bitwise_nan_aware, gate_weights, run_a2a, run_combine, to_dev, \
+    to_host
 from paper_2608_00867_amd import workloads as wl
 
 pytestmark = pytest.mark.gpu
@@ -321,35 +322,13 @@ def test_all_gather(nuna, P, m, dtype, place):
 
 # ---------------------------------------------------------------- workload 4: MoE all-to-all dispatch
 
-def _run_a2a(nuna, send_np, topk, E, place, guard_rows=2):
-    P = len(send_np)
-    lay = nuna.A2ALayout(topk, E).upload()
-    rows = lay.recv_rows()
-    send = [to_dev(a) for a in send_np]
-    H = send_np[0].shape[1]
-    cap = int(rows.max()) if rows.size else 0
-    cap = max(cap, 1)
-    recv_whole = [torch.full((cap + guard_rows, H), 0, dtype=send[0].dtype, device="cuda") for _ in range(P)]
-    for w in recv_whole:
-        w.view(torch.int16 if w.dtype == torch.bfloat16 else torch.int32).fill_(0x3C3C)
-    recv = [w[:cap] for w in recv_whole]
-    nuna.all_to_all(send, recv, lay, placement=place)
-    torch.cuda.synchronize()
-    out = []
-    for d in range(P):
-        whole = to_host(recv_whole[d])
-        tailbits = whole[int(rows[d]):].view(np.uint16 if whole.dtype == np.uint16 else np.uint32)
-        assert np.all(tailbits == 0x3C3C), f"rank {d}: write past its rows"
-        out.append(whole[:int(rows[d])])
-    lay.close()
-    return out
 
 
 @pytest.mark.parametrize("place", PLACES)
 def test_a2a_moe_full(nuna, place):
     send, topk = wl.a2a_moe()
     ref = oracle.all_to_all(send, topk, wl.MOE_EXPERTS)
-    got = _run_a2a(nuna, send, topk, wl.MOE_EXPERTS, place)
+    got = run_a2a(nuna, send, topk, wl.MOE_EXPERTS, place)
     for d in range(8):
         assert_bitwise(got[d], ref[d], f"a2a rank {d}")
 
@@ -363,7 +342,7 @@ def test_a2a_small(nuna, P, T, k, E, H, dtype, place):
     topk = wl.moe_routing(P, T, k, E, 17 * P + T)
     send = [a.reshape(T, H) for a in wl.random_bits(P, T * H, dtype, 19 * P + T)]
     ref = oracle.all_to_all(send, topk, E)
-    got = _run_a2a(nuna, send, topk, E, place)
+    got = run_a2a(nuna, send, topk, E, place)
     for d in range(P):
         assert_bitwise(got[d], ref[d], f"a2a P={P} T={T} H={H} rank {d}")
 
@@ -653,40 +632,6 @@ def test_ar_eight_vector_rule_ragged(nuna):
 
 # ---------------------------------------------------------------- MoE combine (result collection)
 
-def _run_combine(nuna, y_np, topk, E, place, pad=64, weights=None):
-    """Combine on the GPU.  Result buffers are padded past each rank's rows with NaN rows, so a
-    read of a wrong row shows in the output; outputs have `pad` guard elements on both sides
-    (64 elements keep the output 16-byte aligned)."""
-    P, T = int(topk.shape[0]), int(topk.shape[1])
-    lay = nuna.A2ALayout(topk, E).upload()
-    rows = lay.recv_rows()
-    H = y_np[0].shape[1]
-    tdt = torch.bfloat16 if y_np[0].dtype == np.uint16 else torch.float32
-    ibits = torch.int16 if tdt == torch.bfloat16 else torch.int32
-    nan = 0x7FC1 if tdt == torch.bfloat16 else 0x7FC00001
-    cap = max(int(rows.max()), 1) + 1
-    y = []
-    for d in range(P):
-        buf = torch.empty((cap, H), dtype=tdt, device="cuda")
-        buf.view(ibits).fill_(nan)
-        buf[:int(rows[d])] = to_dev(y_np[d])
-        y.append(buf)
-    out_whole = [torch.empty(T * H + 2 * pad, dtype=tdt, device="cuda") for _ in range(P)]
-    for w in out_whole:
-        w.view(ibits).fill_(0x3C3C)
-    out = [w[pad:pad + T * H].view(T, H) for w in out_whole]
-    w = to_dev(weights) if weights is not None else None
-    nuna.all_to_all_combine(y, out, lay, placement=place, weights=w)
-    torch.cuda.synchronize()
-    got = []
-    for s in range(P):
-        whole = to_host(out_whole[s])
-        band = np.concatenate([whole[:pad], whole[pad + T * H:]])
-        assert np.all(band.view(np.uint16 if whole.dtype == np.uint16 else np.uint32) == 0x3C3C), \
-            f"rank {s}: write outside its output rows"
-        got.append(whole[pad:pad + T * H].reshape(T, H))
-    lay.close()
-    return got
 
 
 @pytest.mark.parametrize("place", PLACES)
@@ -695,7 +640,7 @@ def test_combine_moe_full(nuna, place):
     rows = oracle.a2a_counts(topk, wl.MOE_EXPERTS)
     y = wl.result_rows(rows, wl.HIDDEN_MOE, np.uint16, wl.seed_for(4, 7))
     ref = oracle.combine(y, topk, wl.MOE_EXPERTS)
-    got = _run_combine(nuna, y, topk, wl.MOE_EXPERTS, place)
+    got = run_combine(nuna, y, topk, wl.MOE_EXPERTS, place)
     for s in range(8):
         assert_bitwise(got[s], ref[s], f"combine rank {s}")
 
@@ -710,23 +655,11 @@ def test_combine_small(nuna, P, T, k, E, H, dtype, place):
     topk = wl.moe_routing(P, T, k, E, 23 * P + T)
     y = wl.result_rows(oracle.a2a_counts(topk, E), H, dtype, 29 * P + T)
     ref = oracle.combine(y, topk, E)
-    got = _run_combine(nuna, y, topk, E, place)
+    got = run_combine(nuna, y, topk, E, place)
     for s in range(P):
         assert_bitwise(got[s], ref[s], f"combine P={P} T={T} k={k} H={H} rank {s}")
 
 
-def _gate_weights(topk, E, seed):
-    """Dense [P, T, P] weights: with E == P the router's gate of the token's expert on rank d,
-    otherwise any positive weight per destination rank."""
-    P, T, k = topk.shape
-    g = np.random.default_rng(seed)
-    w = np.zeros((P, T, P), dtype=np.float32)
-    per = E // P
-    for s in range(P):
-        for t in range(T):
-            for q in range(k):
-                w[s, t, int(topk[s, t, q]) // per] = np.float32(g.random())
-    return w
 
 
 @pytest.mark.parametrize("place", PLACES)
@@ -737,9 +670,9 @@ def test_combine_weighted(nuna, P, T, k, E, H, dtype, place):
     """Top-k weighted combine: each rank's result row scaled by its weight before the ascending sum."""
     topk = wl.moe_routing(P, T, k, E, 59 * P + T)
     y = wl.result_rows(oracle.a2a_counts(topk, E), H, dtype, 61 * P + T)
-    w = _gate_weights(topk, E, 67 * P + T)
+    w = gate_weights(topk, E, 67 * P + T)
     ref = oracle.combine(y, topk, E, w)
-    got = _run_combine(nuna, y, topk, E, place, weights=w)
+    got = run_combine(nuna, y, topk, E, place, weights=w)
     for s in range(P):
         assert_bitwise(got[s], ref[s], f"weighted combine P={P} T={T} k={k} E={E} H={H} rank {s}")
 
@@ -752,7 +685,7 @@ def test_combine_special_values(nuna):
     for dtype in (np.uint16, np.float32):
         y = [wl.random_bits(1, int(r) * H, dtype, 37 + d)[0].reshape(int(r), H) for d, r in enumerate(rows)]
         ref = oracle.combine(y, topk, E)
-        got = _run_combine(nuna, y, topk, E, "xcd")
+        got = run_combine(nuna, y, topk, E, "xcd")
         for s in range(P):
             assert_bitwise_nan_aware(got[s], ref[s], f"combine specials {dtype.__name__} rank {s}")
 
@@ -785,7 +718,7 @@ def test_combine_persistent_loop(nuna, cap):
     nuna.set_max_workgroups(cap)
     try:
         for place in PLACES:
-            got = _run_combine(nuna, y, topk, E, place)
+            got = run_combine(nuna, y, topk, E, place)
             for s in range(P):
                 assert_bitwise(got[s], ref[s], f"combine cap={cap} {place} rank {s}")
     finally:
@@ -806,12 +739,12 @@ def test_combine_records_match_lists(nuna, P, T, k, E, H, dtype, weighted, cfg):
     record kernel raises the chunk count so that a column chunk fits one pass of the workgroup."""
     topk = wl.moe_routing(P, T, k, E, 71 * P + T)
     y = wl.result_rows(oracle.a2a_counts(topk, E), H, dtype, 73 * P + T)
-    w = _gate_weights(topk, E, 79 * P + T) if weighted else None
+    w = gate_weights(topk, E, 79 * P + T) if weighted else None
     ref = oracle.combine(y, topk, E, w)
     for lists in (0, 1):
         with nuna.tunables(NUNA_COMBINE_LISTS=lists, **cfg):
             for place in PLACES:
-                got = _run_combine(nuna, y, topk, E, place, weights=w)
+                got = run_combine(nuna, y, topk, E, place, weights=w)
                 for s in range(P):
                     assert_bitwise(got[s], ref[s], f"combine lists={lists} {cfg} {place} P={P} T={T} H={H} rank {s}")
 
