@@ -1,15 +1,16 @@
-"""GPU parity on seeded random shapes: the all-reduce, the reduce-scatter, the all-gather and the MoE dispatch
-and combine through the C ABI against the oracle, bit for bit, with guard bands around every output.
+"""GPU: seeded random calls at large sizes through the C ABI against the oracle, bit for bit, with guard
+bands around every output: the all-reduce, the reduce-scatter, the all-gather and the MoE dispatch and combine.
 
-The hand-picked cases elsewhere sit on the launch rules' boundaries; these draw rank counts, per-rank sizes
-(log-uniform from one element to 24 MiB, half of them snapped near a power of two or to whole 16-byte
-vectors: two-shot shards for the all-reduce, shards for the others), dtypes, algorithms, placements and
-in-place forms at random, and half of the cases also set
-one launch-shape tunable (vectors per thread and workgroup size, store pauses, store cache policy, two-shot
-form, shard order, page groups or a workgroup cap).  The MoE cases draw rank counts, experts per rank,
-top-k, tokens per rank, row widths, dtypes, gate weights and placements, and half of the combines set one
-combine tunable.  Tunables change launch shapes only, never results, so every case must give the oracle's
-bits.  The draw is fixed by its seed; each case's id names it.
+The cases of test_gpu_fuzz.py stay below 400,000 elements in all.  These reach 24 MiB per rank (per-rank
+bytes log-uniform from one element, half of them snapped near a power of two or to whole 16-byte vectors:
+two-shot shards for the all-reduce, shards for the others), where the size rules switch to the 8-vector
+one-shot, write-through and paced stores, and the fused or two-kernel two-shot.  Rank counts, dtypes,
+algorithms, placements and in-place forms are drawn at random.  Half of the cases also set one family of
+tunables: vectors per thread and workgroup size, store pauses, store cache policy, two-shot form, shard
+order, page groups, or a workgroup cap.  The MoE cases draw rank counts, experts per rank, top-k, tokens per
+rank, row widths, dtypes, gate weights and placements, and half of the combines set one combine tunable.
+Tunables change launch shapes only, never results, so every case must give the oracle's bits.  The draw is
+fixed by its seed; each case's id names it.
 """
 import numpy as np
 import pytest
