@@ -149,3 +149,14 @@ def test_source_hash_ignores_comments_but_not_code():
     assert bench.kernel_source_sha(edited) == base
     edited["shapes.h"] = texts["shapes.h"] + "\nconstexpr int kUnused = 1;\n"
     assert bench.kernel_source_sha(edited) != base
+
+
+@pytest.mark.parametrize("n", [2, 8])
+def test_more_than_one_gpu_is_refused(n):
+    """bench.py measures one GPU: --gpus above 1 exits with status 2 and says why, before touching a GPU."""
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", str(n)], capture_output=True,
+                       text=True, timeout=300)
+    assert r.returncode == 2
+    assert f"--gpus {n} is not supported" in r.stderr and "one GPU" in r.stderr
+    assert r.stdout == ""
