@@ -1,6 +1,6 @@
 // nuna_allreduce.hip -- gfx950 all-reduce kernels: one-shot (with the
-// destination-split variant), rank-major tile and lane-per-rank for many
-// ranks, and their launchers.
+// destination-split variant), the two-shot with both phases fused per chunk,
+// rank-major tile and lane-per-rank for many ranks, and their launchers.
 //
 // Memory-bound streaming kernels: every lane moves 16-byte vectors
 // (global_load/store_dwordx4), so one wavefront instruction touches 1 KiB of
