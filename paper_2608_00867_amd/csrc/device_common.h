@@ -1,6 +1,8 @@
 // device_common.h -- device helpers shared by the gfx950 kernel sources:
-// bf16/fp32 numerics, 16-byte streaming loads and stores, the rank pointer
-// table, and the launch-grid cap.
+// bf16/fp32 numerics, 16-byte streaming and write-through loads and stores,
+// the pauses between a fan-out's per-destination stores, the rank pointer
+// table, the pinning of kernel arguments and the scalar selects of a run-time
+// rank's pointer, and the launch-grid cap.
 //
 // Everything sits in an unnamed namespace: each kernel source gets its own
 // copy and no symbol leaves the library.
