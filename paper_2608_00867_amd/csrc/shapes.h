@@ -89,8 +89,10 @@ inline int pick_vpt(int64_t vectors_per_rank, int P) {
 // all-reduce (whose members all load the same P chunks at once), only once
 // the message is large enough to be bandwidth-bound.  Otherwise the grouped
 // map measured up to 3.5 % slower than the linear one on MI355X (split
-// all-reduce at 8-16 KiB per rank with 8 ranks; all-gather with 64 ranks and
-// 8 destinations per member), so the launch keeps the linear map there.
+// all-reduce at 8-16 KiB per rank with 8 ranks, and with warm inputs up to
+// 4.7 % at launches of 1-2 MiB; all-gather with 64 ranks and 8 destinations
+// per member, and up to 2 % warm with 8 ranks at small shards), so the launch
+// keeps the linear map there.
 //   reread_num / reread_den: share of the group's loads and stores that are
 //   re-reads; total_bytes: bytes the launch moves; min_total: the size below
 //   which the grouped map is not used.
