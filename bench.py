@@ -961,6 +961,7 @@ INTERF_M = 2560                      # M = N: about 100 output tiles of 256 x 25
 INTERF_K = (0, 2048, 8192, 32768, 131072)
 INTERF_AG_ELEMS = 65536              # bf16 per rank: 128 KiB in, 1 MiB out per rank with P = 8
 INTERF_AR_TOKENS = 64                # split all-reduce: [64, 8192] bf16 per rank (1 MiB)
+INTERF_MOE_TOKENS = 128              # MoE dispatch: 128 tokens x 7168 bf16 per rank, top-8 of 256 experts
 INTERF_CALLS = 200
 INTERF_MAX_SLOWDOWN = 30.0           # the GEMM window covers the collective's graph even this much slower
 
@@ -968,7 +969,10 @@ INTERF_MAX_SLOWDOWN = 30.0           # the GEMM window covers the collective's g
 def interference_cases(wl, oracle):
     """The collectives run beside the GEMM.  The all-gather is the paper's setup (1 MB per output);
     at that size its default map is the same in both placements.  The split all-reduce (each chunk's
-    8 destination groups are separate work items) is a map the placement changes."""
+    8 destination groups are separate work items) and the MoE dispatch (the copies of a token row
+    form one group) are maps the placement changes.  Inputs and outputs are flat bf16 buffers; `ref`
+    holds each rank's expected leading elements (the dispatch's receive buffers have spare rows,
+    which must stay untouched)."""
     P, m = 8, INTERF_AG_ELEMS
     x = wl.normal_bf16(P, m, wl.seed_for(6))
     yield {"workload": "all_gather_bf16_p8_1MiB_beside_gemm", "ins": x, "out_elems": P * m,
@@ -978,6 +982,19 @@ def interference_cases(wl, oracle):
     yield {"workload": f"allreduce_split_bf16_p8_T{INTERF_AR_TOKENS}_beside_gemm", "ins": x,
            "out_elems": x[0].size, "ref": oracle.allreduce(x),
            "call": lambda nuna, ins, outs, p: nuna.allreduce(ins, outs, algo="one_shot_split", placement=p)}
+    T, H, E = INTERF_MOE_TOKENS, wl.HIDDEN_MOE, wl.MOE_EXPERTS
+    send, topk = wl.a2a_moe(T=T)
+    ref = oracle.all_to_all(send, topk, E)
+    cap = max(r.shape[0] for r in ref)
+    held = {}
+
+    def dispatch(nuna, ins, outs, p):
+        nuna.all_to_all([t.view(T, H) for t in ins], [o.view(cap, H) for o in outs], held["layout"], placement=p)
+
+    yield {"workload": f"a2a_moe_dispatch_bf16_p8_T{T}_beside_gemm", "ins": [a.ravel() for a in send],
+           "out_elems": cap * H, "ref": [r.ravel() for r in ref], "call": dispatch,
+           "prepare": lambda nuna: held.update(layout=nuna.A2ALayout(topk, E).upload()),
+           "release": lambda: held.pop("layout").close()}
 
 
 def interference(nuna, torch, args):
@@ -995,6 +1012,8 @@ def interference(nuna, torch, args):
     for case in interference_cases(wl, oracle):
         x, ref, call = case["ins"], case["ref"], case["call"]
         P, m, mo = len(x), x[0].size, case["out_elems"]
+        if "prepare" in case:
+            case["prepare"](nuna)
         src = [dev_copy_of(torch, a) for a in x]
         set_bytes = P * (m + mo) * 2
         for cache in ("warm", "cold"):
@@ -1073,7 +1092,8 @@ def interference(nuna, torch, args):
                     for _, outs in sets[:2]:
                         for d in range(P):
                             got = outs[d].cpu().view(torch.int16).numpy().view(np.uint16)
-                            ok = ok and np.array_equal(got, ref[d])
+                            n_d = ref[d].size
+                            ok = ok and np.array_equal(got[:n_d], ref[d]) and not got[n_d:].any()
                 st = {p: stats(res[p]) for p in res}
                 if not K:
                     alone = {p: st[p]["median"] for p in st}
@@ -1093,6 +1113,8 @@ def interference(nuna, torch, args):
                     del a, b, c
             del graphs, sets
             torch.cuda.empty_cache()
+        if "release" in case:
+            case["release"]()
     f.close()
 
 

@@ -831,6 +831,38 @@ def test_split_allreduce_beside_gemm(nuna):
             assert_bitwise(to_host(outs[p][d]), ref[d], f"split AR beside GEMM {p} rank {d}")
 
 
+
+def test_dispatch_beside_gemm(nuna):
+    """The MoE dispatch (the copies of a token row are one group under XCD placement) beside a GEMM on
+    another stream, 128 tokens x 7168 per rank: every received row bit-exact, no write past a rank's rows."""
+    T = 128
+    send_np, topk = wl.a2a_moe(T=T)
+    E = wl.MOE_EXPERTS
+    ref = oracle.all_to_all(send_np, topk, E)
+    rows = [r.shape[0] for r in ref]
+    cap, H = max(rows) + 2, wl.HIDDEN_MOE
+    send = [to_dev(a) for a in send_np]
+    lay = nuna.A2ALayout(topk, E).upload()
+    recv = {p: [torch.zeros((cap, H), dtype=torch.bfloat16, device="cuda") for _ in range(8)] for p in PLACES}
+    a = torch.randn(2560, 8192, dtype=torch.bfloat16, device="cuda")
+    b = torch.randn(8192, 2560, dtype=torch.bfloat16, device="cuda")
+    s_gemm, s_coll = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s_gemm):
+        for _ in range(8):
+            c = torch.matmul(a, b)
+    with torch.cuda.stream(s_coll):
+        for _ in range(20):
+            for p in PLACES:
+                nuna.all_to_all(send, recv[p], lay, placement=p)
+    torch.cuda.synchronize()
+    lay.close()
+    assert torch.isfinite(c.float()).all()
+    for p in PLACES:
+        for d in range(8):
+            got = to_host(recv[p][d])
+            assert_bitwise(got[:rows[d]], ref[d], f"dispatch beside GEMM {p} rank {d}")
+            assert not got[rows[d]:].any(), f"dispatch beside GEMM {p} rank {d}: write past its rows"
+
 def test_prepared_allreduce_repeats_the_call(nuna):
     """A prepared call gives the oracle's bits every time it runs, on the current stream or a given one."""
     x = wl.ar_bf16_decode(16)
