@@ -472,8 +472,13 @@ def moe_dispatch_summary(nuna, torch, pool, args):
     """The MoE dispatch (8 ranks, 512 tokens x 7168 bf16 per rank, top-8 of 256 experts), cold."""
     recs = []
     a2a_case(nuna, torch, pool, args, recs.append, None, colds=(True,))
-    r = recs[0]
+    r, routed = recs
     annotate_targets(r)
+    r["routed"] = {"workload": routed["workload"], "parity": routed["parity"], "same_map": routed["same_map"],
+                   "xcd_us": routed["xcd_us"], "linear_us": routed["linear_us"], "xcd_gbps": routed["xcd_gbps"],
+                   "xcd_frac_hbm": routed["xcd_frac_hbm"],
+                   "layout_xcd_over_routed_time": routed["layout_xcd_over_routed_time"]}
+    r["parity"] = bool(r["parity"] and routed["parity"])
     return r
 
 
@@ -704,6 +709,42 @@ def a2a_case(nuna, torch, pool, args, emit, T_tokens=None, colds=(True, False)):
               **{f"{p}_frac_hbm": round(alg_bytes / (res[p]["median"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
                  for p in res},
               "linear_over_xcd_time": round(res["linear"]["median"] / res["xcd"]["median"], 4)})
+        del graphs
+        # The allocation-free dispatch on the same buffers: routing on the device, and one workgroup per
+        # token row that reads the row once and stores it to each destination (the row's copies share
+        # that read inside the workgroup, whatever the placement).
+        topk_dev = torch.from_numpy(np.ascontiguousarray(topk, dtype=np.int32)).cuda()
+        rows_dev = torch.zeros(P + 1, dtype=torch.int64, device="cuda")
+        ok_r = True
+        for p in ("linear", "xcd"):
+            for d in range(P):
+                sets[0][1][d].zero_()
+            nuna.all_to_all_routed(sets[0][0], sets[0][1], topk_dev, E, rows_dev, placement=p)
+            torch.cuda.synchronize()
+            ok_r = ok_r and rows_dev.cpu().tolist() == [int(r) for r in rows] + [0]
+            for d in range(P):
+                g = sets[0][1][d][:int(rows[d])].cpu().view(torch.int16).numpy().view(np.uint16)
+                ok_r = ok_r and np.array_equal(g, ref[d])
+        graphs = {p: capture(torch, lambda i, p=p: nuna.all_to_all_routed(sets[i % nsets][0], sets[i % nsets][1],
+                                                                           topk_dev, E, rows_dev, placement=p), calls)
+                  for p in ("linear", "xcd")}
+        t = time_graphs(torch, graphs, calls, args.reps, args.warmup)
+        rr = {p: stats(t[p]) for p in t}
+        for p in ("linear", "xcd"):
+            nuna.all_to_all_routed(sets[0][0], sets[0][1], topk_dev, E, rows_dev, placement=p)
+            li[p] = nuna.last_launch()
+        torch.cuda.synchronize()
+        emit({"workload": "a2a_moe_dispatch_routed_bf16_p8" + ("" if T_tokens is None else f"_T{T}"), "P": P,
+              "same_map": same_map(li["linear"], li["xcd"]), "xcd_map": li["xcd"]["map"],
+              "tokens_per_rank": T, "hidden": H,
+              "rows_received": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
+              "calls_per_graph": calls, "parity": bool(ok_r),
+              **{f"{p}_us": {k: round(v, 3) for k, v in rr[p].items()} for p in rr},
+              **{f"{p}_gbps": round(alg_bytes / (rr[p]["median"] * 1e-6) / 1e9, 1) for p in rr},
+              **{f"{p}_frac_hbm": round(alg_bytes / (rr[p]["median"] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+                 for p in rr},
+              "linear_over_xcd_time": round(rr["linear"]["median"] / rr["xcd"]["median"], 4),
+              "layout_xcd_over_routed_time": round(res["xcd"]["median"] / rr["xcd"]["median"], 4)})
         del graphs, sets
     lay.close()
 

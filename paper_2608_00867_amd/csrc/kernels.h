@@ -105,7 +105,7 @@ inline size_t routed_scratch_need(int P, int T, int k) {
 hipError_t routed_scratch_address(void** ptr);
 hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, const int32_t* topk, int P, int T,
                                   int k, int E, int64_t rowvec, int64_t cap, void* scratch_ptr, int64_t* rows_out,
-                                  hipStream_t stream);
+                                  int mode, hipStream_t stream);
 
 hipError_t launch_probe_xcc(int G, int32_t* xcc, int32_t* hw_id, hipStream_t stream);
 

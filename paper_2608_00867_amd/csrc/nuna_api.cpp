@@ -854,6 +854,7 @@ nuna_status_t nuna_all_to_all_routed(const void* const* send, void* const* recv,
     return hip_status(nuna::launch_routed_dispatch(send, recv, topk_idx, P, T, topk, num_experts,
                                                    static_cast<int64_t>(row_bytes / 16),
                                                    static_cast<int64_t>(recv_capacity_rows), scr, rows_per_rank,
+                                                   place == NUNA_PLACE_XCD ? nuna::kPlaceXcd : nuna::kPlaceLinear,
                                                    stream),
                       "routed dispatch launch");
 } catch (...) {

@@ -15,12 +15,19 @@
 //                  token's record lists its destinations in ascending order as
 //                  (rank within s << 6) | d, padded with all ones; lane d
 //                  finally stores cnt[s][d], the tokens of s sent to d.
-//   k_route_copy   one workgroup per token (s, t).  The receive row of copy d
-//                  is sum over s' < s of cnt[s'][d] plus the rank within s.
-//                  The source row is read once into registers and stored to
-//                  every destination row, column pass by column pass, so the
-//                  copies of a token row (the logical group of Sec. 4.2.1)
-//                  share one read and no L2 re-read is needed.
+//   k_route_copy   one work item per (token (s, t), destination slot j),
+//                  j < R: it copies the token's row to the j-th destination of
+//                  its record (an empty slot does nothing).  The receive row of
+//                  copy d is sum over s' < s of cnt[s'][d] plus the rank within
+//                  s.  The R items of a token read the same row: they are the
+//                  logical group of Sec. 4.2.1, and XCD placement runs them on
+//                  consecutive slots of one XCD (placement.h), so the row is
+//                  fetched from HBM once and re-read from that XCD's L2, as the
+//                  layout-driven dispatch does.  LINEAR runs the items in order.
+//                  A first form with one workgroup per token, storing the row
+//                  it had read to every destination, took 95 us at 512 tokens
+//                  per rank on MI355X, against 55 us for the layout-driven
+//                  dispatch with XCD placement.
 //
 // Scratch layout (device bytes from the start of the array):
 //   cnt  int32 [P][P]           tokens of source s routed to d
@@ -82,17 +89,14 @@ __global__ __launch_bounds__(64) void k_route_count(const int32_t* __restrict__ 
 
 constexpr int kRouteVpt = 4;  // 16-byte vectors per thread per column pass
 
-__global__ __launch_bounds__(kWG) void k_route_copy(Ptrs<64> p, int P, int T, int R, int64_t rowvec, int64_t cap,
-                                                    const unsigned char* scr, int64_t* rows_out) {
+template <int MAXP>
+__global__ __launch_bounds__(kWG) void k_route_copy(Ptrs<MAXP> p, int P, int T, int R, int64_t rowvec, int64_t cap,
+                                                    const unsigned char* scr, int64_t* rows_out, Place pl) {
     const int32_t* cnt = reinterpret_cast<const int32_t*>(scr);
     const int32_t* bad = cnt + P * P;
     const uint32_t* rec = reinterpret_cast<const uint32_t*>(bad + P);
-    __shared__ int64_t s_row[64];
-    __shared__ int s_dst[64];
     const int tid = threadIdx.x;
-    const int64_t w = blockIdx.x;
-    const int64_t ntok = static_cast<int64_t>(P) * T;
-    if (w == 0 && tid <= P) {
+    if (blockIdx.x == 0 && tid <= P) {
         // Rows each rank receives (the caller compares them with its capacity)
         // and the count of invalid top-k entries.
         int64_t sum = 0;
@@ -102,41 +106,29 @@ __global__ __launch_bounds__(kWG) void k_route_copy(Ptrs<64> p, int P, int T, in
             for (int q = 0; q < P; ++q) sum += bad[q];
         rows_out[tid] = sum;
     }
-    if (w >= ntok) return;
-    const int s = static_cast<int>(w / T);
     const RankTable tab = load_rank_table(p, P);
-    if (tid < R) {
-        const uint32_t word = rec[w * R + tid];
-        int d = -1;
-        int64_t row = 0;
-        if (word != ~0u) {
-            d = static_cast<int>(word & 63u);
-            row = word >> 6;
-            for (int q = 0; q < s; ++q) row += cnt[q * P + d];
-        }
-        s_dst[tid] = d;
-        s_row[tid] = row;
-    }
-    __syncthreads();
-    const uint4* src = rank_in(tab, s) + static_cast<int64_t>(w - static_cast<int64_t>(s) * T) * rowvec;
-    for (int64_t c0 = 0; c0 < rowvec; c0 += int64_t(kWG) * kRouteVpt) {
-        uint4 y[kRouteVpt];
+    const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
+    for (int64_t i = it.first; i < it.end; i += it.stride) {
+        const int64_t item = item_at(pl, blockIdx.x, gridDim.x, i);
+        const int64_t w = item / R;  // token (s, t) = w
+        const uint32_t word = rec[item];
+        if (word == ~0u) continue;   // the token has fewer destinations than R
+        const int d = static_cast<int>(word & 63u);
+        const int s = static_cast<int>(w / T);
+        int64_t row = word >> 6;
+        for (int q = 0; q < s; ++q) row += cnt[q * P + d];
+        if (row >= cap) continue;    // beyond the caller's capacity: reported through rows_out
+        const uint4* src = rank_in(tab, s) + (w - static_cast<int64_t>(s) * T) * rowvec;
+        uint4* dst = rank_out(tab, d) + row * rowvec;
+        // The group's other items read the same row: loads go through the caches.
+        for (int64_t v = tid; v < rowvec; v += int64_t(kWG) * kRouteVpt) {
+            uint4 y[kRouteVpt];
 #pragma unroll
-        for (int u = 0; u < kRouteVpt; ++u) {
-            const int64_t v = c0 + u * kWG + tid;
-            if (v < rowvec) y[u] = load16<true>(src + v);
-        }
-        for (int j = 0; j < R; ++j) {
-            const int d = __builtin_amdgcn_readfirstlane(s_dst[j]);
-            if (d < 0) break;
-            const int64_t row = s_row[j];
-            if (row >= cap) continue;  // beyond the caller's capacity: reported through rows_out
-            uint4* dst = rank_out(tab, d) + row * rowvec;
+            for (int u = 0; u < kRouteVpt; ++u)
+                if (v + u * kWG < rowvec) y[u] = src[v + u * kWG];
 #pragma unroll
-            for (int u = 0; u < kRouteVpt; ++u) {
-                const int64_t v = c0 + u * kWG + tid;
-                if (v < rowvec) store_stream(dst + v, y[u]);
-            }
+            for (int u = 0; u < kRouteVpt; ++u)
+                if (v + u * kWG < rowvec) store_stream(dst + v + u * kWG, y[u]);
         }
     }
 }
@@ -147,18 +139,31 @@ hipError_t routed_scratch_address(void** ptr) { return hipGetSymbolAddress(ptr, 
 
 hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, const int32_t* topk, int P, int T,
                                   int k, int E, int64_t rowvec, int64_t cap, void* scratch_ptr, int64_t* rows_out,
-                                  hipStream_t stream) {
+                                  int mode, hipStream_t stream) {
     const int R = k < P ? k : P;
     unsigned char* scr = static_cast<unsigned char*>(scratch_ptr);
     hipLaunchKernelGGL(k_route_count, dim3(static_cast<unsigned>(P)), dim3(64), 0, stream, topk, P, T, k, E, R, scr);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    Ptrs<64> p = make_ptrs<64>(send, recv, P, P);
     const int64_t ntok = static_cast<int64_t>(P) * T;
-    const int64_t G = ntok > 0 ? ntok : 1;
-    note_launch("k_route_count+k_route_copy", kMapLinear, 1, G, kWG, kRouteVpt);
-    hipLaunchKernelGGL(k_route_copy, dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P, T, R, rowvec, cap,
-                       static_cast<const unsigned char*>(scratch_ptr), rows_out);
+    const Place pl = make_place_uniform(mode, ntok, R);
+    // One workgroup per item up to 2^20 workgroups unless the caller caps the
+    // grid, as for the layout-driven dispatch.
+    const int64_t want = place_grid(pl);
+    const int64_t lim = grid_limit(int64_t(1) << 20);
+    const int64_t G = want < 1 ? 1 : (want < lim ? want : lim);
+    note_launch("k_route_count+k_route_copy", pl.mode == kPlaceXcd && !linear_map(pl, G) ? kMapXcdGroups : kMapLinear,
+                R, G, kWG, kRouteVpt);
+    const unsigned char* cs = static_cast<const unsigned char*>(scratch_ptr);
+    if (P <= 8) {
+        const Ptrs<8> p = make_ptrs<8>(send, recv, P, P);
+        hipLaunchKernelGGL(k_route_copy<8>, dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P, T, R, rowvec,
+                           cap, cs, rows_out, pl);
+    } else {
+        const Ptrs<64> p = make_ptrs<64>(send, recv, P, P);
+        hipLaunchKernelGGL(k_route_copy<64>, dim3(static_cast<unsigned>(G)), dim3(kWG), 0, stream, p, P, T, R,
+                           rowvec, cap, cs, rows_out, pl);
+    }
     return hipGetLastError();
 }
 

@@ -178,7 +178,8 @@ hipError_t routed_scratch_address(void** ptr) {
 }
 
 hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, const int32_t* topk, int P, int T, int k,
-                                  int E, int64_t rowvec, int64_t cap, void* scratch_ptr, int64_t*, hipStream_t) {
+                                  int E, int64_t rowvec, int64_t cap, void* scratch_ptr, int64_t*, int mode, hipStream_t) {
+    check(mode == 0 || mode == 1, "routed dispatch placement mode");
     check(send && recv && P >= 1 && P <= 64 && T >= 0 && k >= 1 && E % P == 0 && rowvec > 0 && cap >= 0,
           "routed dispatch arguments");
     check(scratch_ptr != nullptr && routed_scratch_need(P, T, k) <= kRoutedScratchBytes, "routed dispatch scratch");

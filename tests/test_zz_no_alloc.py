@@ -85,6 +85,19 @@ def test_routed_matches_layout_dispatch_twice(nuna, place):
     _check_case(nuna, 8, 16, 8, wl.MOE_EXPERTS, wl.HIDDEN_MOE, 22, place)
 
 
+
+def test_routed_launch_record_names_the_map(nuna):
+    """With XCD placement the copies of a token row run as one group per token (top-8 of 8 ranks: groups of 8);
+    with LINEAR, in order."""
+    P, T, k, E, H = 8, 64, 8, 256, 128
+    send = [_dev_rows(a.reshape(-1)).view(T, H) for a in wl.moe_rows(P, T, H, 51)]
+    topk = wl.moe_routing(P, T, k, E, 52)
+    for place, want in (("xcd", "xcd_groups"), ("linear", "linear")):
+        _routed(nuna, send, topk, E, T * P, H, place)
+        rec = nuna.last_launch()
+        assert rec["kernels"] == "k_route_count+k_route_copy" and rec["map"] == want, rec
+        assert rec["grid"] == P * T * min(k, P), rec
+
 def test_routed_many_ranks_odd_rows_and_edges(nuna):
     """64 ranks; rows of one 16-byte vector and of several column passes; one token per rank; no tokens."""
     _check_case(nuna, 64, 40, 8, 256, 64, 31, "xcd")
