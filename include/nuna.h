@@ -362,8 +362,10 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
  * (it looks up the scratch array's address there; NUNA_ERR_UNSUPPORTED
  * without it).  Every call on a GPU uses that GPU's one array: calls on one
  * stream run in order, calls that overlap on one GPU (other streams, other
- * threads) race and must not be made.  Both placement modes run the same map
- * (one workgroup per token row holds all of its copies).  Capture-safe.
+ * threads) race and must not be made.  One work item copies a token row to
+ * one of its destinations; NUNA_PLACE_XCD runs the copies of a token row on
+ * one XCD (a logical group, as nuna_all_to_all does with its layout),
+ * NUNA_PLACE_LINEAR in order.  Capture-safe.
  */
 nuna_status_t nuna_all_to_all_routed(const void* const* send, void* const* recv, const int32_t* topk_idx, int P,
                                      int tokens_per_rank, int topk, int num_experts, size_t row_elems,
