@@ -8,13 +8,17 @@
 // is device memory and the receive row of every copy is computed on the
 // device:
 //
-//   k_route_count  one wave per source rank s.  Walking its tokens 64 at a
-//                  time, each lane forms its token's destination mask; for
-//                  each destination d a wave ballot of the mask bit gives the
-//                  token's rank among the tokens of s sent to d so far.  Each
-//                  token's record lists its destinations in ascending order as
-//                  (rank within s << 6) | d, padded with all ones; lane d
-//                  finally stores cnt[s][d], the tokens of s sent to d.
+//   k_route_count  one workgroup per source rank s (64 threads per 64
+//                  tokens, up to 1024 per pass), 64 tokens per wave.  Each
+//                  lane forms its token's destination mask; a wave ballot per
+//                  destination d counts
+//                  the wave's tokens sent to d, and a scan of those counts over
+//                  the waves in LDS gives every token its rank among the
+//                  tokens of s sent to d.  Each token's record lists its
+//                  destinations in ascending order as (rank within s << 6) | d,
+//                  padded with all ones; cnt[s][d] is the total.  (A first form,
+//                  one wave per source walking 64 tokens at a time, took 21 us at
+//                  512 tokens per rank on MI355X: one DRAM round trip per step.)
 //   k_route_copy   one work item per (token (s, t), destination slot j),
 //                  j < R: it copies the token's row to the j-th destination of
 //                  its record (an empty slot does nothing).  The receive row of
@@ -46,19 +50,39 @@ static __device__ __align__(256) unsigned char scratch[kRoutedScratchBytes];
 
 namespace {
 
-__global__ __launch_bounds__(64) void k_route_count(const int32_t* __restrict__ topk, int P, int T, int k, int E,
-                                                    int R, unsigned char* scr) {
+constexpr int kRouteCountThreads = 1024;  // most tokens of one source per pass: 16 waves of 64
+constexpr int kRouteCountWaves = kRouteCountThreads / 64;
+
+// One workgroup per source rank s, of 64 threads per 64 tokens up to 1024
+// (a small launch keeps its scan and barriers short); each pass takes
+// blockDim.x tokens, wave w the 64 from t0 + 64 w.  Every lane loads its
+// token's k experts (one round of loads per pass), forms the token's
+// destination mask, and a wave ballot per destination d gives the token's
+// rank among the wave's tokens sent to d.
+// The waves' counts go through LDS, where an exclusive scan per destination
+// over the waves (and the passes before) gives each wave's offset; a second
+// ballot pass then writes the records.  The rank of a token is the number of
+// earlier tokens of s sent to d, whichever wave or pass counts them.
+__global__ __launch_bounds__(kRouteCountThreads) void k_route_count(const int32_t* __restrict__ topk, int P, int T,
+                                                                    int k, int E, int R, unsigned char* scr) {
     int32_t* cnt = reinterpret_cast<int32_t*>(scr);
     int32_t* bad = cnt + P * P;
     uint32_t* rec = reinterpret_cast<uint32_t*>(bad + P);
+    __shared__ int wave_cnt[kRouteCountWaves][64];  // tokens of wave w sent to d (this pass)
+    __shared__ int offset[kRouteCountWaves][64];    // tokens of s sent to d before wave w's first token
+    __shared__ int carry[64];                       // tokens of s sent to d in earlier passes
+    __shared__ int wave_bad[kRouteCountWaves];
     const int s = blockIdx.x;
-    const int lane = threadIdx.x;
+    const int tid = threadIdx.x;
+    const int wave = tid >> 6;
+    const int lane = tid & 63;
     const int per = E / P;
     const uint64_t below = (uint64_t(1) << lane) - 1;
-    int run = 0;   // lane d: tokens of s routed to d so far
+    if (tid < 64) carry[tid] = 0;
     int nbad = 0;  // this lane's invalid entries
-    for (int t0 = 0; t0 < T; t0 += 64) {
-        const int t = t0 + lane;
+    const int nw = static_cast<int>(blockDim.x) >> 6;
+    for (int t0 = 0; t0 < T; t0 += static_cast<int>(blockDim.x)) {
+        const int t = t0 + tid;
         uint64_t mask = 0;
         if (t < T) {
             const int32_t* row = topk + (static_cast<int64_t>(s) * T + t) * k;
@@ -70,21 +94,46 @@ __global__ __launch_bounds__(64) void k_route_count(const int32_t* __restrict__ 
                     ++nbad;
             }
         }
-        uint32_t* my = rec + (static_cast<int64_t>(s) * T + t) * R;
-        int j = 0;
+        int mine = 0;  // lane d: tokens of this wave sent to d
         for (int d = 0; d < P; ++d) {
-            const bool on = (mask >> d) & 1u;
-            const uint64_t bal = __ballot(on);
-            const int before = __builtin_amdgcn_readlane(run, d);
-            if (on) my[j++] = (static_cast<uint32_t>(before + __popcll(bal & below)) << 6) | static_cast<uint32_t>(d);
-            if (lane == d) run += __popcll(bal);
+            const int c = __popcll(__ballot((mask >> d) & 1u));
+            if (lane == d) mine = c;
         }
-        if (t < T)
+        if (lane < P) wave_cnt[wave][lane] = mine;
+        __syncthreads();
+        if (tid < P) {
+            int run = carry[tid];
+            for (int w = 0; w < nw; ++w) {
+                offset[w][tid] = run;
+                run += wave_cnt[w][tid];
+            }
+            carry[tid] = run;
+        }
+        __syncthreads();
+        if (t < T) {
+            uint32_t* my = rec + (static_cast<int64_t>(s) * T + t) * R;
+            int j = 0;
+            for (int d = 0; d < P; ++d) {
+                const bool on = (mask >> d) & 1u;
+                const uint64_t bal = __ballot(on);
+                if (on) my[j++] = (static_cast<uint32_t>(offset[wave][d] + __popcll(bal & below)) << 6) |
+                                  static_cast<uint32_t>(d);
+            }
+            // Lanes past T hold no token and are the wave's last: left out of the ballots, they change
+            // no rank.
             for (; j < R; ++j) my[j] = ~0u;
+        }
+        __syncthreads();  // offset and carry are rewritten by the next pass
     }
-    if (lane < P) cnt[s * P + lane] = run;
+    if (tid < P) cnt[s * P + tid] = carry[tid];
     for (int off = 32; off > 0; off >>= 1) nbad += __shfl_down(nbad, off);
-    if (lane == 0) bad[s] = nbad;
+    if (lane == 0) wave_bad[wave] = nbad;
+    __syncthreads();
+    if (tid == 0) {
+        int total = 0;
+        for (int w = 0; w < nw; ++w) total += wave_bad[w];
+        bad[s] = total;
+    }
 }
 
 constexpr int kRouteVpt = 4;  // 16-byte vectors per thread per column pass
@@ -142,7 +191,9 @@ hipError_t launch_routed_dispatch(const void* const* send, void* const* recv, co
                                   int mode, hipStream_t stream) {
     const int R = k < P ? k : P;
     unsigned char* scr = static_cast<unsigned char*>(scratch_ptr);
-    hipLaunchKernelGGL(k_route_count, dim3(static_cast<unsigned>(P)), dim3(64), 0, stream, topk, P, T, k, E, R, scr);
+    const int nt = T >= kRouteCountThreads ? kRouteCountThreads : (T < 64 ? 64 : (T + 63) / 64 * 64);
+    hipLaunchKernelGGL(k_route_count, dim3(static_cast<unsigned>(P)), dim3(static_cast<unsigned>(nt)), 0, stream, topk,
+                       P, T, k, E, R, scr);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t ntok = static_cast<int64_t>(P) * T;

@@ -99,11 +99,15 @@ def test_routed_launch_record_names_the_map(nuna):
         assert rec["grid"] == P * T * min(k, P), rec
 
 def test_routed_many_ranks_odd_rows_and_edges(nuna):
-    """64 ranks; rows of one 16-byte vector and of several column passes; one token per rank; no tokens."""
+    """64 ranks; rows of one 16-byte vector and of several column passes; one token per rank; several passes
+    of the routing kernel; no tokens."""
     _check_case(nuna, 64, 40, 8, 256, 64, 31, "xcd")
     _check_case(nuna, 3, 50, 2, 6, 8, 32, "linear")
     _check_case(nuna, 5, 7, 5, 10, 8 * 1100, 33, "xcd")
     _check_case(nuna, 8, 1, 8, 64, 128, 34, "linear")
+    # more tokens than one pass of the routing kernel (1024): ranks carried across passes
+    _check_case(nuna, 8, 3000, 8, 256, 64, 35, "xcd")
+    _check_case(nuna, 4, 2500, 3, 16, 32, 36, "linear")
     P, H, E = 4, 64, 8
     send = [torch.zeros((1, H), dtype=torch.bfloat16, device="cuda") for _ in range(P)]
     recv = _recv(P, 4, H)
