@@ -700,8 +700,8 @@ def a2a_case(nuna, torch, pool, args, emit, T_tokens=None, colds=(True, False)):
             li[p] = nuna.last_launch()
         torch.cuda.synchronize()
         emit({"workload": "a2a_moe_dispatch_bf16_p8" + ("" if T_tokens is None else f"_T{T}"), "P": P,
-              "same_map": same_map(li["linear"], li["xcd"]), "xcd_map": li["xcd"]["map"],
-              "tokens_per_rank": T, "hidden": H,
+              "same_map": same_map(li["linear"], li["xcd"]), "xcd_kernels": li["xcd"]["kernels"],
+              "xcd_map": li["xcd"]["map"], "tokens_per_rank": T, "hidden": H,
               "rows_received": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
               "calls_per_graph": calls, "parity": bool(ok),
               **{f"{p}_us": {k: round(v, 3) for k, v in res[p].items()} for p in res},
@@ -735,8 +735,8 @@ def a2a_case(nuna, torch, pool, args, emit, T_tokens=None, colds=(True, False)):
             li[p] = nuna.last_launch()
         torch.cuda.synchronize()
         emit({"workload": "a2a_moe_dispatch_routed_bf16_p8" + ("" if T_tokens is None else f"_T{T}"), "P": P,
-              "same_map": same_map(li["linear"], li["xcd"]), "xcd_map": li["xcd"]["map"],
-              "tokens_per_rank": T, "hidden": H,
+              "same_map": same_map(li["linear"], li["xcd"]), "xcd_kernels": li["xcd"]["kernels"],
+              "xcd_map": li["xcd"]["map"], "tokens_per_rank": T, "hidden": H,
               "rows_received": int(rows.sum()), "cache": "cold" if cold else "warm", "alg_bytes": alg_bytes,
               "calls_per_graph": calls, "parity": bool(ok_r),
               **{f"{p}_us": {k: round(v, 3) for k, v in rr[p].items()} for p in rr},
