@@ -710,9 +710,10 @@ def a2a_case(nuna, torch, pool, args, emit, T_tokens=None, colds=(True, False)):
                  for p in res},
               "linear_over_xcd_time": round(res["linear"]["median"] / res["xcd"]["median"], 4)})
         del graphs
-        # The allocation-free dispatch on the same buffers: routing on the device, and one workgroup per
-        # token row that reads the row once and stores it to each destination (the row's copies share
-        # that read inside the workgroup, whatever the placement).
+        # The allocation-free dispatch on the same buffers: the routing computed on the device from the
+        # top-k table, one work item per (token, destination slot), a token's slots grouped on one XCD
+        # with XCD placement (one kernel up to 256 tokens over all ranks, else a routing kernel and a
+        # copy kernel).
         topk_dev = torch.from_numpy(np.ascontiguousarray(topk, dtype=np.int32)).cuda()
         rows_dev = torch.zeros(P + 1, dtype=torch.int64, device="cuda")
         ok_r = True

@@ -357,10 +357,12 @@ nuna_status_t nuna_all_to_all(const void* const* send, void* const* recv, const 
  *                  [P] = top-k entries outside [0, num_experts).
  * The routing tables need 4*P*P + 4*P + 4*P*tokens_per_rank*min(topk, P)
  * bytes of the scratch: larger calls return NUNA_ERR_INVALID_ARG, as do
- * P*tokens_per_rank >= 2^26.  Rows must be whole 16-byte vectors
- * (NUNA_ERR_UNSUPPORTED otherwise).  Needs nuna_init on the current device
- * (it looks up the scratch array's address there; NUNA_ERR_UNSUPPORTED
- * without it).  Every call on a GPU uses that GPU's one array: calls on one
+ * P*tokens_per_rank >= 2^26.  Calls of at most 256 tokens over all ranks
+ * (and at most 2048 top-k entries) run as one kernel that recomputes the
+ * routing in every workgroup and leaves the scratch alone.  Rows must be
+ * whole 16-byte vectors (NUNA_ERR_UNSUPPORTED otherwise).  Needs nuna_init
+ * on the current device (it looks up the scratch array's address there;
+ * NUNA_ERR_UNSUPPORTED without it).  Every call on a GPU uses that GPU's one array: calls on one
  * stream run in order, calls that overlap on one GPU (other streams, other
  * threads) race and must not be made.  One work item copies a token row to
  * one of its destinations; NUNA_PLACE_XCD runs the copies of a token row on
