@@ -59,6 +59,7 @@
 // R record words, so nothing needs clearing between calls.  The decode path
 // (k_route_small) uses no scratch.
 #include "device_common.h"
+#include "fastdiv.h"
 
 namespace nuna {
 
@@ -75,28 +76,6 @@ constexpr int kRouteBatch = 8;            // top-k entries (or counts) loaded pe
 constexpr int kRouteSmallTokens = kWG;    // decode path: one token per thread
 constexpr int kRouteSmallEntries = 2048;  // decode path: top-k entries every workgroup reads
 constexpr int kRouteVpt = 4;              // 16-byte vectors per thread per column pass
-
-// Division by a divisor known only at run time, for numerators below 2^31.
-// An integer division has no instruction and expands to a long sequence.
-// With l = ceil(log2 d) and
-// m = ceil(2^(31+l) / d) (computed on the host, below 2^32), n / d equals
-// (m * n) >> (31 + l) for every n < 2^31 (Granlund and Montgomery, 1994,
-// Thm. 4.2): one 32 x 32 -> 64-bit multiply and a shift.
-struct Magic {
-    uint32_t m;
-    int32_t sh;
-};
-
-Magic make_magic(uint32_t d) {
-    int l = 0;
-    while ((uint64_t(1) << l) < d) ++l;
-    const uint64_t num = uint64_t(1) << (31 + l);
-    return {static_cast<uint32_t>((num + d - 1) / d), 31 + l};
-}
-
-__device__ __forceinline__ uint32_t udiv(uint32_t n, const Magic& g) {
-    return static_cast<uint32_t>((static_cast<uint64_t>(g.m) * n) >> g.sh);
-}
 
 // Destination mask of one token: bit d set when one of its k experts lives on
 // rank d (expert e on rank e / per); entries outside [0, E) are counted in
