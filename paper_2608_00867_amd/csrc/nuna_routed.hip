@@ -21,12 +21,12 @@
 //                  9.8 us (the layout-driven dispatch: 3.3 us).  Every
 //                  workgroup repeats the routing, so its cost is paid 1024
 //                  times there: 4-byte loads of the entries instead of 16-byte
-//                  ones cost 1.5 us, integer divisions 1 us.
+//                  ones cost 1.5 us, integer divisions 0.9 us.
 //   k_route_count  one workgroup per source rank s (64 threads per 64
 //                  tokens, up to 1024 per pass), 64 tokens per wave.  Each
 //                  lane forms its token's destination mask (its k entries
-//                  loaded together: one load at a time took 5 us at any
-//                  size); a wave ballot per destination d counts the wave's
+//                  loaded together, as in k_route_small); a wave ballot per
+//                  destination d counts the wave's
 //                  tokens sent to d, and a scan of those counts over the waves
 //                  in LDS gives every token its rank among the tokens of s
 //                  sent to d.  Each token's record lists its destinations in
