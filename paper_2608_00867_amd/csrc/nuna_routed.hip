@@ -17,7 +17,7 @@
 //                  same rank: a ballot per wave and a sum over the waves.
 //                  The last workgroup also reports the rows per rank.  At 16
 //                  tokens per rank (8 ranks, 7168 bf16, top-8 of 256) it takes
-//                  5.2 us cold on MI355X, where the two launches below took
+//                  4.9 us cold on MI355X, where the two launches below took
 //                  9.8 us (the layout-driven dispatch: 3.3 us).  Every
 //                  workgroup repeats the routing, so its cost is paid 1024
 //                  times there: 4-byte loads of the entries instead of 16-byte
@@ -143,10 +143,9 @@ __device__ __forceinline__ int wave_sum(int v) {
 }
 
 // One token row to one destination row: the R items of a token read the same
-// row, so loads go through the caches; stores stream.  Columns from v0 on
-// (v0 = tid, or past a first pass already loaded).
-__device__ __forceinline__ void copy_row(const uint4* src, uint4* dst, int64_t rowvec, int64_t v0) {
-    for (int64_t v = v0; v < rowvec; v += int64_t(kWG) * kRouteVpt) {
+// row, so loads go through the caches; stores stream.
+__device__ __forceinline__ void copy_row(const uint4* src, uint4* dst, int64_t rowvec, int tid) {
+    for (int64_t v = tid; v < rowvec; v += int64_t(kWG) * kRouteVpt) {
         uint4 y[kRouteVpt];
 #pragma unroll
         for (int u = 0; u < kRouteVpt; ++u)
@@ -176,26 +175,13 @@ __global__ __launch_bounds__(kWG) void k_route_small(Ptrs<MAXP> p, const int32_t
     const int wave = tid >> 6;
     const int lane = tid & 63;
     const int ntok = P * T;
-    // The source row of the first item does not depend on the routing: its
-    // first column pass is loaded right after the top-k entries and is in
-    // flight while the routing runs.  Vector loads complete in issue order
-    // for the wait counter, so the order is the top-k entries, the row, then
-    // the rank pointers; the row's address comes from the kernel arguments
-    // (a scalar load, counted apart).
+    // The top-k entries are loaded first: the routing waits on them.  (Loading
+    // the first item's row beside them, which does not depend on the routing,
+    // was 0.3 us slower at 16 tokens per rank on MI355X.)
     const int32_t* my_row = topk + static_cast<int64_t>(tid) * k;
     int e0[kRouteBatch] = {};
     if (tid < ntok) load_round(my_row, k, 0, vec != 0, e0);
     const ItemRange it = items_of(pl, blockIdx.x, gridDim.x);
-    uint4 pre[kRouteVpt];
-    if (it.first < it.end) {
-        const uint32_t item = static_cast<uint32_t>(item_at(pl, blockIdx.x, gridDim.x, it.first));
-        const int w = static_cast<int>(udiv(item, byR));
-        const int s = static_cast<int>(udiv(static_cast<uint32_t>(w), byT));
-        const uint4* src = p.in[s] + static_cast<int64_t>(w - s * T) * rowvec;
-#pragma unroll
-        for (int u = 0; u < kRouteVpt; ++u)
-            if (tid + u * kWG < rowvec) pre[u] = src[tid + u * kWG];
-    }
     const RankTable tab = load_rank_table(p, P);
     int nbad = 0;
     uint64_t mask = 0;
@@ -248,14 +234,7 @@ __global__ __launch_bounds__(kWG) void k_route_small(Ptrs<MAXP> p, const int32_t
         const int s = static_cast<int>(udiv(static_cast<uint32_t>(w), byT));
         const uint4* src = rank_in(tab, s) + static_cast<int64_t>(w - s * T) * rowvec;
         uint4* dst = rank_out(tab, d) + row * rowvec;
-        int64_t v0 = tid;
-        if (i == it.first) {  // the first pass is in registers
-#pragma unroll
-            for (int u = 0; u < kRouteVpt; ++u)
-                if (tid + u * kWG < rowvec) store_stream(dst + tid + u * kWG, pre[u]);
-            v0 += int64_t(kWG) * kRouteVpt;
-        }
-        copy_row(src, dst, rowvec, v0);
+        copy_row(src, dst, rowvec, tid);
     }
 }
 
