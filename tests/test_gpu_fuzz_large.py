@@ -1,5 +1,6 @@
 """GPU: seeded random calls at large sizes through the C ABI against the oracle, bit for bit, with guard
-bands around every output: the all-reduce, the reduce-scatter, the all-gather and the MoE dispatch and combine.
+bands around every output: the all-reduce, the reduce-scatter, the all-gather, the MoE dispatch (layout-driven
+and allocation-free) and the combine.
 
 The cases of test_gpu_fuzz.py stay below 400,000 elements in all.  These reach 24 MiB per rank (per-rank
 bytes log-uniform from one element, half of them snapped near a power of two or to whole 16-byte vectors:
@@ -99,6 +100,8 @@ def _moe_cases(kind, count, seed):
         dtype = str(rng.choice(["f32", "bf16"]))
         es = 4 if dtype == "f32" else 2
         H = int(np.exp(rng.uniform(0.0, np.log(8192))))
+        if kind == "routed":  # the routed dispatch moves whole 16-byte vectors
+            H = max(16 // es, H // (16 // es) * (16 // es))
         T = int(np.exp(rng.uniform(0.0, np.log(512))))
         T = max(1, min(T, (96 << 20) // (P * H * es * min(k, P))))
         place = str(rng.choice(PLACES))
@@ -112,10 +115,12 @@ def _moe_cases(kind, count, seed):
                    {"cap": int(rng.choice([1, 13, 200]))} if j == 7 else {})
         elif rng.random() < 0.25:
             tun = {"cap": int(rng.choice([1, 13, 200]))}
+        misalign = kind == "routed" and bool(rng.random() < 0.25)
         desc = [f"{kind}{i:02d}", f"P{P}", f"E{E}", f"k{k}", f"T{T}", f"H{H}", dtype, place] + \
-            (["weighted"] if weighted else []) + [f"{a.replace('NUNA_', '')}={v}" for a, v in tun.items()]
+            (["weighted"] if weighted else []) + (["misaligned"] if misalign else []) + \
+            [f"{a.replace('NUNA_', '')}={v}" for a, v in tun.items()]
         out.append(pytest.param(dict(P=P, E=E, k=k, T=T, H=H, dtype=dtype, place=place, weighted=weighted,
-                                     tun=tun, seed=seed * 1000 + i), id="-".join(desc)))
+                                     misalign=misalign, tun=tun, seed=seed * 1000 + i), id="-".join(desc)))
     return out
 
 
@@ -260,3 +265,39 @@ def test_combine_random(nuna, c):
         got = run_combine(nuna, y, topk, E, c["place"], weights=w)
     for s in range(P):
         assert_bitwise(got[s], ref[s], f"rank {s}")
+
+
+@pytest.mark.parametrize("c", _moe_cases("routed", 48, 7306))
+def test_routed_dispatch_random(nuna, c):
+    """The allocation-free dispatch (one kernel up to 256 tokens over all ranks, else routing then copy):
+    receive rows and row counts against the oracle, sentinel rows past each rank's count untouched; a
+    quarter of the top-k tables sit 4 bytes past a 16-byte boundary."""
+    P, T, H, E = c["P"], c["T"], c["H"], c["E"]
+    dt = np.uint16 if c["dtype"] == "bf16" else np.float32
+    topk = wl.moe_routing(P, T, c["k"], E, c["seed"])
+    send_np = [a.reshape(T, H) for a in wl.random_bits(P, T * H, dt, c["seed"] + 1)]
+    ref = oracle.all_to_all(send_np, topk, E)
+    rows = [r.shape[0] for r in ref]
+    cap = max(rows) + 2
+    send = [to_dev(a) for a in send_np]
+    tdt = send[0].dtype
+    sentinel = 0x7FA5 if tdt == torch.bfloat16 else 0x7FA5A5A5
+    ity = torch.int16 if tdt == torch.bfloat16 else torch.int32
+    recv = [torch.full((cap, H), sentinel, dtype=ity, device="cuda").view(tdt) for _ in range(P)]
+    flat = torch.from_numpy(np.ascontiguousarray(topk, dtype=np.int32).reshape(-1))
+    if c["misalign"]:
+        buf = torch.zeros(flat.numel() + 1, dtype=torch.int32, device="cuda")
+        buf[1:].copy_(flat)
+        topk_dev = buf[1:].view(topk.shape)
+    else:
+        topk_dev = flat.cuda().view(topk.shape)
+    rows_dev = torch.full((P + 1,), -1, dtype=torch.int64, device="cuda")
+    with _Tuned(nuna, c["tun"]):
+        nuna.all_to_all_routed(send, recv, topk_dev, E, rows_dev, placement=c["place"])
+        torch.cuda.synchronize()
+    assert rows_dev.cpu().tolist() == rows + [0]
+    for d in range(P):
+        got = to_host(recv[d])
+        assert_bitwise(got[:rows[d]], ref[d], f"rank {d}")
+        past = got[rows[d]:].view(np.int16 if tdt == torch.bfloat16 else np.int32)
+        assert np.all(past == np.array(sentinel, dtype=past.dtype)), f"rank {d}: rows past the count written"
