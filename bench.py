@@ -1291,9 +1291,19 @@ def moe_alg_bytes():
     return int(rows.sum() * rb + topk.shape[0] * topk.shape[1] * rb)
 
 
+def route_count_bytes():
+    """Algorithmic bytes of the routed dispatch's routing kernel at the MoE shape: the int32 top-k
+    table read once, then min(k, P) 4-byte records per token and the P x P counts and P invalid-entry
+    counts written."""
+    from paper_2608_00867_amd import workloads as wl
+    _, topk = wl.a2a_moe()
+    P, T, k = (int(v) for v in topk.shape)
+    return 4 * P * T * k + 4 * P * T * min(k, P) + 4 * P * P + 4 * P
+
+
 def profile_moe(nuna, torch, pool, n, place="xcd"):
-    """`n` dispatches then `n` combines at the MoE shape, rotating over buffer sets that together
-    exceed the caches."""
+    """`n` dispatches, `n` combines, then `n` allocation-free (routed) dispatches at the MoE shape,
+    rotating over buffer sets that together exceed the caches."""
     from paper_2608_00867_amd import workloads as wl
     send_np, topk = wl.a2a_moe()
     E, H = wl.MOE_EXPERTS, wl.HIDDEN_MOE
@@ -1320,8 +1330,14 @@ def profile_moe(nuna, torch, pool, n, place="xcd"):
         tok, rec = sets[i % nsets]
         nuna.all_to_all_combine(rec, tok, lay, placement=place)
     torch.cuda.synchronize()
+    topk_dev = torch.from_numpy(np.ascontiguousarray(topk, dtype=np.int32)).cuda()
+    rows_dev = torch.zeros(P + 1, dtype=torch.int64, device="cuda")
+    for i in range(n):
+        tok, rec = sets[i % nsets]
+        nuna.all_to_all_routed(tok, rec, topk_dev, E, rows_dev, placement=place)
+    torch.cuda.synchronize()
     lay.close()
-    return {"moe_launches": n, "moe_alg_bytes": moe_alg_bytes()}
+    return {"moe_launches": n, "moe_alg_bytes": moe_alg_bytes(), "routed_launches": n}
 
 
 # ---------------------------------------------------------------------------------------------- rocprofv3 summaries
@@ -1497,11 +1513,13 @@ def summarize_traffic(fetch_csv, write_csv):
                 return 8 * nb, "P n s (in-place shard skipped: (P - 1) n s written, n s read)"
             if name.startswith("k_allreduce"):
                 return dec, "2 P n s"
+            if name.startswith("k_route_count"):
+                return route_count_bytes(), "top-k table read + routing records and counts written"
             return malg, "rows read + rows written"
         print("\nOther kernels of the same runs: the two-kernel two-shot at [256, 8192] bf16 per rank (its "
               "reduce-scatter and all-gather phases), the split all-reduce (decode T=64, 8 destination groups "
               "per chunk) and the MoE kernels (8 ranks, 512 tokens x 7168 bf16 per rank, top-8 of 256 "
-              f"experts):\n")
+              f"experts; the dispatch, the combine and the allocation-free dispatch's routing and copy):\n")
         print("| kernel | grid (threads) | FETCH_SIZE (KiB) | WRITE_SIZE (KiB) | scaled fetch B | scaled write B | "
               "algorithmic B | traffic / algorithmic |")
         print("|---|---|---|---|---|---|---|---|")
@@ -1545,7 +1563,11 @@ def summarize_l2(linear_csv, xcd_csv):
         return by
 
     runs = {"LINEAR": read(linear_csv), "XCD": read(xcd_csv)}
-    keys = [k for k in runs["XCD"] if k[0].startswith(("k_allreduce", "k_all_to_all", "k_combine"))]
+    keys = []  # every kernel of either run, in dispatch order; a placement's grid may differ
+    for run in runs.values():
+        keys += [k for k in run if k not in keys and k[0].startswith(("k_allreduce", "k_all_to_all", "k_combine",
+                                                                       "k_route"))]
+    keys.sort(key=lambda k: (k[0], k[1]))
     print("| kernel | grid (threads) | placement | L2 hits | L2 misses | hit rate |")
     print("|---|---|---|---|---|---|")
     for k in keys:
@@ -1588,7 +1610,8 @@ def summarize_l2_xcc(specs):
             vals[(place.upper(), _short(r["Kernel_Name"]), int(r["Grid_Size"]), r["Counter_Name"])].append(
                 float(r["Counter_Value"]))
     places = sorted({k[0] for k in vals})
-    kernels = sorted({(k[1], k[2]) for k in vals if k[1].startswith(("k_allreduce", "k_all_to_all", "k_combine"))})
+    kernels = sorted({(k[1], k[2]) for k in vals
+                      if k[1].startswith(("k_allreduce", "k_all_to_all", "k_combine", "k_route"))})
     print("| kernel | grid (threads) | placement | " + " | ".join(f"XCD {x}" for x in range(8)) + " | min–max |")
     print("|---|---|---|" + "---|" * 9)
     for kern, grid in kernels:
