@@ -1178,7 +1178,8 @@ def affinity(nuna, torch, pool):
         lab = np.stack([passes[0][v * nb:(v + 1) * nb] for v in range(2 * P)])
         maj = (lab.mean(axis=0) >= 0.5).astype(int)
         print(json.dumps({"layout": f"all-reduce bf16 P=8 [{T},8192]: 16 buffers of {per >> 10} KiB",
-                          "blocks_per_buffer": nb, "probe_repeatability": round(float(np.mean(passes[0] == passes[1])), 3),
+                          "blocks_per_buffer": nb,
+                          "probe_repeatability": round(float(np.mean(passes[0] == passes[1])), 3),
                           "agreement_with_rank0_input": [round(float(np.mean(lab[v] == lab[0])), 3)
                                                          for v in range(2 * P)],
                           "near_fraction_on_majority_die": round(float(np.mean(lab == maj[None, :])), 3)}),
