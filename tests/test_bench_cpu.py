@@ -114,6 +114,34 @@ def test_summarize_traffic_scales_each_counter_by_the_reference_copy(tmp_path, c
     assert f"ratio {rec['traffic_bytes'] / rec['alg_bytes']:.4f}" in out and "k_probe_xcc" not in out
 
 
+def test_summarize_l2_lists_kernels_of_either_placement(tmp_path, capsys):
+    """A kernel whose grid differs between the placements (the layout-driven dispatch sizes its XCD grid
+    for the longest per-XCD list) is listed under each placement; a kernel of neither family is not."""
+    cols = ["Kernel_Name", "Grid_Size", "Counter_Name", "Counter_Value"]
+
+    def rows(grid_a2a, hit):
+        out = []
+        for name, grid in (("k_all_to_all<8, 4>", grid_a2a), ("k_route_copy<8>", 8388608), ("k_copy<1>", 4096)):
+            out.append([_mangled(name), grid, "TCC_HIT_sum", hit])
+            out.append([_mangled(name), grid, "TCC_MISS_sum", 100.0 - hit])
+        return out
+
+    _write_csv(tmp_path / "lin.csv", cols, rows(5544704, 34.0))
+    _write_csv(tmp_path / "xcd.csv", cols, rows(5548032, 60.0))
+    bench.summarize_l2(str(tmp_path / "lin.csv"), str(tmp_path / "xcd.csv"))
+    out = capsys.readouterr().out
+    assert "| `k_all_to_all<8, 4>` | 5544704 | LINEAR | 34 | 66 | 0.340 |" in out
+    assert "| `k_all_to_all<8, 4>` | 5548032 | XCD | 60 | 40 | 0.600 |" in out
+    assert "| `k_route_copy<8>` | 8388608 | LINEAR |" in out and "| `k_route_copy<8>` | 8388608 | XCD |" in out
+    assert "k_copy" not in out
+
+
+def test_route_count_bytes_at_the_moe_shape():
+    """The routing kernel's algorithmic bytes at 8 ranks x 512 tokens, top-8: the table read (4 B per entry),
+    min(k, P) = 8 records per token and the 8 x 8 + 8 counts written."""
+    assert bench.route_count_bytes() == 4 * 8 * 512 * 8 + 4 * 8 * 512 * 8 + 4 * 64 + 4 * 8
+
+
 def test_target_verdicts():
     """No slower: XCD's median within 2 % of LINEAR's, or XCD's p10 at or below LINEAR's p90.  The 70 %
     verdict applies from 4 MiB per rank only."""
