@@ -157,18 +157,15 @@ __device__ __forceinline__ void copy_row(const uint4* src, uint4* dst, int64_t r
 }
 
 // Decode path: P*T <= kRouteSmallTokens tokens, one per thread.  Every
-// workgroup forms all destination masks, keeps them in LDS (and its own in a
-// register), then runs its items: item (w, j) copies token w = s*T + t to the
-// j-th rank d of its mask, at receive row = tokens w' < w (source-major, the
-// receive order) whose mask holds d.  The per-wave counts meet in LDS,
-// double-buffered so that one barrier per item suffices; an item whose slot
-// is empty, identical for the whole workgroup, skips the barrier with it.
+// workgroup forms all destination masks and keeps them in LDS, then runs its
+// items: item (w, j) copies token w = s*T + t to the j-th rank d of its mask,
+// at receive row = tokens w' < w (source-major, the receive order) whose mask
+// holds d, which each wave counts from the masks in LDS.
 template <int MAXP>
 __global__ __launch_bounds__(kWG) void k_route_small(Ptrs<MAXP> p, const int32_t* __restrict__ topk, int P, int T,
                                                      int k, int E, int R, Magic per, Magic byR, Magic byT, int vec,
                                                      int64_t rowvec, int64_t cap, int64_t* rows_out, Place pl) {
     __shared__ uint64_t masks[kRouteSmallTokens];
-    __shared__ int part[2][kWG / 64];        // per wave: earlier tokens sent to the item's rank
     __shared__ int total[kWG / 64][64];      // reporter: per wave, tokens sent to d
     __shared__ int wave_bad[kWG / 64];
     const int tid = threadIdx.x;
@@ -215,7 +212,6 @@ __global__ __launch_bounds__(kWG) void k_route_small(Ptrs<MAXP> p, const int32_t
         for (int w = 0; w < kWG / 64; ++w) sum += tid < P ? total[w][tid] : wave_bad[w];
         rows_out[tid] = sum;
     }
-    int buf = 0;
     for (int64_t i = it.first; i < it.end; i += it.stride) {
         const uint32_t item = static_cast<uint32_t>(item_at(pl, blockIdx.x, gridDim.x, i));  // < 256 * 64
         const int w = static_cast<int>(udiv(item, byR));
@@ -224,12 +220,14 @@ __global__ __launch_bounds__(kWG) void k_route_small(Ptrs<MAXP> p, const int32_t
         for (int q = 0; q < j; ++q) m &= m - 1;
         if (m == 0) continue;  // the token has fewer than j + 1 destinations
         const int d = __builtin_ctzll(m);
-        const int c = __popcll(__ballot(tid < w && ((mask >> d) & 1u)));
-        if (lane == 0) part[buf][wave] = c;
-        __syncthreads();
+        // Every wave counts the earlier tokens itself, lane l looking at tokens l, l + 64, ...: no
+        // barrier per item.
         int64_t row = 0;
-        for (int q = 0; q < kWG / 64; ++q) row += part[buf][q];
-        buf ^= 1;  // the next item that counts writes the other buffer: its barrier orders these reads
+#pragma unroll
+        for (int q = 0; q < kRouteSmallTokens / 64; ++q) {
+            const int x = lane + 64 * q;
+            row += __popcll(__ballot(x < w && ((masks[x] >> d) & 1u)));
+        }
         if (row >= cap) continue;  // beyond the caller's capacity: reported through rows_out
         const int s = static_cast<int>(udiv(static_cast<uint32_t>(w), byT));
         const uint4* src = rank_in(tab, s) + static_cast<int64_t>(w - s * T) * rowvec;
