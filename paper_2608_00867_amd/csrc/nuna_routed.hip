@@ -14,7 +14,7 @@
 //                  its k entries issued together), forms each token's
 //                  destination mask, and takes its copy's receive row as the
 //                  number of earlier tokens (source-major order) sent to the
-//                  same rank: a ballot per wave and a sum over the waves.
+//                  same rank, which each wave counts from the masks in LDS.
 //                  The last workgroup also reports the rows per rank.  At 16
 //                  tokens per rank (8 ranks, 7168 bf16, top-8 of 256) it takes
 //                  4.9 us cold on MI355X, where the two launches below took
