@@ -649,6 +649,8 @@ def full_sweep(nuna, torch, pool, args):
         copy_case(nuna, torch, pool, args, emit)
     if want("ref_stream"):
         ref_stream_case(nuna, torch, pool, args, emit)
+    if want("moe_step"):
+        moe_step_case(nuna, torch, args, emit)
     if want("launch_floor"):
         launch_floor_case(nuna, torch, args, emit)
     f.close()
@@ -751,6 +753,63 @@ def a2a_case(nuna, torch, pool, args, emit, T_tokens=None, colds=(True, False)):
 
 
 EAGER_CALLS = 200
+
+
+MOE_STEP_CALLS = 200
+
+
+def moe_step_case(nuna, torch, args, emit):
+    """One MoE dispatch per serving step with a new routing each step, the top-k table produced on the
+    device (as a gate kernel leaves it), timed on the host per step including a device synchronize:
+    - layout-driven: the table copied to the host, planned (nuna_a2a_layout_create), uploaded (which
+      allocates and copies), dispatched, and the layout freed;
+    - routed: the allocation-free dispatch reading the table where it is.
+    Both give the same receive buffers (checked on the first step)."""
+    from paper_2608_00867_amd import workloads as wl
+    E, H = wl.MOE_EXPERTS, wl.HIDDEN_MOE
+    for T_tok in MOE_DECODE_TOKENS:
+        send_np, _ = wl.a2a_moe(T=T_tok)
+        P, T = len(send_np), send_np[0].shape[0]
+        tables = [wl.moe_routing(P, T, 8, E, wl.seed_for(4, 100 + i)) for i in range(16)]
+        topk_dev = [torch.from_numpy(np.ascontiguousarray(t, dtype=np.int32)).cuda() for t in tables]
+        send = [dev_copy_of(torch, a.reshape(-1)).view(torch.bfloat16).view(T, H) for a in send_np]
+        cap = P * T
+        recv_l = [torch.zeros((cap, H), dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+        recv_r = [torch.zeros((cap, H), dtype=torch.bfloat16, device="cuda") for _ in range(P)]
+        rows_dev = torch.zeros(P + 1, dtype=torch.int64, device="cuda")
+
+        def layout_step(i, out):
+            host = topk_dev[i % len(topk_dev)].cpu().numpy()
+            lay = nuna.A2ALayout(host, E).upload()
+            nuna.all_to_all(send, out, lay, placement="xcd")
+            torch.cuda.synchronize()
+            rows = lay.recv_rows()
+            lay.close()
+            return rows
+
+        def routed_step(i, out):
+            nuna.all_to_all_routed(send, out, topk_dev[i % len(topk_dev)], E, rows_dev, placement="xcd")
+            torch.cuda.synchronize()
+
+        rows = layout_step(0, recv_l)
+        routed_step(0, recv_r)
+        ok = rows_dev.cpu().tolist() == [int(r) for r in rows] + [0] and all(
+            torch.equal(recv_l[d][:int(rows[d])].view(torch.int16), recv_r[d][:int(rows[d])].view(torch.int16))
+            for d in range(P))
+        per = {"layout": [], "routed": []}
+        for rep in range(MOE_STEP_CALLS):
+            for kind in (("layout", "routed") if rep % 2 == 0 else ("routed", "layout")):
+                t0 = time.perf_counter()
+                if kind == "layout":
+                    layout_step(rep, recv_l)
+                else:
+                    routed_step(rep, recv_r)
+                per[kind].append((time.perf_counter() - t0) * 1e6)
+        res = {k: stats(v) for k, v in per.items()}
+        emit({"workload": f"moe_step_bf16_p8_T{T}", "P": P, "tokens_per_rank": T, "hidden": H, "parity": bool(ok),
+              "steps": MOE_STEP_CALLS, "placement": "xcd",
+              **{f"{k}_step_us": {q: round(v, 2) for q, v in r.items()} for k, r in res.items()},
+              "layout_over_routed_step": round(res["layout"]["median"] / res["routed"]["median"], 2)})
 
 
 def eager_case(nuna, torch, pool, args, emit):
